@@ -1,0 +1,378 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test checks the oracle against a closed form, a textbook or library
+routine, brute force on tiny inputs, an invariant of the method, or the
+hand-worked example in ``tests/golden/worked_pair_d4.txt`` (derived by hand
+from Eqs. (1)-(3) of the paper, Section 3).
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.fft
+import scipy.special
+
+import oracle as O
+from synth import WORKLOADS, gen, scaled
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_pair_d4.txt")
+
+
+def _golden():
+    vals = {}
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            name, rest = line.split(":", 1)
+            vals[name.strip()] = np.array([float(x) for x in rest.split()])
+    return vals
+
+
+# ---------------------------------------------------------------- Eq. (1)
+@pytest.mark.parametrize("B", [2, 4, 8])
+def test_dct_is_orthonormal(B):
+    F = O.dct_matrix(B)
+    np.testing.assert_allclose(F @ F.T, np.eye(B), atol=1e-14)
+
+
+def test_dct2_is_haar():
+    h = np.array([[1.0, 1.0], [1.0, -1.0]]) / np.sqrt(2.0)
+    np.testing.assert_allclose(O.dct_matrix(2), h, atol=1e-16)
+
+
+@pytest.mark.parametrize("B", [2, 4])
+def test_factorize_matches_scipy_dct(B):
+    rng = np.random.default_rng(1)
+    X = rng.standard_normal((B, 7, 5))
+    ref = scipy.fft.dct(X, type=2, norm="ortho", axis=0)
+    np.testing.assert_allclose(O.depth_factorize(X), ref, atol=1e-13)
+
+
+def test_round_trip():
+    rng = np.random.default_rng(2)
+    X = rng.standard_normal((2, 33, 16))
+    np.testing.assert_allclose(O.depth_reconstruct(O.depth_factorize(X)), X, atol=1e-14)
+
+
+# ---------------------------------------------------------------- storage rounding
+def test_round_bf16_against_bit_rounding():
+    # float32 -> bf16 by integer round-to-nearest-even on the bit pattern (a
+    # different construction), for inputs exactly representable in float32
+    rng = np.random.default_rng(3)
+    x = np.concatenate([rng.standard_normal(20000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 20000),
+                        np.array([1.00390625, 1.01171875, -1.00390625, 0.0, -0.0, 1e-40, 3.3e38], np.float32)])
+    x = x.astype(np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    ref = r.astype(np.uint32).view(np.float32).astype(np.float64)
+    got = O.round_bf16(x.astype(np.float64))
+    np.testing.assert_array_equal(got, ref)
+
+
+# ---------------------------------------------------------------- residual channels
+def _brute_topk(key, k):
+    """All k-subsets: maximize the descending key vector, then the smallest index set."""
+    d = len(key)
+    best, best_set = None, None
+    for sub in itertools.combinations(range(d), k):
+        v = sorted((key[i] for i in sub), reverse=True)
+        if best is None or v > best:
+            best, best_set = v, sub
+    # among all sets with that key multiset, lexicographically smallest indices
+    cands = [s for s in itertools.combinations(range(d), k)
+             if sorted((key[i] for i in s), reverse=True) == best]
+    return sorted(min(cands))
+
+
+@pytest.mark.parametrize("d,k", [(6, 2), (8, 3), (9, 4), (10, 5), (7, 7), (5, 1)])
+def test_topk_brute_force(d, k):
+    rng = np.random.default_rng(d * 100 + k)
+    for trial in range(40):
+        # small integers force many ties
+        a = rng.integers(-3, 4, size=d).astype(np.float32)
+        b = rng.integers(-3, 4, size=d).astype(np.float32)
+        got = O.residual_channels(a[None], b[None], k)[0].tolist()
+        key = np.abs(a - b).tolist()
+        assert got == _brute_topk(key, k), (a, b)
+
+
+def test_topk_key_is_float32():
+    # a difference that float32 rounds: the key must tie, so the lower index wins
+    a = np.array([1.0, 1.0], dtype=np.float32)
+    b = np.array([np.float32(2.0 ** -25), 0.0], dtype=np.float32)
+    # fl32(1 - 2^-25) = 1 exactly, so both keys are 1.0
+    assert O.residual_channels(a[None], b[None], 1)[0].tolist() == [0]
+
+
+def test_identical_layers_zero_residual():
+    rng = np.random.default_rng(4)
+    X = rng.standard_normal((11, 16)).astype(np.float32)
+    unit = O.compress_unit(np.stack([X, X]), np.stack([X, X]), O.RESIDUAL, 5, "f32")
+    np.testing.assert_array_equal(unit["VK"], 0.0)
+    np.testing.assert_array_equal(unit["VV"], 0.0)
+    np.testing.assert_array_equal(unit["IK"], np.tile(np.arange(5), (11, 1)))
+    np.testing.assert_array_equal(unit["MK"], X.astype(np.float64))
+
+
+def test_k_equals_d_reconstructs_exactly():
+    rng = np.random.default_rng(5)
+    d = 16
+    K = rng.standard_normal((2, 9, d))
+    V = rng.standard_normal((2, 9, d))
+    unit = O.compress_unit(K, V, O.RESIDUAL, d, "f64")
+    for par in (0, 1):
+        np.testing.assert_allclose(O.reconstruct_layer(unit, O.RESIDUAL, par, d, "K"), K[par], atol=1e-14)
+        np.testing.assert_allclose(O.reconstruct_layer(unit, O.RESIDUAL, par, d, "V"), V[par], atol=1e-14)
+
+
+def test_exact_mode_keeps_inputs_bitwise():
+    rng = np.random.default_rng(6)
+    K = gen.round_bf16_f32(rng.standard_normal((2, 5, 8)).astype(np.float32))
+    unit = O.compress_unit(K, K, O.EXACT, 3, "bf16")
+    np.testing.assert_array_equal(unit["K0"], K[0])
+    np.testing.assert_array_equal(unit["K1"], K[1])
+
+
+def test_needle_recovery_tiny():
+    """The planted needle channels are exactly the top-k residual at needle tokens."""
+    w = WORKLOADS["tiny"]
+    for h in range(w.n_kv_heads):
+        K, V, info = gen.segment(w, 0, 0, h)
+        idxK = O.residual_channels(K[0], K[1], w.topk)
+        idxV = O.residual_channels(V[0], V[1], w.topk)
+        for pos, layer, ch in info["needles"]:
+            assert layer == 1
+            assert idxK[pos].tolist() == ch.tolist()
+            assert idxV[pos].tolist() == ch.tolist()
+
+
+# ---------------------------------------------------------------- hand-worked example
+def test_golden_worked_example():
+    g = _golden()
+    K = np.stack([g["K0"].reshape(2, 4), g["K1"].reshape(2, 4)])
+    V = np.stack([g["V0"].reshape(2, 4), g["V1"].reshape(2, 4)])
+    unit = O.compress_unit(K, V, O.RESIDUAL, 1, "f32")
+    np.testing.assert_array_equal(unit["MK"].reshape(-1), g["MK"])
+    np.testing.assert_array_equal(unit["MV"].reshape(-1), g["MV"])
+    np.testing.assert_array_equal(unit["IK"].reshape(-1), g["IK"])
+    np.testing.assert_array_equal(unit["VK"].reshape(-1), g["VK"])
+    np.testing.assert_array_equal(unit["IV"].reshape(-1), g["IV"])
+    np.testing.assert_array_equal(unit["VV"].reshape(-1), g["VV"])
+    q = np.array([[0.0, 0.0, 0.0, math.log(3.0) / 2.0]])
+    out = O.decode_unit(unit, O.RESIDUAL, 0, q, 0.5, 4)
+    np.testing.assert_allclose(out[0], g["OUT_R_L0"], atol=1e-14)
+    # shared mode, layer 1
+    sunit = O.compress_unit(K, V, O.SHARED, 1, "f32")
+    out = O.decode_unit(sunit, O.SHARED, 1, q, 0.5, 4)
+    s3 = 3.0 * math.sqrt(3.0)
+    np.testing.assert_allclose(out[0], (s3 * np.array([1, 0, 1, 0]) + np.array([0, 2, 0, 3])) / (s3 + 1), atol=1e-14)
+    # routing loss
+    Q2 = np.zeros((2, 1, 1, 4))
+    Q2[:, 0, 0, 3] = 2.0
+    np.testing.assert_allclose(O.routing_errors(K, Q2, 1), g["E"], atol=1e-13)
+    om = O.omega(4, 1, "f32")
+    np.testing.assert_array_equal(om, g["OMEGA"])
+    E = g["E"][None]
+    got = [int(O.route(E, om, lam)[0]) for lam in (1.0, 4.0, 100.0)]
+    assert got == g["ROUTE_L1_L4_L100"].astype(int).tolist()
+
+
+# ---------------------------------------------------------------- decode
+def _textbook_attention(q, K, V, scale):
+    return scipy.special.softmax((q @ K.T) * scale, axis=-1) @ V
+
+
+def test_exact_heads_equal_textbook_attention():
+    rng = np.random.default_rng(7)
+    K = rng.standard_normal((2, 40, 8))
+    V = rng.standard_normal((2, 40, 8))
+    unit = O.compress_unit(K, V, O.EXACT, 3, "f64")
+    q = rng.standard_normal((3, 8))
+    for layer in (0, 1):
+        np.testing.assert_allclose(O.decode_unit(unit, O.EXACT, layer, q, 0.3, 8),
+                                   _textbook_attention(q, K[layer], V[layer], 0.3), rtol=1e-13, atol=1e-14)
+
+
+def test_tiny_brute_force_softmax():
+    rng = np.random.default_rng(8)
+    T, d = 5, 3
+    K = rng.standard_normal((T, d))
+    V = rng.standard_normal((T, d))
+    q = rng.standard_normal(d)
+    w = [math.exp(sum(q[c] * K[t][c] for c in range(d)) * 0.7) for t in range(T)]
+    ref = [sum(w[t] * V[t][c] for t in range(T)) / sum(w) for c in range(d)]
+    np.testing.assert_allclose(O.attention(q[None], K, V, 0.7)[0], ref, rtol=1e-13)
+
+
+def test_single_token_and_zero_query():
+    rng = np.random.default_rng(9)
+    K = rng.standard_normal((2, 1, 8))
+    V = rng.standard_normal((2, 1, 8))
+    for mode in O.MODES:
+        unit = O.compress_unit(K, V, mode, 2, "f64")
+        out = O.decode_unit(unit, mode, 1, rng.standard_normal((2, 8)), 1.0, 8)
+        np.testing.assert_allclose(out, np.repeat(O.reconstruct_layer(unit, mode, 1, 8, "V"), 2, 0), atol=1e-14)
+    K = rng.standard_normal((2, 17, 8))
+    V = rng.standard_normal((2, 17, 8))
+    for mode in O.MODES:
+        unit = O.compress_unit(K, V, mode, 2, "f64")
+        out = O.decode_unit(unit, mode, 0, np.zeros((1, 8)), 1.0, 8)
+        np.testing.assert_allclose(out[0], O.reconstruct_layer(unit, mode, 0, 8, "V").mean(0), atol=1e-14)
+
+
+def test_shared_heads_same_output_in_both_layers():
+    rng = np.random.default_rng(10)
+    K = rng.standard_normal((2, 30, 8))
+    V = rng.standard_normal((2, 30, 8))
+    unit = O.compress_unit(K, V, O.SHARED, 2, "f32")
+    q = rng.standard_normal((2, 8))
+    np.testing.assert_array_equal(O.decode_unit(unit, O.SHARED, 0, q, 0.4, 8),
+                                  O.decode_unit(unit, O.SHARED, 1, q, 0.4, 8))
+
+
+def test_shared_mode_is_pair_mean_and_residual_adds_signed_half_difference():
+    rng = np.random.default_rng(11)
+    K = rng.standard_normal((2, 6, 8))
+    unit = O.compress_unit(K, K, O.RESIDUAL, 8, "f64")
+    np.testing.assert_allclose(unit["MK"], (K[0] + K[1]) / 2, atol=1e-15)
+    np.testing.assert_allclose(unit["VK"], (K[0] - K[1]) / 2, atol=1e-15)
+
+
+# ---------------------------------------------------------------- Eq. (2)
+def _brute_routing(K2, Q2, k):
+    """Eq. (2) with explicit loops over layers, heads, probe rows and tokens."""
+    _, T, d = K2.shape
+    nl, G, P, _ = Q2.shape
+    idx = O.residual_channels(K2[0], K2[1], k)
+    res = []
+    for mode in O.MODES:
+        tot = 0.0
+        for l in range(nl):
+            sign = 1.0 if l == 0 else -1.0
+            for g in range(G):
+                for p in range(P):
+                    for t in range(T):
+                        # K^(m) - K for layer l, written out per channel
+                        s = 0.0
+                        for c in range(d):
+                            half = (K2[0, t, c] - K2[1, t, c]) / 2.0
+                            if mode == O.EXACT:
+                                diff = 0.0
+                            elif mode == O.SHARED or c not in idx[t]:
+                                diff = -sign * half
+                            else:
+                                diff = 0.0
+                            s += Q2[l, g, p, c] * diff
+                        tot += (s / math.sqrt(d)) ** 2
+        res.append(tot / (nl * G * P))
+    return np.array(res)
+
+
+def test_routing_errors_brute_force():
+    rng = np.random.default_rng(12)
+    K2 = rng.standard_normal((2, 6, 5)).astype(np.float32).astype(np.float64)
+    Q2 = rng.standard_normal((2, 2, 3, 5))
+    np.testing.assert_allclose(O.routing_errors(K2, Q2, 2), _brute_routing(K2, Q2, 2), rtol=1e-12, atol=1e-15)
+
+
+def test_routing_errors_invariants():
+    rng = np.random.default_rng(13)
+    K2 = rng.standard_normal((2, 20, 8))
+    Q2 = rng.standard_normal((2, 2, 4, 8))
+    E = O.routing_errors(K2, Q2, 3)
+    assert E[O.EXACT] == 0.0
+    assert E[O.RESIDUAL] <= E[O.SHARED]
+    assert O.routing_errors(K2, Q2, 8)[O.RESIDUAL] < 1e-25           # k = d
+    same = np.stack([K2[0], K2[0]])
+    Es = O.routing_errors(same, Q2, 3)
+    # identical layers: zero up to the fp64 noise of reconstructing K through F^T F
+    assert Es[O.SHARED] < 1e-28 and Es[O.RESIDUAL] < 1e-28
+    om = O.omega(8, 3, "bf16")
+    for lam in (1e-20, 1e-3, 1.0, 1e6):
+        assert int(O.route(Es[None], om, lam)[0]) == O.SHARED
+    # with exactly zero errors the tie at lambda = 0 goes to the cheapest mode
+    assert int(O.route(np.zeros((1, 3)), om, 0.0)[0]) == O.SHARED
+
+
+def test_routing_error_statistics():
+    """E_S is about T (1 - rho) / (2 d) for q ~ N(0, I/d)."""
+    rng = np.random.default_rng(14)
+    T, d, rho = 4096, 32, 0.8
+    x0 = rng.standard_normal((T, d))
+    x1 = rho * x0 + math.sqrt(1 - rho * rho) * rng.standard_normal((T, d))
+    Q2 = rng.standard_normal((2, 2, 64, d)) / math.sqrt(d)
+    E = O.routing_errors(np.stack([x0, x1]), Q2, 4)
+    assert abs(E[O.SHARED] / (T * (1 - rho) / (2 * d)) - 1.0) < 0.08
+
+
+# ---------------------------------------------------------------- routing and bytes
+def test_omega_closed_form():
+    np.testing.assert_allclose(O.omega(128, 16, "bf16"), [0.5, 0.59375, 1.0])
+    np.testing.assert_allclose(O.omega(64, 8, "f32"), [0.5, 0.578125, 1.0])
+
+
+def test_cache_bytes_tiny_by_hand():
+    w = WORKLOADS["tiny"]
+    modes = gen.fixed_modes(w)[None]
+    # T*d*e = 512*64*4 = 131072 per dense plane; residual planes 512*8 = 4096 (u8)
+    # and 512*8*4 = 16384 (fp32); S = 2 planes, R = 2 + 4 small, E = 4 planes.
+    assert O.cache_bytes(w.seq_lens, modes, 64, 8, "f32") == 1392640
+
+
+def test_plane_padding():
+    assert O.unit_bytes(O.SHARED, 1, 64, 8, "bf16") == 2 * 256
+    assert O.unit_bytes(O.RESIDUAL, 3, 64, 8, "bf16") == 2 * 512 + 2 * (256 + 256)
+    assert O.unit_bytes(O.EXACT, 2, 128, 16, "bf16") == 4 * 512
+
+
+def test_route_limits():
+    rng = np.random.default_rng(15)
+    E = np.abs(rng.standard_normal((50, 3)))
+    E[:, 1] = E[:, 0] * 0.5
+    E[:, 2] = 0.0
+    om = O.omega(128, 16, "bf16")
+    assert (O.route(E, om, 0.0) == O.EXACT).all()
+    assert (O.route(E, om, math.inf) == O.SHARED).all()
+    assert (O.route(E, om, 1e30) == O.SHARED).all()
+
+
+def test_route_budget_minimal_lambda_brute_force():
+    rng = np.random.default_rng(16)
+    T, d, k = 1000, 64, 8
+    for trial in range(5):
+        E = np.abs(rng.standard_normal((12, 3))) * 10
+        E[:, 1] = E[:, 0] * rng.uniform(0.2, 0.9, 12)
+        E[:, 2] = 0.0
+        om = O.omega(d, k, "bf16")
+        seg = {m: O.unit_bytes(m, T, d, k, "bf16") for m in O.MODES}
+
+        def fp(lam):
+            return sum(seg[int(m)] for m in O.route(E, om, lam))
+
+        lo, hi = fp(math.inf), fp(0.0)
+        budget = int(lo + (hi - lo) * rng.uniform(0.1, 0.9))
+        modes, lam, ok = O.route_budget(E, T, d, k, "bf16", budget)
+        assert ok and fp(lam) <= budget
+        grid = np.linspace(0, lam, 2000, endpoint=False)
+        assert all(fp(x) > budget for x in grid)
+        # footprint never grows with lambda
+        lams = np.linspace(0, 3 * lam + 1, 500)
+        fps = [fp(x) for x in lams]
+        assert all(a >= b for a, b in zip(fps, fps[1:]))
+    modes, lam, ok = O.route_budget(E, T, d, k, "bf16", 10)
+    assert not ok and (modes == O.SHARED).all()
+
+
+def test_gqa_is_per_query_head_attention():
+    rng = np.random.default_rng(17)
+    K = rng.standard_normal((2, 25, 8))
+    V = rng.standard_normal((2, 25, 8))
+    unit = O.compress_unit(K, V, O.RESIDUAL, 3, "f32")
+    q = rng.standard_normal((4, 8))
+    full = O.decode_unit(unit, O.RESIDUAL, 1, q, 0.35, 8)
+    for g in range(4):
+        np.testing.assert_allclose(full[g], O.decode_unit(unit, O.RESIDUAL, 1, q[g:g + 1], 0.35, 8)[0], rtol=1e-14)
