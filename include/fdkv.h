@@ -1,0 +1,171 @@
+/*
+ * fdkv.h - C ABI of the FreqDepthKV compressed-KV path on AMD MI355X (gfx950).
+ *
+ * FreqDepthKV (Section 3 of the paper) compresses a decoder's KV cache along
+ * depth.  Adjacent layers 2b and 2b+1 form a block; an orthonormal DCT along
+ * the layer axis (Eq. 1) splits each block into a low-frequency coefficient
+ * stored once for both layers and a high-frequency coefficient kept only
+ * sparsely (Eq. 3).  An online probe measures, per (block, KV head), how much
+ * each candidate reconstruction moves the attention logits of probe queries
+ * (Eq. 2) and routes the head to one of three modes; decode attention then
+ * rebuilds K/V on the fly inside a fused softmax(q K^T) V.
+ *
+ * Conventions shared by every entry point:
+ *
+ *  - Blocks are layer pairs (B = 2).  With the orthonormal DCT-II the stored
+ *    per-layer images are M = (x[2b] + x[2b+1]) / 2 (shared part) and
+ *    D = (x[2b] - x[2b+1]) / 2 (high-frequency part): layer 2b rebuilds
+ *    M + D, layer 2b+1 rebuilds M - D.
+ *  - The residual of a token keeps the `topk` channels of largest
+ *    |fl32(x[2b] - x[2b+1])| (ties to the lower channel), as uint8 channel
+ *    indices in ascending order plus D at those channels.  K and V choose
+ *    their channels independently.
+ *  - Query head g reads KV head g / (n_q_heads / n_kv_heads).
+ *  - K, V, queries, the cache and attention outputs use one element type,
+ *    `dims.dtype` (fp32 or bf16); all arithmetic is fp32.
+ *  - Device pointers are caller-owned device memory, 16-byte aligned.  The
+ *    library allocates nothing, keeps no state between calls and launches
+ *    work asynchronously on the caller's stream (`stream` is a hipStream_t;
+ *    NULL means the null stream).  Host-side validation happens before any
+ *    HIP call, so an invalid argument never touches the device.
+ *  - Kernel launch failures return FDKV_E_HIP; faults inside a kernel
+ *    surface at the caller's next synchronisation.  Inputs must be finite.
+ *
+ * Compressed cache layout (one device buffer).  It is a sequence of
+ * segments, one per (sequence, pair b, KV head h) in row-major order, each
+ * starting at the offset fdkv_layout() returns.  A segment is a list of
+ * planes, each padded to a multiple of 256 bytes, e = element bytes:
+ *    SHARED   : MK[T][d], MV[T][d]
+ *    RESIDUAL : MK[T][d], MV[T][d], IK[T][k] (u8), VK[T][k] (e), IV[T][k] (u8), VV[T][k] (e)
+ *    EXACT    : K[2b][T][d], K[2b+1][T][d], V[2b][T][d], V[2b+1][T][d]
+ */
+#ifndef FDKV_H
+#define FDKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FDKV_OK = 0,
+  FDKV_E_INVALID_ARG = -1, /* null/misaligned pointer, bad size or shape */
+  FDKV_E_UNSUPPORTED = -2, /* valid but not compiled: head_dim not 64/128, group not 1/2/4/8 */
+  FDKV_E_WORKSPACE = -3,   /* workspace smaller than the *_workspace query returned */
+  FDKV_E_BUDGET = -4,      /* byte budget below the all-shared footprint */
+  FDKV_E_HIP = -5          /* a HIP runtime call failed (see fdkv_last_error) */
+} fdkv_status;
+
+/* Head modes, in increasing memory cost; ties in routing go to the lower value. */
+typedef enum { FDKV_SHARED = 0, FDKV_RESIDUAL = 1, FDKV_EXACT = 2 } fdkv_mode;
+
+typedef enum { FDKV_F32 = 0, FDKV_BF16 = 1 } fdkv_dtype;
+
+typedef struct {
+  int32_t n_layers;   /* L, even, 2..256 */
+  int32_t n_kv_heads; /* Hkv >= 1 */
+  int32_t n_q_heads;  /* Hq, a multiple of Hkv; Hq / Hkv in {1, 2, 4, 8} */
+  int32_t head_dim;   /* d in {64, 128} */
+  int32_t topk;       /* k residual channels per token, 0 <= k <= d */
+  int32_t dtype;      /* fdkv_dtype */
+} fdkv_dims;
+
+/* Message for a status code (static storage). */
+const char* fdkv_status_string(int32_t status);
+
+/* Text of the last FDKV_E_HIP failure in the calling thread ("" if none). */
+const char* fdkv_last_error(void);
+
+/*
+ * fdkv_layout - host only.  Byte layout of a compressed cache (Eq. 3 storage).
+ *   seq_lens     host [batch]                     tokens per sequence, >= 0
+ *   modes        host [batch][L/2][Hkv]           fdkv_mode per unit
+ *   seg_offsets  host [batch][L/2][Hkv] or NULL   out: segment byte offsets
+ *   total_bytes  host                             out: buffer size needed
+ * Segments follow each other in (sequence, pair, head) order; all offsets are
+ * multiples of 256.
+ */
+fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens,
+                        const uint8_t* modes, uint64_t* seg_offsets, uint64_t* total_bytes);
+
+/*
+ * fdkv_route - host only.  Mode choice of Eq. (3), m = argmin E_m + lambda * Omega(m)
+ * with Eq. (2)'s loss, and the budget rule that raises lambda until the cache
+ * fits (end of Section 3).
+ *   seq_len      tokens of the sequence (for the footprint)
+ *   errors       host [L/2][Hkv][2]   E_shared, E_residual per unit (E_exact = 0),
+ *                                     as written by fdkv_probe
+ *   lambda       penalty used when budget_bytes == 0
+ *   budget_bytes 0: route with `lambda`.  Otherwise: the smallest lambda among
+ *                0, the per-unit breakpoints (E_i - E_j)/(Omega_j - Omega_i)
+ *                and +inf whose fdkv_layout footprint is <= budget_bytes.
+ *   modes_out    host [L/2][Hkv]   out
+ *   lambda_out   host, may be NULL out: lambda used (+inf when infeasible)
+ * Omega(m) = bytes per token of mode m / bytes per token of EXACT.  Ties go to
+ * the cheaper mode.  Returns FDKV_E_BUDGET (modes all SHARED) when even
+ * all-shared exceeds the budget.
+ */
+fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* errors, double lambda,
+                       uint64_t budget_bytes, uint8_t* modes_out, double* lambda_out);
+
+/* Device workspace bytes fdkv_probe needs for this shape. */
+fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t n_probe, size_t* bytes);
+
+/*
+ * fdkv_probe - device.  Routing loss of Eq. (2) for every (pair, KV head):
+ *   E_m[b,h] = 1/(2 G P) * sum over l in {2b, 2b+1}, query heads g of KV head h,
+ *              probe rows p, tokens t of ((q_{l,g,p} . (K^(m)_{l,h,t} - K_{l,h,t})) / sqrt(d))^2
+ * for m = SHARED (K^ = M) and m = RESIDUAL (K^ = M +/- D on the token's top-k
+ * channels).  Logits are compared raw, over all T keys, for keys only.
+ *   k_layers   host array of L device pointers, layer l holds K_l [Hkv][T][d]
+ *   qp_layers  host array of L device pointers, layer l holds Q_l [Hq][P][d]
+ *   n_probe    P >= 1 probe rows per query head
+ *   errors_out device float [L/2][Hkv][2]
+ *   ws         device workspace of >= fdkv_probe_workspace() bytes
+ */
+fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
+                       const void* const* qp_layers, int32_t n_probe, float* errors_out,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * fdkv_compress - device.  Writes one sequence's segments of the compressed
+ * cache (Eq. 1 factorization, Eq. 3 storage) for the given modes.
+ *   k_layers, v_layers  host arrays of L device pointers, [Hkv][T][d] each
+ *   modes        device [L/2][Hkv]
+ *   seg_offsets  device [L/2][Hkv], from fdkv_layout (256-byte multiples)
+ *   cache        device buffer the offsets index into
+ */
+fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
+                          const void* const* v_layers, const uint8_t* modes,
+                          const uint64_t* seg_offsets, void* cache, void* stream);
+
+/* Device workspace bytes fdkv_decode_attn needs for this batch shape. */
+fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t max_seq_len, size_t* bytes);
+
+/*
+ * fdkv_decode_attn - device.  One decode step of one layer over the
+ * compressed cache, with the reconstruction of Eq. (3) fused into attention
+ * (Section 3, after Eq. 3): o = softmax(q K~^T * sm_scale) V~ over the T_i
+ * cached tokens of each sequence, K~/V~ rebuilt per head mode.
+ *   seq_lens     device int32 [batch], 0 <= T_i <= max_seq_len (T_i = 0 gives o = 0)
+ *   max_seq_len  host, sizes the launch
+ *   modes        device [batch][L/2][Hkv]
+ *   seg_offsets  device [batch][L/2][Hkv]
+ *   layer        0 <= layer < L
+ *   q            device [batch][Hq][d]
+ *   out          device [batch][Hq][d]
+ *   sm_scale     logit scale (the paper uses 1/sqrt(d))
+ *   ws           device workspace of >= fdkv_decode_workspace() bytes
+ */
+fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens,
+                             int32_t max_seq_len, const uint8_t* modes, const uint64_t* seg_offsets,
+                             const void* cache, int32_t layer, const void* q, void* out,
+                             float sm_scale, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FDKV_H */

@@ -1,0 +1,177 @@
+"""ctypes binding of libfdkv (argument marshalling only).
+
+Each function mirrors one entry point of ``include/fdkv.h`` and takes torch
+tensors for device buffers (their ``data_ptr()`` is passed) and numpy arrays
+for host buffers.  Work is queued on the current torch stream.  Nothing here
+computes any part of the method; a missing library raises ``RuntimeError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfdkv.so")
+_lib = None
+
+SHARED, RESIDUAL, EXACT = 0, 1, 2
+F32, BF16 = 0, 1
+
+STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: "FDKV_E_WORKSPACE",
+          -4: "FDKV_E_BUDGET", -5: "FDKV_E_HIP"}
+
+SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_layout", "fdkv_route", "fdkv_probe_workspace",
+           "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn")
+
+
+class FdkvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        lib = load()
+        msg = lib.fdkv_status_string(status).decode()
+        if status == -5:
+            msg += ": " + lib.fdkv_last_error().decode()
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype) -> Dims:
+    dt = {"f32": F32, "bf16": BF16}.get(dtype, dtype)
+    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt)
+
+
+def load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, U64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    DP = ctypes.POINTER(Dims)
+    lib.fdkv_status_string.restype = ctypes.c_char_p
+    lib.fdkv_status_string.argtypes = [I32]
+    lib.fdkv_last_error.restype = ctypes.c_char_p
+    lib.fdkv_last_error.argtypes = []
+    lib.fdkv_layout.restype = I32
+    lib.fdkv_layout.argtypes = [DP, I32, P, P, P, P]
+    lib.fdkv_route.restype = I32
+    lib.fdkv_route.argtypes = [DP, I32, P, ctypes.c_double, U64, P, P]
+    lib.fdkv_probe_workspace.restype = I32
+    lib.fdkv_probe_workspace.argtypes = [DP, I32, I32, P]
+    lib.fdkv_probe.restype = I32
+    lib.fdkv_probe.argtypes = [DP, I32, P, P, I32, P, P, SZ, P]
+    lib.fdkv_compress.restype = I32
+    lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P]
+    lib.fdkv_decode_workspace.restype = I32
+    lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
+    lib.fdkv_decode_attn.restype = I32
+    lib.fdkv_decode_attn.argtypes = [DP, I32, P, I32, P, P, P, I32, P, P, ctypes.c_float, P, SZ, P]
+    _lib = lib
+    return lib
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise FdkvError(st, where)
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dev(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(int(s.cuda_stream))
+
+
+def _ptr_array(tensors: Sequence) -> ctypes.Array:
+    arr = (ctypes.c_void_p * len(tensors))()
+    for i, t in enumerate(tensors):
+        arr[i] = _dev(t)
+    return arr
+
+
+# ----------------------------------------------------------------- host entry points
+def layout(d: Dims, seq_lens, modes):
+    """``(seg_offsets [batch][L/2][Hkv] uint64, total_bytes)`` for host ``modes``."""
+    lib = load()
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    m = np.ascontiguousarray(modes, dtype=np.uint8)
+    off = np.zeros(m.shape, dtype=np.uint64)
+    total = ctypes.c_uint64(0)
+    _check(lib.fdkv_layout(ctypes.byref(d), int(sl.size), _np_ptr(sl), _np_ptr(m), _np_ptr(off),
+                           ctypes.byref(total)), "fdkv_layout")
+    return off, int(total.value)
+
+
+def route(d: Dims, seq_len: int, errors, lam: float = 0.0, budget_bytes: int = 0, allow_infeasible=False):
+    """``(modes [L/2][Hkv] uint8, lambda_used, status)`` from host ``errors [L/2][Hkv][2]``."""
+    lib = load()
+    e = np.ascontiguousarray(errors, dtype=np.float32)
+    modes = np.zeros(e.shape[:-1], dtype=np.uint8)
+    lam_out = ctypes.c_double(0.0)
+    st = lib.fdkv_route(ctypes.byref(d), int(seq_len), _np_ptr(e), float(lam), int(budget_bytes),
+                        _np_ptr(modes), ctypes.byref(lam_out))
+    if not (st == 0 or (st == -4 and allow_infeasible)):
+        _check(st, "fdkv_route")
+    return modes, float(lam_out.value), st
+
+
+def probe_workspace(d: Dims, seq_len: int, n_probe: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().fdkv_probe_workspace(ctypes.byref(d), int(seq_len), int(n_probe), ctypes.byref(n)),
+           "fdkv_probe_workspace")
+    return int(n.value)
+
+
+def decode_workspace(d: Dims, batch: int, max_seq_len: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().fdkv_decode_workspace(ctypes.byref(d), int(batch), int(max_seq_len), ctypes.byref(n)),
+           "fdkv_decode_workspace")
+    return int(n.value)
+
+
+# ----------------------------------------------------------------- device entry points
+def probe(d: Dims, seq_len: int, k_layers: Sequence, qp_layers: Sequence, n_probe: int, errors_out, ws,
+          stream=None):
+    """Queue fdkv_probe; ``k_layers``/``qp_layers`` are per-layer device tensors."""
+    _check(load().fdkv_probe(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(qp_layers),
+                             int(n_probe), _dev(errors_out), _dev(ws), int(ws.numel() * ws.element_size()),
+                             _stream(stream)), "fdkv_probe")
+
+
+def compress(d: Dims, seq_len: int, k_layers: Sequence, v_layers: Sequence, modes, seg_offsets, cache,
+             stream=None):
+    """Queue fdkv_compress for one sequence (``modes``/``seg_offsets`` device tensors)."""
+    _check(load().fdkv_compress(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(v_layers),
+                                _dev(modes), _dev(seg_offsets), _dev(cache), _stream(stream)), "fdkv_compress")
+
+
+def decode_attn(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offsets, cache, layer: int, q, out,
+                sm_scale: float, ws, stream=None):
+    """Queue fdkv_decode_attn for one layer."""
+    _check(load().fdkv_decode_attn(ctypes.byref(d), int(batch), _dev(seq_lens), int(max_seq_len), _dev(modes),
+                                   _dev(seg_offsets), _dev(cache), int(layer), _dev(q), _dev(out),
+                                   ctypes.c_float(sm_scale), _dev(ws), int(ws.numel() * ws.element_size()),
+                                   _stream(stream)), "fdkv_decode_attn")
+
+
+def decode_attn_raw(d: Dims, batch: int, seq_lens_ptr: int, max_seq_len: int, modes_ptr: int, offs_ptr: int,
+                    cache_ptr: int, layer: int, q_ptr: int, out_ptr: int, sm_scale: float, ws_ptr: int,
+                    ws_bytes: int, stream_ptr: int) -> int:
+    """Same call with raw integer pointers (for tight timing loops); returns the status."""
+    return load().fdkv_decode_attn(ctypes.byref(d), batch, seq_lens_ptr, max_seq_len, modes_ptr, offs_ptr,
+                                   cache_ptr, layer, q_ptr, out_ptr, ctypes.c_float(sm_scale), ws_ptr, ws_bytes,
+                                   ctypes.c_void_p(stream_ptr))

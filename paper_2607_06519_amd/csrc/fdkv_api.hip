@@ -1,0 +1,326 @@
+// C ABI of libfdkv: host-side validation, the closed-form cache layout, the
+// routing rule of Eq. (3) with the budget search of Section 3, and the
+// launches of the HIP kernels on the caller's stream.
+#include <math.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "fdkv.h"
+#include "fdkv_common.h"
+#include "fdkv_kernels.h"
+
+using namespace fdkv;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+bool aligned(const void* p, uintptr_t a) { return p && ((reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0); }
+
+int elem_bytes(const fdkv_dims* d) { return d->dtype == FDKV_BF16 ? 2 : 4; }
+
+fdkv_status check_dims(const fdkv_dims* d) {
+  if (!d) return FDKV_E_INVALID_ARG;
+  if (d->n_layers < 2 || (d->n_layers & 1) || d->n_layers > kMaxPtrLayers) return FDKV_E_INVALID_ARG;
+  if (d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads || d->n_q_heads % d->n_kv_heads) return FDKV_E_INVALID_ARG;
+  if (d->head_dim < 1 || d->head_dim > 256) return FDKV_E_INVALID_ARG;
+  if (d->topk < 0 || d->topk > d->head_dim) return FDKV_E_INVALID_ARG;
+  if (d->dtype != FDKV_F32 && d->dtype != FDKV_BF16) return FDKV_E_INVALID_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return FDKV_E_UNSUPPORTED;
+  const int G = d->n_q_heads / d->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return FDKV_E_UNSUPPORTED;
+  return FDKV_OK;
+}
+
+fdkv_status hip_fail(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return FDKV_E_HIP;
+}
+
+uint64_t bytes_per_token(int mode, int d, int k, int e) {
+  if (mode == kShared) return 2ull * d * e;
+  if (mode == kResidual) return 2ull * d * e + 2ull * k * (1 + e);
+  return 4ull * d * e;
+}
+
+uint64_t probe_chunks(int T) { return (uint64_t)(T + kProbeChunk - 1) / kProbeChunk; }
+
+// Probe workspace regions, each aligned to 256 bytes.
+struct ProbeWs {
+  uint64_t idx, gram, part, total;
+};
+ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
+  const uint64_t units = (uint64_t)(d->n_layers / 2) * d->n_kv_heads;
+  ProbeWs w{};
+  w.idx = 0;
+  w.gram = w.idx + units * plane_bytes((uint64_t)T * d->topk);
+  w.part = w.gram + plane_bytes(units * d->head_dim * d->head_dim * 4);
+  w.total = w.part + plane_bytes(units * probe_chunks(T) * 2 * 4);
+  return w;
+}
+
+uint64_t decode_chunks(int max_T) { return (uint64_t)(max_T + kDecodeWgTokens - 1) / kDecodeWgTokens; }
+
+}  // namespace
+
+extern "C" {
+
+const char* fdkv_status_string(int32_t s) {
+  switch (s) {
+    case FDKV_OK: return "ok";
+    case FDKV_E_INVALID_ARG: return "invalid argument";
+    case FDKV_E_UNSUPPORTED: return "unsupported shape (head_dim must be 64 or 128, Hq/Hkv in 1,2,4,8)";
+    case FDKV_E_WORKSPACE: return "workspace too small";
+    case FDKV_E_BUDGET: return "byte budget below the all-shared footprint";
+    case FDKV_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* fdkv_last_error(void) { return g_last_error.c_str(); }
+
+fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, const uint8_t* modes,
+                        uint64_t* seg_offsets, uint64_t* total_bytes) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (batch < 1 || !seq_lens || !modes || !total_bytes) return FDKV_E_INVALID_ARG;
+  const int units = dims->n_layers / 2 * dims->n_kv_heads;
+  for (int b = 0; b < batch; ++b) {
+    if (seq_lens[b] < 0) return FDKV_E_INVALID_ARG;
+    for (int u = 0; u < units; ++u)
+      if (modes[(size_t)b * units + u] > FDKV_EXACT) return FDKV_E_INVALID_ARG;
+  }
+  const int e = elem_bytes(dims);
+  uint64_t off = 0;
+  for (int b = 0; b < batch; ++b)
+    for (int u = 0; u < units; ++u) {
+      const size_t i = (size_t)b * units + u;
+      if (seg_offsets) seg_offsets[i] = off;
+      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e).total;
+    }
+  *total_bytes = off;
+  return FDKV_OK;
+}
+
+#pragma clang fp contract(off)
+fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* errors, double lambda,
+                       uint64_t budget_bytes, uint8_t* modes_out, double* lambda_out) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (seq_len < 0 || !errors || !modes_out) return FDKV_E_INVALID_ARG;
+  if (budget_bytes == 0 && !(lambda >= 0.0)) return FDKV_E_INVALID_ARG;
+  const int units = dims->n_layers / 2 * dims->n_kv_heads;
+  const int d = dims->head_dim, k = dims->topk, e = elem_bytes(dims);
+  double om[3];
+  const double full = (double)bytes_per_token(kExact, d, k, e);
+  for (int m = 0; m < 3; ++m) om[m] = (double)bytes_per_token(m, d, k, e) / full;
+  uint64_t seg[3];
+  for (int m = 0; m < 3; ++m) seg[m] = seg_layout(m, (uint64_t)seq_len, d, k, e).total;
+
+  auto decide = [&](double lam, uint8_t* out) {
+    uint64_t fp = 0;
+    for (int u = 0; u < units; ++u) {
+      const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
+      int best = 0;
+      double bc = E[0] + lam * om[0];
+      for (int m = 1; m < 3; ++m) {
+        const double c = E[m] + lam * om[m];
+        if (c < bc) {
+          bc = c;
+          best = m;
+        }
+      }
+      out[u] = (uint8_t)best;
+      fp += seg[best];
+    }
+    return fp;
+  };
+
+  if (budget_bytes == 0) {
+    decide(lambda, modes_out);
+    if (lambda_out) *lambda_out = lambda;
+    return FDKV_OK;
+  }
+  std::vector<double> cands;
+  cands.push_back(0.0);
+  for (int u = 0; u < units; ++u) {
+    const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
+    for (int i = 0; i < 3; ++i)
+      for (int j = i + 1; j < 3; ++j) {
+        if (!(om[j] > om[i])) continue;
+        const double lam = (E[i] - E[j]) / (om[j] - om[i]);
+        if (lam > 0.0 && isfinite(lam)) cands.push_back(lam);
+      }
+  }
+  std::sort(cands.begin(), cands.end());
+  cands.erase(std::unique(cands.begin(), cands.end()), cands.end());
+  cands.push_back(INFINITY);
+  std::vector<uint8_t> tmp((size_t)units);
+  for (double lam : cands) {
+    if (decide(lam, tmp.data()) <= budget_bytes) {
+      std::copy(tmp.begin(), tmp.end(), modes_out);
+      if (lambda_out) *lambda_out = lam;
+      return FDKV_OK;
+    }
+  }
+  std::fill(modes_out, modes_out + units, (uint8_t)FDKV_SHARED);
+  if (lambda_out) *lambda_out = INFINITY;
+  return FDKV_E_BUDGET;
+}
+#pragma clang fp contract(on)
+
+fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t n_probe, size_t* bytes) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (seq_len < 1 || n_probe < 1 || !bytes) return FDKV_E_INVALID_ARG;
+  *bytes = (size_t)probe_ws_layout(dims, seq_len).total;
+  return FDKV_OK;
+}
+
+fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
+                       const void* const* qp_layers, int32_t n_probe, float* errors_out, void* ws,
+                       size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (seq_len < 1 || n_probe < 1 || !k_layers || !qp_layers) return FDKV_E_INVALID_ARG;
+  if (!aligned(errors_out, 4) || !aligned(ws, 256)) return FDKV_E_INVALID_ARG;
+  for (int l = 0; l < dims->n_layers; ++l)
+    if (!aligned(k_layers[l], 16) || !aligned(qp_layers[l], 16)) return FDKV_E_INVALID_ARG;
+  const ProbeWs w = probe_ws_layout(dims, seq_len);
+  if (ws_bytes < w.total) return FDKV_E_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+
+  SelectParams sp{};
+  for (int l = 0; l < dims->n_layers; ++l) sp.k[l] = sp.v[l] = k_layers[l];
+  sp.modes = nullptr;
+  sp.idx_out = base + w.idx;
+  sp.seq_len = seq_len;
+  sp.n_pairs = dims->n_layers / 2;
+  sp.hkv = dims->n_kv_heads;
+  sp.d = dims->head_dim;
+  sp.topk = dims->topk;
+  sp.bf16 = dims->dtype == FDKV_BF16;
+  hipError_t e = launch_residual_select(sp, 1, s);
+  if (e != hipSuccess) return hip_fail(e, "residual_select");
+
+  ProbeParams pp{};
+  for (int l = 0; l < dims->n_layers; ++l) {
+    pp.k[l] = k_layers[l];
+    pp.qp[l] = qp_layers[l];
+  }
+  pp.idx = base + w.idx;
+  pp.gram_q = reinterpret_cast<float*>(base + w.gram);
+  pp.partial = reinterpret_cast<float*>(base + w.part);
+  pp.errors = errors_out;
+  pp.seq_len = seq_len;
+  pp.n_pairs = dims->n_layers / 2;
+  pp.hkv = dims->n_kv_heads;
+  pp.hq = dims->n_q_heads;
+  pp.d = dims->head_dim;
+  pp.topk = dims->topk;
+  pp.n_probe = n_probe;
+  pp.n_chunks = (int)probe_chunks(seq_len);
+  pp.bf16 = dims->dtype == FDKV_BF16;
+  e = launch_probe(pp, s);
+  if (e != hipSuccess) return hip_fail(e, "probe");
+  return FDKV_OK;
+}
+
+fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
+                          const void* const* v_layers, const uint8_t* modes, const uint64_t* seg_offsets,
+                          void* cache, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (seq_len < 0 || !k_layers || !v_layers || !modes || !aligned(seg_offsets, 8) || !aligned(cache, 256))
+    return FDKV_E_INVALID_ARG;
+  for (int l = 0; l < dims->n_layers; ++l)
+    if (!aligned(k_layers[l], 16) || !aligned(v_layers[l], 16)) return FDKV_E_INVALID_ARG;
+  if (seq_len == 0) return FDKV_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  CompressParams cp{};
+  for (int l = 0; l < dims->n_layers; ++l) {
+    cp.k[l] = k_layers[l];
+    cp.v[l] = v_layers[l];
+  }
+  cp.modes = modes;
+  cp.seg_off = seg_offsets;
+  cp.cache = static_cast<uint8_t*>(cache);
+  cp.seq_len = seq_len;
+  cp.n_pairs = dims->n_layers / 2;
+  cp.hkv = dims->n_kv_heads;
+  cp.d = dims->head_dim;
+  cp.topk = dims->topk;
+  cp.bf16 = dims->dtype == FDKV_BF16;
+  hipError_t e = launch_compress_dense(cp, s);
+  if (e != hipSuccess) return hip_fail(e, "compress_dense");
+
+  SelectParams sp{};
+  for (int l = 0; l < dims->n_layers; ++l) {
+    sp.k[l] = k_layers[l];
+    sp.v[l] = v_layers[l];
+  }
+  sp.modes = modes;
+  sp.seg_off = seg_offsets;
+  sp.cache = static_cast<uint8_t*>(cache);
+  sp.seq_len = seq_len;
+  sp.n_pairs = cp.n_pairs;
+  sp.hkv = cp.hkv;
+  sp.d = cp.d;
+  sp.topk = cp.topk;
+  sp.bf16 = cp.bf16;
+  e = launch_residual_select(sp, 2, s);
+  if (e != hipSuccess) return hip_fail(e, "residual_select");
+  return FDKV_OK;
+}
+
+fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t max_seq_len, size_t* bytes) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (batch < 1 || max_seq_len < 0 || !bytes) return FDKV_E_INVALID_ARG;
+  const uint64_t G = dims->n_q_heads / dims->n_kv_heads;
+  const uint64_t n = std::max<uint64_t>(1, decode_chunks(max_seq_len));
+  *bytes = (size_t)((uint64_t)batch * dims->n_kv_heads * n * G * (dims->head_dim + 4) * 4);
+  return FDKV_OK;
+}
+
+fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, int32_t max_seq_len,
+                             const uint8_t* modes, const uint64_t* seg_offsets, const void* cache, int32_t layer,
+                             const void* q, void* out, float sm_scale, void* ws, size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (batch < 1 || max_seq_len < 0 || layer < 0 || layer >= dims->n_layers) return FDKV_E_INVALID_ARG;
+  if (!aligned(seq_lens, 4) || !modes || !aligned(seg_offsets, 8) || !aligned(cache, 256) || !aligned(q, 16) ||
+      !aligned(out, 16) || !aligned(ws, 16) || !isfinite(sm_scale))
+    return FDKV_E_INVALID_ARG;
+  size_t need = 0;
+  fdkv_decode_workspace(dims, batch, max_seq_len, &need);
+  if (ws_bytes < need) return FDKV_E_WORKSPACE;
+  DecodeParams p{};
+  p.cache = static_cast<const uint8_t*>(cache);
+  p.seg_off = seg_offsets;
+  p.modes = modes;
+  p.seq_lens = seq_lens;
+  p.q = q;
+  p.out = out;
+  p.ws = static_cast<float*>(ws);
+  p.layer = layer;
+  p.n_pairs = dims->n_layers / 2;
+  p.hkv = dims->n_kv_heads;
+  p.hq = dims->n_q_heads;
+  p.d = dims->head_dim;
+  p.topk = dims->topk;
+  p.n_wgchunks = (int)decode_chunks(max_seq_len);
+  p.batch = batch;
+  p.scale_log2 = sm_scale * 1.4426950408889634f;
+  p.bf16 = dims->dtype == FDKV_BF16;
+  const hipError_t e = launch_decode(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "decode");
+  return FDKV_OK;
+}
+
+}  // extern "C"

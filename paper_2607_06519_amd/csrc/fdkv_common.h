@@ -1,0 +1,103 @@
+// Shared definitions of the HIP path: element types, the segment layout of
+// the compressed cache (Eq. 3 storage), and wavefront helpers for gfx950.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define FDKV_HD __host__ __device__ __forceinline__
+
+namespace fdkv {
+
+constexpr int kPlaneAlign = 256;
+constexpr int kMaxLayers = 256;
+
+enum : int { kShared = 0, kResidual = 1, kExact = 2 };
+
+FDKV_HD float as_f32(uint32_t u) { return __builtin_bit_cast(float, u); }
+FDKV_HD uint32_t as_u32(float f) { return __builtin_bit_cast(uint32_t, f); }
+
+FDKV_HD uint64_t plane_bytes(uint64_t n) { return (n + kPlaneAlign - 1) / kPlaneAlign * kPlaneAlign; }
+
+// Byte offsets of the planes of one (sequence, pair, KV head) segment.
+// Shared:   MK, MV.  Residual: MK, MV, IK, VK, IV, VV.  Exact: K0, K1, V0, V1.
+struct SegLayout {
+  uint64_t mk, mv, ik, vk, iv, vv;  // shared / residual planes
+  uint64_t k0, k1, v0, v1;          // exact planes
+  uint64_t total;
+};
+
+FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e) {
+  SegLayout s{};
+  const uint64_t dense = plane_bytes(T * (uint64_t)d * e);
+  const uint64_t ip = plane_bytes(T * (uint64_t)k);
+  const uint64_t vp = plane_bytes(T * (uint64_t)k * e);
+  if (mode == kExact) {
+    s.k0 = 0;
+    s.k1 = dense;
+    s.v0 = 2 * dense;
+    s.v1 = 3 * dense;
+    s.total = 4 * dense;
+    return s;
+  }
+  s.mk = 0;
+  s.mv = dense;
+  s.total = 2 * dense;
+  if (mode == kResidual) {
+    s.ik = 2 * dense;
+    s.vk = s.ik + ip;
+    s.iv = s.vk + vp;
+    s.vv = s.iv + ip;
+    s.total = s.vv + vp;
+  }
+  return s;
+}
+
+// ---------------------------------------------------------------- bf16
+FDKV_HD float bf16_lo(uint32_t w) { return as_f32(w << 16); }
+FDKV_HD float bf16_hi(uint32_t w) { return as_f32(w & 0xFFFF0000u); }
+FDKV_HD float bf16_to_f32(uint16_t h) { return as_f32((uint32_t)h << 16); }
+
+// Round to nearest even; inputs are finite.
+FDKV_HD uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = as_u32(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+FDKV_HD uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ---------------------------------------------------------------- wavefront helpers
+// DPP lane permutations within rows of 16 lanes (gfx9 encodings).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;     // quad_perm [2,3,0,1]
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+
+// Sum over aligned groups of N lanes (N in 1,2,4,8,16); every lane gets its group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  if constexpr (N >= 2) x += dpp<kDppQuadXor1>(x);
+  if constexpr (N >= 4) x += dpp<kDppQuadXor2>(x);
+  if constexpr (N >= 8) x += dpp<kDppRowHalfMirror>(x);
+  if constexpr (N >= 16) x += dpp<kDppRowMirror>(x);
+  return x;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+}  // namespace fdkv

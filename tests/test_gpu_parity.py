@@ -1,0 +1,221 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars: residual channel indices, head modes and exact-mode planes bit-exact;
+stored M/D values within 1 ulp of the storage type (the oracle rounds its
+float64 DCT coefficients, the kernels round exact fp32 sums); attention
+outputs within relative L2 error 1e-5 (fp32) / 1e-2 (bf16) per (sequence,
+layer, query head); routing losses within 2e-4 relative (bf16 rounding of
+the half differences fed to the MFMA Gram, averaged over the tokens).
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synth import WORKLOADS, gen, scaled
+
+from gpu_cases import (compare_units, oracle_decode_layer, rel_l2, sharpened_queries, unpack_unit)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2607_06519_amd import binding
+    binding.load()          # a missing library must fail here, loudly
+    return torch
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _upload(w, K, V):
+    from paper_2607_06519_amd.cache import to_device
+    Kd = to_device(K, w.dtype)
+    Vd = to_device(V, w.dtype)
+    return Kd, Vd, [Kd[l] for l in range(w.n_layers)], [Vd[l] for l in range(w.n_layers)]
+
+
+def _run_compress(w, modes_b, Ks, Vs):
+    """GPU compress of every sequence; returns (cache, per-seq device layer lists)."""
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache
+    dm = B.dims(**w.dims())
+    cache = CompressedCache(dm, w.seq_lens, modes_b)
+    keep = []
+    for s in range(w.batch):
+        Kd, Vd, kl, vl = _upload(w, Ks[s], Vs[s])
+        keep.append((Kd, Vd))
+        cache.compress(s, kl, vl)
+    return cache, keep
+
+
+def _oracle_units(w, K, V, modes):
+    return {(b, h): O.compress_unit(K[2 * b:2 * b + 2, h], V[2 * b:2 * b + 2, h], int(modes[b, h]), w.topk, w.dtype)
+            for b in range(w.n_pairs) for h in range(w.n_kv_heads)}
+
+
+def _check_compress(w, cache, s, ref_units):
+    buf = cache.host_bytes()
+    T = w.seq_lens[s]
+    nz = {}
+    for (b, h), ref in ref_units.items():
+        got = unpack_unit(buf, int(cache.offsets_host[s, b, h]), int(cache.modes_host[s, b, h]), T,
+                          w.head_dim, w.topk, w.dtype)
+        st = compare_units(got, ref, w.dtype)
+        for k_, v_ in st.items():
+            nz[k_] = nz.get(k_, 0) + v_
+    return nz
+
+
+CASES = {
+    "tiny": WORKLOADS["tiny"],
+    "bf16_ragged": scaled(WORKLOADS["llama8b"], n_layers=4, seq_lens=(1000,), n_needles=6),
+    "bf16_d64_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=5,
+                          seq_lens=(333,), n_needles=3, needle_channels=5),
+    "f32_d128_k128": scaled(WORKLOADS["tiny"], head_dim=128, topk=128, n_q_heads=8, seq_lens=(200,),
+                            needle_channels=8, fixed_modes=(1, 1, 0, 2)),
+    "bf16_g8": scaled(WORKLOADS["long70b"], n_layers=2, n_kv_heads=2, n_q_heads=16, seq_lens=(777,), n_needles=4),
+    "bf16_k0": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=0, seq_lens=(300,),
+                      n_needles=2, fixed_modes=(1, 0)),
+}
+
+
+def _modes(w, s=0):
+    if w.fixed_modes is not None or w.mode_counts is not None:
+        return gen.fixed_modes(w, s)
+    raise ValueError
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_compress_and_decode_parity(torch_dev, name):
+    w = CASES[name]
+    log(f"[case] compress+decode {name} T={w.seq_lens} d={w.head_dim} k={w.topk} {w.dtype}")
+    K, V = gen.layer_cache(w, 0)
+    modes = _modes(w)
+    if name != "bf16_k0" and w.fixed_modes is None:
+        # make sure all three modes appear
+        modes = modes.copy()
+        modes.ravel()[:3] = [0, 1, 2]
+    cache, keep = _run_compress(w, modes[None], [K], [V])
+    torch_dev.cuda.synchronize()
+    ref = _oracle_units(w, K, V, modes)
+    nz = _check_compress(w, cache, 0, ref)
+    log(f"  compress ok; values 1 ulp apart: {nz}")
+    tol = 1e-5 if w.dtype == "f32" else 1e-2
+    worst = 0.0
+    from paper_2607_06519_amd.cache import to_device
+    for qi, qs in enumerate(sharpened_queries(w, 0, K)):
+        for layer in range(w.n_layers):
+            q = to_device(qs[layer], w.dtype)            # [batch=1][Hq][d]
+            out = cache.decode(layer, q).float().cpu().numpy()[0]
+            want = oracle_decode_layer(ref, modes, layer, qs[layer][0].astype(np.float64), w)
+            for hq in range(w.n_q_heads):
+                e = rel_l2(out[hq], want[hq])
+                worst = max(worst, e)
+                assert e <= tol, (name, qi, layer, hq, e)
+    log(f"  decode ok; worst rel-L2 {worst:.3e} (tol {tol})")
+
+
+def test_ragged_batch_decode(torch_dev):
+    base = scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=8, n_needles=2)
+    lens = (1, 100, 513, 1000, 0, 64)
+    w = scaled(base, seq_lens=lens)
+    log(f"[case] ragged batch {lens}")
+    Ks, Vs, ref_units, modes_b = [], [], [], []
+    for s, T in enumerate(lens):
+        ws_ = scaled(base, seq_lens=(max(T, 1),))
+        K, V = gen.layer_cache(ws_, 0)
+        K, V = K[:, :, :T], V[:, :, :T]
+        m = np.array([[s % 3, (s + 1) % 3]], np.uint8)
+        Ks.append(K)
+        Vs.append(V)
+        modes_b.append(m)
+        ref_units.append(_oracle_units(scaled(base, seq_lens=(T,)), K, V, m) if T > 0 else None)
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache, to_device
+    cache = CompressedCache(B.dims(**w.dims()), lens, np.stack(modes_b))
+    keep = []
+    for s, T in enumerate(lens):
+        if T == 0:
+            continue
+        Kd, Vd, kl, vl = _upload(scaled(base, seq_lens=(T,)), Ks[s], Vs[s])
+        keep.append((Kd, Vd))
+        cache.compress(s, kl, vl)
+    qs = gen.decode_queries(w, 1, scale=8.0)
+    for layer in range(2):
+        q = to_device(qs[layer], w.dtype)
+        out = cache.decode(layer, q).float().cpu().numpy()
+        for s, T in enumerate(lens):
+            if T == 0:
+                assert np.all(out[s] == 0.0)
+                continue
+            want = oracle_decode_layer(ref_units[s], modes_b[s], layer, qs[layer][s].astype(np.float64),
+                                       scaled(base, seq_lens=(T,)))
+            for hq in range(w.n_q_heads):
+                assert rel_l2(out[s, hq], want[hq]) <= 1e-2, (s, layer, hq)
+    log("  ragged ok")
+
+
+PROBE_CASES = {
+    "tiny": WORKLOADS["tiny"],
+    "bf16_small": scaled(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=4, n_q_heads=16, seq_lens=(1500,), n_probe=48),
+    "bf16_g1_d64": scaled(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=3, n_q_heads=3, head_dim=64, topk=7,
+                          seq_lens=(700,), n_probe=20, needle_channels=7),
+}
+
+
+@pytest.mark.parametrize("name", list(PROBE_CASES))
+def test_probe_parity(torch_dev, name):
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import probe, to_device
+    w = PROBE_CASES[name]
+    log(f"[case] probe {name}")
+    K, _ = gen.layer_cache(w, 0)
+    Q = gen.probe_queries(w, 0)
+    Kd = to_device(K, w.dtype)
+    Qd = to_device(Q, w.dtype)
+    dm = B.dims(**w.dims())
+    err, ws = probe(dm, w.seq_lens[0], [Kd[l] for l in range(w.n_layers)], [Qd[l] for l in range(w.n_layers)],
+                    w.n_probe)
+    got = err.cpu().numpy().astype(np.float64)
+    G = w.group
+    ref = np.zeros((w.n_pairs, w.n_kv_heads, 3))
+    for b in range(w.n_pairs):
+        for h in range(w.n_kv_heads):
+            ref[b, h] = O.routing_errors(K[2 * b:2 * b + 2, h], Q[2 * b:2 * b + 2, h * G:(h + 1) * G], w.topk)
+    relerr = np.abs(got - ref[..., :2]) / np.abs(ref[..., :2])
+    log(f"  max rel error of E: {relerr.max():.3e}")
+    assert relerr.max() <= 2e-4
+    # modes at several lambdas, ignoring near-ties of the oracle's costs
+    om = O.omega(w.head_dim, w.topk, w.dtype)
+    E3 = ref.reshape(-1, 3)
+    for lam in np.quantile(E3[:, 0], [0.2, 0.5, 0.8]) * 2.0:
+        gm, _, _ = B.route(dm, w.seq_lens[0], got.astype(np.float32), lam=float(lam))
+        om_modes = O.route(E3, om, float(lam))
+        cost = E3 + lam * om
+        srt = np.sort(cost, axis=1)
+        margin = (srt[:, 1] - srt[:, 0]) / np.maximum(srt[:, 0], 1e-30)
+        ok = margin >= 1e-3
+        np.testing.assert_array_equal(gm.ravel()[ok], om_modes[ok])
+
+
+def test_probe_deterministic(torch_dev):
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import probe, to_device
+    w = PROBE_CASES["bf16_small"]
+    K, _ = gen.layer_cache(w, 0)
+    Q = gen.probe_queries(w, 0)
+    Kd, Qd = to_device(K, w.dtype), to_device(Q, w.dtype)
+    dm = B.dims(**w.dims())
+    kl, ql = [Kd[l] for l in range(w.n_layers)], [Qd[l] for l in range(w.n_layers)]
+    a, _ = probe(dm, w.seq_lens[0], kl, ql, w.n_probe)
+    b, _ = probe(dm, w.seq_lens[0], kl, ql, w.n_probe)
+    assert torch_dev.equal(a, b)
