@@ -28,9 +28,11 @@ Readings of the paper adopted here (the paper leaves these open):
 * the residual keeps, for every token, the ``k`` channels of largest
   ``|x[2b] - x[2b+1]|`` (computed in float32 on the stored inputs; ties go to
   the lower channel; indices stored ascending), K and V chosen independently;
-* what is stored is the per-layer image of each coefficient:
-  ``M = F[0,0] * Z0`` (the pair mean) and ``D = F[1,0] * Z1`` (half the
-  difference), so layer 2b reconstructs ``M + D`` and layer 2b+1 ``M - D``;
+* what is stored is the per-layer image of each coefficient, ``P_k X`` with
+  the projector ``P_k = F[k]^T F[k]``: ``M`` (the pair mean) for k = 0 and
+  ``D`` (half the difference) for k = 1, so layer 2b reconstructs ``M + D``
+  and layer 2b+1 ``M - D``; the projector entries are evaluated in 50-digit
+  decimal arithmetic so that stored values are correctly rounded;
 * the routing loss of a (pair, KV head) averages Eq. (2) over both layers of
   the pair and over the query heads of the KV head's group, uses the
   unrounded coefficients (storage rounding is not part of the method), and
@@ -47,6 +49,7 @@ value printed in the paper can be reproduced (it gives no worked example).
 """
 from __future__ import annotations
 
+import functools
 import math
 from typing import Dict, Tuple
 
@@ -101,6 +104,85 @@ def dct_matrix(B: int) -> np.ndarray:
             F[k, n] = s * math.cos(math.pi * (2 * n + 1) * k / (2 * B))
             F[k, B - 1 - n] = F[k, n] if k % 2 == 0 else -F[k, n]
     return F
+
+
+def _dec_pi(prec: int):
+    """pi to ``prec`` decimal digits (Machin's formula)."""
+    import decimal
+    with decimal.localcontext() as ctx:
+        ctx.prec = prec + 10
+
+        def arctan_inv(x):
+            x = decimal.Decimal(x)
+            total, term, n, sign = decimal.Decimal(0), 1 / x, 1, 1
+            x2 = x * x
+            while term > decimal.Decimal(10) ** -(prec + 5):
+                total += sign * term / n
+                term /= x2
+                n += 2
+                sign = -sign
+            return total
+
+        return +(16 * arctan_inv(5) - 4 * arctan_inv(239))
+
+
+def _dec_cos(x, prec: int):
+    """cos of a Decimal by its Taylor series (|x| small after reduction)."""
+    import decimal
+    with decimal.localcontext() as ctx:
+        ctx.prec = prec + 10
+        pi = _dec_pi(prec)
+        x = x % (2 * pi)
+        total, term, n = decimal.Decimal(1), decimal.Decimal(1), 0
+        while abs(term) > decimal.Decimal(10) ** -(prec + 5):
+            n += 2
+            term = -term * x * x / (n * (n - 1))
+            total += term
+        return +total
+
+
+@functools.lru_cache(maxsize=None)
+def _dct_projectors_cached(B: int) -> np.ndarray:
+    return _dct_projectors_exact(B)
+
+
+def dct_projectors(B: int) -> np.ndarray:
+    """Per-layer images of each DCT coefficient (see ``_dct_projectors_exact``)."""
+    return _dct_projectors_cached(B).copy()
+
+
+def _dct_projectors_exact(B: int) -> np.ndarray:
+    """Per-layer images of each DCT coefficient: ``P[k, l, n] = F[k, l] F[k, n]``.
+
+    ``P_k X`` is the part of the block ``X`` carried by frequency ``k`` (Eq. 1:
+    ``X = F^T Z = sum_k F[k]^T F[k] X``).  The products are evaluated in
+    50-digit decimal arithmetic and rounded once to float64, so for B = 2 they
+    are exactly +-1/2 and the stored images come out correctly rounded.
+    """
+    import decimal
+    prec = 50
+    with decimal.localcontext() as ctx:
+        ctx.prec = prec + 10
+        pi = _dec_pi(prec)
+        P = np.empty((B, B, B), dtype=np.float64)
+        for k in range(B):
+            s2 = decimal.Decimal(1 if k == 0 else 2) / B
+            for l in range(B):
+                cl = _dec_cos(pi * (2 * l + 1) * k / (2 * B), prec)
+                for n in range(B):
+                    cn = _dec_cos(pi * (2 * n + 1) * k / (2 * B), prec)
+                    P[k, l, n] = float(s2 * cl * cn)
+    return P
+
+
+def coefficient_image(X, k: int, layer: int) -> np.ndarray:
+    """Layer ``layer``'s share of DCT coefficient ``k`` of the block ``X``: ``sum_n P[k,l,n] x_n``."""
+    X = np.asarray(X, dtype=np.float64)
+    P = dct_projectors(X.shape[0])
+    out = np.zeros_like(X[0])
+    for n in range(X.shape[0]):
+        out += P[k, layer, n] * X[n]
+    return out
 
 
 def depth_factorize(X) -> np.ndarray:
@@ -161,7 +243,6 @@ def compress_unit(K2, V2, mode: int, k: int, dtype: str) -> Dict[str, np.ndarray
     ``K0, K1, V0, V1`` (the inputs) for exact heads.  Values are rounded to
     the storage precision.
     """
-    F = dct_matrix(2)
     out: Dict[str, np.ndarray] = {}
     if mode == EXACT:
         for name, X in (("K", K2), ("V", V2)):
@@ -171,11 +252,10 @@ def compress_unit(K2, V2, mode: int, k: int, dtype: str) -> Dict[str, np.ndarray
         return out
     for name, X in (("K", K2), ("V", V2)):
         X = np.asarray(X, dtype=np.float64)
-        Z = depth_factorize(X)
-        out["M" + name] = round_to_storage(F[0, 0] * Z[0], dtype)
+        out["M" + name] = round_to_storage(coefficient_image(X, 0, 0), dtype)
         if mode == RESIDUAL:
             idx = residual_channels(X[0], X[1], k)
-            D = F[1, 0] * Z[1]
+            D = coefficient_image(X, 1, 0)
             out["I" + name] = idx
             out["V" + name] = round_to_storage(np.take_along_axis(D, idx, axis=-1), dtype)
     return out

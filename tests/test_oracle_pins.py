@@ -52,6 +52,27 @@ def test_factorize_matches_scipy_dct(B):
     np.testing.assert_allclose(O.depth_factorize(X), ref, atol=1e-13)
 
 
+@pytest.mark.parametrize("B", [2, 4, 8])
+def test_projectors_resolve_identity(B):
+    P = O.dct_projectors(B)
+    F = O.dct_matrix(B)
+    for k in range(B):
+        np.testing.assert_allclose(P[k], np.outer(F[k], F[k]), atol=1e-15)
+    np.testing.assert_allclose(P.sum(0), np.eye(B), atol=1e-15)
+
+
+def test_b2_projectors_exact_and_images_correctly_rounded():
+    P = O.dct_projectors(2)
+    np.testing.assert_array_equal(P, [[[0.5, 0.5], [0.5, 0.5]], [[0.5, -0.5], [-0.5, 0.5]]])
+    # bf16 inputs whose mean sits exactly halfway between two bf16 values
+    a = np.array([1.0, 1.0078125, -3.0, 2.0 ** -20])
+    b = np.array([1.0078125, 1.0234375, -3.015625, 2.0 ** -20])
+    X = np.stack([a, b])[:, None, :]
+    unit = O.compress_unit(X, X, O.RESIDUAL, 4, "bf16")
+    np.testing.assert_array_equal(unit["MK"][0], O.round_bf16((a + b) / 2))
+    np.testing.assert_array_equal(np.sort(unit["VK"][0]), np.sort(O.round_bf16((a - b) / 2)))
+
+
 def test_round_trip():
     rng = np.random.default_rng(2)
     X = rng.standard_normal((2, 33, 16))
