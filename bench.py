@@ -1,0 +1,338 @@
+#!/usr/bin/env python3
+"""Benchmark of the compressed-KV decode path on one MI355X.
+
+A step is one decode token through every layer of the workload (default:
+the Llama-3-8B-shaped cache, 32 layers, 32 query heads on 8 KV heads,
+d = 128, 32768 cached tokens, bf16, top-16 residuals, seeded 64/45/19
+shared/residual/exact head mix).  Inputs are resident in HBM before timing.
+Layers run in cold order (all even layers, then all odd ones) so the shared
+planes of a pair are evicted from the 256 MB Infinity Cache before the pair's
+second layer re-reads them; the headline bandwidth is therefore HBM
+bandwidth.  The step is captured once in a HIP graph and replayed.
+
+Printed: one JSON line with the metric, a roofline object for the decode
+launch (split-K + combine per layer, timed with HIP events on the launch
+stream), the prefill path (probe, route, compress) timed on the same cache,
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--order", choices=["cold", "model"], default="cold")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--threads", type=int, default=16)
+    return ap.parse_args()
+
+
+def bytes_per_token(mode, d, k, e):
+    return 2 * d * e if mode != 1 else 2 * d * e + 2 * k * (1 + e)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in ("decode.hip", "fdkv_common.h", "fdkv_kernels.h"):
+        with open(os.path.join(ROOT, "paper_2607_06519_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"decode_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the compressed-KV path here has no multi-GPU leg "
+              f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache, probe, torch_dtype
+    from synth import WORKLOADS, gen
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    B.load()
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    L, H, Hq, d, k = w.n_layers, w.n_kv_heads, w.n_q_heads, w.head_dim, w.topk
+    e = w.elem_bytes
+    tdt = torch_dtype(w.dtype)
+    dm = B.dims(**w.dims())
+
+    # ------------------------------------------------------------ inputs in HBM
+    t0 = time.time()
+    Ks, Vs = [], []
+    for s in range(w.batch):
+        T = w.seq_lens[s]
+        Kd = torch.empty((L, H, T, d), dtype=tdt, device=dev)
+        Vd = torch.empty((L, H, T, d), dtype=tdt, device=dev)
+        for b, h, kk, vv in gen.iter_segments(w, s, threads=args.threads):
+            Kd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(kk).to(dev).to(tdt))
+            Vd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(vv).to(dev).to(tdt))
+        Ks.append(Kd)
+        Vs.append(Vd)
+    torch.cuda.synchronize()
+    log(f"[bench] generated {w.name} K/V in {time.time() - t0:.1f}s")
+
+    modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
+    cache = CompressedCache(dm, w.seq_lens, modes)
+    for s in range(w.batch):
+        cache.compress(s, [Ks[s][l] for l in range(L)], [Vs[s][l] for l in range(L)])
+    torch.cuda.synchronize()
+    log(f"[bench] compressed cache: {cache.total_bytes / 1e9:.3f} GB, mix {np.bincount(modes.ravel(), minlength=3).tolist()}")
+
+    # algorithmic bytes per layer launch: sum over (seq, KV head) of T * bytes per token of the head's mode
+    bytes_layer = []
+    for layer in range(L):
+        b = layer // 2
+        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e)
+                               for s in range(w.batch) for h in range(H)))
+    bytes_step = sum(bytes_layer)
+
+    order = list(range(0, L, 2)) + list(range(1, L, 2)) if args.order == "cold" else list(range(L))
+    n_q = args.steps + args.warmup
+    qs = torch.empty((n_q, L, w.batch, Hq, d), dtype=tdt, device=dev)
+    for i in range(n_q):
+        qs[i].copy_(torch.from_numpy(gen.decode_queries(w, i % w.steps)).to(dev).to(tdt))
+    q_static = torch.empty((L, w.batch, Hq, d), dtype=tdt, device=dev)
+    out_static = torch.empty((L, w.batch, Hq, d), dtype=tdt, device=dev)
+    scale = 1.0 / math.sqrt(d)
+
+    def step(q, out):
+        for layer in order:
+            cache.decode(layer, q[layer], out[layer], scale)
+
+    # ------------------------------------------------------------ decode steps
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    graph = None
+    with torch.cuda.stream(stream):
+        q_static.copy_(qs[0])
+        step(q_static, out_static)
+        if not args.no_graph:
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                step(q_static, out_static)
+        torch.cuda.synchronize()
+
+        def run(i):
+            q_static.copy_(qs[i])
+            if graph is not None:
+                graph.replay()
+            else:
+                step(q_static, out_static)
+
+        for i in range(args.warmup):
+            run(i)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for i in range(args.steps):
+            run(args.warmup + i)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        step_ms = ev0.elapsed_time(ev1) / args.steps
+
+        # per-launch timing of the layer call, HIP events on the launch stream
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in order]
+        n_rep = max(3, min(args.steps, 20))
+        launch_ms = np.zeros(L)
+        for rep in range(n_rep):
+            q_static.copy_(qs[args.warmup + rep % args.steps])
+            for j, layer in enumerate(order):
+                evs[j][0].record(stream)
+                cache.decode(layer, q_static[layer], out_static[layer], scale)
+                evs[j][1].record(stream)
+            torch.cuda.synchronize()
+            for j, layer in enumerate(order):
+                launch_ms[layer] += evs[j][0].elapsed_time(evs[j][1]) / n_rep
+    launch_avg_ms = float(launch_ms.mean())
+    achieved = (bytes_step / L) / (launch_avg_ms * 1e-3) / 1e9
+    step_gbs = bytes_step / (step_ms * 1e-3) / 1e9
+    tokens_per_s = w.batch / (step_ms * 1e-3)
+    log(f"[bench] decode step {step_ms * 1e3:.1f} us -> {tokens_per_s:.1f} tok/s, {step_gbs:.0f} GB/s over the step; "
+        f"layer launch {launch_avg_ms * 1e3:.2f} us -> {achieved:.0f} GB/s")
+
+    # ------------------------------------------------------------ prefill: probe + route + compress
+    prefill = None
+    if not args.no_prefill and w.batch == 1 and w.n_probe > 0:
+        P = w.n_probe
+        T = w.seq_lens[0]
+        Qp = torch.empty((L, Hq, P, d), dtype=tdt, device=dev)
+        for l in range(L):
+            Qp[l].copy_(torch.from_numpy(gen.probe_queries(w, 0, layers=[l])[0]).to(dev).to(tdt))
+        kl = [Ks[0][l] for l in range(L)]
+        vl = [Vs[0][l] for l in range(L)]
+        ql = [Qp[l] for l in range(L)]
+        _, budget = B.layout(dm, [T], gen.fixed_modes(w, 0)[None])   # footprint of the 50/35/15 mix
+        ws = torch.empty(B.probe_workspace(dm, T, P), dtype=torch.uint8, device=dev)
+        err = torch.empty((L // 2, H, 2), dtype=torch.float32, device=dev)
+        _, all_exact = B.layout(dm, [T], np.full((1, L // 2, H), 2, np.uint8))
+        pcache_buf = torch.empty(all_exact, dtype=torch.uint8, device=dev)
+        offs_dev = torch.empty((L // 2, H), dtype=torch.int64, device=dev)
+        modes_dev = torch.empty((L // 2, H), dtype=torch.uint8, device=dev)
+        times = {"probe": [], "route": [], "compress": [], "total": []}
+        pmodes = None
+        for rep in range(4):
+            torch.cuda.synchronize()
+            a0, a1, c0, c1 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
+            tw0 = time.perf_counter()
+            a0.record()
+            B.probe(dm, T, kl, ql, P, err, ws)
+            a1.record()
+            eh = err.cpu().numpy()                      # sync point
+            tr0 = time.perf_counter()
+            pmodes, lam, st = B.route(dm, T, eh, budget_bytes=budget, allow_infeasible=True)
+            offs, total = B.layout(dm, [T], pmodes[None])
+            tr1 = time.perf_counter()
+            modes_dev.copy_(torch.from_numpy(pmodes))
+            offs_dev.copy_(torch.from_numpy(offs[0].astype(np.int64)))
+            c0.record()
+            B.compress(dm, T, kl, vl, modes_dev, offs_dev, pcache_buf)
+            c1.record()
+            torch.cuda.synchronize()
+            tw1 = time.perf_counter()
+            if rep == 0:
+                continue                                 # first pass warms up
+            times["probe"].append(a0.elapsed_time(a1) * 1e-3)
+            times["route"].append(tr1 - tr0)
+            times["compress"].append(c0.elapsed_time(c1) * 1e-3)
+            times["total"].append(tw1 - tw0)
+        tp, trt, tc, tt = (float(np.mean(times[x])) for x in ("probe", "route", "compress", "total"))
+        units = L // 2 * H
+        cmp_read = units * T * 4 * d * e
+        cmp_write = sum(T * (2 * d * e if m == 0 else (4 * d * e if m == 2 else 2 * d * e + 2 * k * (1 + e)))
+                        for m in pmodes.ravel())
+        mfma_flops = units * T * (d // 32) * (d // 32 + 1) // 2 * 2 * (32 * 32 * 2)   # upper tiles, 2 matrices
+        G = Hq // H
+        eq2_flops = units * 2 * G * P * 2 * T * d * 2 * 2                            # literal Eq. 2, 2 modes
+        prefill = {
+            "workload": "prefill8b" if w.name == "llama8b" else w.name,
+            "probe_ms": tp * 1e3, "route_ms": trt * 1e3, "compress_ms": tc * 1e3,
+            "wall_ms": tt * 1e3,
+            "compressed_tokens_per_s": T / tt,
+            "compress_gbs": (cmp_read + cmp_write) / tc / 1e9,
+            "compress_frac_hbm": (cmp_read + cmp_write) / tc / 1e9 / HBM_PEAK_GBS,
+            "probe_read_gbs": units * T * 2 * d * e / tp / 1e9,
+            "probe_mfma_util": mfma_flops / tp / (MFMA_BF16_PEAK_TFLOPS * 1e12),
+            "probe_eq2_equiv_tflops": eq2_flops / tp / 1e12,
+            "probe_mode_mix": np.bincount(pmodes.ravel(), minlength=3).tolist(),
+            "budget_bytes": int(budget), "lambda": lam,
+        }
+        log(f"[bench] prefill: probe {tp * 1e3:.2f} ms, route {trt * 1e3:.2f} ms, compress {tc * 1e3:.2f} ms "
+            f"({prefill['compress_gbs']:.0f} GB/s), mix {prefill['probe_mode_mix']}")
+        del Qp, ws, pcache_buf
+
+    # ------------------------------------------------------------ CPU oracle baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, modes[0])
+
+    traffic = load_traffic(w.name)
+    cfg = {"workload": w.name, "n_layers": L, "n_kv_heads": H, "n_q_heads": Hq, "head_dim": d, "topk": k,
+           "batch": w.batch, "seq_len": w.max_seq_len, "mode_mix": np.bincount(modes.ravel(), minlength=3).tolist(),
+           "layer_order": args.order, "graph": graph is not None, "cache_gb": cache.total_bytes / 1e9,
+           "bytes_per_step": bytes_step}
+    res = {
+        "metric": "compressed-KV decode attn tokens/s + achieved HBM GB/s vs 8 TB/s, 32k ctx",
+        "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic (seeded generator, correlated layer pairs with needles)",
+        "config": cfg,
+        "step_hbm_gbs": step_gbs,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "decode layer launch (decode_splitk_kernel + decode_combine_kernel)",
+                     "bytes_per_launch": bytes_step / L, "launch_us": launch_avg_ms * 1e3},
+        "cpu_baseline": cpu,
+        "prefill": prefill,
+    }
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(w, modes):
+    """The oracle's decode on a bounded sample: a few (pair, KV head) units, both layers, a few steps."""
+    import numpy as np
+
+    import oracle as O
+    from synth import gen
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    cores = len(os.sched_getaffinity(0))
+    rng = np.random.default_rng(0)
+    d, G = w.head_dim, w.group
+    flat = [(b, h) for b in range(w.n_pairs) for h in range(w.n_kv_heads)]
+    pick = []
+    for m in (0, 1, 2):
+        cand = [u for u in flat if modes[u] == m]
+        pick += [cand[i] for i in rng.choice(len(cand), size=min(2, len(cand)), replace=False)]
+    n_steps = 3
+    elapsed, n_calls = 0.0, 0
+    for (b, h) in pick:
+        K, V, _ = gen.segment(w, 0, b, h)
+        unit = O.compress_unit(K, V, int(modes[b, h]), w.topk, w.dtype)
+        for s in range(n_steps):
+            q = gen.decode_queries(w, s)
+            for layer in (2 * b, 2 * b + 1):
+                qq = q[layer][0, h * G:(h + 1) * G].astype(np.float64)
+                t0 = time.perf_counter()
+                O.decode_unit(unit, int(modes[b, h]), layer, qq, 1.0 / math.sqrt(d), d)
+                elapsed += time.perf_counter() - t0
+                n_calls += 1
+    per_unit_layer = elapsed / n_calls
+    step_s = per_unit_layer * w.n_layers * w.n_kv_heads
+    return {"value": w.batch / step_s, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "blas_threads": blas_threads,
+            "sample": f"oracle decode (reconstruct + fp64 softmax attention) of {len(pick)} (pair, KV head) units "
+                      f"x 2 layers x {n_steps} steps = {n_calls} unit-layers ({elapsed:.1f}s), scaled to "
+                      f"{w.n_layers * w.n_kv_heads} unit-layers per step"}
+
+
+if __name__ == "__main__":
+    main()

@@ -10,8 +10,9 @@
 //   exact    : K~ = K_l,                    V~ = V_l
 // Logits use the algebraic form q.K~ = q.MK + sigma * sum_j q[IK_j] D_K,j.
 //
-// decode_splitk: one workgroup = 4 waves = 512 tokens of one (sequence, KV
-// head); each wave takes 128 tokens in two passes over HBM-resident planes:
+// decode_splitk (the fp32 cache path; bf16 caches use decode_stream.hip): one
+// workgroup = 4 waves = 512 tokens of one (sequence, KV head); each wave
+// takes 128 tokens in two passes over HBM-resident planes:
 //   K pass - 4 (G <= 4) or 8 lanes per row read 16-byte pieces; bf16 dot2
 //            against the query pieces held in registers, group reduction by
 //            DPP; logits (log2 domain) to LDS.
@@ -20,8 +21,8 @@
 //            V residual goes into an LDS accumulator with ds_add_f32.
 // The chunk max is exact (two passes), so no rescaling is needed inside a
 // wave; the 4 waves merge in LDS and the workgroup writes one (acc, m, l)
-// record.  decode_combine merges the records of a sequence with the
-// log-sum-exp rule.  Bandwidth bound: no MFMA.
+// record.  decode_merge (decode_stream.hip) merges the records of a
+// sequence with the log-sum-exp rule.
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 
@@ -292,41 +293,15 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
 }
 
 template <int D, bool BF16, int G>
-__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams P) {
-  using S = DecodeShape<D, BF16, G>;
-  const int seq = blockIdx.x / P.hq, qh = blockIdx.x % P.hq;
-  const int head = qh / G, g = qh % G;
-  const int T = P.seq_lens[seq];
-  const int nch = min((T + kDecodeWgTokens - 1) / kDecodeWgTokens, P.n_wgchunks);
-  const int c = threadIdx.x;
-  const float* rec = P.ws + ((uint64_t)(seq * P.hkv + head) * P.n_wgchunks) * G * S::RS + g * S::RS;
-  float M = -INFINITY;
-  for (int i = 0; i < nch; ++i) M = fmaxf(M, rec[(uint64_t)i * G * S::RS + D]);
-  float l = 0.f, o = 0.f;
-  for (int i = 0; i < nch; ++i) {
-    const float* r = rec + (uint64_t)i * G * S::RS;
-    const float f = exp2f(r[D] - M);
-    l = fmaf(f, r[D + 1], l);
-    o = fmaf(f, r[c], o);
-  }
-  const float res = nch > 0 ? o / l : 0.f;
-  const uint64_t oi = ((uint64_t)seq * P.hq + qh) * D + c;
-  if constexpr (BF16)
-    reinterpret_cast<uint16_t*>(P.out)[oi] = (uint16_t)f32_to_bf16_bits(res);
-  else
-    reinterpret_cast<float*>(P.out)[oi] = res;
-}
-
-template <int D, bool BF16, int G>
 static hipError_t launch_decode_t(const DecodeParams& P, hipStream_t s) {
+  static_assert(!BF16, "bf16 caches use decode_stream_kernel");
   const dim3 grid((unsigned)P.batch * P.hkv * P.n_wgchunks);
   if (grid.x > 0) {
     hipLaunchKernelGGL((decode_splitk_kernel<D, BF16, G>), grid, dim3(256), 0, s, P);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((decode_combine_kernel<D, BF16, G>), dim3((unsigned)P.batch * P.hq), dim3(D), 0, s, P);
-  return hipGetLastError();
+  return launch_decode_merge(P, s);
 }
 
 template <int D, bool BF16>
@@ -340,8 +315,12 @@ static hipError_t launch_decode_d(const DecodeParams& P, hipStream_t s) {
 }
 
 hipError_t launch_decode(const DecodeParams& P, hipStream_t s) {
-  if (P.d == 128) return P.bf16 ? launch_decode_d<128, true>(P, s) : launch_decode_d<128, false>(P, s);
-  return P.bf16 ? launch_decode_d<64, true>(P, s) : launch_decode_d<64, false>(P, s);
+  if (P.bf16) {
+    const hipError_t e = launch_decode_stream(P, s);
+    if (e != hipSuccess) return e;
+    return launch_decode_merge(P, s);
+  }
+  return P.d == 128 ? launch_decode_d<128, false>(P, s) : launch_decode_d<64, false>(P, s);
 }
 
 }  // namespace fdkv

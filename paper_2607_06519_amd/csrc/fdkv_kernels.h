@@ -66,6 +66,8 @@ struct ProbeParams {
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s);
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s);
 hipError_t launch_decode(const DecodeParams& P, hipStream_t s);
+hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K part
+hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
 hipError_t launch_probe(const ProbeParams& P, hipStream_t s);
 
 }  // namespace fdkv
