@@ -48,6 +48,16 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--threads", type=int, default=16)
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="before timing, copy this many MiB device-to-device once (a copy kernel of known "
+                         "size that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
+    ap.add_argument("--summarize-trace", metavar="CSV",
+                    help="print a per-kernel summary of a rocprofv3 kernel-trace CSV and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print HBM bytes per dispatch from rocprofv3 FETCH_SIZE and WRITE_SIZE counter CSVs, "
+                         "scaled by the calibration copy, and exit")
+    ap.add_argument("--traffic-json", metavar="PATH", help="with --summarize-pmc: also write the decode "
+                    "traffic record that the bench line reads")
     return ap.parse_args()
 
 
@@ -57,7 +67,7 @@ def bytes_per_token(mode, d, k, e):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for name in ("decode.hip", "fdkv_common.h", "fdkv_kernels.h"):
+    for name in ("decode.hip", "decode_stream.hip", "fdkv_common.h", "fdkv_kernels.h"):
         with open(os.path.join(ROOT, "paper_2607_06519_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -78,8 +88,70 @@ def load_traffic(workload):
     return t.get("bytes_per_launch")
 
 
+def summarize_trace(path):
+    """Per-kernel count / mean / total duration from a rocprofv3 kernel-trace CSV."""
+    import csv
+    from collections import defaultdict
+    dur = defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            dur[r["Kernel_Name"]].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    rows = sorted(dur.items(), key=lambda kv: -sum(kv[1]))
+    print(f"{'calls':>7} {'mean_us':>10} {'min_us':>9} {'max_us':>9} {'total_ms':>10}  kernel")
+    for name, v in rows:
+        print(f"{len(v):7d} {sum(v) / len(v):10.2f} {min(v):9.2f} {max(v):9.2f} {sum(v) * 1e-3:10.3f}  {name[:110]}")
+
+
+def summarize_pmc(fetch_csv, write_csv, traffic_json=None, workload="llama8b"):
+    """Mean FETCH_SIZE / WRITE_SIZE per dispatch and kernel, scaled by the calibration copy."""
+    import csv
+    from collections import defaultdict
+
+    def read(path, counter):
+        out = defaultdict(list)
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter:
+                    out[r["Kernel_Name"]].append((float(r["Counter_Value"]) * 1024.0, int(r["Grid_Size"])))
+        return out
+
+    fetch, write = read(fetch_csv, "FETCH_SIZE"), read(write_csv, "WRITE_SIZE")
+    # the calibration copy: the largest torch copy kernel dispatch (reads and writes N bytes each)
+    cal_name = max((k for k in fetch if "copy" in k.lower() or "elementwise" in k.lower()),
+                   key=lambda k: max(v for v, _ in fetch[k]), default=None)
+    cal_f = max(v for v, _ in fetch[cal_name]) if cal_name else None
+    cal_w = max(v for v, _ in write.get(cal_name, [(0.0, 0)])) if cal_name else None
+    print(f"calibration kernel: {cal_name[:80] if cal_name else None}")
+    print(f"  FETCH_SIZE {cal_f:.4g} B, WRITE_SIZE {cal_w:.4g} B per dispatch")
+    print(f"{'calls':>6} {'fetch_MB':>10} {'write_MB':>10}  kernel  (raw counter bytes per dispatch)")
+    for name in sorted(fetch, key=lambda k: -sum(v for v, _ in fetch[k])):
+        fv = [v for v, _ in fetch[name]]
+        wv = [v for v, _ in write.get(name, [])] or [0.0]
+        print(f"{len(fv):6d} {sum(fv) / len(fv) / 1e6:10.3f} {sum(wv) / len(wv) / 1e6:10.3f}  {name[:100]}")
+    return cal_name, cal_f, cal_w, fetch, write
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        cal_name, cal_f, cal_w, fetch, write = summarize_pmc(*args.summarize_pmc)
+        if args.traffic_json and args.calibrate_copy_mib > 0 and cal_f:
+            n = args.calibrate_copy_mib << 20
+            fs, ws_ = n / cal_f, n / cal_w
+            dec = [k for k in fetch if "decode" in k]
+            fb = sum(sum(v for v, _ in fetch[k]) / len(fetch[k]) for k in dec) * fs
+            wb = sum(sum(v for v, _ in write[k]) / len(write[k]) for k in dec if k in write) * ws_
+            rec = {"source_hash": kernel_source_hash(), "bytes_per_launch": fb + wb, "fetch_bytes": fb,
+                   "write_bytes": wb, "kernels": dec, "fetch_scale": fs, "write_scale": ws_,
+                   "calibration_bytes": n}
+            with open(args.traffic_json, "w") as f:
+                json.dump(rec, f, indent=1)
+            print(f"decode launch traffic: fetch {fb / 1e6:.2f} MB + write {wb / 1e6:.2f} MB per layer call "
+                  f"(scales {fs:.4f}, {ws_:.4f})")
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the compressed-KV path here has no multi-GPU leg "
               f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
@@ -115,6 +187,17 @@ def main():
         Vs.append(Vd)
     torch.cuda.synchronize()
     log(f"[bench] generated {w.name} K/V in {time.time() - t0:.1f}s")
+
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {n} bytes")
+        del src, dst
 
     modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
     cache = CompressedCache(dm, w.seq_lens, modes)
@@ -285,7 +368,7 @@ def main():
         "step_hbm_gbs": step_gbs,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "decode layer launch (decode_splitk_kernel + decode_combine_kernel)",
+                     "kernel": "decode layer launch (decode_stream_kernel + decode_merge_kernel)",
                      "bytes_per_launch": bytes_step / L, "launch_us": launch_avg_ms * 1e3},
         "cpu_baseline": cpu,
         "prefill": prefill,

@@ -15,8 +15,9 @@
 //  K  - bf16 dot2 of the lane's piece with the matching query piece, group
 //       sum over the NP lanes of the row by DPP; residual heads add
 //       sigma * q[IK_j] * D_K,j for the lane's residual entry.
-//  softmax - tile max over the wave, running max/sum, rescale by
-//       exp2(m_old - m_new); probabilities to LDS (fp32 and bf16 pairs).
+//  softmax - against a running reference max that moves (wave max, rescale
+//       by exp2(m_old - m_new)) only when a logit exceeds it by more than
+//       2^8; probabilities to LDS (fp32 and bf16 pairs).
 //  V  - rows r and r + RPV are paired so one dot2 multiplies two tokens'
 //       values by their two bf16 probabilities; residual V entries are added
 //       into LDS accumulators (one copy per row slot r % 4, so the lanes of a
@@ -32,6 +33,7 @@ namespace {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 constexpr int kRsrcDword3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
+constexpr float kSlack = 8.f;            // log2 headroom of the running reference max
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
@@ -224,7 +226,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         s[ks_][g] = row < T ? x : -INFINITY;
       }
     }
-    // online softmax over the tile (m, alpha are uniform over the wave)
+    // online softmax over the tile.  m is a reference value, uniform over the
+    // wave, that only moves when some logit exceeds it by more than kSlack
+    // (probabilities then stay below 2^kSlack); moving it takes a wave max
+    // and rescales the running sums.
     bool rescale = false;
     float alpha[G];
 #pragma unroll
@@ -232,11 +237,15 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       float mt = s[0][g];
 #pragma unroll
       for (int ks_ = 1; ks_ < NKS; ++ks_) mt = fmaxf(mt, s[ks_][g]);
+      float mn = m[g];
+      alpha[g] = 1.f;
+      if (__ballot(mt > m[g] + kSlack) != 0) {
 #pragma unroll
-      for (int o = LPRK; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
-      const float mn = fmaxf(m[g], mt);
-      alpha[g] = (mn == m[g]) ? 1.f : __builtin_amdgcn_exp2f(m[g] - mn);
-      rescale |= (mn != m[g]);
+        for (int o = LPRK; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
+        mn = fmaxf(m[g], mt);
+        alpha[g] = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
+        rescale = true;
+      }
       float ps = 0.f;
 #pragma unroll
       for (int ks_ = 0; ks_ < NKS; ++ks_) {
