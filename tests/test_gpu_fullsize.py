@@ -1,0 +1,140 @@
+"""Parity at the workloads' full per-layer sizes, on sampled units.
+
+A decode launch depends on (T, KV heads, query heads, d, k, batch), not on
+the number of layers, so one layer pair at the full context length runs the
+exact launch configuration the benchmark times.  The GPU path runs on every
+head; the oracle recomputes a sample of (sequence, pair, KV head) units one
+by one: their stored planes (bit-exact indices, values within 1 ulp) and the
+attention outputs of their query heads in both layers of the pair.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synth import WORKLOADS, gen, scaled
+
+from gpu_cases import compare_units, rel_l2, unpack_unit
+
+pytestmark = pytest.mark.gpu
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2607_06519_amd import binding
+    binding.load()
+    return torch
+
+
+def _build_cache(torch, w, modes_b):
+    """Generate every segment of every sequence on the device and compress it."""
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache, torch_dtype
+    tdt = torch_dtype(w.dtype)
+    cache = CompressedCache(B.dims(**w.dims()), w.seq_lens, modes_b)
+    for s in range(w.batch):
+        T = w.seq_lens[s]
+        Kd = torch.empty((w.n_layers, w.n_kv_heads, T, w.head_dim), dtype=tdt, device="cuda")
+        Vd = torch.empty_like(Kd)
+        for b, h, k, v in gen.iter_segments(w, s, threads=16):
+            Kd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(k).cuda().to(tdt))
+            Vd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(v).cuda().to(tdt))
+        cache.compress(s, [Kd[l] for l in range(w.n_layers)], [Vd[l] for l in range(w.n_layers)])
+        torch.cuda.synchronize()
+        del Kd, Vd
+    return cache
+
+
+def _check_units(torch, w, cache, modes_b, samples, qscale=8.0):
+    from paper_2607_06519_amd.cache import to_device
+    buf = cache.host_bytes()
+    G, d = w.group, w.head_dim
+    q = gen.decode_queries(w, 0, scale=qscale)              # [L][batch][Hq][d]
+    outs = [cache.decode(layer, to_device(q[layer], w.dtype)).float().cpu().numpy() for layer in range(w.n_layers)]
+    worst = 0.0
+    for (s, b, h) in samples:
+        T = w.seq_lens[s]
+        mode = int(modes_b[s, b, h])
+        K, V, _ = gen.segment(w, s, b, h)
+        ref = O.compress_unit(K, V, mode, w.topk, w.dtype)
+        got = unpack_unit(buf, int(cache.offsets_host[s, b, h]), mode, T, d, w.topk, w.dtype)
+        compare_units(got, ref, w.dtype)
+        for layer in (2 * b, 2 * b + 1):
+            qq = q[layer][s, h * G:(h + 1) * G].astype(np.float64)
+            want = O.decode_unit(ref, mode, layer, qq, 1.0 / math.sqrt(d), d)
+            for g in range(G):
+                e = rel_l2(outs[layer][s, h * G + g], want[g])
+                worst = max(worst, e)
+                assert e <= 1e-2, (s, b, h, layer, g, e)
+        log(f"  unit seq={s} pair={b} head={h} mode={mode} T={T} ok")
+    return worst
+
+
+def _samples_by_mode(modes_b, per_mode=1, seqs=None):
+    out = []
+    seqs = range(modes_b.shape[0]) if seqs is None else seqs
+    for m in (O.SHARED, O.RESIDUAL, O.EXACT):
+        n = 0
+        for s in seqs:
+            for b in range(modes_b.shape[1]):
+                for h in range(modes_b.shape[2]):
+                    if modes_b[s, b, h] == m and n < per_mode:
+                        out.append((s, b, h))
+                        n += 1
+    return out
+
+
+@pytest.mark.parametrize("name,per_mode", [("llama8b", 2), ("long70b", 1)])
+def test_fullsize_single_sequence(torch_mod, name, per_mode):
+    w = scaled(WORKLOADS[name], n_layers=2)
+    log(f"[case] full-size {name}: T={w.seq_lens[0]} Hkv={w.n_kv_heads} Hq={w.n_q_heads} k={w.topk}")
+    modes = gen.fixed_modes(w)[None].copy()
+    modes[0, 0, :3] = [0, 1, 2]
+    cache = _build_cache(torch_mod, w, modes)
+    worst = _check_units(torch_mod, w, cache, modes, _samples_by_mode(modes, per_mode))
+    log(f"  worst rel-L2 {worst:.3e}")
+
+
+def test_fullsize_ragged_batch(torch_mod):
+    w = scaled(WORKLOADS["batched8b"], n_layers=2)
+    log(f"[case] full-size batched8b: lens {w.seq_lens}")
+    modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
+    for s in range(w.batch):
+        modes[s, 0, :3] = np.roll([0, 1, 2], s)
+    cache = _build_cache(torch_mod, w, modes)
+    samples = [(s, 0, h) for s, h in ((0, 0), (3, 1), (7, 2), (11, 5), (15, 7))]
+    worst = _check_units(torch_mod, w, cache, modes, samples)
+    log(f"  worst rel-L2 {worst:.3e}")
+
+
+def test_fullsize_probe(torch_mod):
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import probe, torch_dtype
+    w = scaled(WORKLOADS["prefill8b"], n_layers=2)
+    T, P, G = w.seq_lens[0], w.n_probe, w.group
+    log(f"[case] full-size probe: T={T} P={P} G={G}")
+    tdt = torch_dtype(w.dtype)
+    Kd = torch_mod.empty((2, w.n_kv_heads, T, w.head_dim), dtype=tdt, device="cuda")
+    segs = {}
+    for b, h, k, v in gen.iter_segments(w, 0, threads=16):
+        Kd[:, h].copy_(torch_mod.from_numpy(k).cuda().to(tdt))
+        segs[h] = k
+    Q = gen.probe_queries(w, 0)
+    Qd = torch_mod.from_numpy(Q).cuda().to(tdt)
+    err, _ = probe(B.dims(**w.dims()), T, [Kd[0], Kd[1]], [Qd[0], Qd[1]], P)
+    got = err.cpu().numpy()[0].astype(np.float64)
+    for h in (0, 5):
+        ref = O.routing_errors(segs[h], Q[:, h * G:(h + 1) * G], w.topk)
+        rel = np.abs(got[h] - ref[:2]) / ref[:2]
+        log(f"  head {h}: E_S {got[h, 0]:.6g} vs {ref[0]:.6g}, E_R {got[h, 1]:.6g} vs {ref[1]:.6g}, rel {rel.max():.2e}")
+        assert rel.max() <= 1e-4
