@@ -150,8 +150,10 @@ fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t 
  * (Section 3, after Eq. 3): o = softmax(q K~^T * sm_scale) V~ over the T_i
  * cached tokens of each sequence, K~/V~ rebuilt per head mode.
  *   seq_lens     device int32 [batch], 0 <= T_i <= max_seq_len (T_i = 0 gives o = 0)
- *   max_seq_len  host, sizes the launch
- *   modes        device [batch][L/2][Hkv]
+ *   max_seq_len  host, sizes the launch; max_seq_len * d * elem_bytes < 2^31
+ *                (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets)
+ *   modes        device [batch][L/2][Hkv], 4-byte aligned (read in aligned 4-byte
+ *                words; bytes past the array inside its last word are ignored)
  *   seg_offsets  device [batch][L/2][Hkv]
  *   layer        0 <= layer < L
  *   q            device [batch][Hq][d]

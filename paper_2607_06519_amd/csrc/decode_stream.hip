@@ -1,31 +1,33 @@
-// Streaming split-K decode over a bf16 compressed cache (Section 3, the
-// reconstruction fused into attention after Eq. 3).
+// Streaming split-K decode over a bf16 compressed cache (Section 3: the
+// reconstruction of Eq. 3 fused into the attention).
 //
 // One workgroup = 4 waves = 512 tokens of one (sequence, KV head); a wave
-// walks its 128 tokens in 16-row tiles with an online softmax and keeps the
-// next tile's loads in flight while it computes the current one (two
-// register buffers).
+// walks its 128 tokens in 16-row tiles with an online softmax, keeping the
+// next tiles' loads in flight while it computes the current one.
 //
-// Lane layout (the same for K and V): NP = d/8 lanes per row, lane holds one
-// 16-byte piece (8 bf16 channels); a load instruction covers RPV = 64/NP
-// consecutive rows (1 KB, fully coalesced).  Loads are raw buffer loads
-// (32-bit offsets, SGPR descriptors); rows past the sequence end read as 0.
-//
-// Per tile:
-//  K  - bf16 dot2 of the lane's piece with the matching query piece, group
-//       sum over the NP lanes of the row by DPP; residual heads add
-//       sigma * q[IK_j] * D_K,j for the lane's residual entry.
-//  softmax - against a running reference max that moves (wave max, rescale
-//       by exp2(m_old - m_new)) only when a logit exceeds it by more than
-//       2^8; probabilities to LDS (fp32 and bf16 pairs).
-//  V  - rows r and r + RPV are paired so one dot2 multiplies two tokens'
-//       values by their two bf16 probabilities; residual V entries are added
-//       into LDS accumulators (one copy per row slot r % 4, so the lanes of a
-//       step never collide), rescaled together with the rest.
+// One lane layout serves the K pass, the softmax and the V pass: NP = d/8
+// lanes per token row, each holding one 16-byte piece (8 channels), so one
+// load instruction covers RPL = 64/NP consecutive rows and a lane owns
+// NL = 16/RPL rows of a tile.  The NP lanes of a row form a DPP row (d = 128)
+// or half row (d = 64).
+//  K   - bf16 dot2 of the lane's piece with its piece of every query (held in
+//        registers); residual heads add the lane's residual entry
+//        sigma * q[IK] * D_K; a DPP butterfly then sums over the row's lanes,
+//        which leaves every lane of the row with the row's logits -- exactly
+//        the probabilities its V pass needs, so nothing goes through LDS;
+//  max - a running reference max, uniform over the wave, that moves (cross-
+//        row max, rescale by exp2(m_old - m_new)) only when a logit exceeds
+//        it by more than 2^8;
+//  V   - the lane's rows are taken in pairs so one dot2 multiplies two
+//        tokens' values by their two bf16 probabilities; residual heads add
+//        sigma * p * D_V into LDS accumulators, one copy per row of a load,
+//        so the distinct channels of one row never collide.
 // The 4 waves merge in LDS and write one (acc, m, l) record per workgroup;
 // decode_merge combines the records.  HBM bound: no MFMA.
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
+
+#include <type_traits>
 
 namespace fdkv {
 
@@ -34,6 +36,7 @@ namespace {
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 constexpr int kRsrcDword3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
 constexpr float kSlack = 8.f;            // log2 headroom of the running reference max
+constexpr uint32_t kOob = 0x80000000u;   // buffer offset past every plane (planes are < 2^31 bytes): loads read 0
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
@@ -50,37 +53,32 @@ __device__ __forceinline__ uint4 ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+__device__ __forceinline__ uint32_t word(const uint4& v, int w) {
+  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+}
+
 template <int D, int G>
 struct SS {
-  static constexpr int NP = D / 8;                 // 16-byte pieces per bf16 row
-  static constexpr int CPP = 8;                    // channels per piece
-  // K pass: LPRK lanes per row, PKK pieces per lane, RSK rows per load set
-  static constexpr int LPRK = (G >= 8 || NP < 8) ? (NP < 8 ? NP : 8) : 4;
-  static constexpr int PKK = NP / LPRK;
-  static constexpr int RSK = 64 / LPRK;
-  // V pass: NP lanes per row (one piece each), RPL rows per load
-  static constexpr int RPL = 64 / NP;
+  static constexpr int NP = D / 8;                 // lanes per row, one 16-byte piece each
+  static constexpr int RPL = 64 / NP;              // rows per load instruction
   static constexpr int TILE = 16;
-  static constexpr int NKS = TILE / RSK;           // K load sets per tile
-  static constexpr int NL = TILE / RPL;            // V loads per tile
-  static constexpr int NPAIR = NL / 2;
+  static constexpr int NL = TILE / RPL;            // rows of a tile per lane
   static constexpr int CW = kDecodeChunk;          // tokens per wave
-  static constexpr int NT = CW / TILE;
-  static constexpr int KEL = 16 / LPRK;            // residual K entries per lane per row (k = 16 path)
   static constexpr int W = kDecodeWaves;
   static constexpr int RS = D + 4;
-  static_assert(NKS >= 1 && NL % 2 == 0 && NT % 2 == 0 && TILE * 16 == 64 * 4, "shape");
+  static constexpr int PD0 = G >= 8 ? 1 : 2;       // tiles in flight behind the current one (dense heads)
+  static constexpr int SP = W * RPL * G * D;       // residual V accumulators (floats)
+  static constexpr int MG = W * G * (D + 2);       // per-wave (acc, m, l) for the workgroup merge
+  static constexpr int LDSF = SP > MG ? SP : MG;
+  static_assert(NL % 2 == 0 && CW % TILE == 0 && RPL * NP == 64, "shape");
 };
 
 template <int D, int G>
 struct TileBuf {
-  using S = SS<D, G>;
-  uint4 k[S::NKS][S::PKK];
-  uint4 v[S::NL];
-  uint32_t ki[S::NKS];            // residual K indices of the lane's entries (k = 16 path)
-  uint32_t kv[S::NKS][2];         // their bf16 values
-  uint32_t vi[4];                 // residual V index of the lane in each 4-row step (k = 16 path)
-  uint32_t vv[4];                 // its bf16 value
+  static constexpr int NL = SS<D, G>::NL;
+  uint4 k[NL], v[NL];
+  // residual entry of the lane in each of its rows (k = NP path): index byte and bf16 value
+  uint32_t ki[NL], kv[NL], vi[NL], vv[NL];
 };
 
 }  // namespace
@@ -88,33 +86,36 @@ struct TileBuf {
 template <int D, int G>
 __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   using S = SS<D, G>;
-  constexpr int NP = S::NP, CPP = S::CPP, LPRK = S::LPRK, PKK = S::PKK, RSK = S::RSK, RPL = S::RPL;
-  constexpr int TILE = S::TILE, NKS = S::NKS, NL = S::NL, NPAIR = S::NPAIR, CW = S::CW, NT = S::NT;
-  constexpr int KEL = S::KEL, W = S::W;
+  constexpr int NP = S::NP, RPL = S::RPL, TILE = S::TILE, NL = S::NL, CW = S::CW, W = S::W;
   constexpr uint32_t RB = D * 2;
-  __shared__ float q_lds[D * G];               // [c][g] fp32, residual K gathers
-  __shared__ uint4 qp_lds[G][NP];              // bf16 query pieces for the K pass
-  __shared__ uint32_t pp_lds[W][G][TILE / 2];  // bf16 probability pairs of the tile
-  __shared__ float p_lds[W][G][TILE];          // fp32 probabilities of the tile
-  __shared__ float sp_lds[W][4][G][D];         // residual V accumulator, one copy per row slot r % 4
-  __shared__ float mg_lds[W][G][D + 2];        // per-wave acc, m, l
+  __shared__ float q_lds[D * G];                        // [c][g] fp32: residual K gathers
+  __shared__ __attribute__((aligned(16))) float big[S::LDSF];  // residual V accumulators, then the merge
+  auto sp = [&](int w, int cp, int g, int c) -> float& { return big[((w * RPL + cp) * G + g) * D + c]; };
+  auto mg = [&](int w, int g, int c) -> float& { return big[(w * G + g) * (D + 2) + c]; };
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wgc = blockIdx.x % P.n_wgchunks;
   const int sh = blockIdx.x / P.n_wgchunks;
   const int head = sh % P.hkv, seq = sh / P.hkv;
-  const int T = P.seq_lens[seq];
-  const int wg_tok0 = wgc * kDecodeWgTokens;
-  if (wg_tok0 >= T) return;
-
   const int pair = P.layer >> 1, parity = P.layer & 1;
-  const float sigma = parity ? -1.f : 1.f;
   const uint64_t unit = ((uint64_t)seq * P.n_pairs + pair) * P.hkv + head;
-  const int mode = P.modes[unit];
+  // The three per-unit values are fetched together, as scalar loads (the
+  // mode byte through its aligned dword; the array is 4-byte aligned), and
+  // the exit test below reads all of them: the start-up costs one round trip
+  // that does not queue behind other waves' tile loads.  (A segment offset is
+  // a multiple of 256 and a mode is at most kExact; a unit that breaks either
+  // is left alone.)
+  const int T = P.seq_lens[seq];
+  const uint32_t mode_word = reinterpret_cast<const uint32_t*>(P.modes)[unit >> 2];
+  const uint64_t seg_off = P.seg_off[unit];
+  const int mode = (int)((mode_word >> (8 * (unit & 3))) & 0xFFu);
+  const int wg_tok0 = wgc * kDecodeWgTokens;
+  if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) return;
+
+  const float sigma = parity ? -1.f : 1.f;
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
-  const bool resid16 = resid && k == 16 && NP == 16;
-  const uint8_t* seg = P.cache + P.seg_off[unit];
+  const uint8_t* seg = P.cache + seg_off;
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2);
   const uint64_t dense = (uint64_t)T * RB;
   const auto kr = rsrc(seg + (mode == kExact ? (parity ? L.k1 : L.k0) : L.mk), dense);
@@ -124,248 +125,252 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k);
   const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * 2);
   const uint8_t* qbase = static_cast<const uint8_t*>(P.q) + ((uint64_t)seq * P.hq + (uint64_t)head * G) * RB;
+  const auto qr = rsrc(qbase, (uint64_t)G * RB);
 
-  for (int i = threadIdx.x; i < D * G; i += 256) {
-    const int g = i / D, c = i % D;
-    q_lds[c * G + g] = bf16_to_f32(reinterpret_cast<const uint16_t*>(qbase)[g * D + c]);
+  const int rg = lane / NP, pc = lane % NP;  // row of a load, piece of the row
+  // the lane's piece of every query, for the whole kernel
+  uint4 qreg[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) qreg[g] = ld128(qr, (uint32_t)(g * RB + pc * 16));
+  // the fp32 query for the residual gathers, read now and staged to LDS after
+  // the first tiles have been requested (the waits are in issue order)
+  constexpr int QPT = (D * G + 255) / 256;
+  uint32_t qraw[QPT];
+#pragma unroll
+  for (int j = 0; j < QPT; ++j) {
+    const uint32_t i = threadIdx.x + 256 * j;
+    qraw[j] = __builtin_amdgcn_raw_buffer_load_b16(qr, i < D * G ? i * 2 : kOob, 0, 0);
   }
-  for (int i = lane; i < 4 * G * D; i += 64) (&sp_lds[wave][0][0][0])[i] = 0.f;
-
-  const int krow = lane / LPRK, ks = lane % LPRK;  // K pass: row in load set, lane in row
-  const int rr = lane / NP, pc = lane % NP;        // V pass: row in load, piece
-  for (int i = threadIdx.x; i < G * NP; i += 256)
-    qp_lds[i / NP][i % NP] = *reinterpret_cast<const uint4*>(qbase + (uint64_t)(i / NP) * RB + (uint64_t)(i % NP) * 16);
-  __syncthreads();
 
   const int wtok0 = wg_tok0 + wave * CW;
-  const int ntiles = wtok0 < T ? min(NT, (T - wtok0 + TILE - 1) / TILE) : 0;
+  const int ntiles = wtok0 < T ? min(CW / TILE, (T - wtok0 + TILE - 1) / TILE) : 0;
 
-  float m[G], l[G], acc[G][CPP];
+  float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     m[g] = -INFINITY;
     l[g] = 0.f;
 #pragma unroll
-    for (int c = 0; c < CPP; ++c) acc[g][c] = 0.f;
+    for (int c = 0; c < 8; ++c) acc[g][c] = 0.f;
   }
 
-  auto load = [&](int t, TileBuf<D, G>& b) {
-    const uint32_t r0 = (uint32_t)(wtok0 + t * TILE);
+  // The tile loop is specialised per residual flavour (RES: 0 none, 1 one
+  // entry per lane (k = NP), 2 any other k) so that every load of a tile is
+  // issued unconditionally: a tile past the wave's range takes the
+  // out-of-range offset and reads zeros without touching memory.  With no
+  // load behind a branch the compiler can wait for exactly the tile it needs
+  // and leave the later tiles' loads in flight.
+  auto run = [&](auto res_tag) {
+    constexpr int RES = decltype(res_tag)::value;
+    constexpr int PD = RES == 0 ? S::PD0 : 1, NB = PD + 1;
+
+    auto load = [&](int t, TileBuf<D, G>& b) {
+      const bool ok = t < ntiles;
+      const uint32_t r0 = (uint32_t)(wtok0 + t * TILE);
 #pragma unroll
-    for (int ks_ = 0; ks_ < NKS; ++ks_) {
-      const uint32_t row = r0 + ks_ * RSK + krow;
-#pragma unroll
-      for (int j = 0; j < PKK; ++j) b.k[ks_][j] = ld128(kr, row * RB + (uint32_t)(j * LPRK + ks) * 16);
-      if (resid16) {
-        const uint32_t e = row * 16 + ks * KEL;
-        if constexpr (KEL == 4) {
-          b.ki[ks_] = __builtin_amdgcn_raw_buffer_load_b32(ikr, e, 0, 0);
-          const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(vkr, e * 2, 0, 0);
-          b.kv[ks_][0] = w2[0];
-          b.kv[ks_][1] = w2[1];
-        } else {
-          b.ki[ks_] = __builtin_amdgcn_raw_buffer_load_b16(ikr, e, 0, 0);
-          b.kv[ks_][0] = __builtin_amdgcn_raw_buffer_load_b32(vkr, e * 2, 0, 0);
+      for (int i = 0; i < NL; ++i) {
+        const uint32_t row = r0 + i * RPL + rg;
+        b.k[i] = ld128(kr, ok ? row * RB + pc * 16 : kOob);
+        if constexpr (RES == 1) {
+          const uint32_t e = row * NP + pc;
+          b.ki[i] = __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, 0);
+          b.kv[i] = __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, 0);
         }
       }
-    }
 #pragma unroll
-    for (int i = 0; i < NL; ++i) b.v[i] = ld128(vr, (r0 + i * RPL + rr) * RB + pc * 16);
-    if (resid16) {
-      // step jj covers rows 4jj..4jj+3 of the tile: lane = (row slot lane / 16, entry lane % 16)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const uint32_t e = (r0 + 4 * jj + (lane >> 4)) * 16 + (lane & 15);
-        b.vi[jj] = __builtin_amdgcn_raw_buffer_load_b8(ivr, e, 0, 0);
-        b.vv[jj] = __builtin_amdgcn_raw_buffer_load_b16(vvr, e * 2, 0, 0);
+      for (int i = 0; i < NL; ++i) {
+        const uint32_t row = r0 + i * RPL + rg;
+        b.v[i] = ld128(vr, ok ? row * RB + pc * 16 : kOob);
+        if constexpr (RES == 1) {
+          const uint32_t e = row * NP + pc;
+          b.vi[i] = __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, 0);
+          b.vv[i] = __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, 0);
+        }
       }
-    }
-  };
+    };
 
-  auto compute = [&](int t, const TileBuf<D, G>& b) {
-    const int r0 = wtok0 + t * TILE;
-    float s[NKS][G];
+    auto compute = [&](int t, const TileBuf<D, G>& b) {
+      const int r0 = wtok0 + t * TILE;
+      float s[NL][G];
 #pragma unroll
-    for (int ks_ = 0; ks_ < NKS; ++ks_) {
-      float a[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) a[g] = 0.f;
-#pragma unroll
-      for (int j = 0; j < PKK; ++j) {
-        const uint32_t* kw = reinterpret_cast<const uint32_t*>(&b.k[ks_][j]);
+      for (int i = 0; i < NL; ++i)
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-          const uint4 qv = qp_lds[g][j * LPRK + ks];
-          const uint32_t* qw = reinterpret_cast<const uint32_t*>(&qv);
+          float a = 0.f;
 #pragma unroll
-          for (int w = 0; w < 4; ++w) a[g] = dot2(kw[w], qw[w], a[g]);
+          for (int w = 0; w < 4; ++w) a = dot2(word(b.k[i], w), word(qreg[g], w), a);
+          s[i][g] = a;
+        }
+      if constexpr (RES == 1) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const int c = b.ki[i] & (D - 1);
+          const float v = sigma * bf16_to_f32((uint16_t)b.kv[i]);
+#pragma unroll
+          for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
+        }
+      } else if constexpr (RES == 2) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const uint32_t rc = (uint32_t)min(r0 + i * RPL + rg, T - 1);
+          for (int e = pc; e < k; e += NP) {
+            const uint32_t x = rc * k + e;
+            const int c = __builtin_amdgcn_raw_buffer_load_b8(ikr, x, 0, 0) & (D - 1);
+            const float v = sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vkr, x * 2, 0, 0));
+#pragma unroll
+            for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
+          }
         }
       }
-      const int row = r0 + ks_ * RSK + krow;
-      if (resid16) {
+      float d = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < KEL; ++e) {
-          const int c = (b.ki[ks_] >> (8 * e)) & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)(b.kv[ks_][e >> 1] >> (16 * (e & 1))));
-#pragma unroll
-          for (int g = 0; g < G; ++g) a[g] = fmaf(q_lds[c * G + g], v, a[g]);
-        }
-      } else if (resid) {
-        const uint32_t rc = (uint32_t)min(row, T - 1);
-        for (int e = ks; e < k; e += LPRK) {
-          const int c = __builtin_amdgcn_raw_buffer_load_b8(ikr, rc * k + e, 0, 0) & (D - 1);
-          const float v =
-              sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vkr, (rc * k + e) * 2, 0, 0));
-#pragma unroll
-          for (int g = 0; g < G; ++g) a[g] = fmaf(q_lds[c * G + g], v, a[g]);
-        }
-      }
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float x = group_sum<LPRK>(a[g]) * P.scale_log2;
-        s[ks_][g] = row < T ? x : -INFINITY;
-      }
-    }
-    // online softmax over the tile.  m is a reference value, uniform over the
-    // wave, that only moves when some logit exceeds it by more than kSlack
-    // (probabilities then stay below 2^kSlack); moving it takes a wave max
-    // and rescales the running sums.
-    bool rescale = false;
-    float alpha[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float mt = s[0][g];
-#pragma unroll
-      for (int ks_ = 1; ks_ < NKS; ++ks_) mt = fmaxf(mt, s[ks_][g]);
-      float mn = m[g];
-      alpha[g] = 1.f;
-      if (__ballot(mt > m[g] + kSlack) != 0) {
-#pragma unroll
-        for (int o = LPRK; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
-        mn = fmaxf(m[g], mt);
-        alpha[g] = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
-        rescale = true;
-      }
-      float ps = 0.f;
-#pragma unroll
-      for (int ks_ = 0; ks_ < NKS; ++ks_) {
-        const float p = (s[ks_][g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s[ks_][g] - mn);
-        ps += p;
-        if (ks == 0) {
-          const int R = ks_ * RSK + krow;  // tile-local row; rows R and R + RPL share a pair slot
-          const int i = R / RPL;
-          p_lds[wave][g][R] = p;
-          reinterpret_cast<uint16_t*>(&pp_lds[wave][g][0])[((i >> 1) * RPL + R % RPL) * 2 + (i & 1)] =
-              (uint16_t)f32_to_bf16_bits(p);
-        }
-      }
-      l[g] = l[g] * alpha[g] + (ks == 0 ? ps : 0.f);
-      m[g] = mn;
-    }
-    if (rescale) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-#pragma unroll
-        for (int c = 0; c < CPP; ++c) acc[g][c] *= alpha[g];
-        if (resid) {
-#pragma unroll
-          for (int cp = 0; cp < 4; ++cp)
-#pragma unroll
-            for (int c = lane; c < D; c += 64) sp_lds[wave][cp][g][c] *= alpha[g];
-        }
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // P V over the dense plane
-#pragma unroll
-    for (int pr = 0; pr < NPAIR; ++pr) {
-      uint32_t pp[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) pp[g] = pp_lds[wave][g][pr * RPL + rr];
-      const uint32_t* wa = reinterpret_cast<const uint32_t*>(&b.v[2 * pr]);
-      const uint32_t* wb = reinterpret_cast<const uint32_t*>(&b.v[2 * pr + 1]);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const uint32_t lo = __builtin_amdgcn_perm(wb[w], wa[w], 0x05040100u);
-        const uint32_t hi = __builtin_amdgcn_perm(wb[w], wa[w], 0x07060302u);
+      for (int i = 0; i < NL; ++i) {
+        const bool valid = r0 + i * RPL + rg < T;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-          acc[g][2 * w] = dot2(lo, pp[g], acc[g][2 * w]);
-          acc[g][2 * w + 1] = dot2(hi, pp[g], acc[g][2 * w + 1]);
+          const float x = group_sum<NP>(s[i][g]) * P.scale_log2;
+          s[i][g] = valid ? x : -INFINITY;
+          d = fmaxf(d, s[i][g] - m[g]);
         }
       }
-    }
-    // residual V entries.  In one step the lanes touch 4 rows (one accumulator
-    // copy each) and the 16 distinct channels of each row, so no two lanes of
-    // an LDS instruction share an address and a plain read-add-write is exact.
-    if (resid16) {
-      const int slot = lane >> 4;
+      // The reference max moves only when some logit exceeds it by more than
+      // kSlack (probabilities then stay below 2^kSlack); moving it takes the
+      // tile max over the wave's rows and rescales the running sums.
+      if (__ballot(d > kSlack) != 0) {
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int rl = 4 * jj + slot;
-        if (r0 + rl < T) {
-          const int c = b.vi[jj] & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)b.vv[jj]);
+        for (int g = 0; g < G; ++g) {
+          float mt = s[0][g];
 #pragma unroll
-          for (int g = 0; g < G; ++g) sp_lds[wave][slot][g][c] += p_lds[wave][g][rl] * v;
+          for (int i = 1; i < NL; ++i) mt = fmaxf(mt, s[i][g]);
+#pragma unroll
+          for (int o = NP; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
+          const float mn = fmaxf(m[g], mt);
+          const float alpha = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
+          l[g] *= alpha;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
+          if constexpr (RES != 0) {
+#pragma unroll
+            for (int cp = 0; cp < RPL; ++cp)
+#pragma unroll
+              for (int c = lane; c < D; c += 64) sp(wave, cp, g, c) *= alpha;
+          }
+          m[g] = mn;
         }
       }
-    } else if (resid) {
-      for (int ent = lane; ent < TILE * k; ent += 64) {
-        const int rl = ent / k;
-        if (r0 + rl < T) {
-          const uint32_t ix = (uint32_t)(r0 + rl) * k + (ent - rl * k);
-          const int c = __builtin_amdgcn_raw_buffer_load_b8(ivr, ix, 0, 0) & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vvr, ix * 2, 0, 0));
+      float p[NL][G];
 #pragma unroll
-          for (int g = 0; g < G; ++g) atomicAdd(&sp_lds[wave][0][g][c], p_lds[wave][g][rl] * v);
+      for (int i = 0; i < NL; ++i)
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          p[i][g] = __builtin_amdgcn_exp2f(s[i][g] - m[g]);  // masked rows: exp2(-inf) = 0
+          l[g] += p[i][g];
+        }
+      // P V over the dense plane: the lane's rows 2pr and 2pr + 1 share one dot2
+#pragma unroll
+      for (int pr = 0; pr < NL / 2; ++pr) {
+        uint32_t pp[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) pp[g] = pack_bf16x2(p[2 * pr][g], p[2 * pr + 1][g]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t wa = word(b.v[2 * pr], w), wb = word(b.v[2 * pr + 1], w);
+          const uint32_t lo = __builtin_amdgcn_perm(wb, wa, 0x05040100u);
+          const uint32_t hi = __builtin_amdgcn_perm(wb, wa, 0x07060302u);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            acc[g][2 * w] = dot2(lo, pp[g], acc[g][2 * w]);
+            acc[g][2 * w + 1] = dot2(hi, pp[g], acc[g][2 * w + 1]);
+          }
         }
       }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  };
+      // residual V entries: the lanes of one row hold distinct channels and
+      // each row of a load has its own accumulator copy, so a plain
+      // read-add-write never collides (masked rows add p = 0)
+      if constexpr (RES == 1) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const int c = b.vi[i] & (D - 1);
+          const float v = sigma * bf16_to_f32((uint16_t)b.vv[i]);
+#pragma unroll
+          for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+        }
+      } else if constexpr (RES == 2) {
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const int row = r0 + i * RPL + rg;
+          const uint32_t rc = (uint32_t)min(row, T - 1);
+          for (int e = pc; e < k; e += NP) {
+            const uint32_t x = rc * k + e;
+            const int c = __builtin_amdgcn_raw_buffer_load_b8(ivr, x, 0, 0) & (D - 1);
+            const float v = sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vvr, x * 2, 0, 0));
+#pragma unroll
+            for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+          }
+        }
+      }
+    };
 
-  if (ntiles > 0) {
-    TileBuf<D, G> A, Bf;
-    load(0, A);
-    for (int t = 0; t < ntiles; t += 2) {
-      if (t + 1 < ntiles) load(t + 1, Bf);
-      compute(t, A);
-      if (t + 1 < ntiles) {
-        if (t + 2 < ntiles) load(t + 2, A);
-        compute(t + 1, Bf);
+    // ring of PD + 1 tile buffers: PD tiles stay in flight behind the one
+    // being computed
+    TileBuf<D, G> buf[NB];
+#pragma unroll
+    for (int i = 0; i < PD; ++i) load(i, buf[i]);
+    if constexpr (RES != 0) {
+      for (int x = lane * 4; x < RPL * G * D; x += 256)
+        *reinterpret_cast<float4*>(&sp(wave, 0, 0, x)) = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int j = 0; j < QPT; ++j) {
+        const int i = threadIdx.x + 256 * j;
+        if (i < D * G) q_lds[(i % D) * G + i / D] = bf16_to_f32((uint16_t)qraw[j]);
+      }
+      __syncthreads();  // the whole workgroup shares one unit, hence one flavour
+    }
+    for (int t = 0; t < ntiles; t += NB) {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        load(t + j + PD, buf[(j + PD) % NB]);
+        if (j == 0 || t + j < ntiles) compute(t + j, buf[j]);
       }
     }
-  }
+  };  // run
 
-  // wave totals
-#pragma unroll
-  for (int g = 0; g < G; ++g) l[g] = wave_sum(l[g]);
+  if (resid && k == NP)
+    run(std::integral_constant<int, 1>{});
+  else if (resid)
+    run(std::integral_constant<int, 2>{});
+  else
+    run(std::integral_constant<int, 0>{});
+
+  // wave totals: the row groups of a load saw different rows
 #pragma unroll
   for (int o = NP; o < 64; o <<= 1)
 #pragma unroll
+    for (int g = 0; g < G; ++g) {
+      l[g] += __shfl_xor(l[g], o, 64);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[g][c] += __shfl_xor(acc[g][c], o, 64);
+    }
+  if (resid && lane < NP) {
+#pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int c = 0; c < CPP; ++c) acc[g][c] += __shfl_xor(acc[g][c], o, 64);
-  __syncthreads();
+      for (int c = 0; c < 8; ++c)
+#pragma unroll
+        for (int cp = 0; cp < RPL; ++cp) acc[g][c] += sp(wave, cp, g, lane * 8 + c);
+  }
+  __syncthreads();  // the accumulator copies are read; the merge reuses their space
   if (lane < NP) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int c = 0; c < CPP; ++c)
-        mg_lds[wave][g][lane * CPP + c] = acc[g][c] + sp_lds[wave][0][g][lane * CPP + c] +
-                                          sp_lds[wave][1][g][lane * CPP + c] + sp_lds[wave][2][g][lane * CPP + c] +
-                                          sp_lds[wave][3][g][lane * CPP + c];
+      for (int c = 0; c < 8; ++c) mg(wave, g, lane * 8 + c) = acc[g][c];
   }
   if (lane == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      mg_lds[wave][g][D] = m[g];
-      mg_lds[wave][g][D + 1] = l[g];
+      mg(wave, g, D) = m[g];
+      mg(wave, g, D + 1) = l[g];
     }
   }
   __syncthreads();
@@ -374,7 +379,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     const int g = i / (D + 2), c = i - g * (D + 2);
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < W; ++w) M = fmaxf(M, mg_lds[w][g][D]);
+    for (int w = 0; w < W; ++w) M = fmaxf(M, mg(w, g, D));
     float o;
     if (c == D) {
       o = M;
@@ -382,9 +387,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       o = 0.f;
 #pragma unroll
       for (int w = 0; w < W; ++w) {
-        const float mw = mg_lds[w][g][D];
+        const float mw = mg(w, g, D);
         const float f = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - M);
-        o = fmaf(f, mg_lds[w][g][c], o);
+        o = fmaf(f, mg(w, g, c), o);
       }
     }
     rec[g * S::RS + c] = o;

@@ -294,7 +294,8 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (batch < 1 || max_seq_len < 0 || layer < 0 || layer >= dims->n_layers) return FDKV_E_INVALID_ARG;
-  if (!aligned(seq_lens, 4) || !modes || !aligned(seg_offsets, 8) || !aligned(cache, 256) || !aligned(q, 16) ||
+  if ((uint64_t)max_seq_len * dims->head_dim * elem_bytes(dims) >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
+  if (!aligned(seq_lens, 4) || !aligned(modes, 4) || !aligned(seg_offsets, 8) || !aligned(cache, 256) || !aligned(q, 16) ||
       !aligned(out, 16) || !aligned(ws, 16) || !isfinite(sm_scale))
     return FDKV_E_INVALID_ARG;
   size_t need = 0;

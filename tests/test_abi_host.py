@@ -121,6 +121,12 @@ def test_validation_errors_before_any_device_call(lib):
     mis = ctypes.c_void_p((1 << 20) + 4)
     assert lib.fdkv_decode_attn(ctypes.byref(good), 1, fake, 16, fake, fake, fake, 0, mis, fake,
                                 ctypes.c_float(0.1), fake, 1 << 30, None) == -1
+    odd = ctypes.c_void_p((1 << 20) + 1)                   # modes are read in aligned 4-byte words
+    assert lib.fdkv_decode_attn(ctypes.byref(good), 1, fake, 16, odd, fake, fake, 0, fake, fake,
+                                ctypes.c_float(0.1), fake, 1 << 30, None) == -1
+    # planes are addressed with 32-bit offsets: T * d * 2 bytes must stay below 2^31
+    assert lib.fdkv_decode_attn(ctypes.byref(good), 1, fake, 1 << 23, fake, fake, fake, 0, fake, fake,
+                                ctypes.c_float(0.1), fake, 1 << 40, None) == -2
     assert lib.fdkv_compress(ctypes.byref(good), 16, ptrs, None, fake, fake, fake, None) == -1
     n = ctypes.c_size_t(0)
     assert lib.fdkv_probe_workspace(ctypes.byref(good), 100, 4, ctypes.byref(n)) == 0 and n.value > 0
