@@ -396,72 +396,99 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   }
 }
 
+// Wave-wide max / sum: DPP within each row of 16 lanes, then the four row
+// results read as uniform values.
+__device__ __forceinline__ float wave_max_dpp(float x) {
+  x = fmaxf(x, dpp<kDppQuadXor1>(x));
+  x = fmaxf(x, dpp<kDppQuadXor2>(x));
+  x = fmaxf(x, dpp<kDppRowHalfMirror>(x));
+  x = fmaxf(x, dpp<kDppRowMirror>(x));
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ float wave_sum_dpp(float x) {
+  x += dpp<kDppQuadXor1>(x);
+  x += dpp<kDppQuadXor2>(x);
+  x += dpp<kDppRowHalfMirror>(x);
+  x += dpp<kDppRowMirror>(x);
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return (a + b) + (c + d);
+}
+
 // Log-sum-exp merge of the workgroup records of one (sequence, query head):
 //   M = max_i m_i,  l = sum_i l_i 2^(m_i - M),  o = sum_i acc_i 2^(m_i - M) / l.
-// One 512-thread workgroup per query head; records are taken in blocks of
-// 512, the channels split over 512 / d thread groups that each sum a strided
-// subset of the block's records.
+// One workgroup of four waves per query head, records taken in blocks of 64.
+// Within a block every wave loads the (m, l) pairs (record i in lane i) and
+// its share of the accumulators (record i to wave i mod 4) in one go -- the
+// accumulators do not depend on the max -- then reduces M and l itself and
+// weights each record with the value read from the lane that owns it.  A
+// running (M, l, o) carries over between blocks; LDS adds the four waves'
+// partial sums.
 template <int D, bool BF16, int G>
-__global__ __launch_bounds__(512) void decode_merge_kernel(DecodeParams P) {
+__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
   constexpr int RS = D + 4;
-  constexpr int NB = 512;            // records per block
-  constexpr int SUB = 512 / D;       // thread groups per channel
-  __shared__ float wgt[NB];
-  __shared__ float red[512];
-  __shared__ float part[SUB][D];
+  constexpr int CPL = D / 64;  // channels per lane
+  constexpr int NR = 16;       // records per wave per block
+  __shared__ float part[4][D];
   const int qh = blockIdx.x % P.hq, seq = blockIdx.x / P.hq;
   const int head = qh / G, g = qh % G;
   const int T = P.seq_lens[seq];
   const int nch = min((T + kDecodeWgTokens - 1) / kDecodeWgTokens, P.n_wgchunks);
-  const float* base = P.ws + ((uint64_t)(seq * P.hkv + head) * P.n_wgchunks) * G * RS + g * RS;
-  const int tid = threadIdx.x;
-  const int c = tid % D, sub = tid / D;
-  float M = -INFINITY, Lsum = 0.f, acc = 0.f;
-  for (int b0 = 0; b0 < nch; b0 += NB) {
-    const int nb = min(NB, nch - b0);
-    const float mi = tid < nb ? base[(uint64_t)(b0 + tid) * G * RS + D] : -INFINITY;
-    red[tid] = mi;
-    __syncthreads();
-    for (int o = 256; o > 0; o >>= 1) {
-      if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
-      __syncthreads();
-    }
-    const float Mb = red[0];
-    __syncthreads();
-    const float wi = tid < nb ? __builtin_amdgcn_exp2f(mi - Mb) : 0.f;
-    wgt[tid] = wi;
-    red[tid] = tid < nb ? wi * base[(uint64_t)(b0 + tid) * G * RS + D + 1] : 0.f;
-    __syncthreads();
-    for (int o = 256; o > 0; o >>= 1) {
-      if (tid < o) red[tid] += red[tid + o];
-      __syncthreads();
-    }
-    const float Lb = red[0];
-    float ab = 0.f;
-#pragma unroll 8
-    for (int i = sub; i < nb; i += SUB) ab = fmaf(wgt[i], base[(uint64_t)(b0 + i) * G * RS + c], ab);
-    part[sub][c] = ab;
-    __syncthreads();
-    if (sub == 0) {
+  const uint64_t stride = (uint64_t)G * RS;  // floats between consecutive records of one query head
+  const float* base = P.ws + ((uint64_t)(seq * P.hkv + head) * P.n_wgchunks) * stride + g * RS;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+  float M = -INFINITY, lsum = 0.f, o[CPL];
 #pragma unroll
-      for (int j = 1; j < SUB; ++j) ab += part[j][c];
+  for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+  for (int b0 = 0; b0 < nch; b0 += 64) {
+    const int last = nch - 1;  // loads past the end repeat the last record and get weight 0
+    const int il = b0 + lane;
+    const float2 ml = *reinterpret_cast<const float2*>(base + (uint64_t)min(il, last) * stride + D);
+    float a[NR][CPL];
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      const float* r = base + (uint64_t)min(b0 + wave + 4 * j, last) * stride;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) a[j][c] = r[lane * CPL + c];
     }
-    // fold the block into the running result (rescale by the new max)
+    const float mi = il < nch ? ml.x : -INFINITY;
+    const float Mb = wave_max_dpp(mi);
     const float Mn = fmaxf(M, Mb);
-    const float fo = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
-    const float fb = __builtin_amdgcn_exp2f(Mb - Mn);
-    Lsum = Lsum * fo + Lb * fb;
-    acc = acc * fo + ab * fb;
+    const float fo = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+    const float w = il < nch ? __builtin_amdgcn_exp2f(mi - Mn) : 0.f;
+    lsum = lsum * fo + wave_sum_dpp(w * ml.y);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[c] *= fo;
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), wave + 4 * j));
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) o[c] = fmaf(wj, a[j][c], o[c]);
+    }
     M = Mn;
-    __syncthreads();
   }
-  if (sub == 0) {
-    const float res = nch > 0 ? acc / Lsum : 0.f;
-    const uint64_t oi = ((uint64_t)seq * P.hq + qh) * D + c;
-    if constexpr (BF16)
-      reinterpret_cast<uint16_t*>(P.out)[oi] = (uint16_t)f32_to_bf16_bits(res);
-    else
-      reinterpret_cast<float*>(P.out)[oi] = res;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) part[wave][lane * CPL + c] = o[c];
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int ch = lane * CPL + c;
+      const float s = (part[0][ch] + part[1][ch]) + (part[2][ch] + part[3][ch]);
+      const float res = nch > 0 ? s / lsum : 0.f;
+      const uint64_t oi = ((uint64_t)seq * P.hq + qh) * D + ch;
+      if constexpr (BF16)
+        reinterpret_cast<uint16_t*>(P.out)[oi] = (uint16_t)f32_to_bf16_bits(res);
+      else
+        reinterpret_cast<float*>(P.out)[oi] = res;
+    }
   }
 }
 
@@ -495,10 +522,10 @@ template <int D, bool BF16>
 static hipError_t launch_merge_d(const DecodeParams& P, hipStream_t s) {
   const dim3 grid((unsigned)P.batch * P.hq);
   switch (P.hq / P.hkv) {
-    case 1: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 1>), grid, dim3(512), 0, s, P); break;
-    case 2: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 2>), grid, dim3(512), 0, s, P); break;
-    case 4: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 4>), grid, dim3(512), 0, s, P); break;
-    default: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 8>), grid, dim3(512), 0, s, P); break;
+    case 1: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 1>), grid, dim3(256), 0, s, P); break;
+    case 2: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 2>), grid, dim3(256), 0, s, P); break;
+    case 4: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 4>), grid, dim3(256), 0, s, P); break;
+    default: hipLaunchKernelGGL((decode_merge_kernel<D, BF16, 8>), grid, dim3(256), 0, s, P); break;
   }
   return hipGetLastError();
 }
