@@ -124,6 +124,8 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
  *   n_probe    P >= 1 probe rows per query head
  *   errors_out device float [L/2][Hkv][2]
  *   ws         device workspace of >= fdkv_probe_workspace() bytes
+ * T * d * elem_bytes and P * G * d * elem_bytes must stay below 2^31
+ * (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets).
  */
 fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                        const void* const* qp_layers, int32_t n_probe, float* errors_out,

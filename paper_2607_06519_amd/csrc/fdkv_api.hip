@@ -186,6 +186,11 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 1 || n_probe < 1 || !k_layers || !qp_layers) return FDKV_E_INVALID_ARG;
+  // key planes and each head's probe rows are addressed with 32-bit offsets
+  const uint64_t row_bytes = (uint64_t)dims->head_dim * elem_bytes(dims);
+  if ((uint64_t)seq_len * row_bytes >= (1ull << 31) ||
+      (uint64_t)n_probe * (dims->n_q_heads / dims->n_kv_heads) * row_bytes >= (1ull << 31))
+    return FDKV_E_UNSUPPORTED;
   if (!aligned(errors_out, 4) || !aligned(ws, 256)) return FDKV_E_INVALID_ARG;
   for (int l = 0; l < dims->n_layers; ++l)
     if (!aligned(k_layers[l], 16) || !aligned(qp_layers[l], 16)) return FDKV_E_INVALID_ARG;

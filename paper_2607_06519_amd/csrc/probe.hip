@@ -15,11 +15,13 @@
 // mode (16x less at G = 4, P = 256, d = 128).
 //
 // Kernels: residual_select (compress.hip) writes every unit's K top-k channel
-// indices; probe_qgram forms S_u in fp32; probe_dgram streams the key pairs,
-// stages bf16(D) and bf16(Dbar) transposed in LDS and accumulates the upper
-// triangle of both Gram matrices with v_mfma_f32_32x32x16_bf16 (one wave
-// per matrix), then contracts them with S_u in its epilogue; probe_finalize
-// sums the per-workgroup partials in a fixed order in fp64.
+// indices; probe_qgram forms S_u (MFMA Gram of the probe rows for bf16
+// queries, fp32 VALU for fp32 ones); probe_dgram streams the key pairs and
+// stages bf16(D) and bf16(Dbar) row-major in LDS; both Gram kernels take
+// their v_mfma_f32_32x32x16_bf16 operands with transposing LDS reads
+// (ds_read_b64_tr_b16) and accumulate the upper-triangular 32x32 blocks.
+// probe_dgram contracts its Gram matrices with S_u in the epilogue and
+// probe_finalize sums the per-workgroup partials in a fixed order in fp64.
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 
@@ -27,6 +29,59 @@ namespace fdkv {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
+typedef i16x4_t __attribute__((address_space(3))) lds_i16x4_t;
+
+namespace {
+
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
+constexpr uint32_t kOobOff = 0x80000000u;  // past every input plane: buffer loads read 0
+constexpr int kGramRows = 64;             // rows staged in LDS per step of the Gram kernels
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
+  const uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, kRsrcWord3);
+}
+
+__device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// Upper-triangular 32x32 blocks (I <= J) of a D x D Gram matrix, in order.
+template <int NB>
+struct TriTiles {
+  int i[NB * (NB + 1) / 2], j[NB * (NB + 1) / 2];
+  constexpr TriTiles() : i(), j() {
+    int t = 0;
+    for (int a = 0; a < NB; ++a)
+      for (int b = a; b < NB; ++b) {
+        i[t] = a;
+        j[t] = b;
+        ++t;
+      }
+  }
+};
+
+// Operand of v_mfma_f32_32x32x16_bf16 for channel block I and rows
+// 16kk .. 16kk+15 of a row-major bf16 tile with LDR elements per row: lane l
+// gets channel 32I + l%32 of rows 16kk + 8(l/32) .. +7, from two transposing
+// reads.  In each 16-lane group, lane i of ds_read_b64_tr_b16 returns element
+// i%4 of the 4-element row addressed by lane 4j + i/4 as its element j; the
+// lanes therefore address rows base + i/4 at channels 32I + 16g + 4(i%4).
+template <int LDR>
+__device__ __forceinline__ bf16x8_t gram_operand(const uint16_t* tile, int kk, int I, int lane) {
+  const int h = lane >> 5, g = (lane >> 4) & 1, li = lane & 15;
+  const int row = 16 * kk + 8 * h + (li >> 2);
+  const int col = 32 * I + 16 * g + 4 * (li & 3);
+  const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(tile + row * LDR + col));
+  const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(tile + (row + 4) * LDR + col));
+  const i16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+}  // namespace
 
 template <int D, bool BF16>
 __device__ __forceinline__ float load_q(const void* base, uint64_t i) {
@@ -86,114 +141,208 @@ __global__ __launch_bounds__(256) void probe_qgram_kernel(ProbeParams P) {
     for (int j = 0; j < BS; ++j) S[(bi + i) * D + bj + j] = acc[i][j];
 }
 
+// S_u as the MFMA Gram matrix of the unit's 2GP bf16 probe rows (exact
+// products, fp32 sums), upper-triangular 32x32 blocks only (the only ones
+// probe_dgram reads).  One workgroup per unit; 64 rows per step, the next
+// step's loads in flight during the current step's MFMAs; the four waves
+// split the blocks.
+template <int D>
+__global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
+  constexpr int NPc = D / 8;                     // 16-byte pieces per row
+  constexpr int NB = D / 32, NT = NB * (NB + 1) / 2;
+  constexpr int TPW = (NT + 3) / 4;              // blocks per wave
+  constexpr int R = kGramRows, LDR = D + 16;     // rows per step, LDS row stride (elements)
+  constexpr int LPT = R * NPc / 256;             // loads per thread per step
+  constexpr TriTiles<NB> tri{};
+  __shared__ __attribute__((aligned(16))) uint16_t tile[R * LDR];
+  const int unit = blockIdx.x;
+  const int pair = unit / P.hkv, head = unit % P.hkv;
+  const int G = P.hq / P.hkv, NP = P.n_probe;
+  const int NR = 2 * G * NP;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const uint32_t RB = D * 2;
+  const uint64_t span = (uint64_t)G * NP * RB;   // bytes of one layer's probe rows for this head
+  const auto q0 = make_rsrc(static_cast<const uint8_t*>(P.qp[2 * pair]) + (uint64_t)head * span, span);
+  const auto q1 = make_rsrc(static_cast<const uint8_t*>(P.qp[2 * pair + 1]) + (uint64_t)head * span, span);
+  f32x16_t acc[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  uint4 buf[LPT];
+  auto load = [&](int r0) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 256 * j, r = r0 + i / NPc, pc = i % NPc;
+      const int ls = r >= G * NP, rl = r - (ls ? G * NP : 0);  // row within its layer's block
+      const uint32_t off = r < NR ? (uint32_t)rl * RB + pc * 16 : kOobOff;
+      buf[j] = ls ? load16(q1, off) : load16(q0, off);
+    }
+  };
+  load(0);
+  for (int r0 = 0; r0 < NR; r0 += R) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 256 * j;
+      *reinterpret_cast<uint4*>(&tile[(i / NPc) * LDR + (i % NPc) * 8]) = buf[j];
+    }
+    load(r0 + R);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < R / 16; ++kk) {
+      bf16x8_t op[NB];
+#pragma unroll
+      for (int I = 0; I < NB; ++I) op[I] = gram_operand<LDR>(tile, kk, I, lane);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)  // block t belongs to wave t / TPW (indices stay compile-time)
+        if (t / TPW == wave) acc[t % TPW] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[tri.i[t]], op[tri.j[t]], acc[t % TPW], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  float* S = P.gram_q + (uint64_t)unit * D * D;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t / TPW != wave) continue;
+    const int col = 32 * tri.j[t] + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 32 * tri.i[t] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      S[row * D + col] = acc[t % TPW][r];
+    }
+  }
+}
+
+// Gram matrices of bf16(D) and bf16(Dbar) over one chunk of kProbeChunk
+// tokens of a unit, contracted with S_u.  64 tokens per step: each thread
+// turns its 16-byte pieces of the two layers into bf16 half differences,
+// zeroes the channels that are among its token's top-k (for Dbar), and
+// writes both rows to LDS; waves 0-1 accumulate the blocks of D, waves 2-3
+// those of Dbar.  The next step's loads are in flight during the MFMAs.
 template <int D, bool BF16>
-__global__ __launch_bounds__(128) void probe_dgram_kernel(ProbeParams P) {
+__global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   constexpr int E = BF16 ? 2 : 4;
-  constexpr int NP = D * E / 16;     // input pieces per row
-  constexpr int CPP = 16 / E;        // channels per piece
-  constexpr int NB = D / 32;         // 32-channel blocks
-  constexpr int NT = NB * (NB + 1) / 2;
-  constexpr int TS = kProbeStep;
-  constexpr int LDT = TS + 8;        // LDS row stride in bf16 elements
-  __shared__ __attribute__((aligned(16))) uint16_t dt[2][D][LDT];  // [shared/residual][channel][token]
+  constexpr int NPc = D * E / 16;                // 16-byte input pieces per row
+  constexpr int CPP = 16 / E;                    // channels per piece
+  constexpr int NB = D / 32, NT = NB * (NB + 1) / 2;
+  constexpr int TPW = (NT + 1) / 2;              // blocks per wave (two waves per matrix)
+  constexpr int R = kGramRows, LDR = D + 16;
+  constexpr int LPT = R * NPc / 256;             // loads per thread per layer per step
+  constexpr TriTiles<NB> tri{};
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][R * LDR];  // [D, Dbar][token][channel]
+  __shared__ float red[4];
 
   const int unit = blockIdx.y, chunk = blockIdx.x;
   const int pair = unit / P.hkv, head = unit % P.hkv;
   const int T = P.seq_len, k = P.topk;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const uint64_t RB = (uint64_t)D * E;
-  const uint8_t* ka = static_cast<const uint8_t*>(P.k[2 * pair]) + (uint64_t)head * T * RB;
-  const uint8_t* kb = static_cast<const uint8_t*>(P.k[2 * pair + 1]) + (uint64_t)head * T * RB;
+  const uint64_t plane = (uint64_t)T * RB;
+  const auto ka = make_rsrc(static_cast<const uint8_t*>(P.k[2 * pair]) + (uint64_t)head * plane, plane);
+  const auto kb = make_rsrc(static_cast<const uint8_t*>(P.k[2 * pair + 1]) + (uint64_t)head * plane, plane);
   const uint8_t* idx = P.idx + (uint64_t)unit * plane_bytes((uint64_t)T * k);
   const int t_begin = chunk * kProbeChunk;
   const int t_end = min(T, t_begin + kProbeChunk);
+  const int mat = wave >> 1;                      // 0: D, 1: Dbar
 
-  f32x16_t acc[NT];
+  f32x16_t acc[TPW];
 #pragma unroll
-  for (int i = 0; i < NT; ++i)
+  for (int i = 0; i < TPW; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
-
-  for (int t0 = t_begin; t0 < t_end; t0 += TS) {
-    // bf16(D) of TS tokens into both planes, transposed to [channel][token]
-    const int piece = tid % NP;
-    for (int r = tid / NP; r < TS; r += 128 / NP) {
-      const int t = t0 + r;
+  // k = 16: a token's indices are one 16-byte load, issued with its keys
+  const bool k16 = k == 16;
+  const auto ir = make_rsrc(idx, k16 ? (uint64_t)T * 16 : 0);
+  uint4 ra[LPT], rb[LPT], ri[LPT];
+  auto load = [&](int t0) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 256 * j, t = t0 + i / NPc, pc = i % NPc;
+      const bool ok = t < t_end;
+      ra[j] = load16(ka, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
+      rb[j] = load16(kb, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
+      ri[j] = load16(ir, ok ? (uint32_t)t * 16 : kOobOff);  // reads 0 unless k = 16
+    }
+  };
+  load(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += R) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 256 * j, row = i / NPc, pc = i % NPc, t = t0 + row;
+      const uint32_t* pa = reinterpret_cast<const uint32_t*>(&ra[j]);
+      const uint32_t* pb = reinterpret_cast<const uint32_t*>(&rb[j]);
       uint16_t h[CPP];
-      if (t < t_end) {
-        const uint64_t off = (uint64_t)t * RB + piece * 16;
-        const uint4 a = *reinterpret_cast<const uint4*>(ka + off);
-        const uint4 b = *reinterpret_cast<const uint4*>(kb + off);
-        const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
-        const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          if constexpr (BF16) {
-            h[2 * w] = (uint16_t)f32_to_bf16_bits((bf16_lo(pa[w]) - bf16_lo(pb[w])) * 0.5f);
-            h[2 * w + 1] = (uint16_t)f32_to_bf16_bits((bf16_hi(pa[w]) - bf16_hi(pb[w])) * 0.5f);
-          } else {
-            h[w] = (uint16_t)f32_to_bf16_bits((as_f32(pa[w]) - as_f32(pb[w])) * 0.5f);
-          }
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (BF16) {
+          h[2 * w] = (uint16_t)f32_to_bf16_bits((bf16_lo(pa[w]) - bf16_lo(pb[w])) * 0.5f);
+          h[2 * w + 1] = (uint16_t)f32_to_bf16_bits((bf16_hi(pa[w]) - bf16_hi(pb[w])) * 0.5f);
+        } else {
+          h[w] = (uint16_t)f32_to_bf16_bits((as_f32(pa[w]) - as_f32(pb[w])) * 0.5f);
         }
+      }
+      uint32_t wd[CPP / 2], wr[CPP / 2];
+#pragma unroll
+      for (int c = 0; c < CPP / 2; ++c) wd[c] = (uint32_t)h[2 * c] | ((uint32_t)h[2 * c + 1] << 16);
+      // Dbar: drop the channels of this piece that are among the token's top-k
+      uint32_t keep = (1u << CPP) - 1;
+      if (k16) {
+        const uint32_t* iw = reinterpret_cast<const uint32_t*>(&ri[j]);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const uint32_t c = ((iw[e >> 2] >> (8 * (e & 3))) & 0xFFu) - (uint32_t)(pc * CPP);
+          keep &= c < (uint32_t)CPP ? ~(1u << c) : ~0u;
+        }
+      } else if (t < t_end) {
+        for (int e = 0; e < k; ++e) {
+          const int c = idx[(uint64_t)t * k + e] - pc * CPP;
+          if (c >= 0 && c < CPP) keep &= ~(1u << c);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CPP / 2; ++c)
+        wr[c] = (((keep >> (2 * c)) & 1) ? (wd[c] & 0xFFFFu) : 0u) | (((keep >> (2 * c + 1)) & 1) ? (wd[c] & 0xFFFF0000u) : 0u);
+      uint16_t* d0 = &tile[0][row * LDR + pc * CPP];
+      uint16_t* d1 = &tile[1][row * LDR + pc * CPP];
+      if constexpr (CPP == 8) {
+        *reinterpret_cast<uint4*>(d0) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        *reinterpret_cast<uint4*>(d1) = make_uint4(wr[0], wr[1], wr[2], wr[3]);
       } else {
-#pragma unroll
-        for (int c = 0; c < CPP; ++c) h[c] = 0;
-      }
-#pragma unroll
-      for (int c = 0; c < CPP; ++c) {
-        dt[0][piece * CPP + c][r] = h[c];
-        dt[1][piece * CPP + c][r] = h[c];
+        *reinterpret_cast<uint2*>(d0) = make_uint2(wd[0], wd[1]);
+        *reinterpret_cast<uint2*>(d1) = make_uint2(wr[0], wr[1]);
       }
     }
+    load(t0 + R);
     __syncthreads();
-    // residual plane: zero each token's top-k channels
-    if (tid < TS) {
-      const int t = t0 + tid;
-      if (t < t_end)
-        for (int j = 0; j < k; ++j) {
-          const int c = idx[(uint64_t)t * k + j];
-          if (c < D) dt[1][c][tid] = 0;
-        }
-    }
-    __syncthreads();
-    // C += Dt Dt^T on the upper-triangular 32x32 tiles, wave w on plane w
 #pragma unroll
-    for (int kk = 0; kk < TS / 16; ++kk) {
-      bf16x8_t blk[NB];
+    for (int kk = 0; kk < R / 16; ++kk) {
+      bf16x8_t op[NB];
 #pragma unroll
-      for (int I = 0; I < NB; ++I)
-        blk[I] = *reinterpret_cast<const bf16x8_t*>(&dt[wave][32 * I + (lane & 31)][16 * kk + 8 * (lane >> 5)]);
-      int ti = 0;
+      for (int I = 0; I < NB; ++I) op[I] = gram_operand<LDR>(tile[mat], kk, I, lane);
 #pragma unroll
-      for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int J = I; J < NB; ++J) {
-          acc[ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(blk[I], blk[J], acc[ti], 0, 0, 0);
-          ++ti;
-        }
+      for (int t = 0; t < NT; ++t)  // block t belongs to wave t / TPW of the pair (indices stay compile-time)
+        if (t / TPW == (wave & 1)) acc[t % TPW] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[tri.i[t]], op[tri.j[t]], acc[t % TPW], 0, 0, 0);
     }
     __syncthreads();
   }
 
-  // < C, S_u >, off-diagonal tiles counted twice (both matrices symmetric)
+  // < C, S_u >, off-diagonal blocks counted twice (both matrices symmetric)
   const float* S = P.gram_q + (uint64_t)unit * D * D;
   float part = 0.f;
-  int ti = 0;
 #pragma unroll
-  for (int I = 0; I < NB; ++I)
+  for (int t = 0; t < NT; ++t) {
+    if (t / TPW != (wave & 1)) continue;
+    const float wgt = (tri.i[t] == tri.j[t]) ? 1.f : 2.f;
+    const int col = 32 * tri.j[t] + (lane & 31);
 #pragma unroll
-    for (int J = I; J < NB; ++J) {
-      const float wgt = (I == J) ? 1.f : 2.f;
-      const int col = 32 * J + (lane & 31);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        part = fmaf(wgt * acc[ti][r], S[row * D + col], part);
-      }
-      ++ti;
+    for (int r = 0; r < 16; ++r) {
+      const int row = 32 * tri.i[t] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      part = fmaf(wgt * acc[t % TPW][r], S[row * D + col], part);
     }
+  }
   part = wave_sum(part);
-  if (lane == 0) P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + wave] = part;
+  if (lane == 0) red[wave] = part;
+  __syncthreads();
+  if (tid < 2) P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + tid] = red[2 * tid] + red[2 * tid + 1];
 }
 
 __global__ void probe_finalize_kernel(ProbeParams P) {
@@ -210,10 +359,13 @@ __global__ void probe_finalize_kernel(ProbeParams P) {
 template <int D, bool BF16>
 static hipError_t launch_probe_t(const ProbeParams& P, hipStream_t s) {
   const int units = P.n_pairs * P.hkv;
-  hipLaunchKernelGGL((probe_qgram_kernel<D, BF16>), dim3(units), dim3(256), 0, s, P);
+  if constexpr (BF16)
+    hipLaunchKernelGGL((probe_qgram_mfma_kernel<D>), dim3(units), dim3(256), 0, s, P);
+  else
+    hipLaunchKernelGGL((probe_qgram_kernel<D, BF16>), dim3(units), dim3(256), 0, s, P);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), dim3(P.n_chunks, units), dim3(128), 0, s, P);
+  hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), dim3(P.n_chunks, units), dim3(256), 0, s, P);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(probe_finalize_kernel, dim3((units * 2 + 255) / 256), dim3(256), 0, s, P);

@@ -132,4 +132,5 @@ def test_validation_errors_before_any_device_call(lib):
     assert lib.fdkv_probe_workspace(ctypes.byref(good), 100, 4, ctypes.byref(n)) == 0 and n.value > 0
     assert lib.fdkv_probe(ctypes.byref(good), 100, ptrs, ptrs, 4, fake, fake, n.value - 1, None) == -3
     assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, fake, n.value, None) == -1
+    assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, fake, 1 << 40, None) == -2
     assert lib.fdkv_layout(None, 1, None, None, None, None) == -1
