@@ -61,8 +61,13 @@ def parse():
     return ap.parse_args()
 
 
-def bytes_per_token(mode, d, k, e):
-    return 2 * d * e if mode != 1 else 2 * d * e + 2 * k * (1 + e)
+def bytes_per_token(mode, d, k, e, c):
+    """Algorithmic bytes one decode layer reads per token of a head: the two
+    dense planes (shared coefficients of c bytes, or exact K/V of e bytes)
+    plus, for residual heads, k (index, value) pairs for K and for V."""
+    if mode == 2:
+        return 2 * d * e
+    return 2 * d * c if mode == 0 else 2 * d * c + 2 * k * (1 + c)
 
 
 def kernel_source_hash():
@@ -210,7 +215,7 @@ def main():
     bytes_layer = []
     for layer in range(L):
         b = layer // 2
-        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e)
+        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e, w.coef_bytes)
                                for s in range(w.batch) for h in range(H)))
     bytes_step = sum(bytes_layer)
 

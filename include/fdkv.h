@@ -61,7 +61,14 @@ typedef enum {
 /* Head modes, in increasing memory cost; ties in routing go to the lower value. */
 typedef enum { FDKV_SHARED = 0, FDKV_RESIDUAL = 1, FDKV_EXACT = 2 } fdkv_mode;
 
-typedef enum { FDKV_F32 = 0, FDKV_BF16 = 1 } fdkv_dtype;
+/*
+ * Cache types.  FDKV_F32 / FDKV_BF16: inputs, queries, outputs and every cache
+ * plane in that type.  FDKV_BF16_E4M3: bf16 inputs, queries, outputs and exact
+ * heads, with the shared planes and residual values of shared / residual heads
+ * stored as OCP FP8 E4M3 (the quantised coefficients Section 3 allows), each
+ * rounded once to nearest-even from its fp32 value and saturated at +-448.
+ */
+typedef enum { FDKV_F32 = 0, FDKV_BF16 = 1, FDKV_BF16_E4M3 = 2 } fdkv_dtype;
 
 typedef struct {
   int32_t n_layers;   /* L, even, 2..256 */

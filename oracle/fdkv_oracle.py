@@ -41,7 +41,12 @@ Readings of the paper adopted here (the paper leaves these open):
   mode; ties in the argmin go to the cheaper mode;
 * the budget rule takes the smallest ``lambda`` among 0, the per-head
   breakpoints and +inf whose footprint fits the budget;
-* decode scales logits by ``1/sqrt(d)`` and attends over the cached tokens.
+* decode scales logits by ``1/sqrt(d)`` and attends over the cached tokens;
+* cache type ``bf16_e4m3`` (the quantised-coefficient variant the paper
+  allows at the end of Section 3): inputs, queries and exact heads are bf16;
+  the shared and residual coefficients (``M`` and the residual values) are
+  stored in OCP FP8 E4M3, rounded once, to nearest with ties to even, from
+  the unrounded coefficient, saturating at +-448; no scale factor.
 
 Parity status: every function here is pinned by tests against closed forms,
 textbook routines, brute force and a hand-worked example, except that no
@@ -59,8 +64,22 @@ SHARED, RESIDUAL, EXACT = 0, 1, 2
 MODES = (SHARED, RESIDUAL, EXACT)
 PLANE_ALIGN = 256
 
-_ELEM_BYTES = {"f32": 4, "bf16": 2, "f64": 8}
 _BF16_MAX = (2.0 - 2.0 ** -7) * 2.0 ** 127
+_E4M3_MAX = 448.0
+# cache types: bytes and rounding of the input (exact-head) planes and of the coefficient planes
+_INPUT_TYPE = {"f32": "f32", "bf16": "bf16", "bf16_e4m3": "bf16"}
+_COEF_TYPE = {"f32": "f32", "bf16": "bf16", "bf16_e4m3": "e4m3"}
+_TYPE_BYTES = {"f32": 4, "bf16": 2, "e4m3": 1, "f64": 8}
+
+
+def input_bytes(dtype: str) -> int:
+    """Bytes per element of the inputs and of exact-head planes."""
+    return _TYPE_BYTES[_INPUT_TYPE.get(dtype, dtype)]
+
+
+def coef_bytes(dtype: str) -> int:
+    """Bytes per element of the stored shared / residual coefficients."""
+    return _TYPE_BYTES[_COEF_TYPE.get(dtype, dtype)]
 
 
 # ----------------------------------------------------------------------------
@@ -75,6 +94,20 @@ def round_bf16(x) -> np.ndarray:
     return np.where(np.abs(y) > _BF16_MAX, np.copysign(np.inf, x), y)
 
 
+def round_e4m3(x) -> np.ndarray:
+    """Nearest OCP FP8 E4M3 value (round half to even), saturating at +-448.
+
+    E4M3 has 4 significant bits for normal values (|x| >= 2**-6) and a
+    subnormal quantum of 2**-9; 480 and above have no finite encoding, so the
+    largest finite value 448 absorbs everything beyond it.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)                       # |x| = m * 2**e with m in [0.5, 1)
+    q = np.maximum(e - 4, -9)                # 4 significant bits; subnormal quantum 2**-9
+    y = np.ldexp(np.round(np.ldexp(x, -q)), q)
+    return np.where(np.abs(y) > _E4M3_MAX, np.copysign(_E4M3_MAX, x), y)
+
+
 def round_to_storage(x, dtype: str) -> np.ndarray:
     x = np.asarray(x, dtype=np.float64)
     if dtype == "f64":
@@ -83,7 +116,19 @@ def round_to_storage(x, dtype: str) -> np.ndarray:
         return x.astype(np.float32).astype(np.float64)
     if dtype == "bf16":
         return round_bf16(x)
+    if dtype == "e4m3":
+        return round_e4m3(x)
     raise ValueError(dtype)
+
+
+def round_input(x, dtype: str) -> np.ndarray:
+    """Rounding of the inputs / exact-head planes of a cache type."""
+    return round_to_storage(x, _INPUT_TYPE.get(dtype, dtype))
+
+
+def round_coef(x, dtype: str) -> np.ndarray:
+    """Rounding of the stored shared / residual coefficients of a cache type."""
+    return round_to_storage(x, _COEF_TYPE.get(dtype, dtype))
 
 
 # ----------------------------------------------------------------------------
@@ -247,17 +292,17 @@ def compress_unit(K2, V2, mode: int, k: int, dtype: str) -> Dict[str, np.ndarray
     if mode == EXACT:
         for name, X in (("K", K2), ("V", V2)):
             X = np.asarray(X, dtype=np.float64)
-            out[name + "0"] = round_to_storage(X[0], dtype)
-            out[name + "1"] = round_to_storage(X[1], dtype)
+            out[name + "0"] = round_input(X[0], dtype)
+            out[name + "1"] = round_input(X[1], dtype)
         return out
     for name, X in (("K", K2), ("V", V2)):
         X = np.asarray(X, dtype=np.float64)
-        out["M" + name] = round_to_storage(coefficient_image(X, 0, 0), dtype)
+        out["M" + name] = round_coef(coefficient_image(X, 0, 0), dtype)
         if mode == RESIDUAL:
             idx = residual_channels(X[0], X[1], k)
             D = coefficient_image(X, 1, 0)
             out["I" + name] = idx
-            out["V" + name] = round_to_storage(np.take_along_axis(D, idx, axis=-1), dtype)
+            out["V" + name] = round_coef(np.take_along_axis(D, idx, axis=-1), dtype)
     return out
 
 
@@ -345,11 +390,11 @@ def routing_errors(K2, Q2, k: int) -> np.ndarray:
 # memory cost, layout bytes and routing
 # ----------------------------------------------------------------------------
 def bytes_per_token(mode: int, d: int, k: int, dtype: str) -> int:
-    e = _ELEM_BYTES[dtype]
+    e, c = input_bytes(dtype), coef_bytes(dtype)
     if mode == SHARED:
-        return 2 * d * e
+        return 2 * d * c
     if mode == RESIDUAL:
-        return 2 * d * e + 2 * k * (1 + e)
+        return 2 * d * c + 2 * k * (1 + c)
     if mode == EXACT:
         return 4 * d * e
     raise ValueError(mode)
@@ -367,14 +412,14 @@ def _plane(nbytes: int) -> int:
 
 def unit_bytes(mode: int, T: int, d: int, k: int, dtype: str) -> int:
     """Bytes of one (sequence, pair, KV head) segment; every plane padded to 256 B."""
-    e = _ELEM_BYTES[dtype]
-    dense = _plane(T * d * e)
+    e, c = input_bytes(dtype), coef_bytes(dtype)
+    coef = _plane(T * d * c)
     if mode == SHARED:
-        return 2 * dense
+        return 2 * coef
     if mode == RESIDUAL:
-        return 2 * dense + 2 * (_plane(T * k) + _plane(T * k * e))
+        return 2 * coef + 2 * (_plane(T * k) + _plane(T * k * c))
     if mode == EXACT:
-        return 4 * dense
+        return 4 * _plane(T * d * e)
     raise ValueError(mode)
 
 

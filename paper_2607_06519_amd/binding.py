@@ -17,7 +17,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfdkv.so
 _lib = None
 
 SHARED, RESIDUAL, EXACT = 0, 1, 2
-F32, BF16 = 0, 1
+F32, BF16, BF16_E4M3 = 0, 1, 2   # cache types (fdkv_dtype)
 
 STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: "FDKV_E_WORKSPACE",
           -4: "FDKV_E_BUDGET", -5: "FDKV_E_HIP"}
@@ -42,7 +42,7 @@ class Dims(ctypes.Structure):
 
 
 def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype) -> Dims:
-    dt = {"f32": F32, "bf16": BF16}.get(dtype, dtype)
+    dt = {"f32": F32, "bf16": BF16, "bf16_e4m3": BF16_E4M3}.get(dtype, dtype)
     return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt)
 
 

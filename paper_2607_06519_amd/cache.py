@@ -22,7 +22,8 @@ def _torch():
 
 def torch_dtype(dtype: str):
     torch = _torch()
-    return {"bf16": torch.bfloat16, "f32": torch.float32}[dtype]
+    # inputs, queries and outputs: FP8-coefficient caches take bf16 tensors
+    return {"bf16": torch.bfloat16, "bf16_e4m3": torch.bfloat16, "f32": torch.float32}[dtype]
 
 
 def to_device(x: np.ndarray, dtype: str, device="cuda"):

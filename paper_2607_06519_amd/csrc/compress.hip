@@ -12,6 +12,7 @@
 //    probe (K indices only, into its workspace).
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
+#include "fp8.h"
 #include "topk_net.h"
 
 namespace fdkv {
@@ -36,6 +37,20 @@ __device__ __forceinline__ uint4 pair_mean(uint4 a, uint4 b) {
   return r;
 }
 
+// 16 bytes of bf16 inputs (8 channels) -> 8 bytes of FP8 E4M3 pair means.
+__device__ __forceinline__ uint2 pair_mean_e4m3(uint4 a, uint4 b) {
+  const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
+  const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
+  uint32_t w[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = f32_to_e4m3((bf16_lo(pa[i]) + bf16_lo(pb[i])) * 0.5f);
+    const uint32_t hi = f32_to_e4m3((bf16_hi(pa[i]) + bf16_hi(pb[i])) * 0.5f);
+    w[i >> 1] |= (lo | (hi << 8)) << (16 * (i & 1));
+  }
+  return make_uint2(w[0], w[1]);
+}
+
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   constexpr int E = BF16 ? 2 : 4;
@@ -52,7 +67,8 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   const uint8_t* v0 = static_cast<const uint8_t*>(P.v[2 * pair]) + head_off;
   const uint8_t* v1 = static_cast<const uint8_t*>(P.v[2 * pair + 1]) + head_off;
   uint8_t* seg = P.cache + P.seg_off[unit];
-  const SegLayout L = seg_layout(mode, T, D, P.topk, E);
+  const bool c8 = BF16 && P.coef8;      // shared planes in FP8 E4M3: 8 bytes per 16-byte input piece
+  const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E);
   const int piece = threadIdx.x % NP;
   const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
 #pragma unroll 2
@@ -69,6 +85,10 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
       *reinterpret_cast<uint4*>(seg + L.k1 + off) = kb;
       *reinterpret_cast<uint4*>(seg + L.v0 + off) = va;
       *reinterpret_cast<uint4*>(seg + L.v1 + off) = vb;
+    } else if (c8) {
+      const uint64_t o8 = (uint64_t)t * D + piece * 8;
+      *reinterpret_cast<uint2*>(seg + L.mk + o8) = pair_mean_e4m3(ka, kb);
+      *reinterpret_cast<uint2*>(seg + L.mv + o8) = pair_mean_e4m3(va, vb);
     } else {
       *reinterpret_cast<uint4*>(seg + L.mk + off) = pair_mean<BF16>(ka, kb);
       *reinterpret_cast<uint4*>(seg + L.mv + off) = pair_mean<BF16>(va, vb);
@@ -166,9 +186,11 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   // 3. ascending channels, half differences, packed stores
   uint8_t* out_idx;
   uint8_t* out_val;
+  const bool c8 = BF16 && P.coef8;      // residual values in FP8 E4M3
+  const int CE = c8 ? 1 : E;            // bytes per stored value
   if (P.modes) {
     uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E);
+    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE);
     out_idx = seg + (tensor ? L.iv : L.ik);
     out_val = seg + (tensor ? L.vv : L.vk);
   } else {
@@ -176,7 +198,7 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
     out_val = nullptr;
   }
   out_idx += (uint64_t)t * k;
-  if (out_val) out_val += (uint64_t)t * k * E;
+  if (out_val) out_val += (uint64_t)t * k * CE;
   const float* drow = reinterpret_cast<const float*>(diff);
   if ((k & 3) == 0 && k <= GS) {
     uint32_t iw[GS / 4];
@@ -189,8 +211,13 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
         if (s % 4 == 0) iw[s / 4] = 0;
         iw[s / 4] |= (uint32_t)c << (8 * (s % 4));
         if constexpr (BF16) {
-          if (s % 2 == 0) vw[s / 2] = 0;
-          vw[s / 2] |= f32_to_bf16_bits(dv) << (16 * (s % 2));
+          if (c8) {
+            if (s % 4 == 0) vw[s / 4] = 0;
+            vw[s / 4] |= (uint32_t)f32_to_e4m3(dv) << (8 * (s % 4));
+          } else {
+            if (s % 2 == 0) vw[s / 2] = 0;
+            vw[s / 2] |= f32_to_bf16_bits(dv) << (16 * (s % 2));
+          }
         } else {
           vw[s] = as_u32(dv);
         }
@@ -204,7 +231,7 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
       uint32_t* ov = reinterpret_cast<uint32_t*>(out_val);
 #pragma unroll
       for (int w = 0; w < GS * E / 4; ++w)
-        if (w < k * E / 4) ov[w] = vw[w];
+        if (w < k * CE / 4) ov[w] = vw[w];
     }
   } else {
     for (int s = 0; s < k; ++s) {
@@ -212,7 +239,9 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
       out_idx[s] = (uint8_t)c;
       if (out_val) {
         const float dv = drow[diff_slot<D>(lane, c >> 2) * 4 + (c & 3)] * 0.5f;
-        if constexpr (BF16)
+        if (c8)
+          out_val[s] = f32_to_e4m3(dv);
+        else if constexpr (BF16)
           reinterpret_cast<uint16_t*>(out_val)[s] = (uint16_t)f32_to_bf16_bits(dv);
         else
           reinterpret_cast<float*>(out_val)[s] = dv;

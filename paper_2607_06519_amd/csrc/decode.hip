@@ -84,7 +84,7 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
   const uint8_t* seg = P.cache + P.seg_off[unit];
-  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E);
+  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E);
   const uint8_t* kplane = seg + (mode == kExact ? (parity ? L.k1 : L.k0) : L.mk);
   const uint8_t* vplane = seg + (mode == kExact ? (parity ? L.v1 : L.v0) : L.mv);
   const uint8_t* ikp = seg + L.ik;

@@ -57,6 +57,22 @@ __device__ __forceinline__ uint32_t word(const uint4& v, int w) {
   return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
 }
 
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+
+// Two FP8 E4M3 codes (bytes 0-1 or 2-3 of w) as a bf16 pair; exact, since
+// every E4M3 value is a bf16 value.
+template <bool HI>
+__device__ __forceinline__ uint32_t e4m3x2_bf16(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
+// A piece of 8 FP8 channels (raw in .x, .y) as the 8 bf16 channels of a
+// bf16 piece.
+__device__ __forceinline__ uint4 widen_e4m3(const uint4& raw) {
+  return make_uint4(e4m3x2_bf16<false>(raw.x), e4m3x2_bf16<true>(raw.x), e4m3x2_bf16<false>(raw.y),
+                    e4m3x2_bf16<true>(raw.y));
+}
+
 template <int D, int G>
 struct SS {
   static constexpr int NP = D / 8;                 // lanes per row, one 16-byte piece each
@@ -83,7 +99,7 @@ struct TileBuf {
 
 }  // namespace
 
-template <int D, int G>
+template <int D, int G, bool C8K>
 __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   using S = SS<D, G>;
   constexpr int NP = S::NP, RPL = S::RPL, TILE = S::TILE, NL = S::NL, CW = S::CW, W = S::W;
@@ -115,15 +131,19 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const float sigma = parity ? -1.f : 1.f;
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
+  // FP8 caches: the shared planes and residual values of shared / residual
+  // heads are E4M3 (one byte per channel); exact heads stay bf16
+  const bool c8 = C8K && mode != kExact;
+  const int ce = c8 ? 1 : 2;
   const uint8_t* seg = P.cache + seg_off;
-  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2);
-  const uint64_t dense = (uint64_t)T * RB;
+  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce);
+  const uint64_t dense = (uint64_t)T * D * ce;
   const auto kr = rsrc(seg + (mode == kExact ? (parity ? L.k1 : L.k0) : L.mk), dense);
   const auto vr = rsrc(seg + (mode == kExact ? (parity ? L.v1 : L.v0) : L.mv), dense);
   const auto ikr = rsrc(seg + L.ik, (uint64_t)T * k);
-  const auto vkr = rsrc(seg + L.vk, (uint64_t)T * k * 2);
+  const auto vkr = rsrc(seg + L.vk, (uint64_t)T * k * ce);
   const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k);
-  const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * 2);
+  const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * ce);
   const uint8_t* qbase = static_cast<const uint8_t*>(P.q) + ((uint64_t)seq * P.hq + (uint64_t)head * G) * RB;
   const auto qr = rsrc(qbase, (uint64_t)G * RB);
 
@@ -160,8 +180,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   // out-of-range offset and reads zeros without touching memory.  With no
   // load behind a branch the compiler can wait for exactly the tile it needs
   // and leave the later tiles' loads in flight.
-  auto run = [&](auto res_tag) {
+  auto run = [&](auto res_tag, auto c8_tag) {
     constexpr int RES = decltype(res_tag)::value;
+    constexpr bool C8 = decltype(c8_tag)::value;  // FP8 planes and residual values
     constexpr int PD = RES == 0 ? S::PD0 : 1, NB = PD + 1;
 
     auto load = [&](int t, TileBuf<D, G>& b) {
@@ -170,21 +191,33 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const uint32_t row = r0 + i * RPL + rg;
-        b.k[i] = ld128(kr, ok ? row * RB + pc * 16 : kOob);
+        if constexpr (C8) {
+          const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? row * D + pc * 8 : kOob, 0, 0);
+          b.k[i] = make_uint4(w2[0], w2[1], 0u, 0u);
+        } else {
+          b.k[i] = ld128(kr, ok ? row * RB + pc * 16 : kOob);
+        }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
           b.ki[i] = __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, 0);
-          b.kv[i] = __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, 0);
+          b.kv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vkr, ok ? e : kOob, 0, 0)
+                       : __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, 0);
         }
       }
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const uint32_t row = r0 + i * RPL + rg;
-        b.v[i] = ld128(vr, ok ? row * RB + pc * 16 : kOob);
+        if constexpr (C8) {
+          const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? row * D + pc * 8 : kOob, 0, 0);
+          b.v[i] = make_uint4(w2[0], w2[1], 0u, 0u);
+        } else {
+          b.v[i] = ld128(vr, ok ? row * RB + pc * 16 : kOob);
+        }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
           b.vi[i] = __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, 0);
-          b.vv[i] = __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, 0);
+          b.vv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vvr, ok ? e : kOob, 0, 0)
+                       : __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, 0);
         }
       }
     };
@@ -196,16 +229,17 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       for (int i = 0; i < NL; ++i)
 #pragma unroll
         for (int g = 0; g < G; ++g) {
+          const uint4 kp = C8 ? widen_e4m3(b.k[i]) : b.k[i];
           float a = 0.f;
 #pragma unroll
-          for (int w = 0; w < 4; ++w) a = dot2(word(b.k[i], w), word(qreg[g], w), a);
+          for (int w = 0; w < 4; ++w) a = dot2(word(kp, w), word(qreg[g], w), a);
           s[i][g] = a;
         }
       if constexpr (RES == 1) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
           const int c = b.ki[i] & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)b.kv[i]);
+          const float v = sigma * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.kv[i]) : b.kv[i]));
 #pragma unroll
           for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
         }
@@ -216,7 +250,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           for (int e = pc; e < k; e += NP) {
             const uint32_t x = rc * k + e;
             const int c = __builtin_amdgcn_raw_buffer_load_b8(ikr, x, 0, 0) & (D - 1);
-            const float v = sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vkr, x * 2, 0, 0));
+            const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vkr, x, 0, 0))
+                                    : __builtin_amdgcn_raw_buffer_load_b16(vkr, x * 2, 0, 0);
+            const float v = sigma * bf16_to_f32((uint16_t)raw);
 #pragma unroll
             for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
           }
@@ -272,9 +308,11 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         uint32_t pp[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) pp[g] = pack_bf16x2(p[2 * pr][g], p[2 * pr + 1][g]);
+        const uint4 va = C8 ? widen_e4m3(b.v[2 * pr]) : b.v[2 * pr];
+        const uint4 vb = C8 ? widen_e4m3(b.v[2 * pr + 1]) : b.v[2 * pr + 1];
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          const uint32_t wa = word(b.v[2 * pr], w), wb = word(b.v[2 * pr + 1], w);
+          const uint32_t wa = word(va, w), wb = word(vb, w);
           const uint32_t lo = __builtin_amdgcn_perm(wb, wa, 0x05040100u);
           const uint32_t hi = __builtin_amdgcn_perm(wb, wa, 0x07060302u);
 #pragma unroll
@@ -291,7 +329,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
           const int c = b.vi[i] & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)b.vv[i]);
+          const float v = sigma * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.vv[i]) : b.vv[i]));
 #pragma unroll
           for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
         }
@@ -303,7 +341,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           for (int e = pc; e < k; e += NP) {
             const uint32_t x = rc * k + e;
             const int c = __builtin_amdgcn_raw_buffer_load_b8(ivr, x, 0, 0) & (D - 1);
-            const float v = sigma * bf16_to_f32((uint16_t)__builtin_amdgcn_raw_buffer_load_b16(vvr, x * 2, 0, 0));
+            const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vvr, x, 0, 0))
+                                    : __builtin_amdgcn_raw_buffer_load_b16(vvr, x * 2, 0, 0);
+            const float v = sigma * bf16_to_f32((uint16_t)raw);
 #pragma unroll
             for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
           }
@@ -335,12 +375,30 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     }
   };  // run
 
-  if (resid && k == NP)
-    run(std::integral_constant<int, 1>{});
-  else if (resid)
-    run(std::integral_constant<int, 2>{});
-  else
-    run(std::integral_constant<int, 0>{});
+  using R0 = std::integral_constant<int, 0>;
+  using R1 = std::integral_constant<int, 1>;
+  using R2 = std::integral_constant<int, 2>;
+  using F = std::false_type;
+  using Tr = std::true_type;
+  if constexpr (C8K) {
+    if (c8) {
+      if (resid && k == NP)
+        run(R1{}, Tr{});
+      else if (resid)
+        run(R2{}, Tr{});
+      else
+        run(R0{}, Tr{});
+    } else {
+      run(R0{}, F{});  // exact heads
+    }
+  } else {
+    if (resid && k == NP)
+      run(R1{}, F{});
+    else if (resid)
+      run(R2{}, F{});
+    else
+      run(R0{}, F{});
+  }
 
   // wave totals: the row groups of a load saw different rows
 #pragma unroll
@@ -495,7 +553,10 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
 template <int D, int G>
 static hipError_t launch_t(const DecodeParams& P, hipStream_t s) {
   const unsigned nsh = (unsigned)P.batch * P.hkv;
-  hipLaunchKernelGGL((decode_stream_kernel<D, G>), dim3(nsh * P.n_wgchunks), dim3(256), 0, s, P);
+  if (P.coef8)
+    hipLaunchKernelGGL((decode_stream_kernel<D, G, true>), dim3(nsh * P.n_wgchunks), dim3(256), 0, s, P);
+  else
+    hipLaunchKernelGGL((decode_stream_kernel<D, G, false>), dim3(nsh * P.n_wgchunks), dim3(256), 0, s, P);
   return hipGetLastError();
 }
 

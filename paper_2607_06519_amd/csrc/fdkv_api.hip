@@ -20,7 +20,9 @@ thread_local std::string g_last_error;
 
 bool aligned(const void* p, uintptr_t a) { return p && ((reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0); }
 
-int elem_bytes(const fdkv_dims* d) { return d->dtype == FDKV_BF16 ? 2 : 4; }
+// bytes per input / exact-plane element, and per stored coefficient
+int elem_bytes(const fdkv_dims* d) { return d->dtype == FDKV_F32 ? 4 : 2; }
+int coef_bytes(const fdkv_dims* d) { return d->dtype == FDKV_F32 ? 4 : d->dtype == FDKV_BF16 ? 2 : 1; }
 
 fdkv_status check_dims(const fdkv_dims* d) {
   if (!d) return FDKV_E_INVALID_ARG;
@@ -28,7 +30,7 @@ fdkv_status check_dims(const fdkv_dims* d) {
   if (d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads || d->n_q_heads % d->n_kv_heads) return FDKV_E_INVALID_ARG;
   if (d->head_dim < 1 || d->head_dim > 256) return FDKV_E_INVALID_ARG;
   if (d->topk < 0 || d->topk > d->head_dim) return FDKV_E_INVALID_ARG;
-  if (d->dtype != FDKV_F32 && d->dtype != FDKV_BF16) return FDKV_E_INVALID_ARG;
+  if (d->dtype != FDKV_F32 && d->dtype != FDKV_BF16 && d->dtype != FDKV_BF16_E4M3) return FDKV_E_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return FDKV_E_UNSUPPORTED;
   const int G = d->n_q_heads / d->n_kv_heads;
   if (G != 1 && G != 2 && G != 4 && G != 8) return FDKV_E_UNSUPPORTED;
@@ -40,9 +42,9 @@ fdkv_status hip_fail(hipError_t e, const char* what) {
   return FDKV_E_HIP;
 }
 
-uint64_t bytes_per_token(int mode, int d, int k, int e) {
-  if (mode == kShared) return 2ull * d * e;
-  if (mode == kResidual) return 2ull * d * e + 2ull * k * (1 + e);
+uint64_t bytes_per_token(int mode, int d, int k, int e, int c) {
+  if (mode == kShared) return 2ull * d * c;
+  if (mode == kResidual) return 2ull * d * c + 2ull * k * (1 + c);
   return 4ull * d * e;
 }
 
@@ -93,13 +95,13 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
     for (int u = 0; u < units; ++u)
       if (modes[(size_t)b * units + u] > FDKV_EXACT) return FDKV_E_INVALID_ARG;
   }
-  const int e = elem_bytes(dims);
+  const int e = elem_bytes(dims), c = coef_bytes(dims);
   uint64_t off = 0;
   for (int b = 0; b < batch; ++b)
     for (int u = 0; u < units; ++u) {
       const size_t i = (size_t)b * units + u;
       if (seg_offsets) seg_offsets[i] = off;
-      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e).total;
+      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e, c).total;
     }
   *total_bytes = off;
   return FDKV_OK;
@@ -113,12 +115,12 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   if (seq_len < 0 || !errors || !modes_out) return FDKV_E_INVALID_ARG;
   if (budget_bytes == 0 && !(lambda >= 0.0)) return FDKV_E_INVALID_ARG;
   const int units = dims->n_layers / 2 * dims->n_kv_heads;
-  const int d = dims->head_dim, k = dims->topk, e = elem_bytes(dims);
+  const int d = dims->head_dim, k = dims->topk, e = elem_bytes(dims), c = coef_bytes(dims);
   double om[3];
-  const double full = (double)bytes_per_token(kExact, d, k, e);
-  for (int m = 0; m < 3; ++m) om[m] = (double)bytes_per_token(m, d, k, e) / full;
+  const double full = (double)bytes_per_token(kExact, d, k, e, c);
+  for (int m = 0; m < 3; ++m) om[m] = (double)bytes_per_token(m, d, k, e, c) / full;
   uint64_t seg[3];
-  for (int m = 0; m < 3; ++m) seg[m] = seg_layout(m, (uint64_t)seq_len, d, k, e).total;
+  for (int m = 0; m < 3; ++m) seg[m] = seg_layout(m, (uint64_t)seq_len, d, k, e, c).total;
 
   auto decide = [&](double lam, uint8_t* out) {
     uint64_t fp = 0;
@@ -208,7 +210,7 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   sp.hkv = dims->n_kv_heads;
   sp.d = dims->head_dim;
   sp.topk = dims->topk;
-  sp.bf16 = dims->dtype == FDKV_BF16;
+  sp.bf16 = dims->dtype != FDKV_F32;
   hipError_t e = launch_residual_select(sp, 1, s);
   if (e != hipSuccess) return hip_fail(e, "residual_select");
 
@@ -229,7 +231,7 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   pp.topk = dims->topk;
   pp.n_probe = n_probe;
   pp.n_chunks = (int)probe_chunks(seq_len);
-  pp.bf16 = dims->dtype == FDKV_BF16;
+  pp.bf16 = dims->dtype != FDKV_F32;
   e = launch_probe(pp, s);
   if (e != hipSuccess) return hip_fail(e, "probe");
   return FDKV_OK;
@@ -260,7 +262,8 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   cp.hkv = dims->n_kv_heads;
   cp.d = dims->head_dim;
   cp.topk = dims->topk;
-  cp.bf16 = dims->dtype == FDKV_BF16;
+  cp.bf16 = dims->dtype != FDKV_F32;
+  cp.coef8 = dims->dtype == FDKV_BF16_E4M3;
   hipError_t e = launch_compress_dense(cp, s);
   if (e != hipSuccess) return hip_fail(e, "compress_dense");
 
@@ -278,6 +281,7 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   sp.d = cp.d;
   sp.topk = cp.topk;
   sp.bf16 = cp.bf16;
+  sp.coef8 = cp.coef8;
   e = launch_residual_select(sp, 2, s);
   if (e != hipSuccess) return hip_fail(e, "residual_select");
   return FDKV_OK;
@@ -323,7 +327,8 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
   p.n_wgchunks = (int)decode_chunks(max_seq_len);
   p.batch = batch;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
-  p.bf16 = dims->dtype == FDKV_BF16;
+  p.bf16 = dims->dtype != FDKV_F32;
+  p.coef8 = dims->dtype == FDKV_BF16_E4M3;
   const hipError_t e = launch_decode(p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode");
   return FDKV_OK;

@@ -27,11 +27,14 @@ struct SegLayout {
   uint64_t total;
 };
 
-FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e) {
+// e: bytes per input / exact-plane element; c: bytes per stored coefficient
+// (shared planes and residual values; c < e for FP8 coefficients).
+FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e, int c) {
   SegLayout s{};
   const uint64_t dense = plane_bytes(T * (uint64_t)d * e);
+  const uint64_t coef = plane_bytes(T * (uint64_t)d * c);
   const uint64_t ip = plane_bytes(T * (uint64_t)k);
-  const uint64_t vp = plane_bytes(T * (uint64_t)k * e);
+  const uint64_t vp = plane_bytes(T * (uint64_t)k * c);
   if (mode == kExact) {
     s.k0 = 0;
     s.k1 = dense;
@@ -41,10 +44,10 @@ FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e) {
     return s;
   }
   s.mk = 0;
-  s.mv = dense;
-  s.total = 2 * dense;
+  s.mv = coef;
+  s.total = 2 * coef;
   if (mode == kResidual) {
-    s.ik = 2 * dense;
+    s.ik = 2 * coef;
     s.vk = s.ik + ip;
     s.iv = s.vk + vp;
     s.vv = s.iv + ip;

@@ -17,6 +17,7 @@ struct CompressParams {
   uint8_t* cache;
   int seq_len, n_pairs, hkv, d, topk;
   bool bf16;
+  bool coef8;                  // shared planes in FP8 E4M3 (bf16 inputs)
 };
 
 struct SelectParams {
@@ -28,6 +29,7 @@ struct SelectParams {
   uint8_t* idx_out;            // probe: [units] planes of plane_bytes(T*k) bytes
   int seq_len, n_pairs, hkv, d, topk;
   bool bf16;
+  bool coef8;                  // residual values in FP8 E4M3 (bf16 inputs)
 };
 
 // decode: tokens per wave and waves per workgroup of the split-K kernel
@@ -46,6 +48,7 @@ struct DecodeParams {
   int layer, n_pairs, hkv, hq, d, topk, n_wgchunks, batch;
   float scale_log2;            // sm_scale * log2(e)
   bool bf16;
+  bool coef8;                  // shared planes and residual values of shared / residual heads in FP8 E4M3
 };
 
 // probe

@@ -51,7 +51,7 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
 
 def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
     x = np.asarray(x, dtype=np.float32)
-    if dtype == "bf16":
+    if dtype in ("bf16", "bf16_e4m3"):  # the FP8-coefficient cache type takes bf16 inputs
         return round_bf16_f32(x)
     if dtype == "f32":
         return np.ascontiguousarray(x)

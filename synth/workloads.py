@@ -36,7 +36,7 @@ class Workload:
     n_q_heads: int
     head_dim: int
     topk: int
-    dtype: str                     # "f32" or "bf16"
+    dtype: str                     # "f32", "bf16" or "bf16_e4m3" (bf16 inputs, FP8 coefficients)
     seq_lens: Tuple[int, ...]      # one entry per sequence of the batch
     rho: Tuple[float, float]       # inter-layer correlation, U(lo, hi) per (seq, pair, head)
     n_needles: int                 # needle tokens per sequence
@@ -68,7 +68,12 @@ class Workload:
 
     @property
     def elem_bytes(self) -> int:
-        return 4 if self.dtype == "f32" else 2
+        return 4 if self.dtype == "f32" else 2   # input elements
+
+    @property
+    def coef_bytes(self) -> int:
+        """Bytes per stored shared / residual coefficient."""
+        return 1 if self.dtype == "bf16_e4m3" else self.elem_bytes
 
     def dims(self) -> dict:
         return dict(n_layers=self.n_layers, n_kv_heads=self.n_kv_heads,
@@ -126,4 +131,9 @@ PREFILL8B = Workload(
     notes="prefill probe + route + compress on the 8B cache, 256 probe rows per query head",
 )
 
-WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B)}
+# the 8B decode workload with its shared / residual coefficients stored as FP8 E4M3
+LLAMA8B_E4M3 = dataclasses.replace(
+    LLAMA8B, name="llama8b_e4m3", dtype="bf16_e4m3",
+    notes="llama8b with FP8 E4M3 shared planes and residual values (bf16 inputs and exact heads)")
+
+WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3)}

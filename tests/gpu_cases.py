@@ -18,38 +18,59 @@ def _pad(n):
     return -(-n // PLANE) * PLANE
 
 
-def values(raw: np.ndarray, dtype: str) -> np.ndarray:
-    if dtype == "bf16":
+# OCP FP8 E4M3 decoding of the 256 codes (sign, 4 exponent bits with bias 7,
+# 3 mantissa bits, subnormals, S.1111.111 = NaN), from the format definition
+_codes = np.arange(256)
+_e, _m = (_codes >> 3) & 15, _codes & 7
+_mag = np.where(_e == 0, _m * 2.0 ** -9, (1.0 + _m / 8.0) * 2.0 ** (_e - 7.0))
+_mag = np.where((_e == 15) & (_m == 7), np.nan, _mag)
+E4M3 = np.where(_codes >= 128, -_mag, _mag)
+_E4M3_POS = np.sort(_mag[:127])          # finite non-negative values, ascending (0 .. 448)
+
+# cache type -> (input / exact-plane type, coefficient type)
+TYPES = {"f32": ("f32", "f32"), "bf16": ("bf16", "bf16"), "bf16_e4m3": ("bf16", "e4m3")}
+BYTES = {"f32": 4, "bf16": 2, "e4m3": 1}
+
+
+def values(raw: np.ndarray, kind: str) -> np.ndarray:
+    if kind == "bf16":
         return (raw.view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if kind == "e4m3":
+        return E4M3[raw]
     return raw.view(np.float32).astype(np.float64)
 
 
 def unpack_unit(buf: np.ndarray, off: int, mode: int, T: int, d: int, k: int, dtype: str) -> dict:
-    e = 4 if dtype == "f32" else 2
-    dense = _pad(T * d * e)
-    ip, vp = _pad(T * k), _pad(T * k * e)
+    ti, tc = TYPES[dtype]
+    e, c = BYTES[ti], BYTES[tc]
+    dense, coef = _pad(T * d * e), _pad(T * d * c)
+    ip, vp = _pad(T * k), _pad(T * k * c)
 
-    def dense_plane(o):
-        return values(buf[off + o: off + o + T * d * e].copy(), dtype).reshape(T, d)
+    def plane(o, width, kind):
+        return values(buf[off + o: off + o + T * width * BYTES[kind]].copy(), kind).reshape(T, width)
 
     if mode == O.EXACT:
-        return {"K0": dense_plane(0), "K1": dense_plane(dense), "V0": dense_plane(2 * dense),
-                "V1": dense_plane(3 * dense)}
-    u = {"MK": dense_plane(0), "MV": dense_plane(dense)}
+        return {"K0": plane(0, d, ti), "K1": plane(dense, d, ti), "V0": plane(2 * dense, d, ti),
+                "V1": plane(3 * dense, d, ti)}
+    u = {"MK": plane(0, d, tc), "MV": plane(coef, d, tc)}
     if mode == O.RESIDUAL:
-        o = 2 * dense
+        o = 2 * coef
         u["IK"] = buf[off + o: off + o + T * k].astype(np.int64).reshape(T, k)
-        u["VK"] = values(buf[off + o + ip: off + o + ip + T * k * e].copy(), dtype).reshape(T, k)
+        u["VK"] = plane(o + ip, k, tc)
         o2 = o + ip + vp
         u["IV"] = buf[off + o2: off + o2 + T * k].astype(np.int64).reshape(T, k)
-        u["VV"] = values(buf[off + o2 + ip: off + o2 + ip + T * k * e].copy(), dtype).reshape(T, k)
+        u["VV"] = plane(o2 + ip, k, tc)
     return u
 
 
-def ulp_distance(a: np.ndarray, b: np.ndarray, dtype: str) -> np.ndarray:
+def ulp_distance(a: np.ndarray, b: np.ndarray, kind: str) -> np.ndarray:
     """|bit distance| between same-precision values (as ordered integers)."""
     def ordered(x):
-        if dtype == "bf16":
+        x = np.asarray(x, np.float64)
+        if kind == "e4m3":
+            i = np.searchsorted(_E4M3_POS, np.abs(x)).astype(np.int64)
+            return np.where(x < 0, -i, i)
+        if kind == "bf16":
             u = (np.asarray(x, np.float32).view(np.uint32) >> 16).astype(np.int64)
             sign = 0x8000
         else:
@@ -79,7 +100,7 @@ def compare_units(gpu_unit: dict, ref_unit: dict, dtype: str, max_ulp: int = 1) 
             np.testing.assert_array_equal(got, ref, err_msg=name)
             stats[name] = 0
         else:
-            dist = ulp_distance(got, ref, dtype)
+            dist = ulp_distance(got, ref, TYPES[dtype][1])
             assert dist.max(initial=0) <= max_ulp, (name, int(dist.max()))
             stats[name] = int((dist > 0).sum())
     return stats

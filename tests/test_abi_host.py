@@ -36,7 +36,8 @@ def test_status_strings(lib):
     assert lib.fdkv_last_error() == b""
 
 
-@pytest.mark.parametrize("dtype,d,k", [("bf16", 128, 16), ("f32", 64, 8), ("bf16", 64, 5), ("f32", 128, 0)])
+@pytest.mark.parametrize("dtype,d,k", [("bf16", 128, 16), ("f32", 64, 8), ("bf16", 64, 5), ("f32", 128, 0),
+                                     ("bf16_e4m3", 128, 16), ("bf16_e4m3", 64, 5)])
 def test_layout_matches_oracle(lib, dtype, d, k):
     rng = np.random.default_rng(d + k)
     L, H, batch = 6, 3, 4
@@ -64,7 +65,7 @@ def _rand_errors(rng, units):
     return E
 
 
-@pytest.mark.parametrize("dtype,d,k", [("bf16", 128, 16), ("f32", 64, 8)])
+@pytest.mark.parametrize("dtype,d,k", [("bf16", 128, 16), ("f32", 64, 8), ("bf16_e4m3", 128, 16)])
 def test_route_lambda_matches_oracle(lib, dtype, d, k):
     rng = np.random.default_rng(5)
     dm = B.dims(32, 8, 32, d, k, dtype)

@@ -87,6 +87,12 @@ CASES = {
     "bf16_g8": scaled(WORKLOADS["long70b"], n_layers=2, n_kv_heads=2, n_q_heads=16, seq_lens=(777,), n_needles=4),
     "bf16_k0": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=0, seq_lens=(300,),
                       n_needles=2, fixed_modes=(1, 0)),
+    # FP8 E4M3 coefficients (bf16 inputs and exact heads)
+    "e4m3_ragged": scaled(WORKLOADS["llama8b"], n_layers=4, seq_lens=(1000,), n_needles=6, dtype="bf16_e4m3"),
+    "e4m3_d64_k8_g8": scaled(WORKLOADS["long70b"], n_layers=2, n_kv_heads=2, n_q_heads=16, head_dim=64, topk=8,
+                             seq_lens=(517,), n_needles=3, needle_channels=8, dtype="bf16_e4m3"),
+    "e4m3_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=5, seq_lens=(333,),
+                      n_needles=3, needle_channels=5, dtype="bf16_e4m3"),
 }
 
 

@@ -397,3 +397,73 @@ def test_gqa_is_per_query_head_attention():
     full = O.decode_unit(unit, O.RESIDUAL, 1, q, 0.35, 8)
     for g in range(4):
         np.testing.assert_allclose(full[g], O.decode_unit(unit, O.RESIDUAL, 1, q[g:g + 1], 0.35, 8)[0], rtol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# OCP FP8 E4M3 coefficient storage (cache type bf16_e4m3)
+# ---------------------------------------------------------------------------
+def _e4m3_grid():
+    """Every finite E4M3 value, enumerated from the format: sign, exponent
+    field 0..15 (bias 7, field 0 subnormal), mantissa 0..7, minus S.1111.111."""
+    vals = []
+    for e in range(16):
+        for m in range(8):
+            if e == 15 and m == 7:
+                continue
+            v = m * 2.0 ** -9 if e == 0 else (1 + m / 8) * 2.0 ** (e - 7)
+            vals.append((v, m))
+    return vals
+
+
+def _nearest_e4m3(x):
+    """Brute force: the grid value nearest to x; at an exact midpoint the one
+    with an even mantissa field; beyond 448 saturate."""
+    grid = _e4m3_grid()
+    a = abs(x)
+    if a >= 448:
+        return math.copysign(448.0, x)
+    best = min(grid, key=lambda vm: (abs(vm[0] - a), vm[1] & 1))
+    return math.copysign(best[0], x)
+
+
+def test_e4m3_grid_is_fixed():
+    grid = np.array([v for v, _ in _e4m3_grid()])
+    assert len(grid) == 127 and grid.max() == 448.0 and grid[1] == 2.0 ** -9
+    np.testing.assert_array_equal(O.round_e4m3(grid), grid)
+    np.testing.assert_array_equal(O.round_e4m3(-grid), -grid)
+
+
+def test_e4m3_rounding_matches_brute_force():
+    rng = np.random.default_rng(71)
+    grid = sorted(v for v, _ in _e4m3_grid())
+    mids = [(a + b) / 2 for a, b in zip(grid[:-1], grid[1:])]           # exact ties
+    xs = np.concatenate([rng.standard_normal(3000) * 3, rng.uniform(-500, 500, 1000),
+                         rng.uniform(-0.02, 0.02, 1000), mids, [-m for m in mids],
+                         [449.0, 464.0, 470.0, 479.9, 480.0, 1e6, -1e6, 2.0 ** -10, 3 * 2.0 ** -10, 0.0]])
+    want = np.array([_nearest_e4m3(float(x)) for x in xs])
+    np.testing.assert_array_equal(O.round_e4m3(xs), want)
+
+
+def test_e4m3_cache_bytes_closed_form():
+    # coefficient planes one byte per element, exact heads bf16, indices uint8
+    T, d, k = 1000, 128, 16
+    pad = lambda n: -(-n // 256) * 256
+    assert O.unit_bytes(O.SHARED, T, d, k, "bf16_e4m3") == 2 * pad(T * d)
+    assert O.unit_bytes(O.RESIDUAL, T, d, k, "bf16_e4m3") == 2 * pad(T * d) + 2 * (pad(T * k) + pad(T * k))
+    assert O.unit_bytes(O.EXACT, T, d, k, "bf16_e4m3") == 4 * pad(T * d * 2)
+    np.testing.assert_allclose(O.omega(d, k, "bf16_e4m3"), [256 / 1024, (256 + 64) / 1024, 1.0])
+
+
+def test_e4m3_unit_stores_rounded_coefficients():
+    rng = np.random.default_rng(5)
+    K2 = O.round_bf16(rng.standard_normal((2, 40, 64)))
+    V2 = O.round_bf16(rng.standard_normal((2, 40, 64)))
+    u = O.compress_unit(K2, V2, O.RESIDUAL, 8, "bf16_e4m3")
+    ub = O.compress_unit(K2, V2, O.RESIDUAL, 8, "bf16")
+    # same channels; values are the E4M3 rounding of the exact mean / half difference
+    np.testing.assert_array_equal(u["IK"], ub["IK"])
+    np.testing.assert_array_equal(u["MK"], O.round_e4m3((K2[0] + K2[1]) / 2))
+    D = (V2[0] - V2[1]) / 2
+    np.testing.assert_array_equal(u["VV"], O.round_e4m3(np.take_along_axis(D, u["IV"], axis=-1)))
+    e = O.compress_unit(K2, V2, O.EXACT, 8, "bf16_e4m3")
+    np.testing.assert_array_equal(e["K1"], K2[1])                   # exact heads keep bf16
