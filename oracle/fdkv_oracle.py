@@ -24,7 +24,10 @@ the paper (Section 3, "Method"), slowly and without any blocking or fusion:
 Readings of the paper adopted here (the paper leaves these open):
 
 * blocks are adjacent layer pairs (B = 2) and ``F_2`` is the orthonormal
-  DCT-II, i.e. the Haar matrix ``[[1, 1], [1, -1]] / sqrt(2)``;
+  DCT-II, i.e. the Haar matrix ``[[1, 1], [1, -1]] / sqrt(2)``; the mixed
+  schedule of Section 4 puts B = 4 blocks (``F_4``, the orthonormal
+  DCT-II(4)) between B = 2 blocks covering the first and the last four
+  layers (``block_schedule``);
 * the residual keeps, for every token, the ``k`` channels of largest
   ``|x[2b] - x[2b+1]|`` (computed in float32 on the stored inputs; ties go to
   the lower channel; indices stored ascending), K and V chosen independently;
@@ -33,8 +36,16 @@ Readings of the paper adopted here (the paper leaves these open):
   ``D`` (half the difference) for k = 1, so layer 2b reconstructs ``M + D``
   and layer 2b+1 ``M - D``; the projector entries are evaluated in 50-digit
   decimal arithmetic so that stored values are correctly rounded;
-* the routing loss of a (pair, KV head) averages Eq. (2) over both layers of
-  the pair and over the query heads of the KV head's group, uses the
+* in a B = 4 block the residual of a token keeps the ``k`` largest of its
+  ``3 d`` high-frequency coefficients ``|Z_j[c]|`` (j = 1..3; by Parseval this
+  minimises the block's squared reconstruction error), ranked in float32 as
+  the DCT-II(4) butterfly evaluates them on the stored inputs
+  (``residual_keys_dct4``), ties to the lower code ``4 c + j``; what is stored
+  is the code (uint16, ascending) and the orthonormal coefficient ``Z_j[c]``
+  itself, and layer ``p`` of the block adds ``F_4[j, p] Z_j[c]``; the shared
+  plane is the image of ``Z_0``, the four-layer mean;
+* the routing loss of a (block, KV head) averages Eq. (2) over the layers of
+  the block and over the query heads of the KV head's group, uses the
   unrounded coefficients (storage rounding is not part of the method), and
   leaves values to follow the keys' decision;
 * ``Omega(m)`` is the bytes per token of mode ``m`` divided by those of exact
@@ -138,16 +149,26 @@ def dct_matrix(B: int) -> np.ndarray:
     """Orthonormal DCT-II basis F_B (rows = frequencies, columns = layers).
 
     ``F[k, n] = s_k cos(pi (2n+1) k / (2B))`` with ``s_0 = sqrt(1/B)`` and
-    ``s_k = sqrt(2/B)``.  The mirror symmetry ``F[k, B-1-n] = (-1)^k F[k, n]``
-    of the DCT-II is applied exactly, so identical layers have exactly zero
-    high-frequency coefficients.
+    ``s_k = sqrt(2/B)``, each entry evaluated in 50-digit decimal arithmetic
+    and rounded once to float64 (so ``F_4[2] = [1/2, -1/2, -1/2, 1/2]``
+    exactly and the mirror symmetry ``F[k, B-1-n] = (-1)^k F[k, n]`` holds
+    bit for bit).
     """
-    F = np.empty((B, B), dtype=np.float64)
-    for k in range(B):
-        s = math.sqrt(1.0 / B) if k == 0 else math.sqrt(2.0 / B)
-        for n in range((B + 1) // 2):
-            F[k, n] = s * math.cos(math.pi * (2 * n + 1) * k / (2 * B))
-            F[k, B - 1 - n] = F[k, n] if k % 2 == 0 else -F[k, n]
+    return _dct_matrix_cached(B).copy()
+
+
+@functools.lru_cache(maxsize=None)
+def _dct_matrix_cached(B: int) -> np.ndarray:
+    import decimal
+    prec = 50
+    with decimal.localcontext() as ctx:
+        ctx.prec = prec + 10
+        pi = _dec_pi(prec)
+        F = np.empty((B, B), dtype=np.float64)
+        for k in range(B):
+            s = (decimal.Decimal(1 if k == 0 else 2) / B).sqrt()
+            for n in range(B):
+                F[k, n] = float(s * _dec_cos(pi * (2 * n + 1) * k / (2 * B), prec))
     return F
 
 
@@ -231,13 +252,23 @@ def coefficient_image(X, k: int, layer: int) -> np.ndarray:
 
 
 def depth_factorize(X) -> np.ndarray:
-    """Z = F_B X along the leading (layer) axis of a block."""
+    """Z = F_B X along the leading (layer) axis of a block.
+
+    Terms are grouped by the mirror symmetry ``F[k, B-1-n] = (-1)^k F[k, n]``:
+    ``Z_k = sum_{n < B/2} F[k, n] (x_n + (-1)^k x_{B-1-n})`` (plus the middle
+    layer when B is odd), the same sum in exact arithmetic; with it, identical
+    or mirror-symmetric layers give exactly zero coefficients.
+    """
     X = np.asarray(X, dtype=np.float64)
-    F = dct_matrix(X.shape[0])
+    B = X.shape[0]
+    F = dct_matrix(B)
     Z = np.zeros_like(X)
-    for k in range(X.shape[0]):
-        for n in range(X.shape[0]):
-            Z[k] += F[k, n] * X[n]
+    for k in range(B):
+        sign = 1.0 if k % 2 == 0 else -1.0
+        for n in range(B // 2):
+            Z[k] += F[k, n] * (X[n] + sign * X[B - 1 - n])
+        if B % 2:
+            Z[k] += F[k, B // 2] * X[B // 2]
     return Z
 
 
@@ -250,6 +281,46 @@ def depth_reconstruct(Z) -> np.ndarray:
         for k in range(Z.shape[0]):
             X[n] += F[k, n] * Z[k]
     return X
+
+
+# ----------------------------------------------------------------------------
+# block schedules (Section 4: B = 4 by default, B = 2 for the first and the
+# last four layers)
+# ----------------------------------------------------------------------------
+PAIRS, MIXED, QUADS = 0, 1, 2
+SCHEDULES = (PAIRS, MIXED, QUADS)
+
+
+def block_schedule(n_layers: int, schedule: int = PAIRS):
+    """``[(first layer, B), ...]`` of the blocks covering layers ``0 .. L-1`` in order.
+
+    PAIRS: every block a pair.  QUADS: every block four layers.  MIXED (the
+    paper's default setting): two pairs, then blocks of four, then two pairs.
+    """
+    L = int(n_layers)
+    if schedule == PAIRS:
+        ok, sizes = L >= 2 and L % 2 == 0, [2] * (L // 2)
+    elif schedule == QUADS:
+        ok, sizes = L >= 4 and L % 4 == 0, [4] * (L // 4)
+    elif schedule == MIXED:
+        ok, sizes = L >= 8 and (L - 8) % 4 == 0, [2, 2] + [4] * ((L - 8) // 4) + [2, 2]
+    else:
+        raise ValueError(f"schedule {schedule}")
+    if not ok:
+        raise ValueError(f"{L} layers do not fit schedule {schedule}")
+    out, first = [], 0
+    for B in sizes:
+        out.append((first, B))
+        first += B
+    return out
+
+
+def block_of_layer(n_layers: int, schedule: int, layer: int) -> Tuple[int, int, int]:
+    """``(block index, B, position of the layer in its block)``."""
+    for i, (first, B) in enumerate(block_schedule(n_layers, schedule)):
+        if first <= layer < first + B:
+            return i, B, layer - first
+    raise ValueError(f"layer {layer}")
 
 
 # ----------------------------------------------------------------------------
@@ -276,50 +347,103 @@ def residual_channels(x_even, x_odd, k: int) -> np.ndarray:
     return np.sort(order[..., :k], axis=-1).astype(np.int64)
 
 
+def residual_keys_dct4(X) -> np.ndarray:
+    """Ranking keys ``|Z_j[c]|``, j = 1..3, of a B = 4 block, ``[..., d, 3]``, in float32.
+
+    ``X``: ``[4][..., d]`` stored inputs of the block's layers.  The
+    coefficients ``Z = F_4 X`` are evaluated by the DCT-II(4) butterfly in
+    float32, every product and sum rounded on its own:
+    ``Z_1 = a (x0 - x3) + b (x1 - x2)``, ``Z_2 = ((x0 + x3) - (x1 + x2)) / 2``,
+    ``Z_3 = b (x0 - x3) - a (x1 - x2)`` with ``a = F_4[1, 0]`` and
+    ``b = F_4[1, 1]`` rounded to float32.
+    """
+    x0, x1, x2, x3 = (np.asarray(X[n], dtype=np.float32) for n in range(4))
+    F = dct_matrix(4)
+    a, b = np.float32(F[1, 0]), np.float32(F[1, 1])
+    d03, d12 = x0 - x3, x1 - x2
+    s03, s12 = x0 + x3, x1 + x2
+    z1 = a * d03 + b * d12
+    z2 = (s03 - s12) * np.float32(0.5)
+    z3 = b * d03 - a * d12
+    return np.abs(np.stack([z1, z2, z3], axis=-1))
+
+
+def residual_codes_dct4(X, k: int) -> np.ndarray:
+    """Ascending codes ``4 c + j`` ``[..., k]`` of the k largest keys per token (ties to the lower code)."""
+    key = residual_keys_dct4(X)
+    d = key.shape[-2]
+    key = key.reshape(key.shape[:-2] + (3 * d,))        # position 3 c + (j - 1): code order
+    pos = np.arange(3 * d)
+    code = 4 * (pos // 3) + pos % 3 + 1
+    if k == 0:
+        return np.zeros(key.shape[:-1] + (0,), dtype=np.int64)
+    order = np.lexsort((np.broadcast_to(pos, key.shape), -key), axis=-1)
+    return code[np.sort(order[..., :k], axis=-1)].astype(np.int64)
+
+
 # ----------------------------------------------------------------------------
-# Eq. (3): compressed representation of one (pair, KV head) unit
+# Eq. (3): compressed representation of one (block, KV head) unit
 # ----------------------------------------------------------------------------
-def compress_unit(K2, V2, mode: int, k: int, dtype: str) -> Dict[str, np.ndarray]:
+def compress_unit(KB, VB, mode: int, k: int, dtype: str) -> Dict[str, np.ndarray]:
     """Stored planes of one unit.
 
-    ``K2, V2``: ``[2][T][d]`` inputs of layers 2b and 2b+1.  Returns a dict
-    with ``MK, MV`` ([T][d]) for shared/residual heads, plus ``IK, VK, IV,
-    VV`` ([T][k] indices and half-difference values) for residual heads, or
-    ``K0, K1, V0, V1`` (the inputs) for exact heads.  Values are rounded to
-    the storage precision.
+    ``KB, VB``: ``[B][T][d]`` inputs of the block's layers (B = 2 or 4).
+    Returns a dict with ``MK, MV`` ([T][d], the image of the low-frequency
+    coefficient) for shared/residual heads, plus ``IK, VK, IV, VV`` ([T][k]
+    indices and values) for residual heads, or ``K0 .. K{B-1}, V0 ..`` (the
+    inputs) for exact heads.  B = 2: indices are channels and values the
+    half difference ``D`` at them.  B = 4: indices are codes ``4 c + j`` and
+    values the coefficients ``Z_j[c]``.  Values are rounded to the storage
+    precision.
     """
+    B = len(KB)
+    if B not in (2, 4):
+        raise ValueError(f"block size {B}")
     out: Dict[str, np.ndarray] = {}
     if mode == EXACT:
-        for name, X in (("K", K2), ("V", V2)):
+        for name, X in (("K", KB), ("V", VB)):
             X = np.asarray(X, dtype=np.float64)
-            out[name + "0"] = round_input(X[0], dtype)
-            out[name + "1"] = round_input(X[1], dtype)
+            for n in range(B):
+                out[name + str(n)] = round_input(X[n], dtype)
         return out
-    for name, X in (("K", K2), ("V", V2)):
+    for name, X in (("K", KB), ("V", VB)):
         X = np.asarray(X, dtype=np.float64)
         out["M" + name] = round_coef(coefficient_image(X, 0, 0), dtype)
-        if mode == RESIDUAL:
+        if mode != RESIDUAL:
+            continue
+        if B == 2:
             idx = residual_channels(X[0], X[1], k)
             D = coefficient_image(X, 1, 0)
             out["I" + name] = idx
             out["V" + name] = round_coef(np.take_along_axis(D, idx, axis=-1), dtype)
+        else:
+            codes = residual_codes_dct4(X, k)
+            Z = depth_factorize(X)
+            t = np.arange(X.shape[1])[:, None]
+            out["I" + name] = codes
+            out["V" + name] = round_coef(Z[codes & 3, t, codes >> 2], dtype)
     return out
 
 
-def reconstruct_layer(unit: Dict[str, np.ndarray], mode: int, parity: int, d: int, which: str) -> np.ndarray:
-    """K~ or V~ (``which`` = "K"/"V") of layer 2b+parity from the stored planes (Eq. 3)."""
+def reconstruct_layer(unit: Dict[str, np.ndarray], mode: int, pos: int, d: int, which: str,
+                      B: int = 2) -> np.ndarray:
+    """K~ or V~ (``which`` = "K"/"V") of layer ``pos`` of a B-layer block from the stored planes (Eq. 3)."""
     if mode == EXACT:
-        return np.asarray(unit[which + str(parity)], dtype=np.float64)
-    F = dct_matrix(2)
+        return np.asarray(unit[which + str(pos)], dtype=np.float64)
+    F = dct_matrix(B)
     M = np.asarray(unit["M" + which], dtype=np.float64)
     T = M.shape[0]
-    Z = np.zeros((2, T, d), dtype=np.float64)
+    Z = np.zeros((B, T, d), dtype=np.float64)
     Z[0] = M / F[0, 0]
     if mode == RESIDUAL and unit["I" + which].shape[-1] > 0:
-        idx = unit["I" + which]
-        vals = np.asarray(unit["V" + which], dtype=np.float64) / F[1, 0]
-        np.put_along_axis(Z[1], idx, vals, axis=-1)
-    return depth_reconstruct(Z)[parity]
+        idx = np.asarray(unit["I" + which])
+        vals = np.asarray(unit["V" + which], dtype=np.float64)
+        if B == 2:
+            np.put_along_axis(Z[1], idx, vals / F[1, 0], axis=-1)
+        else:
+            t = np.broadcast_to(np.arange(T)[:, None], idx.shape)
+            Z[idx & 3, t, idx >> 2] = vals
+    return depth_reconstruct(Z)[pos]
 
 
 # ----------------------------------------------------------------------------
@@ -335,51 +459,61 @@ def attention(q, K, V, scale: float) -> np.ndarray:
     return p @ np.asarray(V, dtype=np.float64)
 
 
-def decode_unit(unit, mode: int, layer: int, q, scale: float, d: int) -> np.ndarray:
-    """Output rows ``[G][d]`` of the G query heads of one KV head at ``layer``."""
-    parity = layer % 2
-    Kt = reconstruct_layer(unit, mode, parity, d, "K")
-    Vt = reconstruct_layer(unit, mode, parity, d, "V")
+def decode_unit(unit, mode: int, layer: int, q, scale: float, d: int, B: int = 2) -> np.ndarray:
+    """Output rows ``[G][d]`` of the G query heads of one KV head at ``layer``.
+
+    ``layer mod B`` is the layer's position in its block: every schedule
+    starts a block of B layers at a multiple of B.
+    """
+    pos = layer % B
+    Kt = reconstruct_layer(unit, mode, pos, d, "K", B)
+    Vt = reconstruct_layer(unit, mode, pos, d, "V", B)
     return attention(q, Kt, Vt, scale)
 
 
 # ----------------------------------------------------------------------------
 # Eq. (2): routing loss
 # ----------------------------------------------------------------------------
-def candidate_keys(K2, mode: int, k: int) -> np.ndarray:
-    """K^(m) of both layers of a pair from unrounded coefficients, ``[2][T][d]``."""
-    K2 = np.asarray(K2, dtype=np.float64)
+def candidate_keys(KB, mode: int, k: int) -> np.ndarray:
+    """K^(m) of every layer of a block from unrounded coefficients, ``[B][T][d]``."""
+    KB = np.asarray(KB, dtype=np.float64)
+    B = KB.shape[0]
     if mode == EXACT:
-        return K2.copy()
-    Z = depth_factorize(K2)
+        return KB.copy()
+    Z = depth_factorize(KB)
     Zk = np.zeros_like(Z)
     Zk[0] = Z[0]
     if mode == RESIDUAL and k > 0:
-        idx = residual_channels(K2[0], K2[1], k)
-        np.put_along_axis(Zk[1], idx, np.take_along_axis(Z[1], idx, axis=-1), axis=-1)
+        if B == 2:
+            idx = residual_channels(KB[0], KB[1], k)
+            np.put_along_axis(Zk[1], idx, np.take_along_axis(Z[1], idx, axis=-1), axis=-1)
+        else:
+            codes = residual_codes_dct4(KB, k)
+            t = np.broadcast_to(np.arange(KB.shape[1])[:, None], codes.shape)
+            Zk[codes & 3, t, codes >> 2] = Z[codes & 3, t, codes >> 2]
     return depth_reconstruct(Zk)
 
 
-def routing_errors(K2, Q2, k: int) -> np.ndarray:
+def routing_errors(KB, QB, k: int) -> np.ndarray:
     """Logit-reconstruction term of Eq. (2) for the three modes, ``[3]``.
 
-    ``K2``: ``[2][T][d]`` keys of the pair's two layers for one KV head.
-    ``Q2``: ``[2][G][P][d]`` probe queries of those layers for the G query
-    heads of the group.  The term is averaged over the two layers and the G
-    heads: ``(1/(2G)) sum_{l,g} (1/P) sum_p ||q K^(m)T/sqrt(d) - q K^T/sqrt(d)||^2``.
+    ``KB``: ``[B][T][d]`` keys of the block's layers for one KV head.
+    ``QB``: ``[B][G][P][d]`` probe queries of those layers for the G query
+    heads of the group.  The term is averaged over the B layers and the G
+    heads: ``(1/(B G)) sum_{l,g} (1/P) sum_p ||q K^(m)T/sqrt(d) - q K^T/sqrt(d)||^2``.
     """
-    K2 = np.asarray(K2, dtype=np.float64)
-    Q2 = np.asarray(Q2, dtype=np.float64)
-    d = K2.shape[-1]
-    n_l, G, P, _ = Q2.shape
+    KB = np.asarray(KB, dtype=np.float64)
+    QB = np.asarray(QB, dtype=np.float64)
+    d = KB.shape[-1]
+    n_l, G, P, _ = QB.shape
     out = np.zeros(3, dtype=np.float64)
     for m in MODES:
-        Kh = candidate_keys(K2, m, k)
+        Kh = candidate_keys(KB, m, k)
         tot = 0.0
         for l in range(n_l):
             for g in range(G):
-                Q = Q2[l, g]
-                exact_logits = Q @ K2[l].T / math.sqrt(d)
+                Q = QB[l, g]
+                exact_logits = Q @ KB[l].T / math.sqrt(d)
                 recon_logits = Q @ Kh[l].T / math.sqrt(d)
                 tot += np.sum((recon_logits - exact_logits) ** 2) / P
         out[m] = tot / (n_l * G)
@@ -389,47 +523,55 @@ def routing_errors(K2, Q2, k: int) -> np.ndarray:
 # ----------------------------------------------------------------------------
 # memory cost, layout bytes and routing
 # ----------------------------------------------------------------------------
-def bytes_per_token(mode: int, d: int, k: int, dtype: str) -> int:
+def _index_bytes(B: int) -> int:
+    """Bytes of one residual index: a channel (B = 2) or a code 4 c + j (B = 4)."""
+    return 1 if B == 2 else 2
+
+
+def bytes_per_token(mode: int, d: int, k: int, dtype: str, B: int = 2) -> int:
     e, c = input_bytes(dtype), coef_bytes(dtype)
     if mode == SHARED:
         return 2 * d * c
     if mode == RESIDUAL:
-        return 2 * d * c + 2 * k * (1 + c)
+        return 2 * d * c + 2 * k * (_index_bytes(B) + c)
     if mode == EXACT:
-        return 4 * d * e
+        return 2 * B * d * e
     raise ValueError(mode)
 
 
-def omega(d: int, k: int, dtype: str) -> np.ndarray:
+def omega(d: int, k: int, dtype: str, B: int = 2) -> np.ndarray:
     """Normalized memory cost Omega(m): bytes per token relative to exact mode."""
-    full = bytes_per_token(EXACT, d, k, dtype)
-    return np.array([bytes_per_token(m, d, k, dtype) / full for m in MODES], dtype=np.float64)
+    full = bytes_per_token(EXACT, d, k, dtype, B)
+    return np.array([bytes_per_token(m, d, k, dtype, B) / full for m in MODES], dtype=np.float64)
 
 
 def _plane(nbytes: int) -> int:
     return -(-nbytes // PLANE_ALIGN) * PLANE_ALIGN
 
 
-def unit_bytes(mode: int, T: int, d: int, k: int, dtype: str) -> int:
-    """Bytes of one (sequence, pair, KV head) segment; every plane padded to 256 B."""
+def unit_bytes(mode: int, T: int, d: int, k: int, dtype: str, B: int = 2) -> int:
+    """Bytes of one (sequence, block, KV head) segment; every plane padded to 256 B."""
     e, c = input_bytes(dtype), coef_bytes(dtype)
     coef = _plane(T * d * c)
     if mode == SHARED:
         return 2 * coef
     if mode == RESIDUAL:
-        return 2 * coef + 2 * (_plane(T * k) + _plane(T * k * c))
+        return 2 * coef + 2 * (_plane(T * k * _index_bytes(B)) + _plane(T * k * c))
     if mode == EXACT:
-        return 4 * _plane(T * d * e)
+        return 2 * B * _plane(T * d * e)
     raise ValueError(mode)
 
 
-def cache_bytes(seq_lens, modes, d: int, k: int, dtype: str) -> int:
-    """Total bytes of a cache; ``modes`` is ``[batch][pairs][Hkv]``."""
+def cache_bytes(seq_lens, modes, d: int, k: int, dtype: str, sizes=None) -> int:
+    """Total bytes of a cache; ``modes`` is ``[batch][blocks][Hkv]``, ``sizes`` the block sizes (pairs if None)."""
     modes = np.asarray(modes)
+    if sizes is None:
+        sizes = [2] * modes.shape[1]
     tot = 0
     for s, T in enumerate(seq_lens):
-        for m in modes[s].reshape(-1):
-            tot += unit_bytes(int(m), int(T), d, k, dtype)
+        for b, B in enumerate(sizes):
+            for m in modes[s, b].reshape(-1):
+                tot += unit_bytes(int(m), int(T), d, k, dtype, B)
     return tot
 
 
@@ -442,28 +584,33 @@ def route(E, om, lam: float) -> np.ndarray:
     return np.argmin(cost, axis=-1).astype(np.uint8)
 
 
-def route_budget(E, T: int, d: int, k: int, dtype: str, budget: int) -> Tuple[np.ndarray, float, bool]:
+def route_budget(E, T: int, d: int, k: int, dtype: str, budget: int,
+                 unit_sizes=None) -> Tuple[np.ndarray, float, bool]:
     """Smallest lambda (among 0, breakpoints, +inf) whose footprint fits ``budget``.
 
-    ``E``: ``[units][3]``.  Returns ``(modes, lambda, feasible)``; when even
-    all-shared exceeds the budget, returns all-shared and ``feasible=False``.
+    ``E``: ``[units][3]``; ``unit_sizes``: the block size B of every unit
+    (pairs if None).  Omega and the footprint of a unit follow its B.
+    Returns ``(modes, lambda, feasible)``; when even all-shared exceeds the
+    budget, returns all-shared and ``feasible=False``.
     """
     E = np.asarray(E, dtype=np.float64)
-    om = omega(d, k, dtype)
+    n = E.shape[0]
+    sizes = [2] * n if unit_sizes is None else [int(B) for B in unit_sizes]
+    om = np.stack([omega(d, k, dtype, B) for B in sizes]) if n else np.zeros((0, 3))
     cands = {0.0}
-    for u in range(E.shape[0]):
+    for u in range(n):
         for i in range(3):
             for j in range(i + 1, 3):
-                if not om[j] > om[i]:
+                if not om[u, j] > om[u, i]:
                     continue
-                lam = (E[u, i] - E[u, j]) / (om[j] - om[i])
+                lam = (E[u, i] - E[u, j]) / (om[u, j] - om[u, i])
                 if lam > 0 and np.isfinite(lam):
                     cands.add(float(lam))
     order = sorted(cands) + [math.inf]
-    seg = {m: unit_bytes(m, T, d, k, dtype) for m in MODES}
+    seg = {(m, B): unit_bytes(m, T, d, k, dtype, B) for m in MODES for B in set(sizes)}
     for lam in order:
         modes = route(E, om, lam)
-        fp = sum(seg[int(m)] for m in modes)
+        fp = sum(seg[(int(m), B)] for m, B in zip(modes, sizes))
         if fp <= budget:
             return modes, lam, True
-    return np.zeros(E.shape[0], dtype=np.uint8), math.inf, False
+    return np.zeros(n, dtype=np.uint8), math.inf, False

@@ -467,3 +467,213 @@ def test_e4m3_unit_stores_rounded_coefficients():
     np.testing.assert_array_equal(u["VV"], O.round_e4m3(np.take_along_axis(D, u["IV"], axis=-1)))
     e = O.compress_unit(K2, V2, O.EXACT, 8, "bf16_e4m3")
     np.testing.assert_array_equal(e["K1"], K2[1])                   # exact heads keep bf16
+
+
+# ---------------------------------------------------------------- B = 4 blocks and the mixed schedule
+def test_block_schedules():
+    # Section 4: blocks of four by default, pairs for the first and the last four layers
+    assert [B for _, B in O.block_schedule(32, O.MIXED)] == [2, 2, 4, 4, 4, 4, 4, 4, 2, 2]
+    for L, sched in [(32, O.MIXED), (8, O.MIXED), (12, O.MIXED), (16, O.QUADS), (6, O.PAIRS)]:
+        blocks = O.block_schedule(L, sched)
+        assert [l for f, B in blocks for l in range(f, f + B)] == list(range(L))
+        assert all(f % B == 0 for f, B in blocks)
+    assert all(B == 2 for f, B in O.block_schedule(40, O.MIXED) if f < 4 or f >= 36)
+    assert all(B == 4 for f, B in O.block_schedule(40, O.MIXED) if 4 <= f < 36)
+    for bad in [(10, O.MIXED), (6, O.MIXED), (6, O.QUADS), (7, O.PAIRS)]:
+        with pytest.raises(ValueError):
+            O.block_schedule(*bad)
+    assert O.block_of_layer(32, O.MIXED, 5) == (2, 4, 1)
+    assert O.block_of_layer(32, O.MIXED, 29) == (8, 2, 1)
+    assert O.block_of_layer(12, O.QUADS, 11) == (2, 4, 3)
+
+
+def test_dct4_keys_are_coefficient_magnitudes():
+    # the float32 butterfly agrees with scipy's orthonormal DCT-II to float32 rounding
+    rng = np.random.default_rng(21)
+    X = O.round_bf16(rng.standard_normal((4, 50, 16)) * 3.0)
+    key = O.residual_keys_dct4(X)
+    assert key.dtype == np.float32 and key.shape == (50, 16, 3)
+    ref = np.abs(np.moveaxis(scipy.fft.dct(X, type=2, norm="ortho", axis=0)[1:], 0, -1))
+    bound = 1e-6 * np.abs(X).max(axis=0)[..., None]
+    assert np.all(np.abs(key.astype(np.float64) - ref) <= bound)
+
+
+def test_dct4_codes_brute_force():
+    rng = np.random.default_rng(22)
+    for trial in range(40):
+        d = int(rng.integers(1, 4))
+        # small integers force ties (zeros, equal second differences)
+        X = rng.integers(-2, 3, size=(4, 1, d)).astype(np.float32)
+        key = O.residual_keys_dct4(X)[0]                       # [d][3]
+        flat = [float(key[c, j]) for c in range(d) for j in range(3)]
+        code_of = [4 * c + j + 1 for c in range(d) for j in range(3)]
+        for k in range(0, 3 * d + 1):
+            got = O.residual_codes_dct4(X, k)[0].tolist()
+            want = [code_of[i] for i in _brute_topk(flat, k)] if k else []
+            assert got == want, (X.ravel(), k)
+
+
+def test_dct4_parseval_block_error():
+    # the reconstruction error over the block is the energy of the dropped coefficients
+    rng = np.random.default_rng(23)
+    T, d = 30, 8
+    X = rng.standard_normal((4, T, d)).astype(np.float32).astype(np.float64)
+    Z = scipy.fft.dct(X, type=2, norm="ortho", axis=0)
+    t = np.arange(T)[:, None]
+    for k in (0, 1, 5, 13, 23):
+        codes = O.residual_codes_dct4(X, k)
+        kept = np.zeros(Z.shape, dtype=bool)
+        kept[0] = True
+        kept[codes & 3, t, codes >> 2] = True
+        dropped = np.sum(np.where(kept, 0.0, Z) ** 2, axis=(0, 2))
+        Kr = O.candidate_keys(X, O.RESIDUAL, k)
+        np.testing.assert_allclose(np.sum((Kr - X) ** 2, axis=(0, 2)), dropped, rtol=1e-10, atol=1e-12)
+        # greedy by magnitude: no dropped coefficient is larger than a kept one
+        if 0 < k < 3 * d:
+            hf = np.abs(Z[1:])
+            kk = kept[1:]
+            assert np.all(np.max(np.where(kk, 0.0, hf), axis=(0, 2)) <=
+                          np.min(np.where(kk, hf, np.inf), axis=(0, 2)) + 1e-6)
+    np.testing.assert_allclose(O.candidate_keys(X, O.RESIDUAL, 3 * d), X, atol=1e-12)   # k = 3d
+    np.testing.assert_allclose(O.candidate_keys(X, O.SHARED, 0), np.broadcast_to(X.mean(0), X.shape), atol=1e-14)
+
+
+def test_dct4_identical_layers():
+    rng = np.random.default_rng(24)
+    X = rng.standard_normal((9, 16)).astype(np.float32)
+    X4 = np.stack([X] * 4)
+    unit = O.compress_unit(X4, X4, O.RESIDUAL, 5, "f32")
+    np.testing.assert_array_equal(unit["IK"], np.tile([1, 2, 3, 5, 6], (9, 1)))
+    np.testing.assert_array_equal(unit["VK"], 0.0)
+    np.testing.assert_array_equal(unit["MK"], X.astype(np.float64))
+    Q = rng.standard_normal((4, 2, 3, 16))
+    E = O.routing_errors(X4.astype(np.float64), Q, 5)
+    assert E[O.SHARED] < 1e-26 and E[O.RESIDUAL] < 1e-26 and E[O.EXACT] == 0.0
+
+
+def _idct_rebuild(unit, which, T, d):
+    """K~ of all four layers: Z from the stored planes, then scipy's inverse DCT-II."""
+    Z = np.zeros((4, T, d))
+    Z[0] = 2.0 * unit["M" + which]                 # the stored plane is Z_0 / 2 (the layer mean)
+    for t in range(T):
+        for code, v in zip(unit["I" + which][t], unit["V" + which][t]):
+            Z[code & 3, t, code >> 2] = v
+    return scipy.fft.idct(Z, type=2, norm="ortho", axis=0)
+
+
+def test_dct4_decode_brute_force():
+    rng = np.random.default_rng(25)
+    T, d, G = 6, 4, 2
+    K = rng.standard_normal((4, T, d))
+    V = rng.standard_normal((4, T, d))
+    for mode in (O.SHARED, O.RESIDUAL, O.EXACT):
+        unit = O.compress_unit(K, V, mode, 3, "f64")
+        if mode == O.EXACT:
+            Kt, Vt = K, V
+        elif mode == O.SHARED:
+            Kt = np.broadcast_to(K.mean(0), K.shape)
+            Vt = np.broadcast_to(V.mean(0), V.shape)
+        else:
+            Kt, Vt = _idct_rebuild(unit, "K", T, d), _idct_rebuild(unit, "V", T, d)
+        for p in range(4):
+            q = rng.standard_normal((G, d))
+            want = np.zeros((G, d))
+            for g in range(G):
+                s = [sum(q[g, c] * Kt[p, t, c] for c in range(d)) * 0.4 for t in range(T)]
+                w = [math.exp(x - max(s)) for x in s]
+                for t in range(T):
+                    want[g] += w[t] / sum(w) * Vt[p, t]
+            got = O.decode_unit(unit, mode, 8 + p, q, 0.4, d, B=4)
+            np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+def test_dct4_unit_stores_codes_and_coefficients():
+    rng = np.random.default_rng(26)
+    X = O.round_bf16(rng.standard_normal((4, 7, 8)))
+    unit = O.compress_unit(X, X, O.RESIDUAL, 6, "bf16")
+    Z = scipy.fft.dct(X, type=2, norm="ortho", axis=0)
+    codes = unit["IK"]
+    assert codes.shape == (7, 6) and np.all(np.diff(codes, axis=-1) > 0)
+    assert np.all((codes & 3) >= 1) and np.all((codes >> 2) < 8)
+    t = np.arange(7)[:, None]
+    z = Z[codes & 3, t, codes >> 2]
+    # nearest bf16 (within half a unit in the last place; scipy's rounding noise decides exact ties)
+    np.testing.assert_array_equal(unit["VK"], O.round_bf16(unit["VK"]))
+    assert np.all(np.abs(unit["VK"] - z) <= 2.0 ** -8 * np.abs(z) * (1 + 1e-12))
+    np.testing.assert_array_equal(unit["MK"], O.round_bf16(X.mean(0)))
+
+
+def _brute_routing4(K4, Q4, k):
+    """Eq. (2) for a block of four with explicit loops; K^ rebuilt by scipy's inverse DCT."""
+    _, T, d = K4.shape
+    _, G, P, _ = Q4.shape
+    Z = scipy.fft.dct(K4, type=2, norm="ortho", axis=0)
+    codes = O.residual_codes_dct4(K4, k)
+    res = []
+    for mode in O.MODES:
+        Zm = np.zeros_like(Z)
+        if mode == O.EXACT:
+            Zm = Z.copy()
+        else:
+            Zm[0] = Z[0]
+            if mode == O.RESIDUAL:
+                for t in range(T):
+                    for code in codes[t]:
+                        Zm[code & 3, t, code >> 2] = Z[code & 3, t, code >> 2]
+        Kh = scipy.fft.idct(Zm, type=2, norm="ortho", axis=0)
+        tot = 0.0
+        for l in range(4):
+            for g in range(G):
+                for p in range(P):
+                    for t in range(T):
+                        s = sum(Q4[l, g, p, c] * (Kh[l, t, c] - K4[l, t, c]) for c in range(d))
+                        tot += (s / math.sqrt(d)) ** 2
+        res.append(tot / (4 * G * P))
+    return np.array(res)
+
+
+def test_dct4_routing_errors_brute_force():
+    rng = np.random.default_rng(27)
+    K4 = rng.standard_normal((4, 5, 4)).astype(np.float32).astype(np.float64)
+    Q4 = rng.standard_normal((4, 2, 3, 4))
+    got = O.routing_errors(K4, Q4, 3)
+    want = _brute_routing4(K4, Q4, 3)
+    np.testing.assert_allclose(got[:2], want[:2], rtol=1e-11)
+    assert got[O.EXACT] == 0.0 and abs(want[O.EXACT]) < 1e-25
+
+
+def test_dct4_bytes_closed_form():
+    # B = 4: 16-bit codes; exact heads keep all four layers
+    np.testing.assert_allclose(O.omega(128, 16, "bf16", 4), [0.25, 0.3125, 1.0])
+    np.testing.assert_allclose(O.omega(64, 8, "bf16_e4m3", 4), [0.125, 0.171875, 1.0])
+    assert O.unit_bytes(O.RESIDUAL, 3, 64, 8, "bf16", 4) == 2 * 512 + 2 * (256 + 256)
+    assert O.unit_bytes(O.RESIDUAL, 100, 64, 8, "bf16", 4) == 2 * 12800 + 2 * (1792 + 1792)
+    assert O.unit_bytes(O.EXACT, 2, 128, 16, "bf16", 4) == 8 * 512
+    # 12 layers mixed = pairs (0,1), (2,3), quad (4..7), pairs (8,9), (10,11); 1 KV head, T = 256
+    modes = np.array([[[O.SHARED], [O.RESIDUAL], [O.EXACT], [O.RESIDUAL], [O.SHARED]]])
+    sizes = [B for _, B in O.block_schedule(12, O.MIXED)]
+    # bf16, d = 64: coefficient plane 32768 B; index planes 256*8 (B = 2) or 256*16 (B = 4)
+    s = 2 * 32768
+    r2 = s + 2 * (2048 + 4096)
+    e4 = 8 * 32768
+    assert O.cache_bytes([256], modes, 64, 8, "bf16", sizes) == s + r2 + e4 + r2 + s
+
+
+def test_route_budget_mixed_sizes_brute_force():
+    rng = np.random.default_rng(28)
+    T, d, k = 1000, 64, 8
+    sizes = [2, 2, 4, 4, 2, 2] * 2
+    for trial in range(5):
+        E = np.abs(rng.standard_normal((12, 3))) * 10
+        E[:, 1] = E[:, 0] * rng.uniform(0.2, 0.9, 12)
+        E[:, 2] = 0.0
+        om = np.stack([O.omega(d, k, "bf16", B) for B in sizes])
+
+        def fp(lam):
+            return sum(O.unit_bytes(int(m), T, d, k, "bf16", B) for m, B in zip(O.route(E, om, lam), sizes))
+
+        lo, hi = fp(math.inf), fp(0.0)
+        budget = int(lo + (hi - lo) * rng.uniform(0.1, 0.9))
+        modes, lam, ok = O.route_budget(E, T, d, k, "bf16", budget, sizes)
+        assert ok and fp(lam) <= budget
+        assert all(fp(x) > budget for x in np.linspace(0, lam, 2000, endpoint=False))
