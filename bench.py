@@ -61,13 +61,14 @@ def parse():
     return ap.parse_args()
 
 
-def bytes_per_token(mode, d, k, e, c):
+def bytes_per_token(mode, d, k, e, c, B=2):
     """Algorithmic bytes one decode layer reads per token of a head: the two
     dense planes (shared coefficients of c bytes, or exact K/V of e bytes)
-    plus, for residual heads, k (index, value) pairs for K and for V."""
+    plus, for residual heads, k (index, value) pairs for K and for V (1-byte
+    channels in pairs, 2-byte codes in blocks of four)."""
     if mode == 2:
         return 2 * d * e
-    return 2 * d * c if mode == 0 else 2 * d * c + 2 * k * (1 + c)
+    return 2 * d * c if mode == 0 else 2 * d * c + 2 * k * ((1 if B == 2 else 2) + c)
 
 
 def kernel_source_hash():
@@ -186,8 +187,9 @@ def main():
         Kd = torch.empty((L, H, T, d), dtype=tdt, device=dev)
         Vd = torch.empty((L, H, T, d), dtype=tdt, device=dev)
         for b, h, kk, vv in gen.iter_segments(w, s, threads=args.threads):
-            Kd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(kk).to(dev).to(tdt))
-            Vd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(vv).to(dev).to(tdt))
+            f, nb = w.blocks[b]
+            Kd[f:f + nb, h].copy_(torch.from_numpy(kk).to(dev).to(tdt))
+            Vd[f:f + nb, h].copy_(torch.from_numpy(vv).to(dev).to(tdt))
         Ks.append(Kd)
         Vs.append(Vd)
     torch.cuda.synchronize()
@@ -212,14 +214,17 @@ def main():
     log(f"[bench] compressed cache: {cache.total_bytes / 1e9:.3f} GB, mix {np.bincount(modes.ravel(), minlength=3).tolist()}")
 
     # algorithmic bytes per layer launch: sum over (seq, KV head) of T * bytes per token of the head's mode
+    block_of = {l: (b, l - f, nb) for b, (f, nb) in enumerate(w.blocks) for l in range(f, f + nb)}
     bytes_layer = []
     for layer in range(L):
-        b = layer // 2
-        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e, w.coef_bytes)
+        b, _, nb = block_of[layer]
+        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e, w.coef_bytes, nb)
                                for s in range(w.batch) for h in range(H)))
     bytes_step = sum(bytes_layer)
 
-    order = list(range(0, L, 2)) + list(range(1, L, 2)) if args.order == "cold" else list(range(L))
+    # cold order: every block's first layers, then its second layers, ...: the layers that share a
+    # block's planes run a whole sweep apart, so each re-read comes from HBM
+    order = sorted(range(L), key=lambda l: (block_of[l][1], l)) if args.order == "cold" else list(range(L))
     n_q = args.steps + args.warmup
     qs = torch.empty((n_q, L, w.batch, Hq, d), dtype=tdt, device=dev)
     for i in range(n_q):
@@ -296,12 +301,13 @@ def main():
         vl = [Vs[0][l] for l in range(L)]
         ql = [Qp[l] for l in range(L)]
         _, budget = B.layout(dm, [T], gen.fixed_modes(w, 0)[None])   # footprint of the 50/35/15 mix
+        nbk = w.n_blocks
         ws = torch.empty(B.probe_workspace(dm, T, P), dtype=torch.uint8, device=dev)
-        err = torch.empty((L // 2, H, 2), dtype=torch.float32, device=dev)
-        _, all_exact = B.layout(dm, [T], np.full((1, L // 2, H), 2, np.uint8))
+        err = torch.empty((nbk, H, 2), dtype=torch.float32, device=dev)
+        _, all_exact = B.layout(dm, [T], np.full((1, nbk, H), 2, np.uint8))
         pcache_buf = torch.empty(all_exact, dtype=torch.uint8, device=dev)
-        offs_dev = torch.empty((L // 2, H), dtype=torch.int64, device=dev)
-        modes_dev = torch.empty((L // 2, H), dtype=torch.uint8, device=dev)
+        offs_dev = torch.empty((nbk, H), dtype=torch.int64, device=dev)
+        modes_dev = torch.empty((nbk, H), dtype=torch.uint8, device=dev)
         times = {"probe": [], "route": [], "compress": [], "total": []}
         pmodes = None
         for rep in range(4):
@@ -330,13 +336,15 @@ def main():
             times["compress"].append(c0.elapsed_time(c1) * 1e-3)
             times["total"].append(tw1 - tw0)
         tp, trt, tc, tt = (float(np.mean(times[x])) for x in ("probe", "route", "compress", "total"))
-        units = L // 2 * H
-        cmp_read = units * T * 4 * d * e
-        cmp_write = sum(T * (2 * d * e if m == 0 else (4 * d * e if m == 2 else 2 * d * e + 2 * k * (1 + e)))
-                        for m in pmodes.ravel())
-        mfma_flops = units * T * (d // 32) * (d // 32 + 1) // 2 * 2 * (32 * 32 * 2)   # upper tiles, 2 matrices
+        units = nbk * H
+        usz = [nb for nb in w.block_sizes for _ in range(H)]
+        cmp_read = T * 2 * d * e * L * H                                             # K and V of every layer
+        cmp_write = sum(T * bytes_per_token(int(m), d, k, e, w.coef_bytes, nb) * (nb if m == 2 else 1)
+                        for m, nb in zip(pmodes.ravel(), usz))                # exact heads copy all nb layers
+        # upper 32x32 tiles of the deviation Gram matrices: 2 per pair, 8 per block of four
+        mfma_flops = sum(T * (d // 32) * (d // 32 + 1) // 2 * (2 if nb == 2 else 8) * (32 * 32 * 2) for nb in usz)
         G = Hq // H
-        eq2_flops = units * 2 * G * P * 2 * T * d * 2 * 2                            # literal Eq. 2, 2 modes
+        eq2_flops = T * L * H * G * P * d * 2 * 2 * 2                                # literal Eq. 2, 2 modes
         prefill = {
             "workload": "prefill8b" if w.name == "llama8b" else w.name,
             "probe_ms": tp * 1e3, "route_ms": trt * 1e3, "compress_ms": tc * 1e3,
@@ -344,7 +352,7 @@ def main():
             "compressed_tokens_per_s": T / tt,
             "compress_gbs": (cmp_read + cmp_write) / tc / 1e9,
             "compress_frac_hbm": (cmp_read + cmp_write) / tc / 1e9 / HBM_PEAK_GBS,
-            "probe_read_gbs": units * T * 2 * d * e / tp / 1e9,
+            "probe_read_gbs": L * H * T * d * e / tp / 1e9,
             "probe_mfma_util": mfma_flops / tp / (MFMA_BF16_PEAK_TFLOPS * 1e12),
             "probe_eq2_equiv_tflops": eq2_flops / tp / 1e12,
             "probe_mode_mix": np.bincount(pmodes.ravel(), minlength=3).tolist(),
@@ -361,14 +369,15 @@ def main():
 
     traffic = load_traffic(w.name)
     cfg = {"workload": w.name, "n_layers": L, "n_kv_heads": H, "n_q_heads": Hq, "head_dim": d, "topk": k,
-           "batch": w.batch, "seq_len": w.max_seq_len, "mode_mix": np.bincount(modes.ravel(), minlength=3).tolist(),
+           "batch": w.batch, "seq_len": w.max_seq_len, "block_sizes": list(w.block_sizes),
+           "mode_mix": np.bincount(modes.ravel(), minlength=3).tolist(),
            "layer_order": args.order, "graph": graph is not None, "cache_gb": cache.total_bytes / 1e9,
            "bytes_per_step": bytes_step}
     res = {
         "metric": "compressed-KV decode attn tokens/s + achieved HBM GB/s vs 8 TB/s, 32k ctx",
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": w.dtype, "data": "synthetic (seeded generator, correlated layer pairs with needles)",
+        "dtype": w.dtype, "data": "synthetic (seeded generator, layers correlated along depth within each block, needles)",
         "config": cfg,
         "step_hbm_gbs": step_gbs,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -382,7 +391,7 @@ def main():
 
 
 def cpu_baseline(w, modes):
-    """The oracle's decode on a bounded sample: a few (pair, KV head) units, both layers, a few steps."""
+    """The oracle's decode on a bounded sample: a few (block, KV head) units, all their layers, a few steps."""
     import numpy as np
 
     import oracle as O
@@ -395,7 +404,7 @@ def cpu_baseline(w, modes):
     cores = len(os.sched_getaffinity(0))
     rng = np.random.default_rng(0)
     d, G = w.head_dim, w.group
-    flat = [(b, h) for b in range(w.n_pairs) for h in range(w.n_kv_heads)]
+    flat = [(b, h) for b in range(w.n_blocks) for h in range(w.n_kv_heads)]
     pick = []
     for m in (0, 1, 2):
         cand = [u for u in flat if modes[u] == m]
@@ -403,22 +412,23 @@ def cpu_baseline(w, modes):
     n_steps = 3
     elapsed, n_calls = 0.0, 0
     for (b, h) in pick:
-        K, V, _ = gen.segment(w, 0, b, h)
+        K, V, _ = gen.block_segment(w, 0, b, h)
+        f, nb = w.blocks[b]
         unit = O.compress_unit(K, V, int(modes[b, h]), w.topk, w.dtype)
         for s in range(n_steps):
             q = gen.decode_queries(w, s)
-            for layer in (2 * b, 2 * b + 1):
+            for layer in range(f, f + nb):
                 qq = q[layer][0, h * G:(h + 1) * G].astype(np.float64)
                 t0 = time.perf_counter()
-                O.decode_unit(unit, int(modes[b, h]), layer, qq, 1.0 / math.sqrt(d), d)
+                O.decode_unit(unit, int(modes[b, h]), layer, qq, 1.0 / math.sqrt(d), d, nb)
                 elapsed += time.perf_counter() - t0
                 n_calls += 1
     per_unit_layer = elapsed / n_calls
     step_s = per_unit_layer * w.n_layers * w.n_kv_heads
     return {"value": w.batch / step_s, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "blas_threads": blas_threads,
-            "sample": f"oracle decode (reconstruct + fp64 softmax attention) of {len(pick)} (pair, KV head) units "
-                      f"x 2 layers x {n_steps} steps = {n_calls} unit-layers ({elapsed:.1f}s), scaled to "
+            "sample": f"oracle decode (reconstruct + fp64 softmax attention) of {len(pick)} (block, KV head) units "
+                      f"x their layers x {n_steps} steps = {n_calls} unit-layers ({elapsed:.1f}s), scaled to "
                       f"{w.n_layers * w.n_kv_heads} unit-layers per step"}
 
 

@@ -2,9 +2,9 @@
  * fdkv.h - C ABI of the FreqDepthKV compressed-KV path on AMD MI355X (gfx950).
  *
  * FreqDepthKV (Section 3 of the paper) compresses a decoder's KV cache along
- * depth.  Adjacent layers 2b and 2b+1 form a block; an orthonormal DCT along
+ * depth.  Adjacent layers form blocks of B = 2 or 4; an orthonormal DCT along
  * the layer axis (Eq. 1) splits each block into a low-frequency coefficient
- * stored once for both layers and a high-frequency coefficient kept only
+ * stored once for the block and high-frequency coefficients kept only
  * sparsely (Eq. 3).  An online probe measures, per (block, KV head), how much
  * each candidate reconstruction moves the attention logits of probe queries
  * (Eq. 2) and routes the head to one of three modes; decode attention then
@@ -12,14 +12,27 @@
  *
  * Conventions shared by every entry point:
  *
- *  - Blocks are layer pairs (B = 2).  With the orthonormal DCT-II the stored
- *    per-layer images are M = (x[2b] + x[2b+1]) / 2 (shared part) and
- *    D = (x[2b] - x[2b+1]) / 2 (high-frequency part): layer 2b rebuilds
- *    M + D, layer 2b+1 rebuilds M - D.
- *  - The residual of a token keeps the `topk` channels of largest
- *    |fl32(x[2b] - x[2b+1])| (ties to the lower channel), as uint8 channel
- *    indices in ascending order plus D at those channels.  K and V choose
- *    their channels independently.
+ *  - `dims.schedule` cuts the layers into blocks (fdkv_blocks lists them):
+ *    all pairs, all blocks of four, or the paper's default setting (Section
+ *    4): pairs for the first four and the last four layers, blocks of four
+ *    between.  A block of B layers starts at a multiple of B.  A "unit" is a
+ *    (block, KV head); unit arrays are [n_blocks][Hkv].
+ *  - Every block stores the mean of its layers, M (the per-layer image of
+ *    the low-frequency DCT-II coefficient), as its shared part.
+ *  - Pairs (layers l, l+1): D = (x[l] - x[l+1]) / 2; layer l rebuilds M + D,
+ *    layer l+1 rebuilds M - D.  The residual of a token keeps the `topk`
+ *    channels of largest |fl32(x[l] - x[l+1])| (ties to the lower channel),
+ *    as uint8 channel indices in ascending order plus D at those channels.
+ *  - Blocks of four: Z_j = sum_n F_4[j][n] x[l+n], j = 1..3, with F_4 the
+ *    orthonormal DCT-II(4), F_4[j][n] = cos(pi (2n+1) j / 8) / sqrt(2).  The
+ *    residual of a token keeps the `topk` largest of its 3d coefficients
+ *    |Z_j[c]|, ranked as fp32 evaluates the butterfly
+ *      Z_1 = a (x0 - x3) + b (x1 - x2),  Z_2 = ((x0 + x3) - (x1 + x2)) / 2,
+ *      Z_3 = b (x0 - x3) - a (x1 - x2),  a = F_4[1][0], b = F_4[1][1]
+ *    (each product and sum rounded), ties to the lower code; it stores the
+ *    uint16 codes 4c + j in ascending order plus Z_j[c].  Layer l+p rebuilds
+ *    M plus F_4[j][p] Z_j[c] at channel c for each kept code.
+ *  - K and V choose their residual entries independently.
  *  - Query head g reads KV head g / (n_q_heads / n_kv_heads).
  *  - K, V, queries, the cache and attention outputs use one element type,
  *    `dims.dtype` (fp32 or bf16); all arithmetic is fp32.
@@ -32,12 +45,14 @@
  *    surface at the caller's next synchronisation.  Inputs must be finite.
  *
  * Compressed cache layout (one device buffer).  It is a sequence of
- * segments, one per (sequence, pair b, KV head h) in row-major order, each
+ * segments, one per (sequence, block, KV head) in row-major order, each
  * starting at the offset fdkv_layout() returns.  A segment is a list of
- * planes, each padded to a multiple of 256 bytes, e = element bytes:
- *    SHARED   : MK[T][d], MV[T][d]
- *    RESIDUAL : MK[T][d], MV[T][d], IK[T][k] (u8), VK[T][k] (e), IV[T][k] (u8), VV[T][k] (e)
- *    EXACT    : K[2b][T][d], K[2b+1][T][d], V[2b][T][d], V[2b+1][T][d]
+ * planes, each padded to a multiple of 256 bytes; e = bytes of an input
+ * element, c = bytes of a stored coefficient, i = 1 (pairs) or 2 (blocks of
+ * four) bytes of a residual index:
+ *    SHARED   : MK[T][d] (c), MV[T][d] (c)
+ *    RESIDUAL : MK, MV, IK[T][k] (i), VK[T][k] (c), IV[T][k] (i), VV[T][k] (c)
+ *    EXACT    : K of the B layers [T][d] (e) in order, then V of the B layers
  */
 #ifndef FDKV_H
 #define FDKV_H
@@ -70,13 +85,21 @@ typedef enum { FDKV_SHARED = 0, FDKV_RESIDUAL = 1, FDKV_EXACT = 2 } fdkv_mode;
  */
 typedef enum { FDKV_F32 = 0, FDKV_BF16 = 1, FDKV_BF16_E4M3 = 2 } fdkv_dtype;
 
+/*
+ * Block schedules.  PAIRS: every block two layers (L even).  MIXED: two
+ * pairs, blocks of four, two pairs (L >= 8, L - 8 a multiple of 4), the
+ * default of Section 4.  QUADS: every block four layers (L a multiple of 4).
+ */
+typedef enum { FDKV_SCHED_PAIRS = 0, FDKV_SCHED_MIXED = 1, FDKV_SCHED_QUADS = 2 } fdkv_schedule;
+
 typedef struct {
-  int32_t n_layers;   /* L, even, 2..256 */
+  int32_t n_layers;   /* L, 2..128, fitting the schedule */
   int32_t n_kv_heads; /* Hkv >= 1 */
   int32_t n_q_heads;  /* Hq, a multiple of Hkv; Hq / Hkv in {1, 2, 4, 8} */
   int32_t head_dim;   /* d in {64, 128} */
   int32_t topk;       /* k residual channels per token, 0 <= k <= d */
   int32_t dtype;      /* fdkv_dtype */
+  int32_t schedule;   /* fdkv_schedule */
 } fdkv_dims;
 
 /* Message for a status code (static storage). */
@@ -86,13 +109,21 @@ const char* fdkv_status_string(int32_t status);
 const char* fdkv_last_error(void);
 
 /*
+ * fdkv_blocks - host only.  The blocks of dims.schedule, in layer order.
+ *   n_blocks     host  out: number of blocks (at most L/2)
+ *   first_layer  host [n_blocks] or NULL  out: first layer of each block
+ *   block_size   host [n_blocks] or NULL  out: 2 or 4
+ */
+fdkv_status fdkv_blocks(const fdkv_dims* dims, int32_t* n_blocks, int32_t* first_layer, int32_t* block_size);
+
+/*
  * fdkv_layout - host only.  Byte layout of a compressed cache (Eq. 3 storage).
  *   seq_lens     host [batch]                     tokens per sequence, >= 0
- *   modes        host [batch][L/2][Hkv]           fdkv_mode per unit
- *   seg_offsets  host [batch][L/2][Hkv] or NULL   out: segment byte offsets
- *   total_bytes  host                             out: buffer size needed
- * Segments follow each other in (sequence, pair, head) order; all offsets are
- * multiples of 256.
+ *   modes        host [batch][n_blocks][Hkv]           fdkv_mode per unit
+ *   seg_offsets  host [batch][n_blocks][Hkv] or NULL   out: segment byte offsets
+ *   total_bytes  host                                  out: buffer size needed
+ * Segments follow each other in (sequence, block, head) order; all offsets
+ * are multiples of 256.
  */
 fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens,
                         const uint8_t* modes, uint64_t* seg_offsets, uint64_t* total_bytes);
@@ -102,16 +133,16 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
  * with Eq. (2)'s loss, and the budget rule that raises lambda until the cache
  * fits (end of Section 3).
  *   seq_len      tokens of the sequence (for the footprint)
- *   errors       host [L/2][Hkv][2]   E_shared, E_residual per unit (E_exact = 0),
- *                                     as written by fdkv_probe
+ *   errors       host [n_blocks][Hkv][2]   E_shared, E_residual per unit
+ *                                          (E_exact = 0), as written by fdkv_probe
  *   lambda       penalty used when budget_bytes == 0
  *   budget_bytes 0: route with `lambda`.  Otherwise: the smallest lambda among
  *                0, the per-unit breakpoints (E_i - E_j)/(Omega_j - Omega_i)
  *                and +inf whose fdkv_layout footprint is <= budget_bytes.
- *   modes_out    host [L/2][Hkv]   out
+ *   modes_out    host [n_blocks][Hkv]   out
  *   lambda_out   host, may be NULL out: lambda used (+inf when infeasible)
- * Omega(m) = bytes per token of mode m / bytes per token of EXACT.  Ties go to
- * the cheaper mode.  Returns FDKV_E_BUDGET (modes all SHARED) when even
+ * Omega(m) = bytes per token of mode m / bytes per token of EXACT, for the
+ * unit's block size.  Ties go to the cheaper mode.  Returns FDKV_E_BUDGET (modes all SHARED) when even
  * all-shared exceeds the budget.
  */
 fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* errors, double lambda,
@@ -121,15 +152,16 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
 fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t n_probe, size_t* bytes);
 
 /*
- * fdkv_probe - device.  Routing loss of Eq. (2) for every (pair, KV head):
- *   E_m[b,h] = 1/(2 G P) * sum over l in {2b, 2b+1}, query heads g of KV head h,
- *              probe rows p, tokens t of ((q_{l,g,p} . (K^(m)_{l,h,t} - K_{l,h,t})) / sqrt(d))^2
- * for m = SHARED (K^ = M) and m = RESIDUAL (K^ = M +/- D on the token's top-k
- * channels).  Logits are compared raw, over all T keys, for keys only.
+ * fdkv_probe - device.  Routing loss of Eq. (2) for every (block, KV head):
+ *   E_m[b,h] = 1/(B G P) * sum over the B layers l of the block, query heads g
+ *              of KV head h, probe rows p, tokens t of
+ *              ((q_{l,g,p} . (K^(m)_{l,h,t} - K_{l,h,t})) / sqrt(d))^2
+ * for m = SHARED (K^ = M) and m = RESIDUAL (K^ = M plus the token's kept
+ * residual entries).  Logits are compared raw, over all T keys, for keys only.
  *   k_layers   host array of L device pointers, layer l holds K_l [Hkv][T][d]
  *   qp_layers  host array of L device pointers, layer l holds Q_l [Hq][P][d]
  *   n_probe    P >= 1 probe rows per query head
- *   errors_out device float [L/2][Hkv][2]
+ *   errors_out device float [n_blocks][Hkv][2]
  *   ws         device workspace of >= fdkv_probe_workspace() bytes
  * T * d * elem_bytes and P * G * d * elem_bytes must stay below 2^31
  * (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets).
@@ -142,8 +174,8 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
  * fdkv_compress - device.  Writes one sequence's segments of the compressed
  * cache (Eq. 1 factorization, Eq. 3 storage) for the given modes.
  *   k_layers, v_layers  host arrays of L device pointers, [Hkv][T][d] each
- *   modes        device [L/2][Hkv]
- *   seg_offsets  device [L/2][Hkv], from fdkv_layout (256-byte multiples)
+ *   modes        device [n_blocks][Hkv]
+ *   seg_offsets  device [n_blocks][Hkv], from fdkv_layout (256-byte multiples)
  *   cache        device buffer the offsets index into
  */
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
@@ -161,9 +193,9 @@ fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t 
  *   seq_lens     device int32 [batch], 0 <= T_i <= max_seq_len (T_i = 0 gives o = 0)
  *   max_seq_len  host, sizes the launch; max_seq_len * d * elem_bytes < 2^31
  *                (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets)
- *   modes        device [batch][L/2][Hkv], 4-byte aligned (read in aligned 4-byte
- *                words; bytes past the array inside its last word are ignored)
- *   seg_offsets  device [batch][L/2][Hkv]
+ *   modes        device [batch][n_blocks][Hkv], 4-byte aligned (read in aligned
+ *                4-byte words; bytes past the array inside its last word are ignored)
+ *   seg_offsets  device [batch][n_blocks][Hkv]
  *   layer        0 <= layer < L
  *   q            device [batch][Hq][d]
  *   out          device [batch][Hq][d]

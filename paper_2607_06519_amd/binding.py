@@ -22,8 +22,9 @@ F32, BF16, BF16_E4M3 = 0, 1, 2   # cache types (fdkv_dtype)
 STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: "FDKV_E_WORKSPACE",
           -4: "FDKV_E_BUDGET", -5: "FDKV_E_HIP"}
 
-SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_layout", "fdkv_route", "fdkv_probe_workspace",
-           "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn")
+SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
+           "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn")
+PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 
 
 class FdkvError(RuntimeError):
@@ -38,12 +39,13 @@ class FdkvError(RuntimeError):
 
 class Dims(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
-                ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("schedule", ctypes.c_int32)]
 
 
-def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype) -> Dims:
+def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype, schedule=PAIRS) -> Dims:
     dt = {"f32": F32, "bf16": BF16, "bf16_e4m3": BF16_E4M3}.get(dtype, dtype)
-    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt)
+    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt, schedule)
 
 
 def load():
@@ -59,6 +61,8 @@ def load():
     lib.fdkv_status_string.argtypes = [I32]
     lib.fdkv_last_error.restype = ctypes.c_char_p
     lib.fdkv_last_error.argtypes = []
+    lib.fdkv_blocks.restype = I32
+    lib.fdkv_blocks.argtypes = [DP, P, P, P]
     lib.fdkv_layout.restype = I32
     lib.fdkv_layout.argtypes = [DP, I32, P, P, P, P]
     lib.fdkv_route.restype = I32
@@ -104,8 +108,19 @@ def _ptr_array(tensors: Sequence) -> ctypes.Array:
 
 
 # ----------------------------------------------------------------- host entry points
+def blocks(d: Dims):
+    """``(first_layer [n_blocks] int32, block_size [n_blocks] int32)`` of the schedule."""
+    lib = load()
+    n = ctypes.c_int32(0)
+    _check(lib.fdkv_blocks(ctypes.byref(d), ctypes.byref(n), None, None), "fdkv_blocks")
+    first = np.zeros(n.value, dtype=np.int32)
+    size = np.zeros(n.value, dtype=np.int32)
+    _check(lib.fdkv_blocks(ctypes.byref(d), ctypes.byref(n), _np_ptr(first), _np_ptr(size)), "fdkv_blocks")
+    return first, size
+
+
 def layout(d: Dims, seq_lens, modes):
-    """``(seg_offsets [batch][L/2][Hkv] uint64, total_bytes)`` for host ``modes``."""
+    """``(seg_offsets [batch][n_blocks][Hkv] uint64, total_bytes)`` for host ``modes``."""
     lib = load()
     sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
     m = np.ascontiguousarray(modes, dtype=np.uint8)
@@ -117,7 +132,7 @@ def layout(d: Dims, seq_lens, modes):
 
 
 def route(d: Dims, seq_len: int, errors, lam: float = 0.0, budget_bytes: int = 0, allow_infeasible=False):
-    """``(modes [L/2][Hkv] uint8, lambda_used, status)`` from host ``errors [L/2][Hkv][2]``."""
+    """``(modes [n_blocks][Hkv] uint8, lambda_used, status)`` from host ``errors [n_blocks][Hkv][2]``."""
     lib = load()
     e = np.ascontiguousarray(errors, dtype=np.float32)
     modes = np.zeros(e.shape[:-1], dtype=np.uint8)

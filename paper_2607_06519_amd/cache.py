@@ -34,7 +34,7 @@ def to_device(x: np.ndarray, dtype: str, device="cuda"):
 
 
 class CompressedCache:
-    """One compressed cache: ``batch`` sequences, modes ``[batch][L/2][Hkv]``."""
+    """One compressed cache: ``batch`` sequences, modes ``[batch][n_blocks][Hkv]``."""
 
     def __init__(self, dims: B.Dims, seq_lens: Sequence[int], modes: np.ndarray, device="cuda"):
         torch = _torch()
@@ -42,7 +42,8 @@ class CompressedCache:
         self.seq_lens_host = [int(t) for t in seq_lens]
         self.batch = len(self.seq_lens_host)
         self.max_seq_len = max(self.seq_lens_host) if self.seq_lens_host else 0
-        m = np.ascontiguousarray(modes, dtype=np.uint8).reshape(self.batch, dims.n_layers // 2, dims.n_kv_heads)
+        self.block_first, self.block_size = B.blocks(dims)
+        m = np.ascontiguousarray(modes, dtype=np.uint8).reshape(self.batch, len(self.block_size), dims.n_kv_heads)
         self.modes_host = m
         self.offsets_host, self.total_bytes = B.layout(dims, self.seq_lens_host, m)
         self.buf = torch.empty(max(self.total_bytes, 256), dtype=torch.uint8, device=device)
@@ -72,10 +73,10 @@ class CompressedCache:
 
 
 def probe(dims: B.Dims, seq_len: int, k_layers, qp_layers, n_probe: int, stream=None):
-    """Queue fdkv_probe and return the device tensor of errors ``[L/2][Hkv][2]``."""
+    """Queue fdkv_probe and return the device tensor of errors ``[n_blocks][Hkv][2]``."""
     torch = _torch()
     dev = k_layers[0].device
     ws = torch.empty(B.probe_workspace(dims, seq_len, n_probe), dtype=torch.uint8, device=dev)
-    err = torch.empty((dims.n_layers // 2, dims.n_kv_heads, 2), dtype=torch.float32, device=dev)
+    err = torch.empty((len(B.blocks(dims)[0]), dims.n_kv_heads, 2), dtype=torch.float32, device=dev)
     B.probe(dims, seq_len, k_layers, qp_layers, n_probe, err, ws, stream)
     return err, ws

@@ -1,15 +1,20 @@
 // Prefill-time compression of the KV cache (Section 3, Eq. 1 and Eq. 3).
 //
-// Two kernels:
-//  * compress_dense - coalesced streaming pass over every (pair, KV head):
-//    shared/residual heads write the pair mean M = (x[2b] + x[2b+1]) / 2
-//    (the per-layer image of the low-frequency DCT coefficient) for K and V;
-//    exact heads copy the four input rows.
-//  * residual_select - one lane per token: the top-k channels of
+// Kernels:
+//  * compress_dense - coalesced streaming pass over every (block, KV head):
+//    shared/residual heads write the block mean M (the per-layer image of
+//    the low-frequency DCT coefficient, the same for every layer of the
+//    block) for K and V; exact heads copy the input rows.
+//  * residual_select (B = 2) - one lane per token: the top-k channels of
 //    |fl32(x[2b] - x[2b+1])| by a register comparator network (topk_net.h),
-//    written as ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those
-//    channels.  Used for residual heads (K and V independently) and by the
-//    probe (K indices only, into its workspace).
+//    written as ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at
+//    those channels.
+//  * residual_select4 (B = 4) - one lane per token: the top-k of the 3d
+//    high-frequency coefficients Z_j[c] (j = 1..3) of the DCT-II(4), ranked
+//    by |Z| as the fp32 butterfly gives them, written as ascending uint16
+//    codes 4c + j plus Z_j[c].
+// The select kernels serve residual heads (K and V independently) and the
+// probe (K indices only, into its workspace).
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 #include "fp8.h"
@@ -17,58 +22,72 @@
 
 namespace fdkv {
 
-// 16 bytes of inputs -> 16 bytes of pair means, fp32 arithmetic.
+// Channel i of a 16-byte piece, as fp32.
 template <bool BF16>
-__device__ __forceinline__ uint4 pair_mean(uint4 a, uint4 b) {
+__device__ __forceinline__ float chan(const uint4& v, int i) {
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(&v);
+  if constexpr (BF16)
+    return (i & 1) ? bf16_hi(p[i >> 1]) : bf16_lo(p[i >> 1]);
+  else
+    return as_f32(p[i]);
+}
+
+// Mean over the NB layers of channel i, fp32: (x0 + x1) / 2, or
+// ((x0 + x3) + (x1 + x2)) / 4 (the butterfly order of the select kernel).
+template <bool BF16, int NB>
+__device__ __forceinline__ float block_mean(const uint4* x, int i) {
+  if constexpr (NB == 2)
+    return (chan<BF16>(x[0], i) + chan<BF16>(x[1], i)) * 0.5f;
+  else
+    return ((chan<BF16>(x[0], i) + chan<BF16>(x[3], i)) + (chan<BF16>(x[1], i) + chan<BF16>(x[2], i))) * 0.25f;
+}
+
+// 16 bytes of inputs per layer -> 16 bytes of block means in the input type.
+template <bool BF16, int NB>
+__device__ __forceinline__ uint4 mean_piece(const uint4* x) {
   uint4 r;
   uint32_t* pr = reinterpret_cast<uint32_t*>(&r);
-  const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
-  const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    if constexpr (BF16) {
-      const float lo = (bf16_lo(pa[w]) + bf16_lo(pb[w])) * 0.5f;
-      const float hi = (bf16_hi(pa[w]) + bf16_hi(pb[w])) * 0.5f;
-      pr[w] = pack_bf16x2(lo, hi);
-    } else {
-      pr[w] = as_u32((as_f32(pa[w]) + as_f32(pb[w])) * 0.5f);
-    }
+    if constexpr (BF16)
+      pr[w] = pack_bf16x2(block_mean<true, NB>(x, 2 * w), block_mean<true, NB>(x, 2 * w + 1));
+    else
+      pr[w] = as_u32(block_mean<false, NB>(x, w));
   }
   return r;
 }
 
-// 16 bytes of bf16 inputs (8 channels) -> 8 bytes of FP8 E4M3 pair means.
-__device__ __forceinline__ uint2 pair_mean_e4m3(uint4 a, uint4 b) {
-  const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
-  const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
+// 16 bytes of bf16 inputs per layer (8 channels) -> 8 bytes of FP8 E4M3 block means.
+template <int NB>
+__device__ __forceinline__ uint2 mean_piece_e4m3(const uint4* x) {
   uint32_t w[2] = {0u, 0u};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t lo = f32_to_e4m3((bf16_lo(pa[i]) + bf16_lo(pb[i])) * 0.5f);
-    const uint32_t hi = f32_to_e4m3((bf16_hi(pa[i]) + bf16_hi(pb[i])) * 0.5f);
-    w[i >> 1] |= (lo | (hi << 8)) << (16 * (i & 1));
-  }
+  for (int i = 0; i < 8; ++i) w[i >> 2] |= (uint32_t)f32_to_e4m3(block_mean<true, NB>(x, i)) << (8 * (i & 3));
   return make_uint2(w[0], w[1]);
 }
 
-template <int D, bool BF16>
+template <int D, bool BF16, int NB>
 __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NP = D * E / 16;        // 16-byte pieces per row
   constexpr int RPP = 256 / NP;         // rows per pass
-  const int unit = blockIdx.y;          // pair * Hkv + head
-  const int pair = unit / P.hkv, head = unit % P.hkv;
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
   const int mode = P.modes[unit];
   const int T = P.seq_len;
   const uint64_t row_bytes = (uint64_t)D * E;
   const uint64_t head_off = (uint64_t)head * T * row_bytes;
-  const uint8_t* k0 = static_cast<const uint8_t*>(P.k[2 * pair]) + head_off;
-  const uint8_t* k1 = static_cast<const uint8_t*>(P.k[2 * pair + 1]) + head_off;
-  const uint8_t* v0 = static_cast<const uint8_t*>(P.v[2 * pair]) + head_off;
-  const uint8_t* v1 = static_cast<const uint8_t*>(P.v[2 * pair + 1]) + head_off;
+  const uint8_t* kx[NB];
+  const uint8_t* vx[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    kx[n] = static_cast<const uint8_t*>(P.k[first + n]) + head_off;
+    vx[n] = static_cast<const uint8_t*>(P.v[first + n]) + head_off;
+  }
   uint8_t* seg = P.cache + P.seg_off[unit];
   const bool c8 = BF16 && P.coef8;      // shared planes in FP8 E4M3: 8 bytes per 16-byte input piece
-  const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E);
+  const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E, NB);
   const int piece = threadIdx.x % NP;
   const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
 #pragma unroll 2
@@ -76,22 +95,25 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
     const int t = row0 + r;
     if (t >= T) break;
     const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
-    const uint4 ka = *reinterpret_cast<const uint4*>(k0 + off);
-    const uint4 kb = *reinterpret_cast<const uint4*>(k1 + off);
-    const uint4 va = *reinterpret_cast<const uint4*>(v0 + off);
-    const uint4 vb = *reinterpret_cast<const uint4*>(v1 + off);
+    uint4 ka[NB], va[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      ka[n] = *reinterpret_cast<const uint4*>(kx[n] + off);
+      va[n] = *reinterpret_cast<const uint4*>(vx[n] + off);
+    }
     if (mode == kExact) {
-      *reinterpret_cast<uint4*>(seg + L.k0 + off) = ka;
-      *reinterpret_cast<uint4*>(seg + L.k1 + off) = kb;
-      *reinterpret_cast<uint4*>(seg + L.v0 + off) = va;
-      *reinterpret_cast<uint4*>(seg + L.v1 + off) = vb;
+#pragma unroll
+      for (int n = 0; n < NB; ++n) {
+        *reinterpret_cast<uint4*>(seg + L.ek[n] + off) = ka[n];
+        *reinterpret_cast<uint4*>(seg + L.ev[n] + off) = va[n];
+      }
     } else if (c8) {
       const uint64_t o8 = (uint64_t)t * D + piece * 8;
-      *reinterpret_cast<uint2*>(seg + L.mk + o8) = pair_mean_e4m3(ka, kb);
-      *reinterpret_cast<uint2*>(seg + L.mv + o8) = pair_mean_e4m3(va, vb);
+      *reinterpret_cast<uint2*>(seg + L.mk + o8) = mean_piece_e4m3<NB>(ka);
+      *reinterpret_cast<uint2*>(seg + L.mv + o8) = mean_piece_e4m3<NB>(va);
     } else {
-      *reinterpret_cast<uint4*>(seg + L.mk + off) = pair_mean<BF16>(ka, kb);
-      *reinterpret_cast<uint4*>(seg + L.mv + off) = pair_mean<BF16>(va, vb);
+      *reinterpret_cast<uint4*>(seg + L.mk + off) = mean_piece<BF16, NB>(ka);
+      *reinterpret_cast<uint4*>(seg + L.mv + off) = mean_piece<BF16, NB>(va);
     }
   }
 }
@@ -114,18 +136,19 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   constexpr int NW = D / 32;
   __shared__ float4 diff[64 * D / 4];
 
-  const int unit = blockIdx.y;
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
   const int tensor = blockIdx.z;        // 0: K, 1: V
   if (P.modes && P.modes[unit] != kResidual) return;
-  const int pair = unit / P.hkv, head = unit % P.hkv;
   const int T = P.seq_len, k = P.topk;
   const int lane = threadIdx.x;
   const int tok0 = blockIdx.x * 64;
   const uint64_t row_bytes = (uint64_t)D * E;
   const void* const* src = tensor ? P.v : P.k;
   const uint64_t head_off = (uint64_t)head * T * row_bytes;
-  const uint8_t* xa = static_cast<const uint8_t*>(src[2 * pair]) + head_off;
-  const uint8_t* xb = static_cast<const uint8_t*>(src[2 * pair + 1]) + head_off;
+  const uint8_t* xa = static_cast<const uint8_t*>(src[first]) + head_off;
+  const uint8_t* xb = static_cast<const uint8_t*>(src[first + 1]) + head_off;
 
   // 1. coalesced load of 64 rows, differences into LDS
   {
@@ -190,11 +213,11 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   const int CE = c8 ? 1 : E;            // bytes per stored value
   if (P.modes) {
     uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE);
+    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 2);
     out_idx = seg + (tensor ? L.iv : L.ik);
     out_val = seg + (tensor ? L.vv : L.vk);
   } else {
-    out_idx = P.idx_out + (uint64_t)unit * plane_bytes((uint64_t)T * k);
+    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
     out_val = nullptr;
   }
   out_idx += (uint64_t)t * k;
@@ -250,22 +273,166 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   }
 }
 
+// ---------------------------------------------------------------- residual select, blocks of four
+// The coefficients of the token's block come 16 channels at a time: the
+// wave loads those channels of its 64 tokens from the four layers
+// (coalesced), evaluates the DCT-II(4) butterfly in fp32 with every product
+// and sum rounded on its own, and leaves Z_1..Z_3 in LDS, [token][channel][j]
+// (float4 slots rotated by the token so one-row-per-lane reads spread over
+// the banks).  Each lane then reads its token's 48 values.
+//  pass 1 - threshold: a running list of the RS largest keys (sorted
+//           descending) absorbs each sorted group of 16 keys (one frequency
+//           of one chunk) by the bitonic merge of topk_net.h; tau is its
+//           k-th entry and the list holds every key above tau.
+//  pass 2 - selection in code order (channel, then frequency): every key
+//           above tau and the first keys equal to tau until k are taken;
+//           each taken entry is stored at the lane's running count.
+__device__ __forceinline__ int z4_slot(int t, int q) {  // float4 slot of quarter q (0..11) of token t's row
+  return t * 12 + (q + t) % 12;
+}
+
+template <int D, bool BF16, int RS>
+__global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
+  constexpr int E = BF16 ? 2 : 4;
+  constexpr int CPP = 16 / E;           // channels per input piece
+  constexpr int PPC = 16 / CPP;         // pieces per chunk of 16 channels
+  constexpr int NC = D / 16;            // chunks
+  __shared__ float4 zs[64 * 12];        // [token][16 channels][3] of one chunk
+
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
+  const int tensor = blockIdx.z;        // 0: K, 1: V
+  if (P.modes && P.modes[unit] != kResidual) return;
+  const int T = P.seq_len, k = P.topk;
+  const int lane = threadIdx.x;
+  const int tok0 = blockIdx.x * 64;
+  const uint64_t row_bytes = (uint64_t)D * E;
+  const void* const* src = tensor ? P.v : P.k;
+  const uint64_t head_off = (uint64_t)head * T * row_bytes;
+  const uint8_t* x[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) x[n] = static_cast<const uint8_t*>(src[first + n]) + head_off;
+
+  auto stage = [&](int ch) {  // Z of channels 16 ch .. 16 ch + 15 into LDS
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < PPC; ++i) {
+      const int r = lane / PPC + (64 / PPC) * i, pc = lane % PPC;
+      const int t = min(tok0 + r, T - 1);
+      const uint64_t off = (uint64_t)t * row_bytes + (uint64_t)(ch * PPC + pc) * 16;
+      uint4 v[4];
+#pragma unroll
+      for (int n = 0; n < 4; ++n) v[n] = *reinterpret_cast<const uint4*>(x[n] + off);
+      float z[3 * CPP];
+#pragma unroll
+      for (int c = 0; c < CPP; ++c)
+        dct4_high(chan<BF16>(v[0], c), chan<BF16>(v[1], c), chan<BF16>(v[2], c), chan<BF16>(v[3], c), z[3 * c],
+                  z[3 * c + 1], z[3 * c + 2]);
+#pragma unroll
+      for (int q = 0; q < 3 * CPP / 4; ++q)
+        zs[z4_slot(r, pc * (3 * CPP / 4) + q)] = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
+    }
+    __syncthreads();
+  };
+  auto row = [&](float (&zr)[48]) {
+#pragma unroll
+    for (int q = 0; q < 12; ++q) {
+      const float4 v = zs[z4_slot(lane, q)];
+      zr[4 * q] = v.x;
+      zr[4 * q + 1] = v.y;
+      zr[4 * q + 2] = v.z;
+      zr[4 * q + 3] = v.w;
+    }
+  };
+
+  // pass 1: the RS largest keys
+  uint32_t R[RS];
+#pragma unroll
+  for (int i = 0; i < RS; ++i) R[i] = 0u;
+  for (int ch = 0; ch < NC; ++ch) {
+    stage(ch);
+    float zr[48];
+    row(zr);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      uint32_t g[16];
+#pragma unroll
+      for (int c = 0; c < 16; ++c) g[c] = as_u32(zr[3 * c + j]) & 0x7FFFFFFFu;
+      net::absorb16<RS>(R, g);
+    }
+  }
+  int need_eq;
+  const uint32_t tau = net::list_threshold<RS>(R, k, &need_eq);
+
+  // pass 2: selection in code order, stored at the running count
+  const int t = tok0 + lane;
+  const bool live = t < T;
+  const bool c8 = BF16 && P.coef8;      // values in FP8 E4M3
+  const int CE = c8 ? 1 : E;
+  uint8_t* out_idx;
+  uint8_t* out_val = nullptr;
+  if (P.modes) {
+    uint8_t* seg = P.cache + P.seg_off[unit];
+    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 4);
+    out_idx = seg + (tensor ? L.iv : L.ik);
+    out_val = seg + (tensor ? L.vv : L.vk);
+  } else {
+    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
+  }
+  uint16_t* oi = reinterpret_cast<uint16_t*>(out_idx) + (uint64_t)t * k;
+  const uint64_t ov = (uint64_t)t * k;
+  int s = 0, eq = 0;
+  for (int ch = 0; ch < NC; ++ch) {
+    stage(ch);
+    float zr[48];
+    row(zr);
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+        const float z = zr[3 * c + j];
+        const uint32_t key = as_u32(z) & 0x7FFFFFFFu;
+        const bool take = key > tau || (key == tau && eq < need_eq);
+        eq += key == tau ? 1 : 0;
+        if (take && live && s < k) {  // exactly k are taken; the bound keeps every store inside the row
+          oi[s] = (uint16_t)(4 * (16 * ch + c) + j + 1);
+          if (out_val) {
+            if (c8)
+              out_val[ov + s] = f32_to_e4m3(z);
+            else if constexpr (BF16)
+              reinterpret_cast<uint16_t*>(out_val)[ov + s] = (uint16_t)f32_to_bf16_bits(z);
+            else
+              reinterpret_cast<float*>(out_val)[ov + s] = z;
+          }
+        }
+        s += take ? 1 : 0;
+      }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
-template <int D, bool BF16>
+template <int D, bool BF16, int NB>
 static hipError_t launch_compress_t(const CompressParams& P, hipStream_t s) {
-  const dim3 grid((P.seq_len + kCompressTile - 1) / kCompressTile, P.n_pairs * P.hkv);
-  hipLaunchKernelGGL((compress_dense_kernel<D, BF16>), grid, dim3(256), 0, s, P);
+  const dim3 grid((P.seq_len + kCompressTile - 1) / kCompressTile, P.bl.n * P.hkv);
+  hipLaunchKernelGGL((compress_dense_kernel<D, BF16, NB>), grid, dim3(256), 0, s, P);
   return hipGetLastError();
 }
 
+template <int NB>
+static hipError_t launch_compress_b(const CompressParams& P, hipStream_t s) {
+  if (P.d == 128) return P.bf16 ? launch_compress_t<128, true, NB>(P, s) : launch_compress_t<128, false, NB>(P, s);
+  return P.bf16 ? launch_compress_t<64, true, NB>(P, s) : launch_compress_t<64, false, NB>(P, s);
+}
+
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s) {
-  if (P.d == 128) return P.bf16 ? launch_compress_t<128, true>(P, s) : launch_compress_t<128, false>(P, s);
-  return P.bf16 ? launch_compress_t<64, true>(P, s) : launch_compress_t<64, false>(P, s);
+  if (P.bl.n == 0 || P.seq_len == 0) return hipSuccess;
+  return P.bsize == 4 ? launch_compress_b<4>(P, s) : launch_compress_b<2>(P, s);
 }
 
 template <int D, bool BF16, int GS>
 static hipError_t launch_select_t(const SelectParams& P, int tensors, hipStream_t s) {
-  const dim3 grid((P.seq_len + 63) / 64, P.n_pairs * P.hkv, tensors);
+  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
   hipLaunchKernelGGL((residual_select_kernel<D, BF16, GS>), grid, dim3(64), 0, s, P);
   return hipGetLastError();
 }
@@ -277,8 +444,27 @@ static hipError_t launch_select_d(const SelectParams& P, int tensors, hipStream_
   return launch_select_t<D, BF16, D>(P, tensors, s);
 }
 
+template <int D, bool BF16, int RS>
+static hipError_t launch_select4_t(const SelectParams& P, int tensors, hipStream_t s) {
+  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
+  hipLaunchKernelGGL((residual_select4_kernel<D, BF16, RS>), grid, dim3(64), 0, s, P);
+  return hipGetLastError();
+}
+
+template <int D, bool BF16>
+static hipError_t launch_select4_d(const SelectParams& P, int tensors, hipStream_t s) {
+  if (P.topk <= 16) return launch_select4_t<D, BF16, 16>(P, tensors, s);
+  if (P.topk <= 32) return launch_select4_t<D, BF16, 32>(P, tensors, s);
+  if (P.topk <= 64) return launch_select4_t<D, BF16, 64>(P, tensors, s);
+  return launch_select4_t<D, BF16, 128>(P, tensors, s);
+}
+
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s) {
-  if (P.topk <= 0) return hipSuccess;
+  if (P.topk <= 0 || P.bl.n == 0 || P.seq_len == 0) return hipSuccess;
+  if (P.bsize == 4) {
+    if (P.d == 128) return P.bf16 ? launch_select4_d<128, true>(P, tensors, s) : launch_select4_d<128, false>(P, tensors, s);
+    return P.bf16 ? launch_select4_d<64, true>(P, tensors, s) : launch_select4_d<64, false>(P, tensors, s);
+  }
   if (P.d == 128) return P.bf16 ? launch_select_d<128, true>(P, tensors, s) : launch_select_d<128, false>(P, tensors, s);
   return P.bf16 ? launch_select_d<64, true>(P, tensors, s) : launch_select_d<64, false>(P, tensors, s);
 }

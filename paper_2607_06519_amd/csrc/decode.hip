@@ -3,12 +3,14 @@
 // per token and the sparse residual is added only at its indexed channels;
 // no reconstructed K/V is ever materialised.
 //
-// For a layer l of pair b (sigma = +1 for l = 2b, -1 for l = 2b+1) and the G
-// query heads of a KV head:
-//   shared   : K~ = MK,                     V~ = MV
-//   residual : K~ = MK + sigma * D_K on IK, V~ = MV + sigma * D_V on IV
-//   exact    : K~ = K_l,                    V~ = V_l
-// Logits use the algebraic form q.K~ = q.MK + sigma * sum_j q[IK_j] D_K,j.
+// For layer p of a block of B layers and the G query heads of a KV head:
+//   shared   : K~ = MK,                             V~ = MV
+//   residual : K~ = MK + sum_e w_e value_e at c_e,  V~ likewise
+//   exact    : K~ = K_p,                            V~ = V_p
+// where an entry e is a channel c_e with w_e = +1 (p = 0) or -1 (p = 1) for
+// the stored half difference of a pair, or a code 4c_e + j with
+// w_e = F_4[j][p] for a block of four.  Logits use the algebraic form
+// q.K~ = q.MK + sum_e w_e q[c_e] value_e.
 //
 // decode_splitk (the fp32 cache path; bf16 caches use decode_stream.hip): one
 // workgroup = 4 waves = 512 tokens of one (sequence, KV head); each wave
@@ -77,16 +79,27 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const int wg_tok0 = wgc * kDecodeWgTokens;
   if (wg_tok0 >= T) return;  // uniform over the workgroup
 
-  const int pair = P.layer >> 1, parity = P.layer & 1;
-  const float sigma = parity ? -1.f : 1.f;
-  const uint64_t unit = ((uint64_t)seq * P.n_pairs + pair) * P.hkv + head;
+  const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
+  const bool q4 = P.bsize == 4;
   const int mode = P.modes[unit];
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
   const uint8_t* seg = P.cache + P.seg_off[unit];
-  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E);
-  const uint8_t* kplane = seg + (mode == kExact ? (parity ? L.k1 : L.k0) : L.mk);
-  const uint8_t* vplane = seg + (mode == kExact ? (parity ? L.v1 : L.v0) : L.mv);
+  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E, P.bsize);
+  const uint64_t xplane = plane_bytes((uint64_t)T * D * E);  // exact planes: K_p at p * xplane, V_p at (B + p) * xplane
+  const uint8_t* kplane = seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk);
+  const uint8_t* vplane = seg + (mode == kExact ? (uint64_t)(P.bsize + P.pos) * xplane : L.mv);
+  // channel and weight of residual entry i of an index plane
+  auto entry = [&](const uint8_t* ip, uint64_t i, float& w) -> int {
+    if (q4) {
+      const uint32_t code = reinterpret_cast<const uint16_t*>(ip)[i];
+      const uint32_t j = code & 3u;
+      w = j == 1u ? P.wres[0] : (j == 2u ? P.wres[1] : P.wres[2]);
+      return (int)(code >> 2) & (D - 1);
+    }
+    w = P.wres[0];
+    return ip[i] & (D - 1);
+  };
   const uint8_t* ikp = seg + L.ik;
   const uint8_t* vkp = seg + L.vk;
   const uint8_t* ivp = seg + L.iv;
@@ -143,8 +156,9 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
     }
     if (resid) {
       for (int e = e0; e < e1; ++e) {
-        const int c = ikp[(uint64_t)rc * k + e];
-        const float v = sigma * load_elem<D, BF16>(vkp, (uint64_t)rc * k + e);
+        float w;
+        const int c = entry(ikp, (uint64_t)rc * k + e, w);
+        const float v = w * load_elem<D, BF16>(vkp, (uint64_t)rc * k + e);
 #pragma unroll
         for (int g = 0; g < G; ++g) a[g] = fmaf(q_lds[c * G + g], v, a[g]);
       }
@@ -240,8 +254,9 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
       const int tl = e / k, j = e - tl * k;
       const int row = wtok0 + tl;
       if (row < T) {
-        const int c = ivp[(uint64_t)row * k + j];
-        const float v = sigma * load_elem<D, BF16>(vvp, (uint64_t)row * k + j);
+        float w;
+        const int c = entry(ivp, (uint64_t)row * k + j, w);
+        const float v = w * load_elem<D, BF16>(vvp, (uint64_t)row * k + j);
 #pragma unroll
         for (int g = 0; g < G; ++g) atomicAdd(&sp_lds[wave][g][c], s_lds[wave][g][tl] * v);
       }

@@ -12,7 +12,9 @@
 // or half row (d = 64).
 //  K   - bf16 dot2 of the lane's piece with its piece of every query (held in
 //        registers); residual heads add the lane's residual entry
-//        sigma * q[IK] * D_K; a DPP butterfly then sums over the row's lanes,
+//        w * q[c] * value (B = 2: c the channel, w = +-1 for the stored half
+//        difference; B = 4: code 4c + j, w = F_4[j][p] for layer p of the
+//        block); a DPP butterfly then sums over the row's lanes,
 //        which leaves every lane of the row with the row's logits -- exactly
 //        the probabilities its V pass needs, so nothing goes through LDS;
 //  max - a running reference max, uniform over the wave, that moves (cross-
@@ -20,8 +22,10 @@
 //        it by more than 2^8;
 //  V   - the lane's rows are taken in pairs so one dot2 multiplies two
 //        tokens' values by their two bf16 probabilities; residual heads add
-//        sigma * p * D_V into LDS accumulators, one copy per row of a load,
-//        so the distinct channels of one row never collide.
+//        w * p * value into LDS accumulators, one copy per row of a load
+//        (a row's entries sit on distinct channels for B = 2, so a plain
+//        read-add-write is safe; for B = 4 two frequencies of one channel
+//        can meet, so those adds are LDS atomics).
 // The 4 waves merge in LDS and write one (acc, m, l) record per workgroup;
 // decode_merge combines the records.  HBM bound: no MFMA.
 #include "fdkv_common.h"
@@ -113,8 +117,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const int wgc = blockIdx.x % P.n_wgchunks;
   const int sh = blockIdx.x / P.n_wgchunks;
   const int head = sh % P.hkv, seq = sh / P.hkv;
-  const int pair = P.layer >> 1, parity = P.layer & 1;
-  const uint64_t unit = ((uint64_t)seq * P.n_pairs + pair) * P.hkv + head;
+  const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   // The three per-unit values are fetched together, as scalar loads (the
   // mode byte through its aligned dword; the array is 4-byte aligned), and
   // the exit test below reads all of them: the start-up costs one round trip
@@ -128,7 +131,6 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const int wg_tok0 = wgc * kDecodeWgTokens;
   if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) return;
 
-  const float sigma = parity ? -1.f : 1.f;
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
   // FP8 caches: the shared planes and residual values of shared / residual
@@ -136,14 +138,17 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const bool c8 = C8K && mode != kExact;
   const int ce = c8 ? 1 : 2;
   const uint8_t* seg = P.cache + seg_off;
-  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce);
+  const int nb = P.bsize, ib = index_bytes(nb);
+  const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce, nb);
   const uint64_t dense = (uint64_t)T * D * ce;
-  const auto kr = rsrc(seg + (mode == kExact ? (parity ? L.k1 : L.k0) : L.mk), dense);
-  const auto vr = rsrc(seg + (mode == kExact ? (parity ? L.v1 : L.v0) : L.mv), dense);
-  const auto ikr = rsrc(seg + L.ik, (uint64_t)T * k);
+  const uint64_t xplane = plane_bytes(dense);  // exact planes: K of layer p at p * xplane, V at (B + p) * xplane
+  const auto kr = rsrc(seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk), dense);
+  const auto vr = rsrc(seg + (mode == kExact ? (uint64_t)(nb + P.pos) * xplane : L.mv), dense);
+  const auto ikr = rsrc(seg + L.ik, (uint64_t)T * k * ib);
   const auto vkr = rsrc(seg + L.vk, (uint64_t)T * k * ce);
-  const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k);
+  const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k * ib);
   const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * ce);
+  const float w1 = P.wres[0], w2 = P.wres[1], w3 = P.wres[2];
   const uint8_t* qbase = static_cast<const uint8_t*>(P.q) + ((uint64_t)seq * P.hq + (uint64_t)head * G) * RB;
   const auto qr = rsrc(qbase, (uint64_t)G * RB);
 
@@ -180,9 +185,27 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   // out-of-range offset and reads zeros without touching memory.  With no
   // load behind a branch the compiler can wait for exactly the tile it needs
   // and leave the later tiles' loads in flight.
-  auto run = [&](auto res_tag, auto c8_tag) {
+  auto run = [&](auto res_tag, auto c8_tag, auto q4_tag) {
     constexpr int RES = decltype(res_tag)::value;
     constexpr bool C8 = decltype(c8_tag)::value;  // FP8 planes and residual values
+    constexpr bool Q4 = decltype(q4_tag)::value;  // block of four: uint16 codes 4c + j
+    // channel and weight of a residual entry
+    auto entry = [&](uint32_t ix, float& w) -> int {
+      if constexpr (Q4) {
+        const uint32_t j = ix & 3u;
+        w = j == 1u ? w1 : (j == 2u ? w2 : w3);
+        return (int)(ix >> 2) & (D - 1);
+      } else {
+        w = w1;
+        return (int)ix & (D - 1);
+      }
+    };
+    auto acc_v = [&](float& dst, float x) {
+      if constexpr (Q4)
+        __hip_atomic_fetch_add(&dst, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      else
+        dst += x;
+    };
     constexpr int PD = RES == 0 ? S::PD0 : 1, NB = PD + 1;
 
     auto load = [&](int t, TileBuf<D, G>& b) {
@@ -199,7 +222,8 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
-          b.ki[i] = __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, 0);
+          b.ki[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ikr, ok ? e * 2 : kOob, 0, 0)
+                       : __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, 0);
           b.kv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vkr, ok ? e : kOob, 0, 0)
                        : __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, 0);
         }
@@ -215,7 +239,8 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
-          b.vi[i] = __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, 0);
+          b.vi[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, ok ? e * 2 : kOob, 0, 0)
+                       : __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, 0);
           b.vv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vvr, ok ? e : kOob, 0, 0)
                        : __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, 0);
         }
@@ -238,8 +263,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       if constexpr (RES == 1) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
-          const int c = b.ki[i] & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.kv[i]) : b.kv[i]));
+          float w;
+          const int c = entry(b.ki[i], w);
+          const float v = w * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.kv[i]) : b.kv[i]));
 #pragma unroll
           for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
         }
@@ -249,10 +275,12 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           const uint32_t rc = (uint32_t)min(r0 + i * RPL + rg, T - 1);
           for (int e = pc; e < k; e += NP) {
             const uint32_t x = rc * k + e;
-            const int c = __builtin_amdgcn_raw_buffer_load_b8(ikr, x, 0, 0) & (D - 1);
+            float w;
+            const int c = entry(Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ikr, x * 2, 0, 0)
+                                   : __builtin_amdgcn_raw_buffer_load_b8(ikr, x, 0, 0), w);
             const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vkr, x, 0, 0))
                                     : __builtin_amdgcn_raw_buffer_load_b16(vkr, x * 2, 0, 0);
-            const float v = sigma * bf16_to_f32((uint16_t)raw);
+            const float v = w * bf16_to_f32((uint16_t)raw);
 #pragma unroll
             for (int g = 0; g < G; ++g) s[i][g] = fmaf(q_lds[c * G + g], v, s[i][g]);
           }
@@ -328,10 +356,11 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       if constexpr (RES == 1) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
-          const int c = b.vi[i] & (D - 1);
-          const float v = sigma * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.vv[i]) : b.vv[i]));
+          float w;
+          const int c = entry(b.vi[i], w);
+          const float v = w * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.vv[i]) : b.vv[i]));
 #pragma unroll
-          for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+          for (int g = 0; g < G; ++g) acc_v(sp(wave, rg, g, c), p[i][g] * v);
         }
       } else if constexpr (RES == 2) {
 #pragma unroll
@@ -340,12 +369,14 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           const uint32_t rc = (uint32_t)min(row, T - 1);
           for (int e = pc; e < k; e += NP) {
             const uint32_t x = rc * k + e;
-            const int c = __builtin_amdgcn_raw_buffer_load_b8(ivr, x, 0, 0) & (D - 1);
+            float w;
+            const int c = entry(Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, x * 2, 0, 0)
+                                   : __builtin_amdgcn_raw_buffer_load_b8(ivr, x, 0, 0), w);
             const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vvr, x, 0, 0))
                                     : __builtin_amdgcn_raw_buffer_load_b16(vvr, x * 2, 0, 0);
-            const float v = sigma * bf16_to_f32((uint16_t)raw);
+            const float v = w * bf16_to_f32((uint16_t)raw);
 #pragma unroll
-            for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+            for (int g = 0; g < G; ++g) acc_v(sp(wave, rg, g, c), p[i][g] * v);
           }
         }
       }
@@ -380,24 +411,34 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   using R2 = std::integral_constant<int, 2>;
   using F = std::false_type;
   using Tr = std::true_type;
+  // residual heads: one entry per lane of a row (k = NP) or any other k, by block size
+  auto run_res = [&](auto c8_tag) {
+    if (nb == 4) {
+      if (k == NP)
+        run(R1{}, c8_tag, Tr{});
+      else
+        run(R2{}, c8_tag, Tr{});
+    } else {
+      if (k == NP)
+        run(R1{}, c8_tag, F{});
+      else
+        run(R2{}, c8_tag, F{});
+    }
+  };
   if constexpr (C8K) {
     if (c8) {
-      if (resid && k == NP)
-        run(R1{}, Tr{});
-      else if (resid)
-        run(R2{}, Tr{});
+      if (resid)
+        run_res(Tr{});
       else
-        run(R0{}, Tr{});
+        run(R0{}, Tr{}, F{});
     } else {
-      run(R0{}, F{});  // exact heads
+      run(R0{}, F{}, F{});  // exact heads
     }
   } else {
-    if (resid && k == NP)
-      run(R1{}, F{});
-    else if (resid)
-      run(R2{}, F{});
+    if (resid)
+      run_res(F{});
     else
-      run(R0{}, F{});
+      run(R0{}, F{}, F{});
   }
 
   // wave totals: the row groups of a load saw different rows

@@ -24,9 +24,66 @@ bool aligned(const void* p, uintptr_t a) { return p && ((reinterpret_cast<uintpt
 int elem_bytes(const fdkv_dims* d) { return d->dtype == FDKV_F32 ? 4 : 2; }
 int coef_bytes(const fdkv_dims* d) { return d->dtype == FDKV_F32 ? 4 : d->dtype == FDKV_BF16 ? 2 : 1; }
 
+// Blocks of a schedule: first layer and size of each, in layer order.
+struct Sched {
+  int n;
+  int first[kMaxBlocks], size[kMaxBlocks];
+};
+
+// Section 4: blocks of four by default, pairs for the first and the last
+// four layers (MIXED); all pairs or all fours otherwise.
+bool make_sched(int L, int schedule, Sched* out) {
+  Sched s{};
+  auto add = [&](int B) {
+    s.first[s.n] = s.n ? s.first[s.n - 1] + s.size[s.n - 1] : 0;
+    s.size[s.n++] = B;
+  };
+  if (schedule == FDKV_SCHED_PAIRS) {
+    if (L < 2 || L % 2) return false;
+    for (int i = 0; i < L / 2; ++i) add(2);
+  } else if (schedule == FDKV_SCHED_QUADS) {
+    if (L < 4 || L % 4) return false;
+    for (int i = 0; i < L / 4; ++i) add(4);
+  } else if (schedule == FDKV_SCHED_MIXED) {
+    if (L < 8 || (L - 8) % 4) return false;
+    add(2);
+    add(2);
+    for (int i = 0; i < (L - 8) / 4; ++i) add(4);
+    add(2);
+    add(2);
+  } else {
+    return false;
+  }
+  *out = s;
+  return true;
+}
+
+// The blocks of one size, as a kernel block list.
+BlockList blocks_of_size(const Sched& s, int B) {
+  BlockList bl{};
+  for (int i = 0; i < s.n; ++i)
+    if (s.size[i] == B) {
+      bl.block[bl.n] = (int16_t)i;
+      bl.first[bl.n] = (int16_t)s.first[i];
+      ++bl.n;
+    }
+  return bl;
+}
+
+// Weight of a stored residual value of frequency j = 1..3 at position p of
+// a block: B = 2 stores the layer-0 image D of the half difference (+1 at
+// p = 0, -1 at p = 1); B = 4 stores the coefficient Z_j, weighted by
+// F_4[j][p] = cos(pi (2p + 1) j / 8) / sqrt(2).
+void layer_weights(int B, int p, float w[3]) {
+  for (int j = 1; j <= 3; ++j)
+    w[j - 1] = B == 2 ? (p ? -1.f : 1.f) : (float)(cos(M_PI * (2 * p + 1) * j / 8.0) / sqrt(2.0));
+}
+
 fdkv_status check_dims(const fdkv_dims* d) {
   if (!d) return FDKV_E_INVALID_ARG;
-  if (d->n_layers < 2 || (d->n_layers & 1) || d->n_layers > kMaxPtrLayers) return FDKV_E_INVALID_ARG;
+  if (d->n_layers < 2 || d->n_layers > kMaxPtrLayers) return FDKV_E_INVALID_ARG;
+  Sched sch;
+  if (!make_sched(d->n_layers, d->schedule, &sch)) return FDKV_E_INVALID_ARG;
   if (d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads || d->n_q_heads % d->n_kv_heads) return FDKV_E_INVALID_ARG;
   if (d->head_dim < 1 || d->head_dim > 256) return FDKV_E_INVALID_ARG;
   if (d->topk < 0 || d->topk > d->head_dim) return FDKV_E_INVALID_ARG;
@@ -42,24 +99,31 @@ fdkv_status hip_fail(hipError_t e, const char* what) {
   return FDKV_E_HIP;
 }
 
-uint64_t bytes_per_token(int mode, int d, int k, int e, int c) {
+uint64_t bytes_per_token(int mode, int d, int k, int e, int c, int B) {
   if (mode == kShared) return 2ull * d * c;
-  if (mode == kResidual) return 2ull * d * c + 2ull * k * (1 + c);
-  return 4ull * d * e;
+  if (mode == kResidual) return 2ull * d * c + 2ull * k * (index_bytes(B) + c);
+  return 2ull * B * d * e;
+}
+
+Sched sched_of(const fdkv_dims* d) {
+  Sched s{};
+  make_sched(d->n_layers, d->schedule, &s);
+  return s;
 }
 
 uint64_t probe_chunks(int T) { return (uint64_t)(T + kProbeChunk - 1) / kProbeChunk; }
 
-// Probe workspace regions, each aligned to 256 bytes.
+// Probe workspace regions, each aligned to 256 bytes: residual indices per
+// unit, probe Gram matrices per (layer, KV head), per-chunk partials.
 struct ProbeWs {
   uint64_t idx, gram, part, total;
 };
 ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
-  const uint64_t units = (uint64_t)(d->n_layers / 2) * d->n_kv_heads;
+  const uint64_t units = (uint64_t)sched_of(d).n * d->n_kv_heads;
   ProbeWs w{};
   w.idx = 0;
-  w.gram = w.idx + units * plane_bytes((uint64_t)T * d->topk);
-  w.part = w.gram + plane_bytes(units * d->head_dim * d->head_dim * 4);
+  w.gram = w.idx + units * probe_idx_stride((uint64_t)T, d->topk);
+  w.part = w.gram + plane_bytes((uint64_t)d->n_layers * d->n_kv_heads * d->head_dim * d->head_dim * 4);
   w.total = w.part + plane_bytes(units * probe_chunks(T) * 2 * 4);
   return w;
 }
@@ -84,12 +148,26 @@ const char* fdkv_status_string(int32_t s) {
 
 const char* fdkv_last_error(void) { return g_last_error.c_str(); }
 
+fdkv_status fdkv_blocks(const fdkv_dims* dims, int32_t* n_blocks, int32_t* first_layer, int32_t* block_size) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (!n_blocks) return FDKV_E_INVALID_ARG;
+  const Sched s = sched_of(dims);
+  *n_blocks = s.n;
+  for (int i = 0; i < s.n; ++i) {
+    if (first_layer) first_layer[i] = s.first[i];
+    if (block_size) block_size[i] = s.size[i];
+  }
+  return FDKV_OK;
+}
+
 fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, const uint8_t* modes,
                         uint64_t* seg_offsets, uint64_t* total_bytes) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (batch < 1 || !seq_lens || !modes || !total_bytes) return FDKV_E_INVALID_ARG;
-  const int units = dims->n_layers / 2 * dims->n_kv_heads;
+  const Sched sch = sched_of(dims);
+  const int units = sch.n * dims->n_kv_heads;
   for (int b = 0; b < batch; ++b) {
     if (seq_lens[b] < 0) return FDKV_E_INVALID_ARG;
     for (int u = 0; u < units; ++u)
@@ -101,7 +179,8 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
     for (int u = 0; u < units; ++u) {
       const size_t i = (size_t)b * units + u;
       if (seg_offsets) seg_offsets[i] = off;
-      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e, c).total;
+      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e, c,
+                        sch.size[u / dims->n_kv_heads]).total;
     }
   *total_bytes = off;
   return FDKV_OK;
@@ -114,17 +193,26 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   if (st != FDKV_OK) return st;
   if (seq_len < 0 || !errors || !modes_out) return FDKV_E_INVALID_ARG;
   if (budget_bytes == 0 && !(lambda >= 0.0)) return FDKV_E_INVALID_ARG;
-  const int units = dims->n_layers / 2 * dims->n_kv_heads;
+  const Sched sch = sched_of(dims);
+  const int units = sch.n * dims->n_kv_heads;
   const int d = dims->head_dim, k = dims->topk, e = elem_bytes(dims), c = coef_bytes(dims);
-  double om[3];
-  const double full = (double)bytes_per_token(kExact, d, k, e, c);
-  for (int m = 0; m < 3; ++m) om[m] = (double)bytes_per_token(m, d, k, e, c) / full;
-  uint64_t seg[3];
-  for (int m = 0; m < 3; ++m) seg[m] = seg_layout(m, (uint64_t)seq_len, d, k, e, c).total;
+  // Omega and segment bytes per block size (index 0: pairs, 1: blocks of four)
+  double omB[2][3];
+  uint64_t segB[2][3];
+  for (int bi = 0; bi < 2; ++bi) {
+    const int B = bi ? 4 : 2;
+    const double full = (double)bytes_per_token(kExact, d, k, e, c, B);
+    for (int m = 0; m < 3; ++m) {
+      omB[bi][m] = (double)bytes_per_token(m, d, k, e, c, B) / full;
+      segB[bi][m] = seg_layout(m, (uint64_t)seq_len, d, k, e, c, B).total;
+    }
+  }
+  auto quad = [&](int u) { return sch.size[u / dims->n_kv_heads] == 4 ? 1 : 0; };
 
   auto decide = [&](double lam, uint8_t* out) {
     uint64_t fp = 0;
     for (int u = 0; u < units; ++u) {
+      const double* om = omB[quad(u)];
       const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
       int best = 0;
       double bc = E[0] + lam * om[0];
@@ -136,7 +224,7 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
         }
       }
       out[u] = (uint8_t)best;
-      fp += seg[best];
+      fp += segB[quad(u)][best];
     }
     return fp;
   };
@@ -149,6 +237,7 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   std::vector<double> cands;
   cands.push_back(0.0);
   for (int u = 0; u < units; ++u) {
+    const double* om = omB[quad(u)];
     const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
     for (int i = 0; i < 3; ++i)
       for (int j = i + 1; j < 3; ++j) {
@@ -201,18 +290,16 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(ws);
 
+  const Sched sch = sched_of(dims);
   SelectParams sp{};
   for (int l = 0; l < dims->n_layers; ++l) sp.k[l] = sp.v[l] = k_layers[l];
   sp.modes = nullptr;
   sp.idx_out = base + w.idx;
   sp.seq_len = seq_len;
-  sp.n_pairs = dims->n_layers / 2;
   sp.hkv = dims->n_kv_heads;
   sp.d = dims->head_dim;
   sp.topk = dims->topk;
   sp.bf16 = dims->dtype != FDKV_F32;
-  hipError_t e = launch_residual_select(sp, 1, s);
-  if (e != hipSuccess) return hip_fail(e, "residual_select");
 
   ProbeParams pp{};
   for (int l = 0; l < dims->n_layers; ++l) {
@@ -224,7 +311,8 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   pp.partial = reinterpret_cast<float*>(base + w.part);
   pp.errors = errors_out;
   pp.seq_len = seq_len;
-  pp.n_pairs = dims->n_layers / 2;
+  pp.n_blocks = sch.n;
+  for (int i = 0; i < sch.n; ++i) pp.bsizes[i] = (int8_t)sch.size[i];
   pp.hkv = dims->n_kv_heads;
   pp.hq = dims->n_q_heads;
   pp.d = dims->head_dim;
@@ -232,8 +320,17 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   pp.n_probe = n_probe;
   pp.n_chunks = (int)probe_chunks(seq_len);
   pp.bf16 = dims->dtype != FDKV_F32;
-  e = launch_probe(pp, s);
-  if (e != hipSuccess) return hip_fail(e, "probe");
+  for (int B = 2; B <= 4; B += 2) {
+    sp.bl = pp.bl = blocks_of_size(sch, B);
+    sp.bsize = pp.bsize = B;
+    if (sp.bl.n == 0) continue;
+    hipError_t e = launch_residual_select(sp, 1, s);
+    if (e != hipSuccess) return hip_fail(e, "residual_select");
+    e = launch_probe(pp, s);
+    if (e != hipSuccess) return hip_fail(e, "probe");
+  }
+  const hipError_t e = launch_probe_finalize(pp, s);
+  if (e != hipSuccess) return hip_fail(e, "probe_finalize");
   return FDKV_OK;
 }
 
@@ -249,41 +346,31 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   if (seq_len == 0) return FDKV_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
 
+  const Sched sch = sched_of(dims);
   CompressParams cp{};
-  for (int l = 0; l < dims->n_layers; ++l) {
-    cp.k[l] = k_layers[l];
-    cp.v[l] = v_layers[l];
-  }
-  cp.modes = modes;
-  cp.seg_off = seg_offsets;
-  cp.cache = static_cast<uint8_t*>(cache);
-  cp.seq_len = seq_len;
-  cp.n_pairs = dims->n_layers / 2;
-  cp.hkv = dims->n_kv_heads;
-  cp.d = dims->head_dim;
-  cp.topk = dims->topk;
-  cp.bf16 = dims->dtype != FDKV_F32;
-  cp.coef8 = dims->dtype == FDKV_BF16_E4M3;
-  hipError_t e = launch_compress_dense(cp, s);
-  if (e != hipSuccess) return hip_fail(e, "compress_dense");
-
   SelectParams sp{};
   for (int l = 0; l < dims->n_layers; ++l) {
-    sp.k[l] = k_layers[l];
-    sp.v[l] = v_layers[l];
+    cp.k[l] = sp.k[l] = k_layers[l];
+    cp.v[l] = sp.v[l] = v_layers[l];
   }
-  sp.modes = modes;
-  sp.seg_off = seg_offsets;
-  sp.cache = static_cast<uint8_t*>(cache);
-  sp.seq_len = seq_len;
-  sp.n_pairs = cp.n_pairs;
-  sp.hkv = cp.hkv;
-  sp.d = cp.d;
-  sp.topk = cp.topk;
-  sp.bf16 = cp.bf16;
-  sp.coef8 = cp.coef8;
-  e = launch_residual_select(sp, 2, s);
-  if (e != hipSuccess) return hip_fail(e, "residual_select");
+  cp.modes = sp.modes = modes;
+  cp.seg_off = sp.seg_off = seg_offsets;
+  cp.cache = sp.cache = static_cast<uint8_t*>(cache);
+  cp.seq_len = sp.seq_len = seq_len;
+  cp.hkv = sp.hkv = dims->n_kv_heads;
+  cp.d = sp.d = dims->head_dim;
+  cp.topk = sp.topk = dims->topk;
+  cp.bf16 = sp.bf16 = dims->dtype != FDKV_F32;
+  cp.coef8 = sp.coef8 = dims->dtype == FDKV_BF16_E4M3;
+  for (int B = 2; B <= 4; B += 2) {
+    cp.bl = sp.bl = blocks_of_size(sch, B);
+    cp.bsize = sp.bsize = B;
+    if (cp.bl.n == 0) continue;
+    hipError_t e = launch_compress_dense(cp, s);
+    if (e != hipSuccess) return hip_fail(e, "compress_dense");
+    e = launch_residual_select(sp, 2, s);
+    if (e != hipSuccess) return hip_fail(e, "residual_select");
+  }
   return FDKV_OK;
 }
 
@@ -318,8 +405,14 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
   p.q = q;
   p.out = out;
   p.ws = static_cast<float*>(ws);
-  p.layer = layer;
-  p.n_pairs = dims->n_layers / 2;
+  const Sched sch = sched_of(dims);
+  int blk = 0;
+  while (!(layer < sch.first[blk] + sch.size[blk])) ++blk;
+  p.block = blk;
+  p.pos = layer - sch.first[blk];
+  p.bsize = sch.size[blk];
+  layer_weights(p.bsize, p.pos, p.wres);
+  p.n_blocks = sch.n;
   p.hkv = dims->n_kv_heads;
   p.hq = dims->n_q_heads;
   p.d = dims->head_dim;

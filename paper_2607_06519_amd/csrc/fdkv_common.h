@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "dct4.h"
+
 #define FDKV_HD __host__ __device__ __forceinline__
 
 namespace fdkv {
@@ -19,28 +21,33 @@ FDKV_HD uint32_t as_u32(float f) { return __builtin_bit_cast(uint32_t, f); }
 
 FDKV_HD uint64_t plane_bytes(uint64_t n) { return (n + kPlaneAlign - 1) / kPlaneAlign * kPlaneAlign; }
 
-// Byte offsets of the planes of one (sequence, pair, KV head) segment.
-// Shared:   MK, MV.  Residual: MK, MV, IK, VK, IV, VV.  Exact: K0, K1, V0, V1.
+// Byte offsets of the planes of one (sequence, block, KV head) segment of a
+// block of B = 2 or 4 layers.
+// Shared:   MK, MV.  Residual: MK, MV, IK, VK, IV, VV.
+// Exact:    K of the B layers, then V of the B layers.
+// Residual indices are uint8 channels (B = 2) or uint16 codes 4c + j (B = 4).
 struct SegLayout {
   uint64_t mk, mv, ik, vk, iv, vv;  // shared / residual planes
-  uint64_t k0, k1, v0, v1;          // exact planes
+  uint64_t ek[4], ev[4];            // exact planes, by position in the block
   uint64_t total;
 };
 
+FDKV_HD int index_bytes(int B) { return B == 2 ? 1 : 2; }
+
 // e: bytes per input / exact-plane element; c: bytes per stored coefficient
 // (shared planes and residual values; c < e for FP8 coefficients).
-FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e, int c) {
+FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e, int c, int B) {
   SegLayout s{};
   const uint64_t dense = plane_bytes(T * (uint64_t)d * e);
   const uint64_t coef = plane_bytes(T * (uint64_t)d * c);
-  const uint64_t ip = plane_bytes(T * (uint64_t)k);
+  const uint64_t ip = plane_bytes(T * (uint64_t)k * index_bytes(B));
   const uint64_t vp = plane_bytes(T * (uint64_t)k * c);
   if (mode == kExact) {
-    s.k0 = 0;
-    s.k1 = dense;
-    s.v0 = 2 * dense;
-    s.v1 = 3 * dense;
-    s.total = 4 * dense;
+    for (int i = 0; i < B; ++i) {
+      s.ek[i] = i * dense;
+      s.ev[i] = (B + i) * dense;
+    }
+    s.total = 2 * B * dense;
     return s;
   }
   s.mk = 0;

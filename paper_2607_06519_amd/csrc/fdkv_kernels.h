@@ -7,15 +7,25 @@
 namespace fdkv {
 
 constexpr int kMaxPtrLayers = 128;  // layer pointers carried in kernel arguments
+constexpr int kMaxBlocks = kMaxPtrLayers / 2;
 constexpr int kCompressTile = 64;   // tokens per compress_dense workgroup
+
+// The blocks one launch covers (all of one block size).  Unit arrays (modes,
+// segment offsets, probe errors) are indexed by block * hkv + head.
+struct BlockList {
+  int n;
+  int16_t block[kMaxBlocks];   // block index
+  int16_t first[kMaxBlocks];   // first layer of the block
+};
 
 struct CompressParams {
   const void* k[kMaxPtrLayers];
   const void* v[kMaxPtrLayers];
-  const uint8_t* modes;        // [pairs][hkv]
-  const uint64_t* seg_off;     // [pairs][hkv]
+  const uint8_t* modes;        // [blocks][hkv]
+  const uint64_t* seg_off;     // [blocks][hkv]
   uint8_t* cache;
-  int seq_len, n_pairs, hkv, d, topk;
+  BlockList bl;                // blocks of size bsize
+  int seq_len, bsize, hkv, d, topk;
   bool bf16;
   bool coef8;                  // shared planes in FP8 E4M3 (bf16 inputs)
 };
@@ -26,8 +36,9 @@ struct SelectParams {
   const uint8_t* modes;        // null: select every unit (probe); else residual units only
   const uint64_t* seg_off;
   uint8_t* cache;
-  uint8_t* idx_out;            // probe: [units] planes of plane_bytes(T*k) bytes
-  int seq_len, n_pairs, hkv, d, topk;
+  uint8_t* idx_out;            // probe: [units] planes of plane_bytes(T*k*index bytes) bytes
+  BlockList bl;                // blocks of size bsize
+  int seq_len, bsize, hkv, d, topk;
   bool bf16;
   bool coef8;                  // residual values in FP8 E4M3 (bf16 inputs)
 };
@@ -39,13 +50,16 @@ constexpr int kDecodeWgTokens = kDecodeChunk * kDecodeWaves;
 
 struct DecodeParams {
   const uint8_t* cache;
-  const uint64_t* seg_off;     // [batch][pairs][hkv]
-  const uint8_t* modes;        // [batch][pairs][hkv]
+  const uint64_t* seg_off;     // [batch][blocks][hkv]
+  const uint8_t* modes;        // [batch][blocks][hkv]
   const int32_t* seq_lens;     // [batch]
   const void* q;               // [batch][hq][d]
   void* out;                   // [batch][hq][d]
   float* ws;                   // partials [batch][hkv][n_wgchunks][G][d + 4]
-  int layer, n_pairs, hkv, hq, d, topk, n_wgchunks, batch;
+  int block, pos, bsize;       // the layer's block, its position in it, the block size
+  int n_blocks, hkv, hq, d, topk, n_wgchunks, batch;
+  float wres[3];               // weight of a residual entry of frequency j = 1..3 at this layer
+                               // (B = 2: +-1 for the stored half difference)
   float scale_log2;            // sm_scale * log2(e)
   bool bf16;
   bool coef8;                  // shared planes and residual values of shared / residual heads in FP8 E4M3
@@ -59,18 +73,26 @@ struct ProbeParams {
   const void* k[kMaxPtrLayers];
   const void* qp[kMaxPtrLayers];
   const uint8_t* idx;          // K residual indices per unit (from residual_select)
-  float* gram_q;               // [units][d][d]  sum of q q^T over the unit's probe rows
+  float* gram_q;               // [layers][hkv][d][d]  sums of q q^T over probe rows (see probe.hip)
   float* partial;              // [units][n_chunks][2]
   float* errors;               // [units][2]
-  int seq_len, n_pairs, hkv, hq, d, topk, n_probe, n_chunks;
+  BlockList bl;                // blocks of size bsize
+  int8_t bsizes[kMaxBlocks];   // every block's size (finalize)
+  int seq_len, bsize, n_blocks, hkv, hq, d, topk, n_probe, n_chunks;
   bool bf16;
 };
+
+// Bytes per unit of the probe's residual-index workspace (room for uint16 codes).
+__host__ __device__ __forceinline__ uint64_t probe_idx_stride(uint64_t T, int k) {
+  return (T * (uint64_t)k * 2 + 255) / 256 * 256;
+}
 
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s);
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s);
 hipError_t launch_decode(const DecodeParams& P, hipStream_t s);
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K part
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
-hipError_t launch_probe(const ProbeParams& P, hipStream_t s);
+hipError_t launch_probe(const ProbeParams& P, hipStream_t s);           // the blocks of P.bl (one size)
+hipError_t launch_probe_finalize(const ProbeParams& P, hipStream_t s);  // every unit
 
 }  // namespace fdkv

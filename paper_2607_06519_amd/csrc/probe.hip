@@ -1,7 +1,7 @@
 // Online routing probe: the logit-reconstruction loss of Eq. (2).
 //
-// For a (pair b, KV head h) unit, let Delta_t be K^(m)_t - K_t of one layer
-// of the pair.  With B = 2 the shared reconstruction misses -D_t for layer
+// Pairs.  For a (pair b, KV head h) unit, let Delta_t be K^(m)_t - K_t of one
+// layer of the pair.  With B = 2 the shared reconstruction misses -D_t for layer
 // 2b and +D_t for layer 2b+1 (D = half the layer difference); the residual
 // reconstruction misses the same vectors with the token's top-k channels
 // zeroed (Dbar).  The squared logit errors summed over probe rows and tokens
@@ -14,14 +14,24 @@
 // logit matrices cuts the work from 2*(2GP)*T*d to 2*T*d^2 multiply-adds per
 // mode (16x less at G = 4, P = 256, d = 128).
 //
-// Kernels: residual_select (compress.hip) writes every unit's K top-k channel
-// indices; probe_qgram forms S_u (MFMA Gram of the probe rows for bf16
-// queries, fp32 VALU for fp32 ones); probe_dgram streams the key pairs and
-// stages bf16(D) and bf16(Dbar) row-major in LDS; both Gram kernels take
-// their v_mfma_f32_32x32x16_bf16 operands with transposing LDS reads
+// Blocks of four.  Layer p of the block misses Delta_{p,t} = M_t - x_{p,t}
+// (shared) or that plus the images F_4[j][p] Z_j[c] of the token's kept
+// coefficients (residual); the layers now differ, so
+//   E_m = sum_p < C_{p,m}, S_p > / (4 G P d)
+// with one Gram matrix per layer of the deviations and of the probe rows.
+//
+// Kernels: residual_select / residual_select4 (compress.hip) write every
+// unit's K top-k indices; probe_qgram forms the probe Gram matrices (MFMA
+// Gram of the probe rows for bf16 queries, fp32 VALU for fp32 ones) into
+// per-(layer, KV head) slots: a pair's S_u sits in the slot of its first
+// layer, a block of four has one slot per layer; probe_dgram (pairs) and
+// probe_dgram4 (blocks of four) stream the keys and stage the bf16
+// deviations row-major in LDS; all Gram kernels take their
+// v_mfma_f32_32x32x16_bf16 operands with transposing LDS reads
 // (ds_read_b64_tr_b16) and accumulate the upper-triangular 32x32 blocks.
-// probe_dgram contracts its Gram matrices with S_u in the epilogue and
-// probe_finalize sums the per-workgroup partials in a fixed order in fp64.
+// The deviation Gram kernels contract with the probe Gram matrices in their
+// epilogue and probe_finalize sums the per-workgroup partials in a fixed
+// order in fp64.
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 
@@ -81,6 +91,21 @@ __device__ __forceinline__ bf16x8_t gram_operand(const uint16_t* tile, int kk, i
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
+// 32-bit word w of a 16-byte value.
+__device__ __forceinline__ uint32_t word16(const uint4& v, int w) {
+  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+}
+
+// Channel i of a 16-byte piece, as fp32.
+template <bool BF16>
+__device__ __forceinline__ float chan_of(const uint4& v, int i) {
+  const uint32_t w = word16(v, BF16 ? i >> 1 : i);
+  if constexpr (BF16)
+    return (i & 1) ? bf16_hi(w) : bf16_lo(w);
+  else
+    return as_f32(w);
+}
+
 }  // namespace
 
 template <int D, bool BF16>
@@ -91,16 +116,36 @@ __device__ __forceinline__ float load_q(const void* base, uint64_t i) {
     return static_cast<const float*>(base)[i];
 }
 
-// S_u = sum of q q^T over the probe rows of both layers and the G query heads.
+// One Gram slot of a launch: (list block bi, KV head, layer slot) from the
+// workgroup index.  Pairs: one slot per unit summing the rows of both
+// layers, stored at the pair's first layer.  Blocks of four: one slot per
+// layer.
+struct GramSlot {
+  int layer, nl, head;
+};
+__device__ __forceinline__ GramSlot gram_slot(const ProbeParams& P, int x) {
+  const int ns = P.bsize == 2 ? 1 : 4;
+  const int bi = x / (P.hkv * ns), rem = x % (P.hkv * ns);
+  GramSlot g;
+  g.head = rem / ns;
+  g.layer = P.bl.first[bi] + rem % ns;
+  g.nl = P.bsize == 2 ? 2 : 1;
+  return g;
+}
+__device__ __forceinline__ float* gram_at(const ProbeParams& P, int layer, int head) {
+  return P.gram_q + ((uint64_t)layer * P.hkv + head) * P.d * P.d;
+}
+
+// S = sum of q q^T over the probe rows of the slot's layers and the G query heads.
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void probe_qgram_kernel(ProbeParams P) {
   constexpr int BS = D / 16;  // each thread owns a BS x BS block of S
   constexpr int RT = 32;      // rows per LDS tile
   __shared__ float rows[RT][D];
-  const int unit = blockIdx.x;
-  const int pair = unit / P.hkv, head = unit % P.hkv;
+  const GramSlot gs = gram_slot(P, blockIdx.x);
+  const int head = gs.head;
   const int G = P.hq / P.hkv, NP = P.n_probe;
-  const int NR = 2 * G * NP;
+  const int NR = gs.nl * G * NP;
   const int tid = threadIdx.x;
   const int bi = (tid / 16) * BS, bj = (tid % 16) * BS;
   float acc[BS][BS];
@@ -115,7 +160,7 @@ __global__ __launch_bounds__(256) void probe_qgram_kernel(ProbeParams P) {
       float v = 0.f;
       if (r < NR) {
         const int ls = r / (G * NP), g = (r / NP) % G, p = r % NP;
-        v = load_q<D, BF16>(P.qp[2 * pair + ls], ((uint64_t)(head * G + g) * NP + p) * D + c);
+        v = load_q<D, BF16>(P.qp[gs.layer + ls], ((uint64_t)(head * G + g) * NP + p) * D + c);
       }
       rows[rr][c] = v;
     }
@@ -134,18 +179,18 @@ __global__ __launch_bounds__(256) void probe_qgram_kernel(ProbeParams P) {
         for (int j = 0; j < BS; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
     }
   }
-  float* S = P.gram_q + (uint64_t)unit * D * D;
+  float* S = gram_at(P, gs.layer, head);
 #pragma unroll
   for (int i = 0; i < BS; ++i)
 #pragma unroll
     for (int j = 0; j < BS; ++j) S[(bi + i) * D + bj + j] = acc[i][j];
 }
 
-// S_u as the MFMA Gram matrix of the unit's 2GP bf16 probe rows (exact
-// products, fp32 sums), upper-triangular 32x32 blocks only (the only ones
-// probe_dgram reads).  One workgroup per unit; 64 rows per step, the next
-// step's loads in flight during the current step's MFMAs; the four waves
-// split the blocks.
+// S as the MFMA Gram matrix of the slot's bf16 probe rows (exact products,
+// fp32 sums), upper-triangular 32x32 blocks only (the only ones the
+// deviation kernels read).  One workgroup per slot; 64 rows per step, the
+// next step's loads in flight during the current step's MFMAs; the four
+// waves split the blocks.
 template <int D>
 __global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
   constexpr int NPc = D / 8;                     // 16-byte pieces per row
@@ -155,15 +200,15 @@ __global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
   constexpr int LPT = R * NPc / 256;             // loads per thread per step
   constexpr TriTiles<NB> tri{};
   __shared__ __attribute__((aligned(16))) uint16_t tile[R * LDR];
-  const int unit = blockIdx.x;
-  const int pair = unit / P.hkv, head = unit % P.hkv;
+  const GramSlot gs = gram_slot(P, blockIdx.x);
+  const int head = gs.head;
   const int G = P.hq / P.hkv, NP = P.n_probe;
-  const int NR = 2 * G * NP;
+  const int NR = gs.nl * G * NP;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const uint32_t RB = D * 2;
   const uint64_t span = (uint64_t)G * NP * RB;   // bytes of one layer's probe rows for this head
-  const auto q0 = make_rsrc(static_cast<const uint8_t*>(P.qp[2 * pair]) + (uint64_t)head * span, span);
-  const auto q1 = make_rsrc(static_cast<const uint8_t*>(P.qp[2 * pair + 1]) + (uint64_t)head * span, span);
+  const auto q0 = make_rsrc(static_cast<const uint8_t*>(P.qp[gs.layer]) + (uint64_t)head * span, span);
+  const auto q1 = make_rsrc(static_cast<const uint8_t*>(P.qp[gs.layer + gs.nl - 1]) + (uint64_t)head * span, span);
   f32x16_t acc[TPW];
 #pragma unroll
   for (int i = 0; i < TPW; ++i)
@@ -199,7 +244,7 @@ __global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
     }
     __syncthreads();
   }
-  float* S = P.gram_q + (uint64_t)unit * D * D;
+  float* S = gram_at(P, gs.layer, head);
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t / TPW != wave) continue;
@@ -231,15 +276,17 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[2][R * LDR];  // [D, Dbar][token][channel]
   __shared__ float red[4];
 
-  const int unit = blockIdx.y, chunk = blockIdx.x;
-  const int pair = unit / P.hkv, head = unit % P.hkv;
+  const int chunk = blockIdx.x;
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
   const int T = P.seq_len, k = P.topk;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const uint64_t RB = (uint64_t)D * E;
   const uint64_t plane = (uint64_t)T * RB;
-  const auto ka = make_rsrc(static_cast<const uint8_t*>(P.k[2 * pair]) + (uint64_t)head * plane, plane);
-  const auto kb = make_rsrc(static_cast<const uint8_t*>(P.k[2 * pair + 1]) + (uint64_t)head * plane, plane);
-  const uint8_t* idx = P.idx + (uint64_t)unit * plane_bytes((uint64_t)T * k);
+  const auto ka = make_rsrc(static_cast<const uint8_t*>(P.k[first]) + (uint64_t)head * plane, plane);
+  const auto kb = make_rsrc(static_cast<const uint8_t*>(P.k[first + 1]) + (uint64_t)head * plane, plane);
+  const uint8_t* idx = P.idx + (uint64_t)unit * probe_idx_stride(T, k);
   const int t_begin = chunk * kProbeChunk;
   const int t_end = min(T, t_begin + kProbeChunk);
   const int mat = wave >> 1;                      // 0: D, 1: Dbar
@@ -326,7 +373,7 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   }
 
   // < C, S_u >, off-diagonal blocks counted twice (both matrices symmetric)
-  const float* S = P.gram_q + (uint64_t)unit * D * D;
+  const float* S = gram_at(P, first, head);
   float part = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -345,36 +392,194 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   if (tid < 2) P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + tid] = red[2 * tid] + red[2 * tid + 1];
 }
 
+// Blocks of four: Gram matrices of the eight deviation matrices (4 layers x
+// shared / residual) over one chunk of kProbeChunk tokens, contracted with
+// the layers' probe Gram matrices.  R tokens per step: each thread takes
+// one or two 16-byte pieces of a token row from all four layers, forms the
+// block mean, the layer deviations, the coefficients Z_1..Z_3 (the same fp32
+// butterfly as residual_select4) and the images of the token's kept
+// coefficients, and writes the eight bf16 rows to LDS; wave w accumulates
+// layer w / 2, shared (w even) or residual (w odd).
+template <int D, bool BF16>
+__global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
+  constexpr int E = BF16 ? 2 : 4;
+  constexpr int NPc = D * E / 16;                // 16-byte input pieces per row
+  constexpr int CPP = 16 / E;                    // channels per piece
+  constexpr int NB = D / 32, NT = NB * (NB + 1) / 2;
+  constexpr int R = 512 / NPc > 32 ? 512 / NPc : 32, LDR = D + 16;
+  constexpr int LPT = R * NPc / 512;             // pieces per thread per step
+  constexpr TriTiles<NB> tri{};
+  static_assert(LPT >= 1 && R % 16 == 0, "shape");
+  __shared__ __attribute__((aligned(16))) uint16_t tile[8][R * LDR];  // [layer * 2 + residual][token][channel]
+  __shared__ float red[8];
+
+  const int chunk = blockIdx.x;
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
+  const int T = P.seq_len, k = P.topk;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const uint64_t RB = (uint64_t)D * E;
+  const uint64_t plane = (uint64_t)T * RB;
+  __amdgpu_buffer_rsrc_t kr[4];
+#pragma unroll
+  for (int n = 0; n < 4; ++n) kr[n] = make_rsrc(static_cast<const uint8_t*>(P.k[first + n]) + (uint64_t)head * plane, plane);
+  const uint16_t* codes = reinterpret_cast<const uint16_t*>(P.idx + (uint64_t)unit * probe_idx_stride(T, k));
+  const bool k16 = k == 16;                       // a token's codes are two 16-byte loads
+  const auto ir = make_rsrc(codes, k16 ? (uint64_t)T * 32 : 0);
+  const int t_begin = chunk * kProbeChunk;
+  const int t_end = min(T, t_begin + kProbeChunk);
+  const float F1[4] = {kDct4A, kDct4B, -kDct4B, -kDct4A};   // F_4[1][p]
+  const float F2[4] = {0.5f, -0.5f, -0.5f, 0.5f};           // F_4[2][p]
+  const float F3[4] = {kDct4B, -kDct4A, kDct4A, -kDct4B};   // F_4[3][p]
+
+  f32x16_t acc[NT];
+#pragma unroll
+  for (int i = 0; i < NT; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  uint4 rx[LPT][4], rc[LPT][2];
+  auto load = [&](int t0) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 512 * j, t = t0 + i / NPc, pc = i % NPc;
+      const bool ok = t < t_end;
+#pragma unroll
+      for (int n = 0; n < 4; ++n) rx[j][n] = load16(kr[n], ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
+      rc[j][0] = load16(ir, ok ? (uint32_t)t * 32 : kOobOff);       // reads 0 unless k = 16
+      rc[j][1] = load16(ir, ok ? (uint32_t)t * 32 + 16 : kOobOff);
+    }
+  };
+  load(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += R) {
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int i = tid + 512 * j, row = i / NPc, pc = i % NPc, t = t0 + row;
+      // kept (channel, frequency) pairs of this piece: bit 3 c + j - 1
+      uint32_t kept = 0;
+      if (k16) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const uint32_t w = word16(rc[j][e >> 3], (e >> 1) & 3);
+          const uint32_t code = (e & 1) ? (w >> 16) : (w & 0xFFFFu);
+          const uint32_t c = (code >> 2) - (uint32_t)(pc * CPP);
+          kept |= (c < (uint32_t)CPP && (code & 3u) != 0u) ? 1u << (3 * c + (code & 3u) - 1) : 0u;
+        }
+      } else if (t < t_end) {
+        for (int e = 0; e < k; ++e) {
+          const uint32_t code = codes[(uint64_t)t * k + e];
+          const uint32_t c = (code >> 2) - (uint32_t)(pc * CPP);
+          if (c < (uint32_t)CPP && (code & 3u) != 0u) kept |= 1u << (3 * c + (code & 3u) - 1);
+        }
+      }
+      uint32_t hw[8][CPP / 2];
+#pragma unroll
+      for (int c = 0; c < CPP; ++c) {
+        float x[4];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) x[n] = chan_of<BF16>(rx[j][n], c);
+        float z1, z2, z3;
+        dct4_high(x[0], x[1], x[2], x[3], z1, z2, z3);
+        const float m = ((x[0] + x[3]) + (x[1] + x[2])) * 0.25f;
+        const float k1 = (kept >> (3 * c)) & 1u ? z1 : 0.f;
+        const float k2 = (kept >> (3 * c + 1)) & 1u ? z2 : 0.f;
+        const float k3 = (kept >> (3 * c + 2)) & 1u ? z3 : 0.f;
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          const float dev = m - x[n];
+          const float dres = dev + (F1[n] * k1 + F2[n] * k2 + F3[n] * k3);
+          const uint32_t hs = f32_to_bf16_bits(dev), hr = f32_to_bf16_bits(dres);
+          if (c & 1) {
+            hw[2 * n][c >> 1] |= hs << 16;
+            hw[2 * n + 1][c >> 1] |= hr << 16;
+          } else {
+            hw[2 * n][c >> 1] = hs;
+            hw[2 * n + 1][c >> 1] = hr;
+          }
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        uint16_t* dst = &tile[m][row * LDR + pc * CPP];
+        if constexpr (CPP == 8)
+          *reinterpret_cast<uint4*>(dst) = make_uint4(hw[m][0], hw[m][1], hw[m][2], hw[m][3]);
+        else
+          *reinterpret_cast<uint2*>(dst) = make_uint2(hw[m][0], hw[m][1]);
+      }
+    }
+    load(t0 + R);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < R / 16; ++kk) {
+      bf16x8_t op[NB];
+#pragma unroll
+      for (int I = 0; I < NB; ++I) op[I] = gram_operand<LDR>(tile[wave], kk, I, lane);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[tri.i[t]], op[tri.j[t]], acc[t], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // < C, S_p >, off-diagonal blocks counted twice (both matrices symmetric)
+  const float* S = gram_at(P, first + (wave >> 1), head);
+  float part = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const float wgt = (tri.i[t] == tri.j[t]) ? 1.f : 2.f;
+    const int col = 32 * tri.j[t] + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 32 * tri.i[t] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      part = fmaf(wgt * acc[t][r], S[row * D + col], part);
+    }
+  }
+  part = wave_sum(part);
+  if (lane == 0) red[wave] = part;
+  __syncthreads();
+  if (tid < 2)
+    P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + tid] = (red[tid] + red[2 + tid]) + (red[4 + tid] + red[6 + tid]);
+}
+
 __global__ void probe_finalize_kernel(ProbeParams P) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  const int units = P.n_pairs * P.hkv;
+  const int units = P.n_blocks * P.hkv;
   if (i >= units * 2) return;
   const int unit = i >> 1, m = i & 1;
   double s = 0.0;
   for (int c = 0; c < P.n_chunks; ++c) s += (double)P.partial[((uint64_t)unit * P.n_chunks + c) * 2 + m];
   const int G = P.hq / P.hkv;
-  P.errors[unit * 2 + m] = (float)(s / (2.0 * G * (double)P.n_probe * (double)P.d));
+  const double nl = (double)P.bsizes[unit / P.hkv];
+  P.errors[unit * 2 + m] = (float)(s / (nl * G * (double)P.n_probe * (double)P.d));
 }
 
 template <int D, bool BF16>
 static hipError_t launch_probe_t(const ProbeParams& P, hipStream_t s) {
-  const int units = P.n_pairs * P.hkv;
+  const int slots = P.bl.n * P.hkv * (P.bsize == 2 ? 1 : 4);
   if constexpr (BF16)
-    hipLaunchKernelGGL((probe_qgram_mfma_kernel<D>), dim3(units), dim3(256), 0, s, P);
+    hipLaunchKernelGGL((probe_qgram_mfma_kernel<D>), dim3(slots), dim3(256), 0, s, P);
   else
-    hipLaunchKernelGGL((probe_qgram_kernel<D, BF16>), dim3(units), dim3(256), 0, s, P);
+    hipLaunchKernelGGL((probe_qgram_kernel<D, BF16>), dim3(slots), dim3(256), 0, s, P);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), dim3(P.n_chunks, units), dim3(256), 0, s, P);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(probe_finalize_kernel, dim3((units * 2 + 255) / 256), dim3(256), 0, s, P);
+  const dim3 grid(P.n_chunks, P.bl.n * P.hkv);
+  if (P.bsize == 4)
+    hipLaunchKernelGGL((probe_dgram4_kernel<D, BF16>), grid, dim3(512), 0, s, P);
+  else
+    hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), grid, dim3(256), 0, s, P);
   return hipGetLastError();
 }
 
 hipError_t launch_probe(const ProbeParams& P, hipStream_t s) {
+  if (P.bl.n == 0) return hipSuccess;
   if (P.d == 128) return P.bf16 ? launch_probe_t<128, true>(P, s) : launch_probe_t<128, false>(P, s);
   return P.bf16 ? launch_probe_t<64, true>(P, s) : launch_probe_t<64, false>(P, s);
+}
+
+hipError_t launch_probe_finalize(const ProbeParams& P, hipStream_t s) {
+  const int units = P.n_blocks * P.hkv;
+  hipLaunchKernelGGL(probe_finalize_kernel, dim3((units * 2 + 255) / 256), dim3(256), 0, s, P);
+  return hipGetLastError();
 }
 
 }  // namespace fdkv

@@ -13,6 +13,9 @@
 // cascade sorts).  Selection: every key above tau, then the lowest channels
 // whose key equals tau until k are chosen.
 //
+// Blocks of four rank 3D keys per token with a streaming variant
+// (absorb16, list_threshold): see below.
+//
 // Everything here is plain C++ usable on the host, so the network can be
 // checked on the CPU against a sort.
 #pragma once
@@ -87,6 +90,39 @@ FDKV_NET_HD uint32_t kth_largest(uint32_t* a, int k) {
 #pragma unroll
   for (int i = 1; i < GS; ++i)
     if (i == k - 1) tau = a[i];
+  return tau;
+}
+
+// Streaming form (blocks of four, 3D keys per token): a list R of the RS
+// largest keys seen so far, sorted descending and starting at zero, absorbs
+// a group of 16 keys (destroyed).  The elementwise max of R's last 16
+// entries against the sorted group reversed leaves R bitonic and holding the
+// RS largest of both; the half-cleaner cascade sorts it again.
+template <int RS>
+FDKV_NET_HD void absorb16(uint32_t* R, uint32_t* g) {
+  static_assert(RS >= 16 && (RS & (RS - 1)) == 0, "list size");
+  sort_desc<16>(g);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint32_t o = g[15 - i];
+    R[RS - 16 + i] = R[RS - 16 + i] > o ? R[RS - 16 + i] : o;
+  }
+  merge_bitonic_desc<RS>(R);
+}
+
+// tau = the k-th largest key (1 <= k <= RS) and the number of keys equal to
+// tau that a selection of k takes (k minus the keys above tau, all of which
+// are in the list).
+template <int RS>
+FDKV_NET_HD uint32_t list_threshold(const uint32_t* R, int k, int* need_eq) {
+  uint32_t tau = R[0];
+#pragma unroll
+  for (int i = 1; i < RS; ++i)
+    if (i == k - 1) tau = R[i];
+  int n = k;
+#pragma unroll
+  for (int i = 0; i < RS; ++i) n -= R[i] > tau ? 1 : 0;
+  *need_eq = n;
   return tau;
 }
 

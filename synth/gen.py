@@ -4,14 +4,15 @@ Every array comes from its own ``numpy`` PCG64 substream keyed by
 ``SeedSequence([seed, cfg_id, tag, ...])``, so any (sequence, layer pair, KV
 head) segment can be regenerated on its own, in any order and on any host.
 
-Recipe of one (sequence, pair b, KV head h) segment, for K and for V alike:
+Recipe of one (sequence, block, KV head h) segment of B layers, for K and for
+V alike (a first-order autoregression along depth):
 
-* ``x[2b]   ~ N(0, 1)`` per token and channel;
-* ``x[2b+1] = rho * x[2b] + sqrt(1 - rho^2) * eps`` with ``eps ~ N(0, 1)``,
+* ``x[l0] ~ N(0, 1)`` per token and channel;
+* ``x[l+1] = rho * x[l] + sqrt(1 - rho^2) * eps`` with ``eps ~ N(0, 1)``,
   one ``rho ~ U(lo, hi)`` per segment shared by K and V, independent ``eps``;
 * needle tokens (positions drawn once per sequence) get ``+amp`` on a seeded
-  set of distinct channels in one layer of the pair (always the odd layer, or
-  a seeded coin per needle), the same channels and layer for K and V;
+  set of distinct channels in one layer of the block (the last layer, or a
+  seeded choice per needle), the same channels and layer for K and V;
 * values are finally rounded to the storage precision (bf16 round to
   nearest even, or kept as fp32).
 
@@ -28,7 +29,7 @@ import numpy as np
 
 from .workloads import Workload
 
-_TAG_SEGMENT, _TAG_POS, _TAG_DECODE_Q, _TAG_PROBE_Q, _TAG_MODES = 1, 2, 3, 4, 5
+_TAG_SEGMENT, _TAG_POS, _TAG_DECODE_Q, _TAG_PROBE_Q, _TAG_MODES, _TAG_SEGMENT4 = 1, 2, 3, 4, 5, 6
 
 
 def _rng(w: Workload, *tags: int) -> np.random.Generator:
@@ -105,12 +106,46 @@ def segment(w: Workload, seq: int, pair: int, head: int):
     return K, V, {"rho": rho, "needles": plan}
 
 
+def block_segment(w: Workload, seq: int, block: int, head: int):
+    """K and V ``[B][T][d]`` of one (sequence, block, KV head) segment of the workload's schedule.
+
+    A pair is the segment of ``segment`` (keyed by its pair index); a block of
+    four draws a four-layer chain from its own substream.
+    """
+    first, B = w.blocks[block]
+    if B == 2:
+        return segment(w, seq, first // 2, head)
+    T, d = w.seq_lens[seq], w.head_dim
+    rng = _rng(w, _TAG_SEGMENT4, seq, first, head)
+    lo, hi = w.rho
+    rho = float(lo) if lo == hi else float(rng.uniform(lo, hi))
+    c1 = np.float32(rho)
+    c2 = np.float32(math.sqrt(1.0 - rho * rho))
+    out = []
+    for _ in range(2):  # K, then V
+        x = np.empty((B, T, d), dtype=np.float32)
+        x[0] = rng.standard_normal((T, d), dtype=np.float32)
+        for n in range(1, B):
+            np.multiply(x[n - 1], c1, out=x[n])
+            x[n] += c2 * rng.standard_normal((T, d), dtype=np.float32)
+        out.append(x)
+    K, V = out
+    plan = []
+    for pos in needle_positions(w, seq):
+        layer = B - 1 if w.needle_layer == "odd" else int(rng.integers(0, B))
+        ch = np.sort(rng.choice(d, size=min(w.needle_channels, d), replace=False))
+        K[layer, pos, ch] += np.float32(w.needle_amp)
+        V[layer, pos, ch] += np.float32(w.needle_amp)
+        plan.append((int(pos), layer, ch))
+    return to_storage(K, w.dtype), to_storage(V, w.dtype), {"rho": rho, "needles": plan}
+
+
 def iter_segments(w: Workload, seq: int, threads: int = 8) -> Iterator[Tuple[int, int, np.ndarray, np.ndarray]]:
-    """Yield ``(pair, head, K, V)`` for every segment of one sequence, drawn in parallel."""
-    units = [(b, h) for b in range(w.n_pairs) for h in range(w.n_kv_heads)]
+    """Yield ``(block, head, K, V)`` for every segment of one sequence, drawn in parallel."""
+    units = [(b, h) for b in range(w.n_blocks) for h in range(w.n_kv_heads)]
 
     def one(u):
-        K, V, _ = segment(w, seq, u[0], u[1])
+        K, V, _ = block_segment(w, seq, u[0], u[1])
         return u[0], u[1], K, V
 
     if threads <= 1:
@@ -135,8 +170,9 @@ def layer_cache(w: Workload, seq: int = 0, threads: int = 1):
     K = np.empty((L, H, T, d), dtype=np.float32)
     V = np.empty((L, H, T, d), dtype=np.float32)
     for b, h, k, v in iter_segments(w, seq, threads):
-        K[2 * b:2 * b + 2, h] = k
-        V[2 * b:2 * b + 2, h] = v
+        first, B = w.blocks[b]
+        K[first:first + B, h] = k
+        V[first:first + B, h] = v
     return K, V
 
 
@@ -161,17 +197,17 @@ def probe_queries(w: Workload, seq: int = 0, layers=None) -> np.ndarray:
 
 
 def fixed_modes(w: Workload, seq: int = 0) -> np.ndarray:
-    """Head modes ``[L/2][Hkv]`` (0 shared, 1 residual, 2 exact) for decode timing.
+    """Head modes ``[blocks][Hkv]`` (0 shared, 1 residual, 2 exact) for decode timing.
 
-    Either the workload's explicit list, or a seeded shuffle of its exact
-    shared/residual/exact counts.
+    Either the workload's explicit list, or a seeded shuffle of its
+    shared/residual/exact counts (scaled to the number of units).
     """
-    n = w.n_pairs * w.n_kv_heads
+    n = w.n_blocks * w.n_kv_heads
     if w.fixed_modes is not None:
         m = np.asarray(w.fixed_modes, dtype=np.uint8)
         if m.size != n:
             m = np.resize(m, n)
-        return m.reshape(w.n_pairs, w.n_kv_heads)
+        return m.reshape(w.n_blocks, w.n_kv_heads)
     if w.mode_counts is None:
         raise ValueError(f"workload {w.name} has no fixed modes")
     cs, cr, ce = w.mode_counts
@@ -181,4 +217,4 @@ def fixed_modes(w: Workload, seq: int = 0) -> np.ndarray:
     m = np.array([0] * ns + [1] * nr + [2] * ne, dtype=np.uint8)
     rng = _rng(w, _TAG_MODES, seq)
     rng.shuffle(m)
-    return m.reshape(w.n_pairs, w.n_kv_heads)
+    return m.reshape(w.n_blocks, w.n_kv_heads)

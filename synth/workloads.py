@@ -17,6 +17,9 @@ The five named workloads are:
 * ``prefill8b`` - the llama8b cache (same seeded draws) plus a 256-row probe window per query
                   head; modes come from the probe and the byte budget of the
                   50/35/15 mix.
+
+Variants: ``llama8b_e4m3`` (FP8 coefficients) and ``llama8b_mixed`` (blocks of
+four layers between pairs at both ends).
 """
 from __future__ import annotations
 
@@ -48,6 +51,7 @@ class Workload:
     n_probe: int = 0               # probe rows per query head
     steps: int = 1                 # decode steps the workload describes
     seed: int = 0
+    schedule: int = 0              # layer blocks: 0 pairs, 1 pairs-fours-pairs (first / last four layers in pairs), 2 fours
     notes: str = field(default="", compare=False)
 
     @property
@@ -57,6 +61,29 @@ class Workload:
     @property
     def n_pairs(self) -> int:
         return self.n_layers // 2
+
+    @property
+    def block_sizes(self) -> Tuple[int, ...]:
+        """Layers per block, in layer order."""
+        L = self.n_layers
+        if self.schedule == 0:
+            return (2,) * (L // 2)
+        if self.schedule == 2:
+            return (4,) * (L // 4)
+        return (2, 2) + (4,) * ((L - 8) // 4) + (2, 2)
+
+    @property
+    def blocks(self) -> Tuple[Tuple[int, int], ...]:
+        """``(first layer, size)`` of every block."""
+        out, first = [], 0
+        for B in self.block_sizes:
+            out.append((first, B))
+            first += B
+        return tuple(out)
+
+    @property
+    def n_blocks(self) -> int:
+        return len(self.block_sizes)
 
     @property
     def group(self) -> int:
@@ -78,7 +105,7 @@ class Workload:
     def dims(self) -> dict:
         return dict(n_layers=self.n_layers, n_kv_heads=self.n_kv_heads,
                     n_q_heads=self.n_q_heads, head_dim=self.head_dim,
-                    topk=self.topk, dtype=self.dtype)
+                    topk=self.topk, dtype=self.dtype, schedule=self.schedule)
 
 
 def _ragged_lengths(seed: int, cfg_id: int, batch: int, lo: int, hi: int) -> Tuple[int, ...]:
@@ -136,4 +163,10 @@ LLAMA8B_E4M3 = dataclasses.replace(
     LLAMA8B, name="llama8b_e4m3", dtype="bf16_e4m3",
     notes="llama8b with FP8 E4M3 shared planes and residual values (bf16 inputs and exact heads)")
 
-WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3)}
+# the 8B decode workload under the paper's default block setting: pairs for the first
+# and last four layers, blocks of four between (10 blocks of 8 KV heads)
+LLAMA8B_MIXED = dataclasses.replace(
+    LLAMA8B, name="llama8b_mixed", schedule=1,
+    notes="llama8b with blocks of four layers between pairs at both ends (the default block setting)")
+
+WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3, LLAMA8B_MIXED)}

@@ -135,3 +135,60 @@ def test_validation_errors_before_any_device_call(lib):
     assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, fake, n.value, None) == -1
     assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, fake, 1 << 40, None) == -2
     assert lib.fdkv_layout(None, 1, None, None, None, None) == -1
+
+
+# ---------------------------------------------------------------- block schedules
+@pytest.mark.parametrize("L,sched", [(32, B.MIXED), (8, B.MIXED), (12, B.MIXED), (16, B.QUADS), (4, B.QUADS),
+                                     (6, B.PAIRS), (128, B.MIXED)])
+def test_blocks_match_oracle(lib, L, sched):
+    first, size = B.blocks(B.dims(L, 2, 4, 64, 8, "bf16", sched))
+    want = O.block_schedule(L, sched)
+    assert list(zip(first.tolist(), size.tolist())) == [tuple(x) for x in want]
+
+
+def test_schedule_validation(lib):
+    n = ctypes.c_int32(0)
+    for L, sched in [(10, B.MIXED), (6, B.MIXED), (6, B.QUADS), (7, B.PAIRS), (8, 3), (8, -1), (130, B.PAIRS)]:
+        assert lib.fdkv_blocks(ctypes.byref(B.dims(L, 2, 4, 64, 8, "bf16", sched)), ctypes.byref(n), None, None) == -1
+
+
+@pytest.mark.parametrize("dtype,d,k,sched", [("bf16", 128, 16, B.MIXED), ("f32", 64, 8, B.QUADS),
+                                             ("bf16_e4m3", 128, 16, B.MIXED), ("bf16", 64, 5, B.QUADS),
+                                             ("f32", 128, 0, B.MIXED)])
+def test_layout_blocks_match_oracle(lib, dtype, d, k, sched):
+    rng = np.random.default_rng(d + k + 7 * sched)
+    L, H, batch = 12, 3, 3
+    dm = B.dims(L, H, 2 * H, d, k, dtype, sched)
+    sizes = [Bs for _, Bs in O.block_schedule(L, sched)]
+    seq = rng.integers(0, 3000, size=batch)
+    seq[1] = 1
+    modes = rng.integers(0, 3, size=(batch, len(sizes), H)).astype(np.uint8)
+    off, total = B.layout(dm, seq, modes)
+    assert total == O.cache_bytes(seq, modes, d, k, dtype, sizes)
+    unit = [O.unit_bytes(int(modes[b, i, h]), int(seq[b]), d, k, dtype, sizes[i])
+            for b in range(batch) for i in range(len(sizes)) for h in range(H)]
+    np.testing.assert_array_equal(off.ravel(), np.concatenate([[0], np.cumsum(unit)[:-1]]))
+
+
+@pytest.mark.parametrize("frac", [0.0, 0.2, 0.6, 1.0])
+def test_route_budget_mixed_matches_oracle(lib, frac):
+    rng = np.random.default_rng(60)
+    d, k, T, H = 128, 16, 32768, 8
+    dm = B.dims(32, H, 32, d, k, "bf16", B.MIXED)
+    sizes = [Bs for _, Bs in O.block_schedule(32, O.MIXED)]
+    usz = [Bs for Bs in sizes for _ in range(H)]
+    n = len(usz)
+    E = _rand_errors(rng, n)
+    E3 = np.concatenate([E.astype(np.float64), np.zeros((n, 1))], axis=1)
+    lo = sum(O.unit_bytes(O.SHARED, T, d, k, "bf16", Bs) for Bs in usz)
+    hi = sum(O.unit_bytes(O.EXACT, T, d, k, "bf16", Bs) for Bs in usz)
+    budget = int(lo + frac * (hi - lo))
+    modes, lam, st = B.route(dm, T, E.reshape(len(sizes), H, 2), budget_bytes=budget)
+    om_modes, om_lam, ok = O.route_budget(E3, T, d, k, "bf16", budget, usz)
+    assert st == 0 and ok
+    np.testing.assert_array_equal(modes.ravel(), om_modes)
+    assert lam == om_lam
+    for lam_fixed in (0.0, 3.0, 40.0):
+        om = np.stack([O.omega(d, k, "bf16", Bs) for Bs in usz])
+        m2, _, _ = B.route(dm, T, E.reshape(len(sizes), H, 2), lam=lam_fixed)
+        np.testing.assert_array_equal(m2.ravel(), O.route(E3, om, lam_fixed))

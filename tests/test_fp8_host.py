@@ -42,3 +42,4 @@ def test_encoder_matches_oracle_rounding(driver):
     np.testing.assert_array_equal(got, want)
     # the sign survives on zero
     assert codes[-1] == 0x80 and codes[-2] == 0x00
+

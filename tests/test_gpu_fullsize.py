@@ -47,8 +47,9 @@ def _build_cache(torch, w, modes_b):
         Kd = torch.empty((w.n_layers, w.n_kv_heads, T, w.head_dim), dtype=tdt, device="cuda")
         Vd = torch.empty_like(Kd)
         for b, h, k, v in gen.iter_segments(w, s, threads=16):
-            Kd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(k).cuda().to(tdt))
-            Vd[2 * b:2 * b + 2, h].copy_(torch.from_numpy(v).cuda().to(tdt))
+            f, nb = w.blocks[b]
+            Kd[f:f + nb, h].copy_(torch.from_numpy(k).cuda().to(tdt))
+            Vd[f:f + nb, h].copy_(torch.from_numpy(v).cuda().to(tdt))
         cache.compress(s, [Kd[l] for l in range(w.n_layers)], [Vd[l] for l in range(w.n_layers)])
         torch.cuda.synchronize()
         del Kd, Vd
@@ -65,18 +66,19 @@ def _check_units(torch, w, cache, modes_b, samples, qscale=8.0):
     for (s, b, h) in samples:
         T = w.seq_lens[s]
         mode = int(modes_b[s, b, h])
-        K, V, _ = gen.segment(w, s, b, h)
+        K, V, _ = gen.block_segment(w, s, b, h)
+        f, nb = w.blocks[b]
         ref = O.compress_unit(K, V, mode, w.topk, w.dtype)
-        got = unpack_unit(buf, int(cache.offsets_host[s, b, h]), mode, T, d, w.topk, w.dtype)
+        got = unpack_unit(buf, int(cache.offsets_host[s, b, h]), mode, T, d, w.topk, w.dtype, nb)
         compare_units(got, ref, w.dtype)
-        for layer in (2 * b, 2 * b + 1):
+        for layer in range(f, f + nb):
             qq = q[layer][s, h * G:(h + 1) * G].astype(np.float64)
-            want = O.decode_unit(ref, mode, layer, qq, 1.0 / math.sqrt(d), d)
+            want = O.decode_unit(ref, mode, layer, qq, 1.0 / math.sqrt(d), d, nb)
             for g in range(G):
                 e = rel_l2(outs[layer][s, h * G + g], want[g])
                 worst = max(worst, e)
                 assert e <= 1e-2, (s, b, h, layer, g, e)
-        log(f"  unit seq={s} pair={b} head={h} mode={mode} T={T} ok")
+        log(f"  unit seq={s} block={b} head={h} mode={mode} T={T} ok")
     return worst
 
 
@@ -94,9 +96,12 @@ def _samples_by_mode(modes_b, per_mode=1, seqs=None):
     return out
 
 
-@pytest.mark.parametrize("name,per_mode", [("llama8b", 2), ("long70b", 1)])
+@pytest.mark.parametrize("name,per_mode", [("llama8b", 2), ("long70b", 1), ("llama8b_quads", 2)])
 def test_fullsize_single_sequence(torch_mod, name, per_mode):
-    w = scaled(WORKLOADS[name], n_layers=2)
+    if name == "llama8b_quads":    # one block of four layers at the full 8B shape
+        w = scaled(WORKLOADS["llama8b_mixed"], n_layers=4, schedule=2)
+    else:
+        w = scaled(WORKLOADS[name], n_layers=2)
     log(f"[case] full-size {name}: T={w.seq_lens[0]} Hkv={w.n_kv_heads} Hq={w.n_q_heads} k={w.topk}")
     modes = gen.fixed_modes(w)[None].copy()
     modes[0, 0, :3] = [0, 1, 2]
@@ -117,21 +122,22 @@ def test_fullsize_ragged_batch(torch_mod):
     log(f"  worst rel-L2 {worst:.3e}")
 
 
-def test_fullsize_probe(torch_mod):
+@pytest.mark.parametrize("nl,sched", [(2, 0), (4, 2)])
+def test_fullsize_probe(torch_mod, nl, sched):
     from paper_2607_06519_amd import binding as B
     from paper_2607_06519_amd.cache import probe, torch_dtype
-    w = scaled(WORKLOADS["prefill8b"], n_layers=2)
+    w = scaled(WORKLOADS["prefill8b"], n_layers=nl, schedule=sched)
     T, P, G = w.seq_lens[0], w.n_probe, w.group
-    log(f"[case] full-size probe: T={T} P={P} G={G}")
+    log(f"[case] full-size probe: T={T} P={P} G={G} block of {nl}")
     tdt = torch_dtype(w.dtype)
-    Kd = torch_mod.empty((2, w.n_kv_heads, T, w.head_dim), dtype=tdt, device="cuda")
+    Kd = torch_mod.empty((nl, w.n_kv_heads, T, w.head_dim), dtype=tdt, device="cuda")
     segs = {}
     for b, h, k, v in gen.iter_segments(w, 0, threads=16):
         Kd[:, h].copy_(torch_mod.from_numpy(k).cuda().to(tdt))
         segs[h] = k
     Q = gen.probe_queries(w, 0)
     Qd = torch_mod.from_numpy(Q).cuda().to(tdt)
-    err, _ = probe(B.dims(**w.dims()), T, [Kd[0], Kd[1]], [Qd[0], Qd[1]], P)
+    err, _ = probe(B.dims(**w.dims()), T, [Kd[l] for l in range(nl)], [Qd[l] for l in range(nl)], P)
     got = err.cpu().numpy()[0].astype(np.float64)
     for h in (0, 5):
         ref = O.routing_errors(segs[h], Q[:, h * G:(h + 1) * G], w.topk)

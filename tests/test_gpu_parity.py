@@ -60,18 +60,20 @@ def _run_compress(w, modes_b, Ks, Vs):
 
 
 def _oracle_units(w, K, V, modes):
-    return {(b, h): O.compress_unit(K[2 * b:2 * b + 2, h], V[2 * b:2 * b + 2, h], int(modes[b, h]), w.topk, w.dtype)
-            for b in range(w.n_pairs) for h in range(w.n_kv_heads)}
+    return {(b, h): O.compress_unit(K[f:f + B, h], V[f:f + B, h], int(modes[b, h]), w.topk, w.dtype)
+            for b, (f, B) in enumerate(w.blocks) for h in range(w.n_kv_heads)}
 
 
-def _check_compress(w, cache, s, ref_units):
+def _check_compress(w, cache, s, ref_units, K=None, V=None):
     buf = cache.host_bytes()
     T = w.seq_lens[s]
     nz = {}
     for (b, h), ref in ref_units.items():
+        f, B = w.blocks[b]
         got = unpack_unit(buf, int(cache.offsets_host[s, b, h]), int(cache.modes_host[s, b, h]), T,
-                          w.head_dim, w.topk, w.dtype)
-        st = compare_units(got, ref, w.dtype)
+                          w.head_dim, w.topk, w.dtype, B)
+        inputs = (K[f:f + B, h], V[f:f + B, h]) if (B == 4 and K is not None) else None
+        st = compare_units(got, ref, w.dtype, inputs=inputs)
         for k_, v_ in st.items():
             nz[k_] = nz.get(k_, 0) + v_
     return nz
@@ -93,6 +95,19 @@ CASES = {
                              seq_lens=(517,), n_needles=3, needle_channels=8, dtype="bf16_e4m3"),
     "e4m3_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=5, seq_lens=(333,),
                       n_needles=3, needle_channels=5, dtype="bf16_e4m3"),
+    # blocks of four layers (DCT-II(4)): all fours, and the mixed setting (pairs at both ends)
+    "quads_bf16": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(1000,),
+                         n_needles=6, schedule=2, fixed_modes=(1, 1)),
+    "mixed_bf16_l12": scaled(WORKLOADS["llama8b"], n_layers=12, n_kv_heads=2, n_q_heads=8, seq_lens=(777,),
+                             n_needles=4, schedule=1, fixed_modes=(0, 1, 2, 1, 1, 2, 0, 1, 1, 0)),
+    "quads_f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=7, seq_lens=(300,),
+                               needle_channels=7, schedule=2, fixed_modes=(1, 2)),
+    "quads_e4m3_g8": scaled(WORKLOADS["long70b"], n_layers=4, n_kv_heads=2, n_q_heads=16, seq_lens=(517,),
+                            n_needles=3, dtype="bf16_e4m3", schedule=2, fixed_modes=(1, 0)),
+    "quads_bf16_d64_k8": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=8,
+                                seq_lens=(450,), n_needles=3, needle_channels=8, schedule=2, fixed_modes=(1, 1)),
+    "quads_bf16_k40": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=40,
+                             seq_lens=(260,), n_needles=2, schedule=2, fixed_modes=(1, 2)),
 }
 
 
@@ -116,7 +131,7 @@ def test_compress_and_decode_parity(torch_dev, name):
     cache, keep = _run_compress(w, modes[None], [K], [V])
     torch_dev.cuda.synchronize()
     ref = _oracle_units(w, K, V, modes)
-    nz = _check_compress(w, cache, 0, ref)
+    nz = _check_compress(w, cache, 0, ref, K, V)
     log(f"  compress ok; values 1 ulp apart: {nz}")
     tol = 1e-5 if w.dtype == "f32" else 1e-2
     worst = 0.0
@@ -178,6 +193,12 @@ PROBE_CASES = {
     "bf16_small": scaled(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=4, n_q_heads=16, seq_lens=(1500,), n_probe=48),
     "bf16_g1_d64": scaled(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=3, n_q_heads=3, head_dim=64, topk=7,
                           seq_lens=(700,), n_probe=20, needle_channels=7),
+    "quads_bf16": scaled(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(1500,), n_probe=48,
+                         schedule=2),
+    "mixed_bf16_d64_k7": scaled(WORKLOADS["prefill8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
+                                seq_lens=(700,), n_probe=20, needle_channels=7, schedule=1),
+    "quads_f32": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, seq_lens=(600,), n_probe=24,
+                        schedule=2),
 }
 
 
@@ -196,15 +217,15 @@ def test_probe_parity(torch_dev, name):
                     w.n_probe)
     got = err.cpu().numpy().astype(np.float64)
     G = w.group
-    ref = np.zeros((w.n_pairs, w.n_kv_heads, 3))
-    for b in range(w.n_pairs):
+    ref = np.zeros((w.n_blocks, w.n_kv_heads, 3))
+    for b, (f, Bs) in enumerate(w.blocks):
         for h in range(w.n_kv_heads):
-            ref[b, h] = O.routing_errors(K[2 * b:2 * b + 2, h], Q[2 * b:2 * b + 2, h * G:(h + 1) * G], w.topk)
+            ref[b, h] = O.routing_errors(K[f:f + Bs, h], Q[f:f + Bs, h * G:(h + 1) * G], w.topk)
     relerr = np.abs(got - ref[..., :2]) / np.abs(ref[..., :2])
     log(f"  max rel error of E: {relerr.max():.3e}")
     assert relerr.max() <= 5e-4
     # modes at several lambdas, ignoring near-ties of the oracle's costs
-    om = O.omega(w.head_dim, w.topk, w.dtype)
+    om = np.stack([O.omega(w.head_dim, w.topk, w.dtype, Bs) for Bs in w.block_sizes for _ in range(w.n_kv_heads)])
     E3 = ref.reshape(-1, 3)
     for lam in np.quantile(E3[:, 0], [0.2, 0.5, 0.8]) * 2.0:
         gm, _, _ = B.route(dm, w.seq_lens[0], got.astype(np.float32), lam=float(lam))

@@ -74,3 +74,27 @@ def test_query_scale():
     p = gen.probe_queries(scaled(w, n_layers=2))
     assert p.shape == (2, 32, 256, 128)
     assert abs(p.std() * math.sqrt(128) - 1.0) < 0.01
+
+
+def test_block_of_four_segments():
+    w = scaled(WORKLOADS["llama8b_mixed"], n_layers=12, n_kv_heads=2, seq_lens=(3000,), n_needles=3)
+    assert w.block_sizes == (2, 2, 4, 2, 2) and w.blocks[2] == (4, 4) and w.n_blocks == 5
+    K, V, info = gen.block_segment(w, 0, 2, 1)
+    K2, V2, _ = gen.block_segment(w, 0, 2, 1)
+    assert K.shape == (4, 3000, 128) and np.array_equal(K, K2) and np.array_equal(V, V2)
+    assert np.array_equal(K, gen.to_storage(K, w.dtype))            # bf16 values
+    # first-order chain along depth: adjacent layers correlate by rho, layers two apart by rho^2
+    mask = np.ones(3000, bool)
+    mask[[p for p, _, _ in info["needles"]]] = False
+    c01 = np.corrcoef(K[0, mask].ravel(), K[1, mask].ravel())[0, 1]
+    c02 = np.corrcoef(K[0, mask].ravel(), K[2, mask].ravel())[0, 1]
+    rho = info["rho"]
+    assert abs(c01 - rho) < 0.01 and abs(c02 - rho * rho) < 0.01
+    # pairs of the mixed schedule are the pair recipe's segments
+    Kp, _, _ = gen.segment(w, 0, 5, 0)
+    Kb, _, _ = gen.block_segment(w, 0, 4, 0)
+    assert np.array_equal(Kp, Kb)
+    Kfull, _ = gen.layer_cache(w, 0)
+    assert np.array_equal(Kfull[4:8, 1], K)
+    m = gen.fixed_modes(w)
+    assert m.shape == (5, 2)
