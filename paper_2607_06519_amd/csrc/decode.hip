@@ -94,7 +94,8 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
     if (q4) {
       const uint32_t code = reinterpret_cast<const uint16_t*>(ip)[i];
       const uint32_t j = code & 3u;
-      w = j == 1u ? P.wres[0] : (j == 2u ? P.wres[1] : P.wres[2]);
+      const uint32_t m1 = 0u - (uint32_t)(j == 1u), m2 = 0u - (uint32_t)(j == 2u), m3 = 0u - (uint32_t)(j == 3u);
+      w = as_f32((as_u32(P.wres[0]) & m1) | (as_u32(P.wres[1]) & m2) | (as_u32(P.wres[2]) & m3));
       return (int)(code >> 2) & (D - 1);
     }
     w = P.wres[0];

@@ -24,8 +24,11 @@
 //        tokens' values by their two bf16 probabilities; residual heads add
 //        w * p * value into LDS accumulators, one copy per row of a load
 //        (a row's entries sit on distinct channels for B = 2, so a plain
-//        read-add-write is safe; for B = 4 two frequencies of one channel
-//        can meet, so those adds are LDS atomics).
+//        read-add-write is safe; for B = 4 up to three frequencies of one
+//        channel sit in adjacent lanes, since codes 4c + j are stored
+//        ascending: a DPP pass hands each run's sum to its first lane and
+//        only that lane writes, which keeps the adds plain as well -- LDS
+//        float atomics tripled the layer time).
 // The 4 waves merge in LDS and write one (acc, m, l) record per workgroup;
 // decode_merge combines the records.  HBM bound: no MFMA.
 #include "fdkv_common.h"
@@ -75,6 +78,26 @@ __device__ __forceinline__ uint32_t e4m3x2_bf16(uint32_t w) {
 __device__ __forceinline__ uint4 widen_e4m3(const uint4& raw) {
   return make_uint4(e4m3x2_bf16<false>(raw.x), e4m3x2_bf16<true>(raw.x), e4m3x2_bf16<false>(raw.y),
                     e4m3x2_bf16<true>(raw.y));
+}
+
+// Runs of equal channels among the residual V entries of one row (blocks of
+// four: codes 4c + j ascending, so a channel's frequencies are adjacent
+// entries, at most three).  Lane pc holds entry e with channel c and
+// contribution x; entries e - 1, e + 1, e + 2 sit in lanes pc - 1, pc + 1,
+// pc + 2 of the same group of NP lanes when they exist (ok1 / ok2 say whether
+// e + 1 / e + 2 exist).  Returns the run's sum on the run's first lane.
+template <int NP>
+__device__ __forceinline__ float run_sum(int c, float x, int pc, bool valid, bool ok1, bool ok2, bool& first) {
+  constexpr int kRowShr1 = 0x111, kRowShl1 = 0x101, kRowShl2 = 0x102;
+  const int cl = __builtin_amdgcn_update_dpp(-1, c, kRowShr1, 0xF, 0xF, false);
+  const int c1 = __builtin_amdgcn_update_dpp(-1, c, kRowShl1, 0xF, 0xF, false);
+  const int c2 = __builtin_amdgcn_update_dpp(-1, c, kRowShl2, 0xF, 0xF, false);
+  const float x1 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kRowShl1, 0xF, 0xF, false));
+  const float x2 = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kRowShl2, 0xF, 0xF, false));
+  first = valid && (pc == 0 || cl != c);
+  const bool n1 = ok1 && pc + 1 < NP && c1 == c;
+  const bool n2 = n1 && ok2 && pc + 2 < NP && c2 == c;
+  return x + (n1 ? x1 : 0.f) + (n2 ? x2 : 0.f);
 }
 
 template <int D, int G>
@@ -189,23 +212,20 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     constexpr int RES = decltype(res_tag)::value;
     constexpr bool C8 = decltype(c8_tag)::value;  // FP8 planes and residual values
     constexpr bool Q4 = decltype(q4_tag)::value;  // block of four: uint16 codes 4c + j
-    // channel and weight of a residual entry
+    // channel and weight of a residual entry (the weight by bit masks: a
+    // select chain here compiles to divergent branches)
     auto entry = [&](uint32_t ix, float& w) -> int {
       if constexpr (Q4) {
         const uint32_t j = ix & 3u;
-        w = j == 1u ? w1 : (j == 2u ? w2 : w3);
+        const uint32_t m1 = 0u - (uint32_t)(j == 1u), m2 = 0u - (uint32_t)(j == 2u), m3 = 0u - (uint32_t)(j == 3u);
+        w = as_f32((as_u32(w1) & m1) | (as_u32(w2) & m2) | (as_u32(w3) & m3));
         return (int)(ix >> 2) & (D - 1);
       } else {
         w = w1;
         return (int)ix & (D - 1);
       }
     };
-    auto acc_v = [&](float& dst, float x) {
-      if constexpr (Q4)
-        __hip_atomic_fetch_add(&dst, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      else
-        dst += x;
-    };
+
     constexpr int PD = RES == 0 ? S::PD0 : 1, NB = PD + 1;
 
     auto load = [&](int t, TileBuf<D, G>& b) {
@@ -358,25 +378,38 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         for (int i = 0; i < NL; ++i) {
           float w;
           const int c = entry(b.vi[i], w);
-          const float v = w * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.vv[i]) : b.vv[i]));
+          float v = w * bf16_to_f32((uint16_t)(C8 ? e4m3x2_bf16<false>(b.vv[i]) : b.vv[i]));
+          bool first = true;
+          if constexpr (Q4) v = run_sum<NP>(c, v, pc, true, true, true, first);
+          if (first) {
 #pragma unroll
-          for (int g = 0; g < G; ++g) acc_v(sp(wave, rg, g, c), p[i][g] * v);
+            for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+          }
         }
       } else if constexpr (RES == 2) {
+        // the lanes of a row walk the row's entries NP at a time, all lanes
+        // in every step (entries past k read nothing and write nothing)
+        const int steps = (k + NP - 1) / NP;
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
           const int row = r0 + i * RPL + rg;
           const uint32_t rc = (uint32_t)min(row, T - 1);
-          for (int e = pc; e < k; e += NP) {
+          for (int st = 0; st < steps; ++st) {
+            const int e = st * NP + pc;
+            const bool valid = e < k;
             const uint32_t x = rc * k + e;
             float w;
-            const int c = entry(Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, x * 2, 0, 0)
-                                   : __builtin_amdgcn_raw_buffer_load_b8(ivr, x, 0, 0), w);
-            const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vvr, x, 0, 0))
-                                    : __builtin_amdgcn_raw_buffer_load_b16(vvr, x * 2, 0, 0);
-            const float v = w * bf16_to_f32((uint16_t)raw);
+            const int c = entry(Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, valid ? x * 2 : kOob, 0, 0)
+                                   : __builtin_amdgcn_raw_buffer_load_b8(ivr, valid ? x : kOob, 0, 0), w);
+            const uint32_t raw = C8 ? e4m3x2_bf16<false>(__builtin_amdgcn_raw_buffer_load_b8(vvr, valid ? x : kOob, 0, 0))
+                                    : __builtin_amdgcn_raw_buffer_load_b16(vvr, valid ? x * 2 : kOob, 0, 0);
+            float v = w * bf16_to_f32((uint16_t)raw);
+            bool first = valid;
+            if constexpr (Q4) v = run_sum<NP>(c, v, pc, valid, e + 1 < k, e + 2 < k, first);
+            if (first) {
 #pragma unroll
-            for (int g = 0; g < G; ++g) acc_v(sp(wave, rg, g, c), p[i][g] * v);
+              for (int g = 0; g < G; ++g) sp(wave, rg, g, c) += p[i][g] * v;
+            }
           }
         }
       }
