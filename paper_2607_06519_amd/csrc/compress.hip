@@ -286,7 +286,10 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
 //           k-th entry and the list holds every key above tau.
 //  pass 2 - selection in code order (channel, then frequency): every key
 //           above tau and the first keys equal to tau until k are taken;
-//           each taken entry is stored at the lane's running count.
+//           each candidate is written to the lane's LDS slot at its running
+//           count, which advances only when it is taken (the count stops at
+//           k, hence k + 1 slots), and the k slots are then stored as packed
+//           words.
 __device__ __forceinline__ int z4_slot(int t, int q) {  // float4 slot of quarter q (0..11) of token t's row
   return t * 12 + (q + t) % 12;
 }
@@ -298,6 +301,7 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
   constexpr int PPC = 16 / CPP;         // pieces per chunk of 16 channels
   constexpr int NC = D / 16;            // chunks
   __shared__ float4 zs[64 * 12];        // [token][16 channels][3] of one chunk
+  __shared__ uint2 slot[64 * (RS + 1)];  // per lane: (code, value bits) of the taken entries
 
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
   const int first = P.bl.first[bi];
@@ -365,23 +369,8 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
   int need_eq;
   const uint32_t tau = net::list_threshold<RS>(R, k, &need_eq);
 
-  // pass 2: selection in code order, stored at the running count
-  const int t = tok0 + lane;
-  const bool live = t < T;
-  const bool c8 = BF16 && P.coef8;      // values in FP8 E4M3
-  const int CE = c8 ? 1 : E;
-  uint8_t* out_idx;
-  uint8_t* out_val = nullptr;
-  if (P.modes) {
-    uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 4);
-    out_idx = seg + (tensor ? L.iv : L.ik);
-    out_val = seg + (tensor ? L.vv : L.vk);
-  } else {
-    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
-  }
-  uint16_t* oi = reinterpret_cast<uint16_t*>(out_idx) + (uint64_t)t * k;
-  const uint64_t ov = (uint64_t)t * k;
+  // pass 2: selection in code order into the lane's slots
+  uint2* my = slot + lane * (RS + 1);
   int s = 0, eq = 0;
   for (int ch = 0; ch < NC; ++ch) {
     stage(ch);
@@ -395,19 +384,66 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
         const uint32_t key = as_u32(z) & 0x7FFFFFFFu;
         const bool take = key > tau || (key == tau && eq < need_eq);
         eq += key == tau ? 1 : 0;
-        if (take && live && s < k) {  // exactly k are taken; the bound keeps every store inside the row
-          oi[s] = (uint16_t)(4 * (16 * ch + c) + j + 1);
-          if (out_val) {
-            if (c8)
-              out_val[ov + s] = f32_to_e4m3(z);
-            else if constexpr (BF16)
-              reinterpret_cast<uint16_t*>(out_val)[ov + s] = (uint16_t)f32_to_bf16_bits(z);
-            else
-              reinterpret_cast<float*>(out_val)[ov + s] = z;
-          }
-        }
+        my[s] = make_uint2((uint32_t)(4 * (16 * ch + c) + j + 1), as_u32(z));
         s += take ? 1 : 0;
       }
+  }
+
+  // store: codes as uint16, values in the coefficient type, packed in words
+  const int t = tok0 + lane;
+  if (t >= T) return;
+  const bool c8 = BF16 && P.coef8;      // values in FP8 E4M3
+  const int CE = c8 ? 1 : E;
+  uint8_t* out_idx;
+  uint8_t* out_val = nullptr;
+  if (P.modes) {
+    uint8_t* seg = P.cache + P.seg_off[unit];
+    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 4);
+    out_idx = seg + (tensor ? L.iv : L.ik);
+    out_val = seg + (tensor ? L.vv : L.vk);
+  } else {
+    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
+  }
+  auto value_bits = [&](int e) -> uint32_t {  // entry e in the coefficient type
+    const float z = as_f32(my[e].y);
+    if (c8) return f32_to_e4m3(z);
+    if constexpr (BF16)
+      return f32_to_bf16_bits(z);
+    else
+      return as_u32(z);
+  };
+  uint32_t* oi = reinterpret_cast<uint32_t*>(out_idx + (uint64_t)t * k * 2);
+  if ((k & 1) == 0) {
+#pragma unroll
+    for (int w = 0; w < RS / 2; ++w)
+      if (2 * w < k) oi[w] = my[2 * w].x | (my[2 * w + 1].x << 16);
+  } else {
+    for (int e = 0; e < k; ++e) reinterpret_cast<uint16_t*>(oi)[e] = (uint16_t)my[e].x;
+  }
+  if (!out_val) return;
+  uint8_t* ov = out_val + (uint64_t)t * k * CE;
+  if (CE == 4) {
+#pragma unroll
+    for (int e = 0; e < RS; ++e)
+      if (e < k) reinterpret_cast<uint32_t*>(ov)[e] = value_bits(e);
+  } else if (CE == 2 && (k & 1) == 0) {
+#pragma unroll
+    for (int w = 0; w < RS / 2; ++w)
+      if (2 * w < k) reinterpret_cast<uint32_t*>(ov)[w] = value_bits(2 * w) | (value_bits(2 * w + 1) << 16);
+  } else if (CE == 1 && (k & 3) == 0) {
+#pragma unroll
+    for (int w = 0; w < RS / 4; ++w)
+      if (4 * w < k)
+        reinterpret_cast<uint32_t*>(ov)[w] = value_bits(4 * w) | (value_bits(4 * w + 1) << 8) |
+                                             (value_bits(4 * w + 2) << 16) | (value_bits(4 * w + 3) << 24);
+  } else {
+    for (int e = 0; e < k; ++e) {
+      const uint32_t v = value_bits(e);
+      if (CE == 1)
+        ov[e] = (uint8_t)v;
+      else
+        reinterpret_cast<uint16_t*>(ov)[e] = (uint16_t)v;
+    }
   }
 }
 
