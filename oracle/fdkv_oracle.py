@@ -19,7 +19,11 @@ the paper (Section 3, "Method"), slowly and without any blocking or fusion:
   modes (Eq. 3), the budget rule raising ``lambda`` until the footprint fits
   (end of Section 3);
 * decode attention over the reconstructed K/V (Section 3, the paragraph after
-  Eq. 3), a full softmax with max subtraction.
+  Eq. 3), a full softmax with max subtraction;
+* generation (the end of Section 3's method): tokens produced while decoding
+  are kept exact in a tail; a refresh compresses the tail into a new span of
+  the cache, routed by Eq. (2) on the tail's own keys with the most recent
+  decode queries as probe rows; decode attends over every span and the tail.
 
 Readings of the paper adopted here (the paper leaves these open):
 
@@ -53,6 +57,9 @@ Readings of the paper adopted here (the paper leaves these open):
 * the budget rule takes the smallest ``lambda`` among 0, the per-head
   breakpoints and +inf whose footprint fits the budget;
 * decode scales logits by ``1/sqrt(d)`` and attends over the cached tokens;
+* a refresh re-decides routing only for the tokens it compresses (earlier
+  spans keep their modes: a shared head's dropped coefficients cannot be
+  recovered), and a span's probe rows are the last decode queries;
 * cache type ``bf16_e4m3`` (the quantised-coefficient variant the paper
   allows at the end of Section 3): inputs, queries and exact heads are bf16;
   the shared and residual coefficients (``M`` and the residual values) are
@@ -469,6 +476,43 @@ def decode_unit(unit, mode: int, layer: int, q, scale: float, d: int, B: int = 2
     Kt = reconstruct_layer(unit, mode, pos, d, "K", B)
     Vt = reconstruct_layer(unit, mode, pos, d, "V", B)
     return attention(q, Kt, Vt, scale)
+
+
+# ----------------------------------------------------------------------------
+# generation: appended tokens and refreshed routing (Section 3, last
+# paragraph of the method: routing is decided after prefill and reused while
+# decoding, with an optional refresh every fixed number of generated tokens)
+# ----------------------------------------------------------------------------
+def decode_spans(spans, tail_K, tail_V, layer: int, q, scale: float, d: int) -> np.ndarray:
+    """Decode over a cache made of compressed spans followed by an exact tail.
+
+    ``spans``: list of ``(unit, mode, B)`` for this (sequence, KV head), each
+    a compressed stretch of consecutive tokens; ``tail_K``/``tail_V``:
+    ``[n][d]`` exact rows of the generated tokens not yet compressed (n may
+    be 0).  Attention runs over the concatenation of every span's
+    reconstruction at ``layer`` and the tail: ``softmax(q K^T s) V``.
+    """
+    Ks, Vs = [], []
+    for unit, mode, B in spans:
+        pos = layer % B
+        Ks.append(reconstruct_layer(unit, mode, pos, d, "K", B))
+        Vs.append(reconstruct_layer(unit, mode, pos, d, "V", B))
+    Ks.append(np.asarray(tail_K, dtype=np.float64).reshape(-1, d))
+    Vs.append(np.asarray(tail_V, dtype=np.float64).reshape(-1, d))
+    K = np.concatenate(Ks, axis=0)
+    V = np.concatenate(Vs, axis=0)
+    if K.shape[0] == 0:
+        return np.zeros((np.asarray(q).shape[0], d))
+    return attention(q, K, V, scale)
+
+
+def refresh_modes(KB_tail, QB_recent, k: int, dtype: str, lam: float) -> int:
+    """Mode of one (block, KV head) for a refreshed span: Eq. (2) on the span's
+    own keys with the most recent decode queries as the probe rows, then the
+    argmin of Eq. (3) at ``lam`` (the span's Omega follows its block size)."""
+    E = routing_errors(KB_tail, QB_recent, k)
+    B = np.asarray(KB_tail).shape[0]
+    return int(route(E[None], omega(np.asarray(KB_tail).shape[-1], k, dtype, B), lam)[0])
 
 
 # ----------------------------------------------------------------------------

@@ -677,3 +677,54 @@ def test_route_budget_mixed_sizes_brute_force():
         modes, lam, ok = O.route_budget(E, T, d, k, "bf16", budget, sizes)
         assert ok and fp(lam) <= budget
         assert all(fp(x) > budget for x in np.linspace(0, lam, 2000, endpoint=False))
+
+
+# ---------------------------------------------------------------- generation: spans and the exact tail
+@pytest.mark.parametrize("B", [2, 4])
+def test_spans_are_token_local(B):
+    """Compressing a sequence in pieces gives the same cache as compressing it whole
+    (every per-token quantity is token-local), so decode over the spans is decode
+    over the whole."""
+    rng = np.random.default_rng(40 + B)
+    T, d = 37, 16
+    K = O.round_bf16(rng.standard_normal((B, T, d)))
+    V = O.round_bf16(rng.standard_normal((B, T, d)))
+    for mode in O.MODES:
+        whole = O.compress_unit(K, V, mode, 5, "bf16")
+        cut = [0, 11, 12, 30, T]
+        spans = [(O.compress_unit(K[:, a:b], V[:, a:b], mode, 5, "bf16"), mode, B) for a, b in zip(cut, cut[1:])]
+        for layer in range(B):
+            q = rng.standard_normal((3, d))
+            want = O.decode_unit(whole, mode, layer, q, 0.25, d, B)
+            got = O.decode_spans(spans, np.zeros((0, d)), np.zeros((0, d)), layer, q, 0.25, d)
+            np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+def test_tail_is_exact_attention():
+    rng = np.random.default_rng(44)
+    T, n, d = 20, 7, 8
+    K = rng.standard_normal((2, T, d))
+    V = rng.standard_normal((2, T, d))
+    tk, tv = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    q = rng.standard_normal((2, d))
+    unit = O.compress_unit(K, V, O.EXACT, 3, "f64")
+    for layer in (0, 1):
+        got = O.decode_spans([(unit, O.EXACT, 2)], tk, tv, layer, q, 0.3, d)
+        Kc, Vc = np.concatenate([K[layer], tk]), np.concatenate([V[layer], tv])
+        want = scipy.special.softmax(q @ Kc.T * 0.3, axis=-1) @ Vc
+        np.testing.assert_allclose(got, want, rtol=1e-12)
+    only_tail = O.decode_spans([], tk, tv, 0, q, 0.3, d)
+    np.testing.assert_allclose(only_tail, scipy.special.softmax(q @ tk.T * 0.3, axis=-1) @ tv, rtol=1e-12)
+    assert np.all(O.decode_spans([], np.zeros((0, d)), np.zeros((0, d)), 0, q, 0.3, d) == 0.0)
+
+
+def test_refresh_routes_the_span():
+    rng = np.random.default_rng(45)
+    X = rng.standard_normal((9, 16))
+    same = np.stack([X, X])
+    Q = rng.standard_normal((2, 2, 5, 16))
+    # identical layers: E_S is zero up to the fp64 noise of F^T F, so any positive penalty picks shared
+    assert O.refresh_modes(same, Q, 4, "bf16", 1e-20) == O.SHARED
+    far = np.stack([X, -X])
+    assert O.refresh_modes(far, Q, 4, "bf16", 0.0) == O.EXACT             # lambda 0: zero error wins
+    assert O.refresh_modes(far, Q, 4, "bf16", math.inf) == O.SHARED
