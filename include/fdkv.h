@@ -207,6 +207,62 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
                              const void* cache, int32_t layer, const void* q, void* out,
                              float sm_scale, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Generation (the end of Section 3's method): routing is decided once after
+ * prefill and reused while decoding, with an optional refresh every fixed
+ * number of generated tokens.  Here a cache is a list of compressed spans
+ * (prefill is span 0; each refresh compresses the tokens generated since
+ * the last one into a new span, routed by fdkv_probe / fdkv_route on those
+ * tokens' own keys) followed by an exact tail that holds the tokens not yet
+ * compressed.  Every span is an ordinary compressed cache (fdkv_layout,
+ * fdkv_compress) of its own tokens; decode attends over all spans and the
+ * tail in one softmax.
+ */
+typedef struct {
+  const int32_t* seq_lens;      /* device [batch]: tokens of each sequence in this span */
+  int32_t max_seq_len;          /* host: the largest entry of seq_lens (sizes the launch) */
+  const uint8_t* modes;         /* device [batch][n_blocks][Hkv], 4-byte aligned */
+  const uint64_t* seg_offsets;  /* device [batch][n_blocks][Hkv] */
+  const void* cache;            /* device, 256-byte aligned */
+} fdkv_span;
+
+typedef struct {
+  const int32_t* lens;          /* device [batch]: rows held by each sequence's tail, 0..cap */
+  int32_t cap;                  /* host: rows per (sequence, KV head) */
+  const void* k;                /* device [batch][Hkv][cap][d] of the decoded layer */
+  const void* v;
+} fdkv_tail;
+
+/*
+ * fdkv_append - device.  Writes one layer's new K and V rows into the exact
+ * tail: row pos[s] of every (sequence s, KV head).
+ *   pos            device int32 [batch]; a sequence whose pos is outside
+ *                  [0, cap) is skipped (nothing written)
+ *   cap            rows per (sequence, KV head) of the tail
+ *   k_new, v_new   device [batch][Hkv][d] (the layer's new token)
+ *   tail_k, tail_v device [batch][Hkv][cap][d] (the layer's tail)
+ */
+fdkv_status fdkv_append(const fdkv_dims* dims, int32_t batch, const int32_t* pos, int32_t cap,
+                        const void* k_new, const void* v_new, void* tail_k, void* tail_v, void* stream);
+
+/* Device workspace bytes fdkv_decode_spans needs: max_seq_lens host [n_spans],
+ * tail_cap the tail's cap, or -1 for no tail.  At most 16 parts (spans + tail). */
+fdkv_status fdkv_decode_spans_workspace(const fdkv_dims* dims, int32_t batch, int32_t n_spans,
+                                        const int32_t* max_seq_lens, int32_t tail_cap, size_t* bytes);
+
+/*
+ * fdkv_decode_spans - device.  One decode step of one layer over n_spans
+ * compressed spans and an optional exact tail (NULL: none):
+ * o = softmax(q K~^T * sm_scale) V~ over every span's reconstructed tokens
+ * and the tail's rows, as fdkv_decode_attn computes it for one span.  A
+ * sequence with no token in any part gets o = 0.  spans is a host array of
+ * n_spans descriptors; the same limits as fdkv_decode_attn apply to each
+ * span, and cap * d * elem_bytes < 2^31 to the tail.
+ */
+fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_spans, const fdkv_span* spans,
+                              const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale,
+                              void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,8 @@ STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: 
           -4: "FDKV_E_BUDGET", -5: "FDKV_E_HIP"}
 
 SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
-           "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn")
+           "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
+           "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 
 
@@ -41,6 +42,15 @@ class Dims(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("schedule", ctypes.c_int32)]
+
+
+class Span(ctypes.Structure):
+    _fields_ = [("seq_lens", ctypes.c_void_p), ("max_seq_len", ctypes.c_int32), ("modes", ctypes.c_void_p),
+                ("seg_offsets", ctypes.c_void_p), ("cache", ctypes.c_void_p)]
+
+
+class Tail(ctypes.Structure):
+    _fields_ = [("lens", ctypes.c_void_p), ("cap", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p)]
 
 
 def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype, schedule=PAIRS) -> Dims:
@@ -77,6 +87,12 @@ def load():
     lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_decode_attn.restype = I32
     lib.fdkv_decode_attn.argtypes = [DP, I32, P, I32, P, P, P, I32, P, P, ctypes.c_float, P, SZ, P]
+    lib.fdkv_append.restype = I32
+    lib.fdkv_append.argtypes = [DP, I32, P, I32, P, P, P, P, P]
+    lib.fdkv_decode_spans_workspace.restype = I32
+    lib.fdkv_decode_spans_workspace.argtypes = [DP, I32, I32, P, I32, P]
+    lib.fdkv_decode_spans.restype = I32
+    lib.fdkv_decode_spans.argtypes = [DP, I32, I32, P, P, I32, P, P, ctypes.c_float, P, SZ, P]
     _lib = lib
     return lib
 
@@ -190,3 +206,28 @@ def decode_attn_raw(d: Dims, batch: int, seq_lens_ptr: int, max_seq_len: int, mo
     return load().fdkv_decode_attn(ctypes.byref(d), batch, seq_lens_ptr, max_seq_len, modes_ptr, offs_ptr,
                                    cache_ptr, layer, q_ptr, out_ptr, ctypes.c_float(sm_scale), ws_ptr, ws_bytes,
                                    ctypes.c_void_p(stream_ptr))
+
+
+# ----------------------------------------------------------------- generation: spans and the exact tail
+def append(d: Dims, batch: int, pos, cap: int, k_new, v_new, tail_k, tail_v, stream=None):
+    """Queue fdkv_append: row ``pos[s]`` of the layer's tail gets the new K / V rows."""
+    _check(load().fdkv_append(ctypes.byref(d), int(batch), _dev(pos), int(cap), _dev(k_new), _dev(v_new),
+                              _dev(tail_k), _dev(tail_v), _stream(stream)), "fdkv_append")
+
+
+def decode_spans_workspace(d: Dims, batch: int, max_seq_lens, tail_cap: int) -> int:
+    m = np.ascontiguousarray(max_seq_lens, dtype=np.int32)
+    n = ctypes.c_size_t(0)
+    _check(load().fdkv_decode_spans_workspace(ctypes.byref(d), int(batch), int(m.size), _np_ptr(m),
+                                              int(tail_cap), ctypes.byref(n)), "fdkv_decode_spans_workspace")
+    return int(n.value)
+
+
+def decode_spans(d: Dims, batch: int, spans: Sequence[Span], tail, layer: int, q, out, sm_scale: float, ws,
+                 stream=None):
+    """Queue fdkv_decode_spans; ``spans`` are ``Span`` descriptors, ``tail`` a ``Tail`` or None."""
+    arr = (Span * max(len(spans), 1))(*spans)
+    _check(load().fdkv_decode_spans(ctypes.byref(d), int(batch), len(spans), ctypes.cast(arr, ctypes.c_void_p),
+                                    None if tail is None else ctypes.byref(tail), int(layer), _dev(q), _dev(out),
+                                    ctypes.c_float(sm_scale), _dev(ws), int(ws.numel() * ws.element_size()),
+                                    _stream(stream)), "fdkv_decode_spans")

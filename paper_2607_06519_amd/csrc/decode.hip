@@ -81,14 +81,17 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
 
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   const bool q4 = P.bsize == 4;
-  const int mode = P.modes[unit];
+  const int mode = P.tail ? kExact : P.modes[unit];   // the exact tail of a generation has no unit arrays
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
-  const uint8_t* seg = P.cache + P.seg_off[unit];
+  const uint8_t* seg = P.tail ? static_cast<const uint8_t*>(P.tail_k) : P.cache + P.seg_off[unit];
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E, P.bsize);
   const uint64_t xplane = plane_bytes((uint64_t)T * D * E);  // exact planes: K_p at p * xplane, V_p at (B + p) * xplane
-  const uint8_t* kplane = seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk);
-  const uint8_t* vplane = seg + (mode == kExact ? (uint64_t)(P.bsize + P.pos) * xplane : L.mv);
+  const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * D * E;
+  const uint8_t* kplane = P.tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
+                                 : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk);
+  const uint8_t* vplane = P.tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
+                                 : seg + (mode == kExact ? (uint64_t)(P.bsize + P.pos) * xplane : L.mv);
   // channel and weight of residual entry i of an index plane
   auto entry = [&](const uint8_t* ip, uint64_t i, float& w) -> int {
     if (q4) {
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   __syncthreads();
 
   // ------------------------------------------------------------ merge waves
-  float* rec = P.ws + ((uint64_t)sh * P.n_wgchunks + wgc) * G * S::RS;
+  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + P.chunk_base + wgc) * G * S::RS;
   for (int i = threadIdx.x; i < G * (D + 2); i += 256) {
     const int g = i / (D + 2), c = i - g * (D + 2);
     float M = -INFINITY;
@@ -312,12 +315,8 @@ template <int D, bool BF16, int G>
 static hipError_t launch_decode_t(const DecodeParams& P, hipStream_t s) {
   static_assert(!BF16, "bf16 caches use decode_stream_kernel");
   const dim3 grid((unsigned)P.batch * P.hkv * P.n_wgchunks);
-  if (grid.x > 0) {
-    hipLaunchKernelGGL((decode_splitk_kernel<D, BF16, G>), grid, dim3(256), 0, s, P);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return launch_decode_merge(P, s);
+  if (grid.x > 0) hipLaunchKernelGGL((decode_splitk_kernel<D, BF16, G>), grid, dim3(256), 0, s, P);
+  return hipGetLastError();
 }
 
 template <int D, bool BF16>
@@ -331,11 +330,7 @@ static hipError_t launch_decode_d(const DecodeParams& P, hipStream_t s) {
 }
 
 hipError_t launch_decode(const DecodeParams& P, hipStream_t s) {
-  if (P.bf16) {
-    const hipError_t e = launch_decode_stream(P, s);
-    if (e != hipSuccess) return e;
-    return launch_decode_merge(P, s);
-  }
+  if (P.bf16) return launch_decode_stream(P, s);
   return P.d == 128 ? launch_decode_d<128, false>(P, s) : launch_decode_d<64, false>(P, s);
 }
 

@@ -147,10 +147,15 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   // that does not queue behind other waves' tile loads.  (A segment offset is
   // a multiple of 256 and a mode is at most kExact; a unit that breaks either
   // is left alone.)
+  // (The exact tail of a generation has no unit arrays: its rows are exact.)
   const int T = P.seq_lens[seq];
-  const uint32_t mode_word = reinterpret_cast<const uint32_t*>(P.modes)[unit >> 2];
-  const uint64_t seg_off = P.seg_off[unit];
-  const int mode = (int)((mode_word >> (8 * (unit & 3))) & 0xFFu);
+  uint32_t mode_word = (uint32_t)kExact;
+  uint64_t seg_off = 0;
+  if (!P.tail) {
+    mode_word = reinterpret_cast<const uint32_t*>(P.modes)[unit >> 2] >> (8 * (unit & 3));
+    seg_off = P.seg_off[unit];
+  }
+  const int mode = (int)(mode_word & 0xFFu);
   const int wg_tok0 = wgc * kDecodeWgTokens;
   if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) return;
 
@@ -165,8 +170,11 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce, nb);
   const uint64_t dense = (uint64_t)T * D * ce;
   const uint64_t xplane = plane_bytes(dense);  // exact planes: K of layer p at p * xplane, V at (B + p) * xplane
-  const auto kr = rsrc(seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk), dense);
-  const auto vr = rsrc(seg + (mode == kExact ? (uint64_t)(nb + P.pos) * xplane : L.mv), dense);
+  const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * RB;
+  const auto kr = rsrc(P.tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
+                              : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk), dense);
+  const auto vr = rsrc(P.tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
+                              : seg + (mode == kExact ? (uint64_t)(nb + P.pos) * xplane : L.mv), dense);
   const auto ikr = rsrc(seg + L.ik, (uint64_t)T * k * ib);
   const auto vkr = rsrc(seg + L.vk, (uint64_t)T * k * ce);
   const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k * ib);
@@ -506,7 +514,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     }
   }
   __syncthreads();
-  float* rec = P.ws + ((uint64_t)sh * P.n_wgchunks + wgc) * G * S::RS;
+  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + P.chunk_base + wgc) * G * S::RS;
   for (int i = threadIdx.x; i < G * (D + 2); i += 256) {
     const int g = i / (D + 2), c = i - g * (D + 2);
     float M = -INFINITY;
@@ -553,7 +561,8 @@ __device__ __forceinline__ float wave_sum_dpp(float x) {
   return (a + b) + (c + d);
 }
 
-// Log-sum-exp merge of the workgroup records of one (sequence, query head):
+// Log-sum-exp merge of the workgroup records of one (sequence, query head),
+// over every part of the call (compressed spans, then the exact tail):
 //   M = max_i m_i,  l = sum_i l_i 2^(m_i - M),  o = sum_i acc_i 2^(m_i - M) / l.
 // One workgroup of four waves per query head, records taken in blocks of 64.
 // Within a block every wave loads the (m, l) pairs (record i in lane i) and
@@ -570,15 +579,19 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
   __shared__ float part[4][D];
   const int qh = blockIdx.x % P.hq, seq = blockIdx.x / P.hq;
   const int head = qh / G, g = qh % G;
-  const int T = P.seq_lens[seq];
-  const int nch = min((T + kDecodeWgTokens - 1) / kDecodeWgTokens, P.n_wgchunks);
   const uint64_t stride = (uint64_t)G * RS;  // floats between consecutive records of one query head
-  const float* base = P.ws + ((uint64_t)(seq * P.hkv + head) * P.n_wgchunks) * stride + g * RS;
+  const float* head_base = P.ws + ((uint64_t)(seq * P.hkv + head) * P.n_chunks_total) * stride + g * RS;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
   float M = -INFINITY, lsum = 0.f, o[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) o[c] = 0.f;
+  int total = 0;
+  for (int part = 0; part < P.n_parts; ++part) {
+    const int Tp = P.part_lens[part][seq];
+    const int nch = min((Tp + kDecodeWgTokens - 1) / kDecodeWgTokens, P.part_chunks[part]);
+    const float* base = head_base + (uint64_t)P.part_base[part] * stride;
+    total += nch;
   for (int b0 = 0; b0 < nch; b0 += 64) {
     const int last = nch - 1;  // loads past the end repeat the last record and get weight 0
     const int il = b0 + lane;
@@ -606,6 +619,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
     }
     M = Mn;
   }
+  }
 #pragma unroll
   for (int c = 0; c < CPL; ++c) part[wave][lane * CPL + c] = o[c];
   __syncthreads();
@@ -614,7 +628,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
     for (int c = 0; c < CPL; ++c) {
       const int ch = lane * CPL + c;
       const float s = (part[0][ch] + part[1][ch]) + (part[2][ch] + part[3][ch]);
-      const float res = nch > 0 ? s / lsum : 0.f;
+      const float res = total > 0 ? s / lsum : 0.f;
       const uint64_t oi = ((uint64_t)seq * P.hq + qh) * D + ch;
       if constexpr (BF16)
         reinterpret_cast<uint16_t*>(P.out)[oi] = (uint16_t)f32_to_bf16_bits(res);

@@ -375,33 +375,80 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
 }
 
 fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t max_seq_len, size_t* bytes) {
+  return fdkv_decode_spans_workspace(dims, batch, 1, &max_seq_len, -1, bytes);
+}
+
+fdkv_status fdkv_decode_spans_workspace(const fdkv_dims* dims, int32_t batch, int32_t n_spans,
+                                        const int32_t* max_seq_lens, int32_t tail_cap, size_t* bytes) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
-  if (batch < 1 || max_seq_len < 0 || !bytes) return FDKV_E_INVALID_ARG;
+  if (batch < 1 || n_spans < 0 || n_spans + (tail_cap >= 0 ? 1 : 0) > kMaxParts || !bytes ||
+      (n_spans > 0 && !max_seq_lens))
+    return FDKV_E_INVALID_ARG;
+  uint64_t n = 0;
+  for (int i = 0; i < n_spans; ++i) {
+    if (max_seq_lens[i] < 0) return FDKV_E_INVALID_ARG;
+    n += decode_chunks(max_seq_lens[i]);
+  }
+  if (tail_cap >= 0) n += decode_chunks(tail_cap);
   const uint64_t G = dims->n_q_heads / dims->n_kv_heads;
-  const uint64_t n = std::max<uint64_t>(1, decode_chunks(max_seq_len));
-  *bytes = (size_t)((uint64_t)batch * dims->n_kv_heads * n * G * (dims->head_dim + 4) * 4);
+  *bytes = (size_t)((uint64_t)batch * dims->n_kv_heads * std::max<uint64_t>(n, 1) * G * (dims->head_dim + 4) * 4);
   return FDKV_OK;
 }
 
-fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, int32_t max_seq_len,
-                             const uint8_t* modes, const uint64_t* seg_offsets, const void* cache, int32_t layer,
-                             const void* q, void* out, float sm_scale, void* ws, size_t ws_bytes, void* stream) {
+fdkv_status fdkv_append(const fdkv_dims* dims, int32_t batch, const int32_t* pos, int32_t cap, const void* k_new,
+                        const void* v_new, void* tail_k, void* tail_v, void* stream) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
-  if (batch < 1 || max_seq_len < 0 || layer < 0 || layer >= dims->n_layers) return FDKV_E_INVALID_ARG;
-  if ((uint64_t)max_seq_len * dims->head_dim * elem_bytes(dims) >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
-  if (!aligned(seq_lens, 4) || !aligned(modes, 4) || !aligned(seg_offsets, 8) || !aligned(cache, 256) || !aligned(q, 16) ||
-      !aligned(out, 16) || !aligned(ws, 16) || !isfinite(sm_scale))
+  if (batch < 1 || cap < 1 || !aligned(pos, 4) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
+      !aligned(tail_k, 16) || !aligned(tail_v, 16))
     return FDKV_E_INVALID_ARG;
+  AppendParams ap{};
+  ap.pos = pos;
+  ap.k_new = k_new;
+  ap.v_new = v_new;
+  ap.tail_k = tail_k;
+  ap.tail_v = tail_v;
+  ap.batch = batch;
+  ap.hkv = dims->n_kv_heads;
+  ap.cap = cap;
+  ap.row_bytes = dims->head_dim * elem_bytes(dims);
+  const hipError_t e = launch_append(ap, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "append");
+  return FDKV_OK;
+}
+
+fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_spans, const fdkv_span* spans,
+                              const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale,
+                              void* ws, size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  const int n_parts = n_spans + (tail ? 1 : 0);
+  if (batch < 1 || n_spans < 0 || n_parts > kMaxParts || (n_spans > 0 && !spans) || layer < 0 ||
+      layer >= dims->n_layers)
+    return FDKV_E_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(out, 16) || !aligned(ws, 16) || !isfinite(sm_scale)) return FDKV_E_INVALID_ARG;
+  const uint64_t row = (uint64_t)dims->head_dim * elem_bytes(dims);
+  int32_t maxes[kMaxParts];
+  for (int i = 0; i < n_spans; ++i) {
+    const fdkv_span& sp = spans[i];
+    if (sp.max_seq_len < 0 || !aligned(sp.seq_lens, 4) || !aligned(sp.modes, 4) || !aligned(sp.seg_offsets, 8) ||
+        !aligned(sp.cache, 256))
+      return FDKV_E_INVALID_ARG;
+    if ((uint64_t)sp.max_seq_len * row >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
+    maxes[i] = sp.max_seq_len;
+  }
+  if (tail) {
+    if (tail->cap < 0 || !aligned(tail->lens, 4) || !aligned(tail->k, 16) || !aligned(tail->v, 16))
+      return FDKV_E_INVALID_ARG;
+    if ((uint64_t)tail->cap * row >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
+  }
   size_t need = 0;
-  fdkv_decode_workspace(dims, batch, max_seq_len, &need);
+  st = fdkv_decode_spans_workspace(dims, batch, n_spans, maxes, tail ? tail->cap : -1, &need);
+  if (st != FDKV_OK) return st;
   if (ws_bytes < need) return FDKV_E_WORKSPACE;
+
   DecodeParams p{};
-  p.cache = static_cast<const uint8_t*>(cache);
-  p.seg_off = seg_offsets;
-  p.modes = modes;
-  p.seq_lens = seq_lens;
   p.q = q;
   p.out = out;
   p.ws = static_cast<float*>(ws);
@@ -417,14 +464,54 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
   p.hq = dims->n_q_heads;
   p.d = dims->head_dim;
   p.topk = dims->topk;
-  p.n_wgchunks = (int)decode_chunks(max_seq_len);
   p.batch = batch;
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.bf16 = dims->dtype != FDKV_F32;
   p.coef8 = dims->dtype == FDKV_BF16_E4M3;
-  const hipError_t e = launch_decode(p, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "decode");
+  // record slots: every part's chunks, spans first, then the tail
+  int total = 0;
+  for (int i = 0; i < n_parts; ++i) {
+    const int maxT = i < n_spans ? spans[i].max_seq_len : tail->cap;
+    p.part_base[i] = total;
+    p.part_chunks[i] = (int)decode_chunks(maxT);
+    p.part_lens[i] = i < n_spans ? spans[i].seq_lens : tail->lens;
+    total += p.part_chunks[i];
+  }
+  p.n_parts = n_parts;
+  p.n_chunks_total = std::max(total, 1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int i = 0; i < n_parts; ++i) {
+    DecodeParams pi = p;
+    pi.chunk_base = p.part_base[i];
+    pi.n_wgchunks = p.part_chunks[i];
+    if (i < n_spans) {
+      pi.cache = static_cast<const uint8_t*>(spans[i].cache);
+      pi.seg_off = spans[i].seg_offsets;
+      pi.modes = spans[i].modes;
+      pi.seq_lens = spans[i].seq_lens;
+    } else {
+      pi.tail = true;
+      pi.seq_lens = tail->lens;
+      pi.tail_k = tail->k;
+      pi.tail_v = tail->v;
+      pi.tail_cap = tail->cap;
+    }
+    const hipError_t e = launch_decode(pi, s);
+    if (e != hipSuccess) return hip_fail(e, "decode");
+  }
+  const hipError_t e = launch_decode_merge(p, s);
+  if (e != hipSuccess) return hip_fail(e, "decode_merge");
   return FDKV_OK;
+}
+
+fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, int32_t max_seq_len,
+                             const uint8_t* modes, const uint64_t* seg_offsets, const void* cache, int32_t layer,
+                             const void* q, void* out, float sm_scale, void* ws, size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (max_seq_len < 0) return FDKV_E_INVALID_ARG;
+  fdkv_span sp{seq_lens, max_seq_len, modes, seg_offsets, cache};
+  return fdkv_decode_spans(dims, batch, 1, &sp, nullptr, layer, q, out, sm_scale, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -47,6 +47,7 @@ struct SelectParams {
 constexpr int kDecodeChunk = 128;
 constexpr int kDecodeWaves = 4;
 constexpr int kDecodeWgTokens = kDecodeChunk * kDecodeWaves;
+constexpr int kMaxParts = 16;       // compressed spans plus the exact tail of one decode call
 
 struct DecodeParams {
   const uint8_t* cache;
@@ -63,6 +64,29 @@ struct DecodeParams {
   float scale_log2;            // sm_scale * log2(e)
   bool bf16;
   bool coef8;                  // shared planes and residual values of shared / residual heads in FP8 E4M3
+  // Records of one (sequence, KV head) sit in n_chunks_total slots; a launch
+  // over one part (a compressed span or the exact tail) fills chunk_base +
+  // its chunk index.
+  int chunk_base, n_chunks_total;
+  bool tail;                   // this launch reads the exact tail (seq_lens = its row counts)
+  const void* tail_k;          // [batch][hkv][tail_cap][d] of the decoded layer
+  const void* tail_v;
+  int tail_cap;
+  // the merge combines the parts' records: part i starts at part_base[i],
+  // has part_chunks[i] slots, and sequence s has part_lens[i][s] tokens in it
+  int n_parts;
+  int part_base[kMaxParts], part_chunks[kMaxParts];
+  const int32_t* part_lens[kMaxParts];
+};
+
+// generation: append one token's K / V rows of one layer to the exact tail
+struct AppendParams {
+  const int32_t* pos;          // [batch] row to write; rows outside [0, cap) are skipped
+  const void* k_new;           // [batch][hkv][d]
+  const void* v_new;
+  void* tail_k;                // [batch][hkv][cap][d]
+  void* tail_v;
+  int batch, hkv, cap, row_bytes;
 };
 
 // probe
@@ -89,9 +113,10 @@ __host__ __device__ __forceinline__ uint64_t probe_idx_stride(uint64_t T, int k)
 
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s);
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s);
-hipError_t launch_decode(const DecodeParams& P, hipStream_t s);
+hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // one part's split-K launch (bf16 or fp32)
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K part
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
+hipError_t launch_append(const AppendParams& P, hipStream_t s);
 hipError_t launch_probe(const ProbeParams& P, hipStream_t s);           // the blocks of P.bl (one size)
 hipError_t launch_probe_finalize(const ProbeParams& P, hipStream_t s);  // every unit
 

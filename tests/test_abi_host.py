@@ -192,3 +192,30 @@ def test_route_budget_mixed_matches_oracle(lib, frac):
         om = np.stack([O.omega(d, k, "bf16", Bs) for Bs in usz])
         m2, _, _ = B.route(dm, T, E.reshape(len(sizes), H, 2), lam=lam_fixed)
         np.testing.assert_array_equal(m2.ravel(), O.route(E3, om, lam_fixed))
+
+
+def test_generation_entry_points_validate(lib):
+    good = B.dims(4, 2, 8, 128, 16, "bf16")
+    fake = ctypes.c_void_p(1 << 20)
+    n = ctypes.c_size_t(0)
+    m = (ctypes.c_int32 * 3)(1000, 513, 0)
+    assert lib.fdkv_decode_spans_workspace(ctypes.byref(good), 2, 3, m, 64, ctypes.byref(n)) == 0
+    # chunks of 512 tokens: 2 + 2 + 0 spans + 1 tail, per (sequence, KV head), G = 4, d + 4 floats
+    assert n.value == 2 * 2 * 5 * 4 * 132 * 4
+    assert lib.fdkv_decode_spans_workspace(ctypes.byref(good), 2, 16, (ctypes.c_int32 * 16)(), 64, ctypes.byref(n)) == -1
+    assert lib.fdkv_decode_spans_workspace(ctypes.byref(good), 2, 16, (ctypes.c_int32 * 16)(), -1, ctypes.byref(n)) == 0
+    sp = (B.Span * 1)(B.Span(1 << 20, 16, 1 << 20, 1 << 20, 1 << 20))
+    tl = B.Tail(1 << 20, 8, 1 << 20, 1 << 20)
+    call = lambda spans, tail, **kw: lib.fdkv_decode_spans(ctypes.byref(good), 1, kw.get("n", 1), spans, tail,
+                                                          kw.get("layer", 0), fake, fake, ctypes.c_float(0.1), fake,
+                                                          kw.get("ws", 0), None)
+    assert call(ctypes.cast(sp, ctypes.c_void_p), ctypes.byref(tl)) == -3          # workspace too small
+    assert call(ctypes.cast(sp, ctypes.c_void_p), ctypes.byref(tl), layer=4) == -1
+    assert call(None, ctypes.byref(tl), n=1) == -1                                  # spans missing
+    bad = (B.Span * 1)(B.Span(1 << 20, 16, (1 << 20) + 1, 1 << 20, 1 << 20))      # modes not 4-byte aligned
+    assert call(ctypes.cast(bad, ctypes.c_void_p), None, ws=1 << 30) == -1
+    big = B.Tail(1 << 20, 1 << 23, 1 << 20, 1 << 20)                                 # cap * d * 2 >= 2^31
+    assert call(ctypes.cast(sp, ctypes.c_void_p), ctypes.byref(big), ws=1 << 40) == -2
+    assert lib.fdkv_append(ctypes.byref(good), 1, fake, 0, fake, fake, fake, fake, None) == -1     # cap 0
+    assert lib.fdkv_append(ctypes.byref(good), 1, ctypes.c_void_p((1 << 20) + 2), 8, fake, fake, fake, fake,
+                           None) == -1

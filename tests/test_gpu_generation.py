@@ -1,0 +1,152 @@
+"""Generation on the GPU through the C ABI (decode-time append, decode over
+compressed spans plus the exact tail, and refresh of the routing), against
+the oracle: every decode output within relative L2 1e-2 (bf16) / 1e-5 (fp32)
+per (sequence, layer, query head), refreshed modes equal to the oracle's
+wherever its cost margin is at least 1e-3, and the refreshed spans bit-exact
+in their indices (the compress parity bar)."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synth import WORKLOADS, gen, scaled
+
+from gpu_cases import compare_units, rel_l2, unpack_unit
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2607_06519_amd import binding
+    binding.load()
+    return torch
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+CASES = {
+    "pairs_bf16": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(700, 333),
+                         n_needles=3, fixed_modes=(1, 2, 0, 1)),
+    "mixed_bf16": scaled(WORKLOADS["llama8b_mixed"], n_layers=12, n_kv_heads=2, n_q_heads=8, seq_lens=(520,),
+                         n_needles=2, fixed_modes=(0, 1, 1, 2, 0, 1, 1, 0, 2, 1)),
+    "quads_f32_k7": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=7, seq_lens=(300, 129),
+                           schedule=2, needle_channels=7, fixed_modes=(1, 2)),
+}
+
+
+def _new_token(w, rng):
+    """One generated token's K, V ``[L][batch][Hkv][d]``: a depth chain per block."""
+    L, b, H, d = w.n_layers, w.batch, w.n_kv_heads, w.head_dim
+    out = []
+    for _ in range(2):
+        x = np.empty((L, b, H, d), np.float32)
+        for f, B in w.blocks:
+            x[f] = rng.standard_normal((b, H, d))
+            for n in range(1, B):
+                x[f + n] = 0.9 * x[f + n - 1] + math.sqrt(1 - 0.81) * rng.standard_normal((b, H, d))
+        out.append(gen.to_storage(x, w.dtype))
+    return out
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_generation_parity(torch_dev, name):
+    torch = torch_dev
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, Generation, to_device
+    w = CASES[name]
+    cap, P, steps = 40, 16, 2 * 40 + 5
+    L, H, G, d, k = w.n_layers, w.n_kv_heads, w.group, w.head_dim, w.topk
+    log(f"[case] generation {name}: prefix {w.seq_lens}, tail {cap}, {steps} steps, blocks {w.block_sizes}")
+    dm = Bn.dims(**w.dims())
+    tol = 1e-5 if w.dtype == "f32" else 1e-2
+    # prefill: span 0
+    modes0 = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
+    cache = CompressedCache(dm, w.seq_lens, modes0)
+    spans = [[] for _ in range(w.batch)]        # oracle: per sequence, list of {(block, head): (unit, mode)}
+    keep = []
+    for s, T in enumerate(w.seq_lens):
+        ws_ = scaled(w, seq_lens=(T,))
+        K, V = gen.layer_cache(ws_, 0)
+        Kd, Vd = to_device(K, w.dtype), to_device(V, w.dtype)
+        keep.append((Kd, Vd))
+        cache.compress(s, [Kd[l] for l in range(L)], [Vd[l] for l in range(L)])
+        spans[s].append({(b, h): (O.compress_unit(K[f:f + B, h], V[f:f + B, h], int(modes0[s, b, h]), k, w.dtype),
+                                  int(modes0[s, b, h]), B)
+                         for b, (f, B) in enumerate(w.blocks) for h in range(H)})
+    g = Generation(dm, cache, cap)
+    rng = np.random.default_rng(7)
+    tailK = [[[] for _ in range(w.batch)] for _ in range(L)]
+    tailV = [[[] for _ in range(w.batch)] for _ in range(L)]
+    recent = [[] for _ in range(L)]             # last decode queries per layer, [batch][Hq][d] each
+    worst, refreshes, checked_modes = 0.0, 0, 0
+    blk = {l: (b, f, B) for b, (f, B) in enumerate(w.blocks) for l in range(f, f + B)}
+    for step in range(steps):
+        if g.full:
+            # refresh: GPU probe + route on each sequence's tail, oracle check of the modes
+            Qr = [np.stack(recent[l][-P:], axis=2) for l in range(L)]          # [batch][Hq][P][d]
+            Kt = np.array([[np.stack(tailK[l][s], axis=1) for s in range(w.batch)] for l in range(L)])  # [L][b][H][n][d]
+            Vt = np.array([[np.stack(tailV[l][s], axis=1) for s in range(w.batch)] for l in range(L)])
+            E = np.zeros((w.batch, w.n_blocks, H, 3))
+            for s in range(w.batch):
+                for b, (f, B) in enumerate(w.blocks):
+                    for h in range(H):
+                        E[s, b, h] = O.routing_errors(Kt[f:f + B, s, h], np.stack(Qr[f:f + B])[:, s, h * G:(h + 1) * G], k)
+            lam = float(np.median(E[..., 0])) * 2.0
+            probe_rows = [to_device(Qr[l], w.dtype) for l in range(L)]
+            modes = g.refresh(probe_rows, P, lam=lam)
+            refreshes += 1
+            for s in range(w.batch):
+                om = np.stack([O.omega(d, k, w.dtype, B) for B in w.block_sizes for _ in range(H)])
+                E3 = E[s].reshape(-1, 3)
+                want = O.route(E3, om, lam)
+                cost = E3 + lam * om
+                srt = np.sort(cost, axis=1)
+                ok = (srt[:, 1] - srt[:, 0]) / np.maximum(srt[:, 0], 1e-30) >= 1e-3
+                np.testing.assert_array_equal(modes[s].ravel()[ok], want[ok])
+                checked_modes += int(ok.sum())
+                span = {}
+                buf = g.spans[-1].host_bytes()
+                for b, (f, B) in enumerate(w.blocks):
+                    for h in range(H):
+                        m = int(modes[s, b, h])
+                        unit = O.compress_unit(Kt[f:f + B, s, h], Vt[f:f + B, s, h], m, k, w.dtype)
+                        got = unpack_unit(buf, int(g.spans[-1].offsets_host[s, b, h]), m, cap, d, k, w.dtype, B)
+                        compare_units(got, unit, w.dtype,
+                                      inputs=(Kt[f:f + B, s, h], Vt[f:f + B, s, h]) if B == 4 else None)
+                        span[(b, h)] = (unit, m, B)
+                spans[s].append(span)
+            tailK = [[[] for _ in range(w.batch)] for _ in range(L)]
+            tailV = [[[] for _ in range(w.batch)] for _ in range(L)]
+            log(f"  refresh {refreshes}: modes {np.bincount(modes.ravel(), minlength=3).tolist()}, lambda {lam:.4g}")
+        kn, vn = _new_token(w, rng)
+        qs = gen.decode_queries(w, step, scale=4.0)
+        for layer in range(L):
+            g.append(layer, to_device(kn[layer], w.dtype), to_device(vn[layer], w.dtype))
+            out = g.decode(layer, to_device(qs[layer], w.dtype)).float().cpu().numpy()
+            b, f, B = blk[layer]
+            for s in range(w.batch):
+                tailK[layer][s].append(kn[layer][s])
+                tailV[layer][s].append(vn[layer][s])
+                for h in range(H):
+                    tk = np.stack([r[h] for r in tailK[layer][s]])
+                    tv = np.stack([r[h] for r in tailV[layer][s]])
+                    sp = [span_[(b, h)] for span_ in spans[s]]
+                    want = O.decode_spans(sp, tk, tv, layer, qs[layer][s, h * G:(h + 1) * G].astype(np.float64),
+                                          1.0 / math.sqrt(d), d)
+                    for gg in range(G):
+                        e = rel_l2(out[s, h * G + gg], want[gg])
+                        worst = max(worst, e)
+                        assert e <= tol, (name, step, layer, s, h, gg, e)
+            recent[layer].append(qs[layer])
+        g.advance()
+    assert refreshes == 2 and len(g.spans) == 3
+    log(f"  {steps} steps ok; worst rel-L2 {worst:.3e} (tol {tol}); {checked_modes} refreshed modes checked")
