@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--threads", type=int, default=16)
+    ap.add_argument("--gen-tail", type=int, default=512,
+                    help="generation leg: exact-tail rows between refreshes (0 skips the leg)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="before timing, copy this many MiB device-to-device once (a copy kernel of known "
                          "size that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -362,6 +364,69 @@ def main():
             f"({prefill['compress_gbs']:.0f} GB/s), mix {prefill['probe_mode_mix']}")
         del Qp, ws, pcache_buf
 
+    # ------------------------------------------------------------ generation: append + spans + tail, refresh
+    generation = None
+    if args.gen_tail > 0 and w.batch == 1 and w.n_probe > 0:
+        from paper_2607_06519_amd.cache import Generation
+        cap, Pr = args.gen_tail, min(w.n_probe, 64)
+        g = Generation(dm, cache, cap)
+        gq = torch.from_numpy(gen.decode_queries(w, 0)).to(dev).to(tdt)
+        gk = torch.from_numpy(gen.decode_queries(w, 1)).to(dev).to(tdt)[:, :, :H].contiguous()  # stand-in K / V rows
+        gv = torch.from_numpy(gen.decode_queries(w, 2)).to(dev).to(tdt)[:, :, :H].contiguous()
+        gout = torch.empty_like(gq)
+        rows = [torch.from_numpy(gen.probe_queries(w, 0, layers=[l])[0][:, :Pr]).to(dev).to(tdt)[None]
+                for l in range(L)]
+
+        def gstep():
+            for layer in order:
+                g.append(layer, gk[layer], gv[layer])
+                g.decode(layer, gq[layer], gout[layer], scale)
+
+        refresh_s = []
+        for r in range(2):                      # two refreshes: the prefix plus two spans of `cap` tokens
+            for _ in range(cap):
+                gstep()
+                g.advance()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            g.refresh(rows, Pr, lam=float("inf"))
+            torch.cuda.synchronize()
+            refresh_s.append(time.perf_counter() - t0)
+        for _ in range(cap // 2):               # the tail half full
+            gstep()
+            g.advance()
+        gstream = torch.cuda.Stream()
+        gstream.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(gstream):
+            gstep()
+            torch.cuda.synchronize()
+            ggraph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(ggraph, stream=gstream):
+                gstep()
+            for _ in range(args.warmup):
+                ggraph.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(gstream)
+            for _ in range(args.steps):
+                ggraph.replay()
+            e1.record(gstream)
+            torch.cuda.synchronize()
+        gen_ms = e0.elapsed_time(e1) / args.steps
+        generation = {
+            "tail_cap": cap, "spans": len(g.spans), "tail_rows": g.n_tail + 1,
+            "context_tokens": w.max_seq_len + 2 * cap + g.n_tail + 1,
+            "step_ms": gen_ms, "tokens_per_s": w.batch / (gen_ms * 1e-3),
+            "refresh_ms": float(np.mean(refresh_s)) * 1e3,
+            "refresh_ms_per_token": float(np.mean(refresh_s)) * 1e3 / cap,
+            "note": "one step = for every layer an append into the exact tail and a decode over the "
+                    "prefix span, two refreshed spans and the tail (graph replay); refresh = probe, route "
+                    "(lambda = inf, all shared) and compress of the full tail, wall time",
+        }
+        log(f"[bench] generation: step {gen_ms * 1e3:.1f} us over {len(g.spans)} spans + tail, "
+            f"refresh {generation['refresh_ms']:.2f} ms per {cap} tokens")
+        del g
+
     # ------------------------------------------------------------ CPU oracle baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -386,6 +451,7 @@ def main():
                      "bytes_per_launch": bytes_step / L, "launch_us": launch_avg_ms * 1e3},
         "cpu_baseline": cpu,
         "prefill": prefill,
+        "generation": generation,
     }
     print(json.dumps(res), flush=True)
 

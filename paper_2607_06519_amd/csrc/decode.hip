@@ -72,26 +72,29 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   __shared__ float mg_lds[W][G][D + 2];     // per-wave acc, m, l
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wgc = blockIdx.x % P.n_wgchunks;
-  const int sh = blockIdx.x / P.n_wgchunks;  // seq * hkv + head
+  const int slot = blockIdx.x % P.n_chunks_total;
+  const int sh = blockIdx.x / P.n_chunks_total;  // seq * hkv + head
   const int head = sh % P.hkv, seq = sh / P.hkv;
-  const int T = P.seq_lens[seq];
+  const int part = decode_part(P, slot);
+  const int wgc = slot - P.part[part].base;
+  const bool tail = part == P.tail_part;
+  const int T = P.part[part].lens[seq];
   const int wg_tok0 = wgc * kDecodeWgTokens;
   if (wg_tok0 >= T) return;  // uniform over the workgroup
 
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   const bool q4 = P.bsize == 4;
-  const int mode = P.tail ? kExact : P.modes[unit];   // the exact tail of a generation has no unit arrays
+  const int mode = tail ? kExact : P.part[part].modes[unit];   // the exact tail of a generation has no unit arrays
   const int k = P.topk;
   const bool resid = (mode == kResidual) && k > 0;
-  const uint8_t* seg = P.tail ? static_cast<const uint8_t*>(P.tail_k) : P.cache + P.seg_off[unit];
+  const uint8_t* seg = tail ? static_cast<const uint8_t*>(P.tail_k) : P.part[part].cache + P.part[part].seg_off[unit];
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E, P.bsize);
   const uint64_t xplane = plane_bytes((uint64_t)T * D * E);  // exact planes: K_p at p * xplane, V_p at (B + p) * xplane
   const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * D * E;
-  const uint8_t* kplane = P.tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
-                                 : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk);
-  const uint8_t* vplane = P.tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
-                                 : seg + (mode == kExact ? (uint64_t)(P.bsize + P.pos) * xplane : L.mv);
+  const uint8_t* kplane = tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
+                               : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk);
+  const uint8_t* vplane = tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
+                               : seg + (mode == kExact ? (uint64_t)(P.bsize + P.pos) * xplane : L.mv);
   // channel and weight of residual entry i of an index plane
   auto entry = [&](const uint8_t* ip, uint64_t i, float& w) -> int {
     if (q4) {
@@ -289,7 +292,7 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   __syncthreads();
 
   // ------------------------------------------------------------ merge waves
-  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + P.chunk_base + wgc) * G * S::RS;
+  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
   for (int i = threadIdx.x; i < G * (D + 2); i += 256) {
     const int g = i / (D + 2), c = i - g * (D + 2);
     float M = -INFINITY;
@@ -314,7 +317,7 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
 template <int D, bool BF16, int G>
 static hipError_t launch_decode_t(const DecodeParams& P, hipStream_t s) {
   static_assert(!BF16, "bf16 caches use decode_stream_kernel");
-  const dim3 grid((unsigned)P.batch * P.hkv * P.n_wgchunks);
+  const dim3 grid((unsigned)P.batch * P.hkv * P.n_chunks_total);
   if (grid.x > 0) hipLaunchKernelGGL((decode_splitk_kernel<D, BF16, G>), grid, dim3(256), 0, s, P);
   return hipGetLastError();
 }

@@ -126,7 +126,10 @@ struct TileBuf {
 
 }  // namespace
 
-template <int D, int G, bool C8K>
+// MULTI: the call has several parts (spans and the exact tail); otherwise
+// part 0 is the only one, a compile-time constant, so the per-unit scalars
+// load straight from fixed argument offsets with no lookup in front.
+template <int D, int G, bool C8K, bool MULTI>
 __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   using S = SS<D, G>;
   constexpr int NP = S::NP, RPL = S::RPL, TILE = S::TILE, NL = S::NL, CW = S::CW, W = S::W;
@@ -137,9 +140,12 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   auto mg = [&](int w, int g, int c) -> float& { return big[(w * G + g) * (D + 2) + c]; };
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wgc = blockIdx.x % P.n_wgchunks;
-  const int sh = blockIdx.x / P.n_wgchunks;
+  const int slot = blockIdx.x % P.n_chunks_total;
+  const int sh = blockIdx.x / P.n_chunks_total;
   const int head = sh % P.hkv, seq = sh / P.hkv;
+  const int part = MULTI ? decode_part(P, slot) : 0;
+  const int wgc = MULTI ? slot - P.part[part].base : slot;
+  const bool tail = MULTI && part == P.tail_part;
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   // The three per-unit values are fetched together, as scalar loads (the
   // mode byte through its aligned dword; the array is 4-byte aligned), and
@@ -148,12 +154,12 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   // a multiple of 256 and a mode is at most kExact; a unit that breaks either
   // is left alone.)
   // (The exact tail of a generation has no unit arrays: its rows are exact.)
-  const int T = P.seq_lens[seq];
+  const int T = P.part[part].lens[seq];
   uint32_t mode_word = (uint32_t)kExact;
   uint64_t seg_off = 0;
-  if (!P.tail) {
-    mode_word = reinterpret_cast<const uint32_t*>(P.modes)[unit >> 2] >> (8 * (unit & 3));
-    seg_off = P.seg_off[unit];
+  if (!tail) {
+    mode_word = reinterpret_cast<const uint32_t*>(P.part[part].modes)[unit >> 2] >> (8 * (unit & 3));
+    seg_off = P.part[part].seg_off[unit];
   }
   const int mode = (int)(mode_word & 0xFFu);
   const int wg_tok0 = wgc * kDecodeWgTokens;
@@ -165,16 +171,16 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   // heads are E4M3 (one byte per channel); exact heads stay bf16
   const bool c8 = C8K && mode != kExact;
   const int ce = c8 ? 1 : 2;
-  const uint8_t* seg = P.cache + seg_off;
+  const uint8_t* seg = P.part[part].cache + seg_off;
   const int nb = P.bsize, ib = index_bytes(nb);
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce, nb);
   const uint64_t dense = (uint64_t)T * D * ce;
   const uint64_t xplane = plane_bytes(dense);  // exact planes: K of layer p at p * xplane, V at (B + p) * xplane
   const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * RB;
-  const auto kr = rsrc(P.tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
-                              : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk), dense);
-  const auto vr = rsrc(P.tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
-                              : seg + (mode == kExact ? (uint64_t)(nb + P.pos) * xplane : L.mv), dense);
+  const auto kr = rsrc(tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
+                            : seg + (mode == kExact ? (uint64_t)P.pos * xplane : L.mk), dense);
+  const auto vr = rsrc(tail ? static_cast<const uint8_t*>(P.tail_v) + tail_off
+                            : seg + (mode == kExact ? (uint64_t)(nb + P.pos) * xplane : L.mv), dense);
   const auto ikr = rsrc(seg + L.ik, (uint64_t)T * k * ib);
   const auto vkr = rsrc(seg + L.vk, (uint64_t)T * k * ce);
   const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k * ib);
@@ -514,7 +520,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     }
   }
   __syncthreads();
-  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + P.chunk_base + wgc) * G * S::RS;
+  float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
   for (int i = threadIdx.x; i < G * (D + 2); i += 256) {
     const int g = i / (D + 2), c = i - g * (D + 2);
     float M = -INFINITY;
@@ -588,9 +594,9 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
   for (int c = 0; c < CPL; ++c) o[c] = 0.f;
   int total = 0;
   for (int part = 0; part < P.n_parts; ++part) {
-    const int Tp = P.part_lens[part][seq];
-    const int nch = min((Tp + kDecodeWgTokens - 1) / kDecodeWgTokens, P.part_chunks[part]);
-    const float* base = head_base + (uint64_t)P.part_base[part] * stride;
+    const int Tp = P.part[part].lens[seq];
+    const int nch = min((Tp + kDecodeWgTokens - 1) / kDecodeWgTokens, P.part[part].chunks);
+    const float* base = head_base + (uint64_t)P.part[part].base * stride;
     total += nch;
   for (int b0 = 0; b0 < nch; b0 += 64) {
     const int last = nch - 1;  // loads past the end repeat the last record and get weight 0
@@ -640,16 +646,24 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
 
 template <int D, int G>
 static hipError_t launch_t(const DecodeParams& P, hipStream_t s) {
-  const unsigned nsh = (unsigned)P.batch * P.hkv;
-  if (P.coef8)
-    hipLaunchKernelGGL((decode_stream_kernel<D, G, true>), dim3(nsh * P.n_wgchunks), dim3(256), 0, s, P);
-  else
-    hipLaunchKernelGGL((decode_stream_kernel<D, G, false>), dim3(nsh * P.n_wgchunks), dim3(256), 0, s, P);
+  const dim3 grid((unsigned)P.batch * P.hkv * P.n_chunks_total);
+  const bool multi = P.n_parts > 1 || P.tail_part >= 0;
+  if (P.coef8) {
+    if (multi)
+      hipLaunchKernelGGL((decode_stream_kernel<D, G, true, true>), grid, dim3(256), 0, s, P);
+    else
+      hipLaunchKernelGGL((decode_stream_kernel<D, G, true, false>), grid, dim3(256), 0, s, P);
+  } else {
+    if (multi)
+      hipLaunchKernelGGL((decode_stream_kernel<D, G, false, true>), grid, dim3(256), 0, s, P);
+    else
+      hipLaunchKernelGGL((decode_stream_kernel<D, G, false, false>), grid, dim3(256), 0, s, P);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s) {
-  if (P.n_wgchunks <= 0) return hipSuccess;
+  if (P.n_chunks_total <= 0) return hipSuccess;
   const int G = P.hq / P.hkv;
   if (P.d == 128) {
     switch (G) {

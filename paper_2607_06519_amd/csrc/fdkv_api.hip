@@ -471,32 +471,28 @@ fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_sp
   // record slots: every part's chunks, spans first, then the tail
   int total = 0;
   for (int i = 0; i < n_parts; ++i) {
-    const int maxT = i < n_spans ? spans[i].max_seq_len : tail->cap;
-    p.part_base[i] = total;
-    p.part_chunks[i] = (int)decode_chunks(maxT);
-    p.part_lens[i] = i < n_spans ? spans[i].seq_lens : tail->lens;
-    total += p.part_chunks[i];
+    const bool t = i == n_spans;
+    p.part[i].base = total;
+    p.part[i].chunks = (int)decode_chunks(t ? tail->cap : spans[i].max_seq_len);
+    p.part[i].lens = t ? tail->lens : spans[i].seq_lens;
+    if (!t) {
+      p.part[i].cache = static_cast<const uint8_t*>(spans[i].cache);
+      p.part[i].modes = spans[i].modes;
+      p.part[i].seg_off = spans[i].seg_offsets;
+    }
+    total += p.part[i].chunks;
   }
   p.n_parts = n_parts;
-  p.n_chunks_total = std::max(total, 1);
+  p.n_chunks_total = total;
+  p.tail_part = tail ? n_spans : -1;
+  if (tail) {
+    p.tail_k = tail->k;
+    p.tail_v = tail->v;
+    p.tail_cap = tail->cap;
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  for (int i = 0; i < n_parts; ++i) {
-    DecodeParams pi = p;
-    pi.chunk_base = p.part_base[i];
-    pi.n_wgchunks = p.part_chunks[i];
-    if (i < n_spans) {
-      pi.cache = static_cast<const uint8_t*>(spans[i].cache);
-      pi.seg_off = spans[i].seg_offsets;
-      pi.modes = spans[i].modes;
-      pi.seq_lens = spans[i].seq_lens;
-    } else {
-      pi.tail = true;
-      pi.seq_lens = tail->lens;
-      pi.tail_k = tail->k;
-      pi.tail_v = tail->v;
-      pi.tail_cap = tail->cap;
-    }
-    const hipError_t e = launch_decode(pi, s);
+  if (total > 0) {
+    const hipError_t e = launch_decode(p, s);
     if (e != hipSuccess) return hip_fail(e, "decode");
   }
   const hipError_t e = launch_decode_merge(p, s);

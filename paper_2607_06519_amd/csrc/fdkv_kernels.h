@@ -49,35 +49,44 @@ constexpr int kDecodeWaves = 4;
 constexpr int kDecodeWgTokens = kDecodeChunk * kDecodeWaves;
 constexpr int kMaxParts = 16;       // compressed spans plus the exact tail of one decode call
 
-struct DecodeParams {
+// One part of a decode call (a compressed span or the exact tail); its
+// fields sit together so that part 0 loads in one go.
+struct DecodePart {
+  const int32_t* lens;         // [batch] tokens of each sequence in the part
   const uint8_t* cache;
+  const uint8_t* modes;        // [batch][blocks][hkv], 4-byte aligned
   const uint64_t* seg_off;     // [batch][blocks][hkv]
-  const uint8_t* modes;        // [batch][blocks][hkv]
-  const int32_t* seq_lens;     // [batch]
+  int base, chunks;            // record slots [base, base + chunks) of each (sequence, KV head)
+};
+
+struct DecodeParams {
   const void* q;               // [batch][hq][d]
   void* out;                   // [batch][hq][d]
-  float* ws;                   // partials [batch][hkv][n_wgchunks][G][d + 4]
+  float* ws;                   // records [batch][hkv][n_chunks_total][G][d + 4]
   int block, pos, bsize;       // the layer's block, its position in it, the block size
-  int n_blocks, hkv, hq, d, topk, n_wgchunks, batch;
+  int n_blocks, hkv, hq, d, topk, batch;
+  // Parts of one call: compressed spans, then (if tail_part >= 0) the exact
+  // tail.  The records of one (sequence, KV head) sit in n_chunks_total
+  // slots.  One split-K launch covers every part: workgroup x is slot
+  // x % n_chunks_total of (sequence, KV head) x / n_chunks_total.
+  int n_parts, n_chunks_total, tail_part;
+  DecodePart part[kMaxParts];
   float wres[3];               // weight of a residual entry of frequency j = 1..3 at this layer
                                // (B = 2: +-1 for the stored half difference)
   float scale_log2;            // sm_scale * log2(e)
   bool bf16;
   bool coef8;                  // shared planes and residual values of shared / residual heads in FP8 E4M3
-  // Records of one (sequence, KV head) sit in n_chunks_total slots; a launch
-  // over one part (a compressed span or the exact tail) fills chunk_base +
-  // its chunk index.
-  int chunk_base, n_chunks_total;
-  bool tail;                   // this launch reads the exact tail (seq_lens = its row counts)
   const void* tail_k;          // [batch][hkv][tail_cap][d] of the decoded layer
   const void* tail_v;
   int tail_cap;
-  // the merge combines the parts' records: part i starts at part_base[i],
-  // has part_chunks[i] slots, and sequence s has part_lens[i][s] tokens in it
-  int n_parts;
-  int part_base[kMaxParts], part_chunks[kMaxParts];
-  const int32_t* part_lens[kMaxParts];
 };
+
+// Part of a decode workgroup's record slot r (parts in slot order; uniform).
+__device__ __forceinline__ int decode_part(const DecodeParams& P, int r) {
+  int part = 0;
+  while (part + 1 < P.n_parts && r >= P.part[part + 1].base) ++part;
+  return part;
+}
 
 // generation: append one token's K / V rows of one layer to the exact tail
 struct AppendParams {
@@ -113,8 +122,8 @@ __host__ __device__ __forceinline__ uint64_t probe_idx_stride(uint64_t T, int k)
 
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s);
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s);
-hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // one part's split-K launch (bf16 or fp32)
-hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K part
+hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // split-K over every part (bf16 or fp32)
+hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
 hipError_t launch_append(const AppendParams& P, hipStream_t s);
 hipError_t launch_probe(const ProbeParams& P, hipStream_t s);           // the blocks of P.bl (one size)
