@@ -20,6 +20,9 @@ the paper (Section 3, "Method"), slowly and without any blocking or fusion:
   (end of Section 3);
 * decode attention over the reconstructed K/V (Section 3, the paragraph after
   Eq. 3), a full softmax with max subtraction;
+* token-level residual set (Section 3, after Eq. 2): residual heads keep every
+  high-frequency coefficient of the ``r T`` tokens with the largest score
+  ``s_t = max_q |q (K_t - K^S_t)^T|``;
 * generation (the end of Section 3's method): tokens produced while decoding
   are kept exact in a tail; a refresh compresses the tail into a new span of
   the cache, routed by Eq. (2) on the tail's own keys with the most recent
@@ -57,6 +60,12 @@ Readings of the paper adopted here (the paper leaves these open):
 * the budget rule takes the smallest ``lambda`` among 0, the per-head
   breakpoints and +inf whose footprint fits the budget;
 * decode scales logits by ``1/sqrt(d)`` and attends over the cached tokens;
+* the token score is taken at the kernel's precision: the deviations
+  ``x_l - M`` in fp32 on the stored inputs, rounded to bf16 (exact products,
+  the sum in fp64 here); its maximum runs over the probe rows of every layer
+  of the block and every query head of the group; ``r`` is one fraction per
+  cache (parts per million), ``n = ceil(r T)``, ties to the lower token; the
+  stored rows are the unrounded coefficients rounded to the coefficient type;
 * a refresh re-decides routing only for the tokens it compresses (earlier
   spans keep their modes: a shared head's dropped coefficients cannot be
   recovered), and a span's probe rows are the last decode queries;
@@ -476,6 +485,163 @@ def decode_unit(unit, mode: int, layer: int, q, scale: float, d: int, B: int = 2
     Kt = reconstruct_layer(unit, mode, pos, d, "K", B)
     Vt = reconstruct_layer(unit, mode, pos, d, "V", B)
     return attention(q, Kt, Vt, scale)
+
+
+# ----------------------------------------------------------------------------
+# token-level residual set (Section 3, the paragraph after Eq. 2): a residual
+# head keeps every high-frequency coefficient of its top r*T tokens, ranked by
+# the largest logit change the token's removal would cause at a probe row
+# ----------------------------------------------------------------------------
+def token_deviations(KB) -> np.ndarray:
+    """Deviations of each layer's keys from the shared reconstruction, ``[B][T][d]``,
+    at the precision the token score is taken in: fp32 arithmetic on the
+    stored inputs, rounded to bf16.  Pairs: ``x0 - M = (x0 - x1) / 2`` and its
+    negation; fours: ``x_l - M`` with ``M = ((x0 + x3) + (x1 + x2)) / 4``."""
+    X = [np.asarray(x, dtype=np.float32) for x in KB]
+    B = len(X)
+    if B == 2:
+        D = (X[0] - X[1]) * np.float32(0.5)
+        dev = np.stack([D, -D])
+    else:
+        M = ((X[0] + X[3]) + (X[1] + X[2])) * np.float32(0.25)
+        dev = np.stack([x - M for x in X])
+    return round_bf16(dev.astype(np.float64))
+
+
+def token_scores(KB, QB) -> Tuple[np.ndarray, np.ndarray]:
+    """``(s, e)`` per token: ``s_t = max |q . dev_{l,t}|`` over the probe rows q of every
+    layer l of the block and every query head of the group, and ``e_t`` the sum of
+    the squares of those dot products (fp64 on the bf16 deviations)."""
+    dev = token_deviations(KB)
+    QB = np.asarray(QB, dtype=np.float64)
+    s = np.zeros(dev.shape[1])
+    e = np.zeros(dev.shape[1])
+    for l in range(dev.shape[0]):
+        Q = QB[l].reshape(-1, QB.shape[-1])                 # [G*P][d]
+        L = Q @ dev[l].T                                     # [G*P][T]
+        s = np.maximum(s, np.abs(L).max(axis=0))
+        e += (L * L).sum(axis=0)
+    return s, e
+
+
+def n_residual_tokens(T: int, ppm: int) -> int:
+    """r*T rounded up, r = ppm / 10^6."""
+    return (int(T) * int(ppm) + 999999) // 1000000
+
+
+def residual_tokens(scores, n: int) -> np.ndarray:
+    """Ascending indices of the ``n`` highest scores, ties to the lower token."""
+    scores = np.asarray(scores, dtype=np.float64)
+    if n == 0:
+        return np.zeros(0, dtype=np.int64)
+    order = np.lexsort((np.arange(scores.size), -scores))
+    return np.sort(order[:n]).astype(np.int64)
+
+
+def compress_unit_tokens(KB, VB, mode: int, tokens, dtype: str) -> Dict[str, np.ndarray]:
+    """Stored planes of one unit with a token-level residual set ``tokens``.
+
+    Shared / exact heads are as in ``compress_unit``.  A residual head stores
+    ``MK, MV`` plus, for its tokens (ascending, ``TS``), every high-frequency
+    coefficient of K and V: ``HK, HV`` of shape ``[n][B-1][d]`` (pairs: the half
+    difference D; fours: Z_1..Z_3), rounded to the coefficient type.
+    """
+    if mode != RESIDUAL:
+        return compress_unit(KB, VB, mode, 0, dtype)
+    out = compress_unit(KB, VB, SHARED, 0, dtype)
+    tokens = np.asarray(tokens, dtype=np.int64)
+    out["TS"] = tokens
+    B = len(KB)
+    for name, X in (("K", KB), ("V", VB)):
+        X = np.asarray(X, dtype=np.float64)
+        if B == 2:
+            H = coefficient_image(X, 1, 0)[tokens][:, None, :]
+        else:
+            H = np.moveaxis(depth_factorize(X)[1:, tokens], 0, 1)
+        out["H" + name] = round_coef(H, dtype)
+    return out
+
+
+def reconstruct_layer_tokens(unit, mode: int, pos: int, d: int, which: str, B: int = 2) -> np.ndarray:
+    """K~ or V~ of layer ``pos`` of a block from a token-level residual unit (Eq. 3)."""
+    if mode != RESIDUAL:
+        return reconstruct_layer(unit, mode, pos, d, which, B)
+    F = dct_matrix(B)
+    M = np.asarray(unit["M" + which], dtype=np.float64)
+    Z = np.zeros((B,) + M.shape)
+    Z[0] = M / F[0, 0]
+    tokens = unit["TS"]
+    H = np.asarray(unit["H" + which], dtype=np.float64)
+    if B == 2:
+        Z[1, tokens] = H[:, 0] / F[1, 0]
+    else:
+        Z[1:, tokens] = np.moveaxis(H, 1, 0)
+    return depth_reconstruct(Z)[pos]
+
+
+def decode_unit_tokens(unit, mode: int, layer: int, q, scale: float, d: int, B: int = 2) -> np.ndarray:
+    pos = layer % B
+    return attention(q, reconstruct_layer_tokens(unit, mode, pos, d, "K", B),
+                     reconstruct_layer_tokens(unit, mode, pos, d, "V", B), scale)
+
+
+def routing_errors_tokens(KB, QB, ppm: int) -> np.ndarray:
+    """Eq. (2) for the three modes with the token-level residual: the residual
+    reconstruction keeps every high-frequency coefficient of the ``ppm``-fraction
+    of tokens with the highest scores (unrounded coefficients)."""
+    KB = np.asarray(KB, dtype=np.float64)
+    QB = np.asarray(QB, dtype=np.float64)
+    T, d = KB.shape[1], KB.shape[-1]
+    s, _ = token_scores(KB, QB)
+    keep = residual_tokens(s, n_residual_tokens(T, ppm))
+    Z = depth_factorize(KB)
+    out = np.zeros(3)
+    n_l, G, P, _ = QB.shape
+    for m in MODES:
+        if m == EXACT:
+            continue
+        Zk = np.zeros_like(Z)
+        Zk[0] = Z[0]
+        if m == RESIDUAL:
+            Zk[1:, keep] = Z[1:, keep]
+        Kh = depth_reconstruct(Zk)
+        tot = 0.0
+        for l in range(n_l):
+            for g in range(G):
+                Q = QB[l, g]
+                tot += np.sum((Q @ Kh[l].T / math.sqrt(d) - Q @ KB[l].T / math.sqrt(d)) ** 2) / P
+        out[m] = tot / (n_l * G)
+    return out
+
+
+_TOKEN_MASK_BYTES_PER_TOKEN = 1.0 / 8 + 4.0 / 128   # 1-bit token mask + a uint32 count per 128 tokens
+
+
+def bytes_per_token_tokens(mode: int, d: int, ppm: int, dtype: str, B: int = 2) -> float:
+    """Average bytes per token; residual heads pay r of the (B-1) high-frequency rows of K and V."""
+    e, c = input_bytes(dtype), coef_bytes(dtype)
+    if mode == RESIDUAL:
+        return 2 * d * c + 2 * (B - 1) * d * c * (ppm / 1e6) + _TOKEN_MASK_BYTES_PER_TOKEN
+    return float(bytes_per_token(mode, d, 0, dtype, B))
+
+
+def omega_tokens(d: int, ppm: int, dtype: str, B: int = 2) -> np.ndarray:
+    full = bytes_per_token_tokens(EXACT, d, ppm, dtype, B)
+    return np.array([bytes_per_token_tokens(m, d, ppm, dtype, B) / full for m in MODES])
+
+
+def unit_bytes_tokens(mode: int, T: int, d: int, ppm: int, dtype: str, B: int = 2) -> int:
+    """Segment bytes with a token-level residual: M planes, the token mask
+    (``ceil(T/32)`` uint32 words), the running count of residual tokens before
+    every 128-token chunk (``ceil(T/128) + 1`` uint32), then the K and V
+    high-frequency rows of the ``n`` residual tokens; every plane padded."""
+    if mode != RESIDUAL:
+        return unit_bytes(mode, T, d, 0, dtype, B)
+    c = coef_bytes(dtype)
+    n = n_residual_tokens(T, ppm)
+    coef = _plane(T * d * c)
+    return (2 * coef + _plane(-(-T // 32) * 4) + _plane((-(-T // 128) + 1) * 4)
+            + 2 * _plane(n * (B - 1) * d * c))
 
 
 # ----------------------------------------------------------------------------

@@ -728,3 +728,111 @@ def test_refresh_routes_the_span():
     far = np.stack([X, -X])
     assert O.refresh_modes(far, Q, 4, "bf16", 0.0) == O.EXACT             # lambda 0: zero error wins
     assert O.refresh_modes(far, Q, 4, "bf16", math.inf) == O.SHARED
+
+
+# ---------------------------------------------------------------- token-level residual set
+@pytest.mark.parametrize("B", [2, 4])
+def test_token_score_is_the_shared_logit_change(B):
+    """s_t = max over probe rows of |q . (K_t - K^S_t)| (the paper's score), up to the bf16
+    rounding of the deviations; e_t sums the squares, so sum_t e_t / (B G P d) is E_S."""
+    rng = np.random.default_rng(50 + B)
+    T, d, G, P = 40, 16, 2, 3
+    K = O.round_bf16(rng.standard_normal((B, T, d)))
+    Q = O.round_bf16(rng.standard_normal((B, G, P, d)))
+    s, e = O.token_scores(K, Q)
+    Ks = O.candidate_keys(K, O.SHARED, 0)
+    brute_s = np.zeros(T)
+    brute_e = np.zeros(T)
+    for l in range(B):
+        for g in range(G):
+            for p in range(P):
+                for t in range(T):
+                    v = sum(Q[l, g, p, c] * (K[l, t, c] - Ks[l, t, c]) for c in range(d))
+                    brute_s[t] = max(brute_s[t], abs(v))
+                    brute_e[t] += v * v
+    np.testing.assert_allclose(s, brute_s, rtol=2 ** -7, atol=1e-12)
+    np.testing.assert_allclose(e, brute_e, rtol=2 ** -6, atol=1e-12)
+    E = O.routing_errors(K, Q, 0)
+    np.testing.assert_allclose(e.sum() / (B * G * P * d), E[O.SHARED], rtol=2 ** -6)
+
+
+def test_token_deviation_precision():
+    # pairs: bf16(fl32(x0 - x1) * 0.5); fours: bf16(fl32(x_l - fl32(((x0+x3)+(x1+x2)) * 0.25)))
+    x = np.array([[1.0, 3.0], [1.0 + 2 ** -7, -5.0]], np.float32)[:, None, :]     # [2][1][2]
+    dev = O.token_deviations(x)
+    want = O.round_bf16(np.float64((np.float32(1.0) - np.float32(1.0 + 2 ** -7)) * np.float32(0.5)))
+    assert dev[0, 0, 0] == want and dev[1, 0, 0] == -want and dev[0, 0, 1] == 4.0
+    X4 = np.array([1.0, 2.0, 4.0, 1.0 + 2 ** -20], np.float32)[:, None, None]
+    x4 = X4[:, 0, 0]
+    M = np.float32((np.float32(x4[0] + x4[3]) + np.float32(x4[1] + x4[2])) * np.float32(0.25))
+    np.testing.assert_array_equal(O.token_deviations(X4)[:, 0, 0], O.round_bf16((x4 - M).astype(np.float64)))
+
+
+def test_residual_tokens_brute_force():
+    rng = np.random.default_rng(53)
+    for trial in range(30):
+        T = int(rng.integers(1, 9))
+        s = rng.integers(0, 3, size=T).astype(np.float64)
+        for n in range(T + 1):
+            got = O.residual_tokens(s, n).tolist()
+            assert got == (_brute_topk(s.tolist(), n) if n else [])
+    assert O.n_residual_tokens(32768, 50000) == 1639 and O.n_residual_tokens(100, 0) == 0
+    assert O.n_residual_tokens(3, 1) == 1 and O.n_residual_tokens(1000000, 1) == 1
+
+
+@pytest.mark.parametrize("B", [2, 4])
+def test_token_routing_errors_limits_and_split(B):
+    rng = np.random.default_rng(54 + B)
+    T, d, G, P = 60, 8, 2, 4
+    K = O.round_bf16(rng.standard_normal((B, T, d)))
+    Q = rng.standard_normal((B, G, P, d))
+    E0 = O.routing_errors_tokens(K, Q, 0)
+    Eall = O.routing_errors_tokens(K, Q, 1000000)
+    Ech = O.routing_errors(K, Q, 0)
+    assert Eall[O.RESIDUAL] < 1e-25 and E0[O.EXACT] == 0.0
+    np.testing.assert_allclose(E0[O.RESIDUAL], Ech[O.SHARED], rtol=1e-12)
+    np.testing.assert_allclose(E0[O.SHARED], Ech[O.SHARED], rtol=1e-12)
+    # E_R = E_S minus the kept tokens' own contributions (Eq. 2 splits over tokens)
+    ppm = 150000
+    E = O.routing_errors_tokens(K, Q, ppm)
+    s, _ = O.token_scores(K, Q)
+    keep = O.residual_tokens(s, O.n_residual_tokens(T, ppm))
+    Ks = O.candidate_keys(K, O.SHARED, 0)
+    contrib = sum(np.sum((Q[l].reshape(-1, d) @ (Ks[l, keep] - K[l, keep]).T) ** 2) / (P * d)
+                  for l in range(B)) / (B * G)
+    np.testing.assert_allclose(E[O.RESIDUAL], E[O.SHARED] - contrib, rtol=1e-10)
+    assert E[O.RESIDUAL] < E[O.SHARED]
+
+
+@pytest.mark.parametrize("B", [2, 4])
+def test_token_unit_reconstruction(B):
+    rng = np.random.default_rng(56 + B)
+    T, d = 25, 8
+    K = rng.standard_normal((B, T, d))
+    V = rng.standard_normal((B, T, d))
+    tokens = np.array([0, 3, 4, 17, 24])
+    unit = O.compress_unit_tokens(K, V, O.RESIDUAL, tokens, "f64")
+    assert unit["HK"].shape == (5, B - 1, d)
+    mean = K.mean(0)
+    for p in range(B):
+        Kt = O.reconstruct_layer_tokens(unit, O.RESIDUAL, p, d, "K", B)
+        np.testing.assert_allclose(Kt[tokens], K[p, tokens], atol=1e-12)        # kept tokens: exact
+        rest = np.setdiff1d(np.arange(T), tokens)
+        np.testing.assert_allclose(Kt[rest], mean[rest], atol=1e-12)            # others: the shared mean
+        # decode through scipy's inverse DCT of the stored coefficients, brute-force softmax
+        Z = np.zeros((B, T, d))
+        Z[0] = 2.0 * unit["MK"] if B == 4 else unit["MK"] * math.sqrt(2.0)
+        Z[1:, tokens] = np.moveaxis(unit["HK"], 1, 0) if B == 4 else np.moveaxis(unit["HK"], 1, 0) * math.sqrt(2.0)
+        np.testing.assert_allclose(scipy.fft.idct(Z, type=2, norm="ortho", axis=0)[p], Kt, atol=1e-12)
+
+
+def test_token_bytes_closed_form():
+    # d = 64, bf16, B = 2, T = 1000, r = 5%: n = 50 tokens
+    # M planes 2 * 128000; mask ceil(1000/32)*4 = 128 -> 256; counts (8+1)*4 = 36 -> 256;
+    # rows 2 * pad(50 * 64 * 2 = 6400) = 2 * 6400
+    assert O.unit_bytes_tokens(O.RESIDUAL, 1000, 64, 50000, "bf16", 2) == 2 * 128000 + 256 + 256 + 2 * 6400
+    # fours: three rows per token
+    assert O.unit_bytes_tokens(O.RESIDUAL, 1000, 64, 50000, "bf16", 4) == 2 * 128000 + 256 + 256 + 2 * 19200
+    assert O.unit_bytes_tokens(O.SHARED, 1000, 64, 50000, "bf16", 4) == O.unit_bytes(O.SHARED, 1000, 64, 0, "bf16", 4)
+    np.testing.assert_allclose(O.omega_tokens(128, 50000, "bf16", 2),
+                               [0.5, (512 + 2 * 256 * 0.05 + 5 / 32) / 1024, 1.0])
