@@ -33,6 +33,16 @@
  *    uint16 codes 4c + j in ascending order plus Z_j[c].  Layer l+p rebuilds
  *    M plus F_4[j][p] Z_j[c] at channel c for each kept code.
  *  - K and V choose their residual entries independently.
+ *  - dims.residual = FDKV_RES_TOKENS switches residual heads to the
+ *    paper's token-level set (Section 3, after Eq. 2): every high-frequency
+ *    coefficient (pairs: D; fours: Z_1..Z_3) of the n = ceil(r T) tokens,
+ *    r = res_ppm / 10^6, with the largest score
+ *      s_t = max over the probe rows q of every layer of the block and every
+ *            query head of the group of |q . (K_t - K^S_t)|,
+ *    K - K^S computed in fp32 on the stored inputs and rounded to bf16 (pairs:
+ *    (x0 - x1) / 2 up to sign; fours: x_l - ((x0 + x3) + (x1 + x2)) / 4);
+ *    ties go to the lower token.  fdkv_probe writes the scores and
+ *    fdkv_compress selects from them (K and V share the set).
  *  - Query head g reads KV head g / (n_q_heads / n_kv_heads).
  *  - K, V, queries, the cache and attention outputs use one element type,
  *    `dims.dtype` (fp32 or bf16); all arithmetic is fp32.
@@ -53,6 +63,10 @@
  *    SHARED   : MK[T][d] (c), MV[T][d] (c)
  *    RESIDUAL : MK, MV, IK[T][k] (i), VK[T][k] (c), IV[T][k] (i), VV[T][k] (c)
  *    EXACT    : K of the B layers [T][d] (e) in order, then V of the B layers
+ * With FDKV_RES_TOKENS a residual segment is instead
+ *    MK, MV, MASK[ceil(T/32)] (u32, bit t%32 of word t/32: token t is in the
+ *    set), COUNT[ceil(T/128) + 1] (u32, set tokens before each 128-token
+ *    chunk, then n), HK[n][B-1][d] (c), HV[n][B-1][d] (c)  (set tokens ascending)
  */
 #ifndef FDKV_H
 #define FDKV_H
@@ -92,6 +106,9 @@ typedef enum { FDKV_F32 = 0, FDKV_BF16 = 1, FDKV_BF16_E4M3 = 2 } fdkv_dtype;
  */
 typedef enum { FDKV_SCHED_PAIRS = 0, FDKV_SCHED_MIXED = 1, FDKV_SCHED_QUADS = 2 } fdkv_schedule;
 
+/* Residual kinds: per-token top-k channel entries, or the token-level set. */
+typedef enum { FDKV_RES_CHANNELS = 0, FDKV_RES_TOKENS = 1 } fdkv_residual;
+
 typedef struct {
   int32_t n_layers;   /* L, 2..128, fitting the schedule */
   int32_t n_kv_heads; /* Hkv >= 1 */
@@ -100,6 +117,8 @@ typedef struct {
   int32_t topk;       /* k residual channels per token, 0 <= k <= d */
   int32_t dtype;      /* fdkv_dtype */
   int32_t schedule;   /* fdkv_schedule */
+  int32_t residual;   /* fdkv_residual */
+  int32_t res_ppm;    /* FDKV_RES_TOKENS: the set's fraction of tokens, 0..10^6 parts per million */
 } fdkv_dims;
 
 /* Message for a status code (static storage). */
@@ -162,13 +181,15 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
  *   qp_layers  host array of L device pointers, layer l holds Q_l [Hq][P][d]
  *   n_probe    P >= 1 probe rows per query head
  *   errors_out device float [n_blocks][Hkv][2]
+ *   token_scores_out  FDKV_RES_TOKENS: device float [n_blocks][Hkv][T], out: s_t
+ *                     (the residual loss then keeps the top ceil(r T) tokens); else unused
  *   ws         device workspace of >= fdkv_probe_workspace() bytes
  * T * d * elem_bytes and P * G * d * elem_bytes must stay below 2^31
  * (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets).
  */
 fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                        const void* const* qp_layers, int32_t n_probe, float* errors_out,
-                       void* ws, size_t ws_bytes, void* stream);
+                       float* token_scores_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * fdkv_compress - device.  Writes one sequence's segments of the compressed
@@ -176,11 +197,12 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
  *   k_layers, v_layers  host arrays of L device pointers, [Hkv][T][d] each
  *   modes        device [n_blocks][Hkv]
  *   seg_offsets  device [n_blocks][Hkv], from fdkv_layout (256-byte multiples)
+ *   token_scores FDKV_RES_TOKENS: device float [n_blocks][Hkv][T] from fdkv_probe; else unused
  *   cache        device buffer the offsets index into
  */
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                           const void* const* v_layers, const uint8_t* modes,
-                          const uint64_t* seg_offsets, void* cache, void* stream);
+                          const uint64_t* seg_offsets, const float* token_scores, void* cache, void* stream);
 
 /* Device workspace bytes fdkv_decode_attn needs for this batch shape. */
 fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t max_seq_len, size_t* bytes);

@@ -26,6 +26,7 @@ SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout"
            "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
            "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
+RES_CHANNELS, RES_TOKENS = 0, 1  # residual kinds (fdkv_residual)
 
 
 class FdkvError(RuntimeError):
@@ -41,7 +42,7 @@ class FdkvError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("schedule", ctypes.c_int32)]
+                ("schedule", ctypes.c_int32), ("residual", ctypes.c_int32), ("res_ppm", ctypes.c_int32)]
 
 
 class Span(ctypes.Structure):
@@ -53,9 +54,10 @@ class Tail(ctypes.Structure):
     _fields_ = [("lens", ctypes.c_void_p), ("cap", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p)]
 
 
-def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype, schedule=PAIRS) -> Dims:
+def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype, schedule=PAIRS, residual=RES_CHANNELS,
+         res_ppm=0) -> Dims:
     dt = {"f32": F32, "bf16": BF16, "bf16_e4m3": BF16_E4M3}.get(dtype, dtype)
-    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt, schedule)
+    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt, schedule, residual, res_ppm)
 
 
 def load():
@@ -80,9 +82,9 @@ def load():
     lib.fdkv_probe_workspace.restype = I32
     lib.fdkv_probe_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_probe.restype = I32
-    lib.fdkv_probe.argtypes = [DP, I32, P, P, I32, P, P, SZ, P]
+    lib.fdkv_probe.argtypes = [DP, I32, P, P, I32, P, P, P, SZ, P]
     lib.fdkv_compress.restype = I32
-    lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P]
+    lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P, P]
     lib.fdkv_decode_workspace.restype = I32
     lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_decode_attn.restype = I32
@@ -176,18 +178,21 @@ def decode_workspace(d: Dims, batch: int, max_seq_len: int) -> int:
 
 # ----------------------------------------------------------------- device entry points
 def probe(d: Dims, seq_len: int, k_layers: Sequence, qp_layers: Sequence, n_probe: int, errors_out, ws,
-          stream=None):
-    """Queue fdkv_probe; ``k_layers``/``qp_layers`` are per-layer device tensors."""
+          stream=None, token_scores=None):
+    """Queue fdkv_probe; ``k_layers``/``qp_layers`` are per-layer device tensors;
+    ``token_scores`` (token-level residual set) receives s_t ``[n_blocks][Hkv][T]``."""
     _check(load().fdkv_probe(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(qp_layers),
-                             int(n_probe), _dev(errors_out), _dev(ws), int(ws.numel() * ws.element_size()),
-                             _stream(stream)), "fdkv_probe")
+                             int(n_probe), _dev(errors_out), _dev(token_scores), _dev(ws),
+                             int(ws.numel() * ws.element_size()), _stream(stream)), "fdkv_probe")
 
 
 def compress(d: Dims, seq_len: int, k_layers: Sequence, v_layers: Sequence, modes, seg_offsets, cache,
-             stream=None):
-    """Queue fdkv_compress for one sequence (``modes``/``seg_offsets`` device tensors)."""
+             stream=None, token_scores=None):
+    """Queue fdkv_compress for one sequence (``modes``/``seg_offsets`` device tensors; ``token_scores``
+    from the probe when residual heads hold a token-level set)."""
     _check(load().fdkv_compress(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(v_layers),
-                                _dev(modes), _dev(seg_offsets), _dev(cache), _stream(stream)), "fdkv_compress")
+                                _dev(modes), _dev(seg_offsets), _dev(token_scores), _dev(cache), _stream(stream)),
+           "fdkv_compress")
 
 
 def decode_attn(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offsets, cache, layer: int, q, out,

@@ -86,7 +86,8 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const bool q4 = P.bsize == 4;
   const int mode = tail ? kExact : P.part[part].modes[unit];   // the exact tail of a generation has no unit arrays
   const int k = P.topk;
-  const bool resid = (mode == kResidual) && k > 0;
+  const bool resid = !P.tokres && (mode == kResidual) && k > 0;
+  const bool tokres = P.tokres && mode == kResidual;   // token-level residual set
   const uint8_t* seg = tail ? static_cast<const uint8_t*>(P.tail_k) : P.part[part].cache + P.part[part].seg_off[unit];
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E, P.bsize);
   const uint64_t xplane = plane_bytes((uint64_t)T * D * E);  // exact planes: K_p at p * xplane, V_p at (B + p) * xplane
@@ -182,6 +183,46 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
       for (int g = 0; g < G; ++g) s_lds[wave][g][pass * RPK + kr] = a[g];
     }
   }
+  // Token-level residual set: the wave's 128 tokens are one chunk of the
+  // running counts; the logits of the set's tokens get q . sum_f w_f H_f
+  // (lanes over channels, one token at a time) before the max.
+  const int NF = P.bsize - 1;
+  int ntr = 0;
+  uint32_t tbase = 0;
+  const uint8_t* hkp = nullptr;
+  const uint8_t* hvp = nullptr;
+  const uint32_t* tmask = nullptr;
+  if (tokres) {
+    const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, P.res_ppm, E, E, P.bsize);
+    tmask = reinterpret_cast<const uint32_t*>(seg + Lt.mask);
+    tbase = reinterpret_cast<const uint32_t*>(seg + Lt.count)[wtok0 / kTokChunk];
+    hkp = seg + Lt.hk;
+    hvp = seg + Lt.hv;
+    __syncthreads();  // the K pass's logits are in LDS
+    for (int tl = 0; tl < CH; ++tl) {
+      const int row = wtok0 + tl;
+      if (row >= T || !((tmask[row >> 5] >> (row & 31)) & 1u)) continue;
+      const uint64_t h0 = (uint64_t)(tbase + ntr) * NF * D;
+      for (int g = 0; g < G; ++g) {
+        float a = 0.f;
+        for (int c = lane; c < D; c += 64) {
+          float hsum = 0.f;
+          for (int f = 0; f < NF; ++f) hsum = fmaf(P.wres[f], load_elem<D, BF16>(hkp, h0 + (uint64_t)f * D + c), hsum);
+          a = fmaf(q_lds[c * G + g], hsum, a);
+        }
+        a = wave_sum(a) * P.scale_log2;
+        if (lane == 0) s_lds[wave][g][tl] += a;
+      }
+      ++ntr;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float x = -INFINITY;
+      for (int tl = lane; tl < CH; tl += 64) x = fmaxf(x, s_lds[wave][g][tl]);
+      mx[g] = x;
+    }
+  }
   float m[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) m[g] = wave_max(mx[g]);
@@ -253,6 +294,22 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
         acc[g][2] = fmaf(p, v.z, acc[g][2]);
         acc[g][3] = fmaf(p, v.w, acc[g][3]);
       }
+    }
+  }
+  if (tokres) {
+    // V of the set's tokens: each lane owns distinct channels of the accumulator
+    int j = 0;
+    for (int tl = 0; tl < CH; ++tl) {
+      const int row = wtok0 + tl;
+      if (row >= T || !((tmask[row >> 5] >> (row & 31)) & 1u)) continue;
+      const uint64_t h0 = (uint64_t)(tbase + j) * NF * D;
+      for (int c = lane; c < D; c += 64) {
+        float hsum = 0.f;
+        for (int f = 0; f < NF; ++f) hsum = fmaf(P.wres[f], load_elem<D, BF16>(hvp, h0 + (uint64_t)f * D + c), hsum);
+#pragma unroll
+        for (int g = 0; g < G; ++g) sp_lds[wave][g][c] += s_lds[wave][g][tl] * hsum;
+      }
+      ++j;
     }
   }
   if (resid) {

@@ -122,6 +122,7 @@ struct TileBuf {
   uint4 k[NL], v[NL];
   // residual entry of the lane in each of its rows (k = NP path): index byte and bf16 value
   uint32_t ki[NL], kv[NL], vi[NL], vv[NL];
+  uint32_t tm;  // token-level residual set: the tile's word of the token mask
 };
 
 }  // namespace
@@ -166,7 +167,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) return;
 
   const int k = P.topk;
-  const bool resid = (mode == kResidual) && k > 0;
+  // residual heads hold either per-token channel entries or a token-level set
+  const bool tokres = P.tokres && mode == kResidual;
+  const bool resid = !P.tokres && (mode == kResidual) && k > 0;
   // FP8 caches: the shared planes and residual values of shared / residual
   // heads are E4M3 (one byte per channel); exact heads stay bf16
   const bool c8 = C8K && mode != kExact;
@@ -186,6 +189,13 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const auto ivr = rsrc(seg + L.iv, (uint64_t)T * k * ib);
   const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * ce);
   const float w1 = P.wres[0], w2 = P.wres[1], w3 = P.wres[2];
+  // token-level residual set: token mask, running counts, rows of the set's tokens
+  const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, P.res_ppm, 2, ce, nb);
+  const uint64_t ntok = residual_token_count((uint64_t)T, P.res_ppm);
+  const auto tmr = rsrc(seg + Lt.mask, (uint64_t)(T + 31) / 32 * 4);
+  const auto tcr = rsrc(seg + Lt.count, ((uint64_t)(T + kTokChunk - 1) / kTokChunk + 1) * 4);
+  const auto hkr = rsrc(seg + Lt.hk, ntok * (uint64_t)(nb - 1) * D * ce);
+  const auto hvr = rsrc(seg + Lt.hv, ntok * (uint64_t)(nb - 1) * D * ce);
   const uint8_t* qbase = static_cast<const uint8_t*>(P.q) + ((uint64_t)seq * P.hq + (uint64_t)head * G) * RB;
   const auto qr = rsrc(qbase, (uint64_t)G * RB);
 
@@ -217,7 +227,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   }
 
   // The tile loop is specialised per residual flavour (RES: 0 none, 1 one
-  // entry per lane (k = NP), 2 any other k) so that every load of a tile is
+  // entry per lane (k = NP), 2 any other k, 3 a token-level set: the set's
+  // tokens are masked out of the tile loop and taken afterwards in a pass of
+  // their own, rebuilt in full) so that every load of a tile is
   // issued unconditionally: a tile past the wave's range takes the
   // out-of-range offset and reads zeros without touching memory.  With no
   // load behind a branch the compiler can wait for exactly the tile it needs
@@ -240,11 +252,12 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       }
     };
 
-    constexpr int PD = RES == 0 ? S::PD0 : 1, NB = PD + 1;
+    constexpr int PD = (RES == 0 || RES == 3) ? S::PD0 : 1, NB = PD + 1;
 
     auto load = [&](int t, TileBuf<D, G>& b) {
       const bool ok = t < ntiles;
       const uint32_t r0 = (uint32_t)(wtok0 + t * TILE);
+      if constexpr (RES == 3) b.tm = __builtin_amdgcn_raw_buffer_load_b32(tmr, ok ? (r0 >> 5) * 4 : kOob, 0, 0);
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const uint32_t row = r0 + i * RPL + rg;
@@ -323,7 +336,8 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       float d = -INFINITY;
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
-        const bool valid = r0 + i * RPL + rg < T;
+        const int row = r0 + i * RPL + rg;
+        const bool valid = row < T && (RES != 3 || ((b.tm >> (row & 31)) & 1u) == 0u);
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           const float x = group_sum<NP>(s[i][g]) * P.scale_log2;
@@ -347,7 +361,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           l[g] *= alpha;
 #pragma unroll
           for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
-          if constexpr (RES != 0) {
+          if constexpr (RES == 1 || RES == 2) {
 #pragma unroll
             for (int cp = 0; cp < RPL; ++cp)
 #pragma unroll
@@ -434,7 +448,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     TileBuf<D, G> buf[NB];
 #pragma unroll
     for (int i = 0; i < PD; ++i) load(i, buf[i]);
-    if constexpr (RES != 0) {
+    if constexpr (RES == 1 || RES == 2) {
       for (int x = lane * 4; x < RPL * G * D; x += 256)
         *reinterpret_cast<float4*>(&sp(wave, 0, 0, x)) = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
@@ -451,11 +465,114 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         if (j == 0 || t + j < ntiles) compute(t + j, buf[j]);
       }
     }
+
+    if constexpr (RES == 3) {
+      // The wave's tokens of the residual set (its 128 tokens are one chunk
+      // of the running counts), RPL at a time: the lanes of row group rg
+      // rebuild the rg-th one in full, K~ = M + sum_f w_f H_f and V~ alike,
+      // and fold it into the online softmax.
+      constexpr int NF = Q4 ? 3 : 1;
+      static_assert(CW == kTokChunk, "one count per wave");
+      const uint32_t tw = (uint32_t)wtok0 >> 5;
+      const bool in_a = wtok0 < T, in_b = wtok0 + 64 < T;
+      const uint32_t wa = __builtin_amdgcn_raw_buffer_load_b32(tmr, in_a ? (tw + (lane >> 5)) * 4 : kOob, 0, 0);
+      const uint32_t wb = __builtin_amdgcn_raw_buffer_load_b32(tmr, in_b ? (tw + 2 + (lane >> 5)) * 4 : kOob, 0, 0);
+      const uint32_t base = __builtin_amdgcn_raw_buffer_load_b32(tcr, in_a ? ((uint32_t)wtok0 / kTokChunk) * 4 : kOob,
+                                                                 0, 0);
+      const bool bit_a = (wa >> (lane & 31)) & 1u, bit_b = (wb >> (lane & 31)) & 1u;
+      const uint64_t ba = __ballot(bit_a), bb = __ballot(bit_b);
+      const int na = __builtin_popcountll(ba), nres = na + __builtin_popcountll(bb);
+      int* lst = reinterpret_cast<int*>(big) + wave * CW;  // wave-private (this flavour has no V accumulators)
+      const uint64_t below = (1ull << lane) - 1ull;
+      if (bit_a) lst[__builtin_popcountll(ba & below)] = lane;
+      if (bit_b) lst[na + __builtin_popcountll(bb & below)] = 64 + lane;
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      const float wf[3] = {w1, w2, w3};
+      for (int j0 = 0; j0 < nres; j0 += RPL) {
+        const int j = j0 + rg;
+        const bool ok = j < nres;
+        const uint32_t row = (uint32_t)(wtok0 + (ok ? lst[j] : 0));
+        const uint32_t hrow = (base + (uint32_t)j) * NF * D;  // element index of the token's first row
+        uint4 mk, mv, hk[NF], hv[NF];
+        if constexpr (C8) {
+          const auto a = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? row * D + pc * 8 : kOob, 0, 0);
+          const auto b2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? row * D + pc * 8 : kOob, 0, 0);
+          mk = widen_e4m3(make_uint4(a[0], a[1], 0u, 0u));
+          mv = widen_e4m3(make_uint4(b2[0], b2[1], 0u, 0u));
+#pragma unroll
+          for (int f = 0; f < NF; ++f) {
+            const uint32_t e = hrow + f * D + pc * 8;
+            const auto x = __builtin_amdgcn_raw_buffer_load_b64(hkr, ok ? e : kOob, 0, 0);
+            const auto y = __builtin_amdgcn_raw_buffer_load_b64(hvr, ok ? e : kOob, 0, 0);
+            hk[f] = widen_e4m3(make_uint4(x[0], x[1], 0u, 0u));
+            hv[f] = widen_e4m3(make_uint4(y[0], y[1], 0u, 0u));
+          }
+        } else {
+          mk = ld128(kr, ok ? row * RB + pc * 16 : kOob);
+          mv = ld128(vr, ok ? row * RB + pc * 16 : kOob);
+#pragma unroll
+          for (int f = 0; f < NF; ++f) {
+            const uint32_t e = (hrow + f * D + pc * 8) * 2;
+            hk[f] = ld128(hkr, ok ? e : kOob);
+            hv[f] = ld128(hvr, ok ? e : kOob);
+          }
+        }
+        float kf[8], vf[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const int w = c >> 1;
+          auto ch = [&](const uint4& v) { return (c & 1) ? bf16_hi(word(v, w)) : bf16_lo(word(v, w)); };
+          kf[c] = ch(mk);
+          vf[c] = ch(mv);
+#pragma unroll
+          for (int f = 0; f < NF; ++f) {
+            kf[c] = fmaf(wf[f], ch(hk[f]), kf[c]);
+            vf[c] = fmaf(wf[f], ch(hv[f]), vf[c]);
+          }
+        }
+        float sres[G];
+        float dmax = -INFINITY;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          float a = 0.f;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) {
+            const uint32_t qw = word(qreg[g], c >> 1);
+            a = fmaf(kf[c], (c & 1) ? bf16_hi(qw) : bf16_lo(qw), a);
+          }
+          sres[g] = ok ? group_sum<NP>(a) * P.scale_log2 : -INFINITY;
+          dmax = fmaxf(dmax, sres[g] - m[g]);
+        }
+        if (__ballot(dmax > kSlack) != 0) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            float mt = sres[g];
+#pragma unroll
+            for (int o = NP; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
+            const float mn = fmaxf(m[g], mt);
+            const float alpha = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
+            l[g] *= alpha;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
+            m[g] = mn;
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float pg = __builtin_amdgcn_exp2f(sres[g] - m[g]);  // rows past the set: exp2(-inf) = 0
+          l[g] += pg;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) acc[g][c] = fmaf(pg, vf[c], acc[g][c]);
+        }
+      }
+    }
   };  // run
 
   using R0 = std::integral_constant<int, 0>;
   using R1 = std::integral_constant<int, 1>;
   using R2 = std::integral_constant<int, 2>;
+  using R3 = std::integral_constant<int, 3>;
   using F = std::false_type;
   using Tr = std::true_type;
   // residual heads: one entry per lane of a row (k = NP) or any other k, by block size
@@ -472,10 +589,18 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         run(R2{}, c8_tag, F{});
     }
   };
+  auto run_tok = [&](auto c8_tag) {
+    if (nb == 4)
+      run(R3{}, c8_tag, Tr{});
+    else
+      run(R3{}, c8_tag, F{});
+  };
   if constexpr (C8K) {
     if (c8) {
       if (resid)
         run_res(Tr{});
+      else if (tokres)
+        run_tok(Tr{});
       else
         run(R0{}, Tr{}, F{});
     } else {
@@ -484,6 +609,8 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   } else {
     if (resid)
       run_res(F{});
+    else if (tokres)
+      run_tok(F{});
     else
       run(R0{}, F{}, F{});
   }

@@ -88,6 +88,8 @@ fdkv_status check_dims(const fdkv_dims* d) {
   if (d->head_dim < 1 || d->head_dim > 256) return FDKV_E_INVALID_ARG;
   if (d->topk < 0 || d->topk > d->head_dim) return FDKV_E_INVALID_ARG;
   if (d->dtype != FDKV_F32 && d->dtype != FDKV_BF16 && d->dtype != FDKV_BF16_E4M3) return FDKV_E_INVALID_ARG;
+  if (d->residual != FDKV_RES_CHANNELS && d->residual != FDKV_RES_TOKENS) return FDKV_E_INVALID_ARG;
+  if (d->residual == FDKV_RES_TOKENS && (d->res_ppm < 0 || d->res_ppm > 1000000)) return FDKV_E_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return FDKV_E_UNSUPPORTED;
   const int G = d->n_q_heads / d->n_kv_heads;
   if (G != 1 && G != 2 && G != 4 && G != 8) return FDKV_E_UNSUPPORTED;
@@ -103,6 +105,24 @@ uint64_t bytes_per_token(int mode, int d, int k, int e, int c, int B) {
   if (mode == kShared) return 2ull * d * c;
   if (mode == kResidual) return 2ull * d * c + 2ull * k * (index_bytes(B) + c);
   return 2ull * B * d * e;
+}
+
+bool tokens_mode(const fdkv_dims* d) { return d->residual == FDKV_RES_TOKENS; }
+
+// Average bytes per token of a mode for Omega: the token-level residual pays
+// r of the (B - 1) high-frequency rows of K and V plus its 1-bit mask and a
+// uint32 count per 128 tokens.
+double omega_bytes(const fdkv_dims* dm, int mode, int B) {
+  const int d = dm->head_dim, e = elem_bytes(dm), c = coef_bytes(dm);
+  if (tokens_mode(dm) && mode == kResidual)
+    return 2.0 * d * c + 2.0 * (B - 1) * d * c * (dm->res_ppm / 1e6) + 1.0 / 8 + 4.0 / kTokChunk;
+  return (double)bytes_per_token(mode, d, dm->topk, e, c, B);
+}
+
+uint64_t segment_bytes(const fdkv_dims* dm, int mode, uint64_t T, int B) {
+  const int e = elem_bytes(dm), c = coef_bytes(dm);
+  if (tokens_mode(dm)) return tok_layout(mode, T, dm->head_dim, dm->res_ppm, e, c, B).total;
+  return seg_layout(mode, T, dm->head_dim, dm->topk, e, c, B).total;
 }
 
 Sched sched_of(const fdkv_dims* d) {
@@ -121,6 +141,10 @@ struct ProbeWs {
 ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
   const uint64_t units = (uint64_t)sched_of(d).n * d->n_kv_heads;
   ProbeWs w{};
+  if (tokens_mode(d)) {  // the token scores' sums of squares
+    w.total = plane_bytes(units * (uint64_t)T * 4);
+    return w;
+  }
   w.idx = 0;
   w.gram = w.idx + units * probe_idx_stride((uint64_t)T, d->topk);
   w.part = w.gram + plane_bytes((uint64_t)d->n_layers * d->n_kv_heads * d->head_dim * d->head_dim * 4);
@@ -179,8 +203,7 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
     for (int u = 0; u < units; ++u) {
       const size_t i = (size_t)b * units + u;
       if (seg_offsets) seg_offsets[i] = off;
-      off += seg_layout(modes[i], (uint64_t)seq_lens[b], dims->head_dim, dims->topk, e, c,
-                        sch.size[u / dims->n_kv_heads]).total;
+      off += segment_bytes(dims, modes[i], (uint64_t)seq_lens[b], sch.size[u / dims->n_kv_heads]);
     }
   *total_bytes = off;
   return FDKV_OK;
@@ -201,10 +224,10 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   uint64_t segB[2][3];
   for (int bi = 0; bi < 2; ++bi) {
     const int B = bi ? 4 : 2;
-    const double full = (double)bytes_per_token(kExact, d, k, e, c, B);
+    const double full = omega_bytes(dims, kExact, B);
     for (int m = 0; m < 3; ++m) {
-      omB[bi][m] = (double)bytes_per_token(m, d, k, e, c, B) / full;
-      segB[bi][m] = seg_layout(m, (uint64_t)seq_len, d, k, e, c, B).total;
+      omB[bi][m] = omega_bytes(dims, m, B) / full;
+      segB[bi][m] = segment_bytes(dims, m, (uint64_t)seq_len, B);
     }
   }
   auto quad = [&](int u) { return sch.size[u / dims->n_kv_heads] == 4 ? 1 : 0; };
@@ -272,8 +295,8 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
 }
 
 fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
-                       const void* const* qp_layers, int32_t n_probe, float* errors_out, void* ws,
-                       size_t ws_bytes, void* stream) {
+                       const void* const* qp_layers, int32_t n_probe, float* errors_out, float* token_scores_out,
+                       void* ws, size_t ws_bytes, void* stream) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 1 || n_probe < 1 || !k_layers || !qp_layers) return FDKV_E_INVALID_ARG;
@@ -291,6 +314,35 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   uint8_t* base = static_cast<uint8_t*>(ws);
 
   const Sched sch = sched_of(dims);
+  if (tokens_mode(dims)) {
+    if (!aligned(token_scores_out, 4)) return FDKV_E_INVALID_ARG;
+    TokenParams tp{};
+    for (int l = 0; l < dims->n_layers; ++l) {
+      tp.k[l] = k_layers[l];
+      tp.qp[l] = qp_layers[l];
+    }
+    tp.modes = nullptr;
+    tp.scores = token_scores_out;
+    tp.sumsq = reinterpret_cast<float*>(base);
+    tp.errors = errors_out;
+    tp.seq_len = seq_len;
+    tp.hkv = dims->n_kv_heads;
+    tp.hq = dims->n_q_heads;
+    tp.d = dims->head_dim;
+    tp.n_probe = n_probe;
+    tp.res_ppm = dims->res_ppm;
+    tp.bf16 = dims->dtype != FDKV_F32;
+    for (int B = 2; B <= 4; B += 2) {
+      tp.bl = blocks_of_size(sch, B);
+      tp.bsize = B;
+      if (tp.bl.n == 0) continue;
+      hipError_t e = launch_token_scores(tp, s);
+      if (e != hipSuccess) return hip_fail(e, "token_scores");
+      e = launch_token_select(tp, s);
+      if (e != hipSuccess) return hip_fail(e, "token_select");
+    }
+    return FDKV_OK;
+  }
   SelectParams sp{};
   for (int l = 0; l < dims->n_layers; ++l) sp.k[l] = sp.v[l] = k_layers[l];
   sp.modes = nullptr;
@@ -336,7 +388,7 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
 
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                           const void* const* v_layers, const uint8_t* modes, const uint64_t* seg_offsets,
-                          void* cache, void* stream) {
+                          const float* token_scores, void* cache, void* stream) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 0 || !k_layers || !v_layers || !modes || !aligned(seg_offsets, 8) || !aligned(cache, 256))
@@ -362,14 +414,39 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   cp.topk = sp.topk = dims->topk;
   cp.bf16 = sp.bf16 = dims->dtype != FDKV_F32;
   cp.coef8 = sp.coef8 = dims->dtype == FDKV_BF16_E4M3;
+  const bool tok = tokens_mode(dims);
+  if (tok && !aligned(token_scores, 4)) return FDKV_E_INVALID_ARG;
+  TokenParams tp{};
+  for (int l = 0; l < dims->n_layers; ++l) {
+    tp.k[l] = k_layers[l];
+    tp.v[l] = v_layers[l];
+  }
+  tp.modes = modes;
+  tp.seg_off = seg_offsets;
+  tp.cache = cp.cache;
+  tp.scores = const_cast<float*>(token_scores);
+  tp.seq_len = seq_len;
+  tp.hkv = cp.hkv;
+  tp.hq = dims->n_q_heads;
+  tp.d = cp.d;
+  tp.res_ppm = dims->res_ppm;
+  tp.bf16 = cp.bf16;
+  tp.coef8 = cp.coef8;
   for (int B = 2; B <= 4; B += 2) {
-    cp.bl = sp.bl = blocks_of_size(sch, B);
-    cp.bsize = sp.bsize = B;
+    cp.bl = sp.bl = tp.bl = blocks_of_size(sch, B);
+    cp.bsize = sp.bsize = tp.bsize = B;
     if (cp.bl.n == 0) continue;
     hipError_t e = launch_compress_dense(cp, s);
     if (e != hipSuccess) return hip_fail(e, "compress_dense");
-    e = launch_residual_select(sp, 2, s);
-    if (e != hipSuccess) return hip_fail(e, "residual_select");
+    if (tok) {
+      e = launch_token_select(tp, s);
+      if (e != hipSuccess) return hip_fail(e, "token_select");
+      e = launch_token_rows(tp, s);
+      if (e != hipSuccess) return hip_fail(e, "token_rows");
+    } else {
+      e = launch_residual_select(sp, 2, s);
+      if (e != hipSuccess) return hip_fail(e, "residual_select");
+    }
   }
   return FDKV_OK;
 }
@@ -436,6 +513,9 @@ fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_sp
         !aligned(sp.cache, 256))
       return FDKV_E_INVALID_ARG;
     if ((uint64_t)sp.max_seq_len * row >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
+    // the rows of a token-level residual set are addressed with 32-bit offsets too
+    if (tokens_mode(dims) && residual_token_count((uint64_t)sp.max_seq_len, dims->res_ppm) * 3 * row >= (1ull << 31))
+      return FDKV_E_UNSUPPORTED;
     maxes[i] = sp.max_seq_len;
   }
   if (tail) {
@@ -468,6 +548,8 @@ fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_sp
   p.scale_log2 = sm_scale * 1.4426950408889634f;
   p.bf16 = dims->dtype != FDKV_F32;
   p.coef8 = dims->dtype == FDKV_BF16_E4M3;
+  p.tokres = tokens_mode(dims);
+  p.res_ppm = dims->res_ppm;
   // record slots: every part's chunks, spans first, then the tail
   int total = 0;
   for (int i = 0; i < n_parts; ++i) {

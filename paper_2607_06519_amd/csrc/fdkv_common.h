@@ -63,6 +63,40 @@ FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e, int c, i
   return s;
 }
 
+// Token-level residual set (residual heads keep every high-frequency
+// coefficient of n tokens): the shared planes, a 1-bit token mask
+// (ceil(T/32) uint32 words), the count of residual tokens before every
+// 128-token chunk (ceil(T/128) + 1 uint32), then the K and V rows of the n
+// tokens, each (B - 1) x d coefficients.
+constexpr int kTokChunk = 128;
+
+struct TokLayout {
+  uint64_t mk, mv, mask, count, hk, hv, total;
+};
+
+FDKV_HD uint64_t residual_token_count(uint64_t T, int ppm) { return (T * (uint64_t)ppm + 999999) / 1000000; }
+
+FDKV_HD TokLayout tok_layout(int mode, uint64_t T, int d, int ppm, int e, int c, int B) {
+  TokLayout s{};
+  const uint64_t coef = plane_bytes(T * (uint64_t)d * c);
+  if (mode == kExact) {
+    s.total = 2 * B * plane_bytes(T * (uint64_t)d * e);
+    return s;
+  }
+  s.mk = 0;
+  s.mv = coef;
+  s.total = 2 * coef;
+  if (mode == kResidual) {
+    const uint64_t n = residual_token_count(T, ppm);
+    s.mask = 2 * coef;
+    s.count = s.mask + plane_bytes((T + 31) / 32 * 4);
+    s.hk = s.count + plane_bytes(((T + kTokChunk - 1) / kTokChunk + 1) * 4);
+    s.hv = s.hk + plane_bytes(n * (uint64_t)(B - 1) * d * c);
+    s.total = s.hv + plane_bytes(n * (uint64_t)(B - 1) * d * c);
+  }
+  return s;
+}
+
 // ---------------------------------------------------------------- bf16
 FDKV_HD float bf16_lo(uint32_t w) { return as_f32(w << 16); }
 FDKV_HD float bf16_hi(uint32_t w) { return as_f32(w & 0xFFFF0000u); }

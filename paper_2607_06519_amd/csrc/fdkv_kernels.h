@@ -28,6 +28,25 @@ struct CompressParams {
   int seq_len, bsize, hkv, d, topk;
   bool bf16;
   bool coef8;                  // shared planes in FP8 E4M3 (bf16 inputs)
+  bool tokres;                 // token-level residual set (else per-token channel top-k)
+  int res_ppm;                 // its fraction of tokens, parts per million
+  const float* scores;         // token scores [blocks][hkv][T] (token-level residual set)
+};
+
+// Token-level residual set: score kernel (probe), selection and rows.
+struct TokenParams {
+  const void* k[kMaxPtrLayers];
+  const void* v[kMaxPtrLayers];
+  const void* qp[kMaxPtrLayers];
+  const uint8_t* modes;        // null: every unit (probe); else residual units only (compress)
+  const uint64_t* seg_off;
+  uint8_t* cache;
+  float* scores;               // [blocks][hkv][T]
+  float* sumsq;                // [blocks][hkv][T] (probe)
+  float* errors;               // [blocks][hkv][2] (probe)
+  BlockList bl;
+  int seq_len, bsize, hkv, hq, d, n_probe, res_ppm;
+  bool bf16, coef8;
 };
 
 struct SelectParams {
@@ -61,6 +80,8 @@ struct DecodePart {
 
 struct DecodeParams {
   const void* q;               // [batch][hq][d]
+  bool tokres;                 // residual heads hold a token-level residual set
+  int res_ppm;
   void* out;                   // [batch][hq][d]
   float* ws;                   // records [batch][hkv][n_chunks_total][G][d + 4]
   int block, pos, bsize;       // the layer's block, its position in it, the block size
@@ -126,6 +147,9 @@ hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // split-
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
 hipError_t launch_append(const AppendParams& P, hipStream_t s);
+hipError_t launch_token_scores(const TokenParams& P, hipStream_t s);   // the blocks of P.bl (one size)
+hipError_t launch_token_select(const TokenParams& P, hipStream_t s);   // probe: errors; compress: mask, counts
+hipError_t launch_token_rows(const TokenParams& P, hipStream_t s);     // compress: rows of the selected tokens
 hipError_t launch_probe(const ProbeParams& P, hipStream_t s);           // the blocks of P.bl (one size)
 hipError_t launch_probe_finalize(const ProbeParams& P, hipStream_t s);  // every unit
 

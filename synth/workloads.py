@@ -18,8 +18,9 @@ The five named workloads are:
                   head; modes come from the probe and the byte budget of the
                   50/35/15 mix.
 
-Variants: ``llama8b_e4m3`` (FP8 coefficients) and ``llama8b_mixed`` (blocks of
-four layers between pairs at both ends).
+Variants: ``llama8b_e4m3`` (FP8 coefficients), ``llama8b_mixed`` (blocks of
+four layers between pairs at both ends) and ``llama8b_tokres`` (token-level
+residual sets of 5% of the tokens).
 """
 from __future__ import annotations
 
@@ -52,6 +53,8 @@ class Workload:
     steps: int = 1                 # decode steps the workload describes
     seed: int = 0
     schedule: int = 0              # layer blocks: 0 pairs, 1 pairs-fours-pairs (first / last four layers in pairs), 2 fours
+    residual: int = 0              # residual heads: 0 per-token channel top-k, 1 token-level set
+    res_ppm: int = 0               # the token-level set's fraction of tokens (parts per million)
     notes: str = field(default="", compare=False)
 
     @property
@@ -105,7 +108,8 @@ class Workload:
     def dims(self) -> dict:
         return dict(n_layers=self.n_layers, n_kv_heads=self.n_kv_heads,
                     n_q_heads=self.n_q_heads, head_dim=self.head_dim,
-                    topk=self.topk, dtype=self.dtype, schedule=self.schedule)
+                    topk=self.topk, dtype=self.dtype, schedule=self.schedule,
+                    residual=self.residual, res_ppm=self.res_ppm)
 
 
 def _ragged_lengths(seed: int, cfg_id: int, batch: int, lo: int, hi: int) -> Tuple[int, ...]:
@@ -169,4 +173,11 @@ LLAMA8B_MIXED = dataclasses.replace(
     LLAMA8B, name="llama8b_mixed", schedule=1,
     notes="llama8b with blocks of four layers between pairs at both ends (the default block setting)")
 
-WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3, LLAMA8B_MIXED)}
+# the 8B workload with the paper's token-level residual rule: residual heads keep every
+# high-frequency coefficient of the 5% of tokens with the largest probe-logit change
+LLAMA8B_TOKRES = dataclasses.replace(
+    LLAMA8B, name="llama8b_tokres", topk=0, residual=1, res_ppm=50000,
+    notes="llama8b with token-level residual sets (5% of tokens per residual head)")
+
+WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3, LLAMA8B_MIXED,
+                                 LLAMA8B_TOKRES)}

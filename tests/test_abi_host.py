@@ -128,12 +128,12 @@ def test_validation_errors_before_any_device_call(lib):
     # planes are addressed with 32-bit offsets: T * d * 2 bytes must stay below 2^31
     assert lib.fdkv_decode_attn(ctypes.byref(good), 1, fake, 1 << 23, fake, fake, fake, 0, fake, fake,
                                 ctypes.c_float(0.1), fake, 1 << 40, None) == -2
-    assert lib.fdkv_compress(ctypes.byref(good), 16, ptrs, None, fake, fake, fake, None) == -1
+    assert lib.fdkv_compress(ctypes.byref(good), 16, ptrs, None, fake, fake, None, fake, None) == -1
     n = ctypes.c_size_t(0)
     assert lib.fdkv_probe_workspace(ctypes.byref(good), 100, 4, ctypes.byref(n)) == 0 and n.value > 0
-    assert lib.fdkv_probe(ctypes.byref(good), 100, ptrs, ptrs, 4, fake, fake, n.value - 1, None) == -3
-    assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, fake, n.value, None) == -1
-    assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, fake, 1 << 40, None) == -2
+    assert lib.fdkv_probe(ctypes.byref(good), 100, ptrs, ptrs, 4, fake, None, fake, n.value - 1, None) == -3
+    assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, None, fake, n.value, None) == -1
+    assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, None, fake, 1 << 40, None) == -2
     assert lib.fdkv_layout(None, 1, None, None, None, None) == -1
 
 
@@ -219,3 +219,43 @@ def test_generation_entry_points_validate(lib):
     assert lib.fdkv_append(ctypes.byref(good), 1, fake, 0, fake, fake, fake, fake, None) == -1     # cap 0
     assert lib.fdkv_append(ctypes.byref(good), 1, ctypes.c_void_p((1 << 20) + 2), 8, fake, fake, fake, fake,
                            None) == -1
+
+
+# ---------------------------------------------------------------- token-level residual set
+@pytest.mark.parametrize("dtype,d,ppm,sched", [("bf16", 128, 50000, B.PAIRS), ("f32", 64, 123456, B.QUADS),
+                                               ("bf16_e4m3", 128, 1000000, B.MIXED), ("bf16", 64, 0, B.MIXED)])
+def test_layout_tokens_match_oracle(lib, dtype, d, ppm, sched):
+    rng = np.random.default_rng(ppm % 97 + d)
+    L, H, batch = 12, 2, 3
+    dm = B.dims(L, H, 2 * H, d, 0, dtype, sched, B.RES_TOKENS, ppm)
+    sizes = [Bs for _, Bs in O.block_schedule(L, sched)]
+    seq = rng.integers(0, 5000, size=batch)
+    seq[0] = 1
+    modes = rng.integers(0, 3, size=(batch, len(sizes), H)).astype(np.uint8)
+    off, total = B.layout(dm, seq, modes)
+    unit = [O.unit_bytes_tokens(int(modes[b, i, h]), int(seq[b]), d, ppm, dtype, sizes[i])
+            for b in range(batch) for i in range(len(sizes)) for h in range(H)]
+    assert total == sum(unit)
+    np.testing.assert_array_equal(off.ravel(), np.concatenate([[0], np.cumsum(unit)[:-1]]))
+
+
+def test_route_tokens_matches_oracle(lib):
+    rng = np.random.default_rng(61)
+    d, T, H, ppm = 128, 32768, 8, 50000
+    dm = B.dims(32, H, 32, d, 0, "bf16", B.MIXED, B.RES_TOKENS, ppm)
+    usz = [Bs for _, Bs in O.block_schedule(32, O.MIXED) for _ in range(H)]
+    E = _rand_errors(rng, len(usz))
+    E3 = np.concatenate([E.astype(np.float64), np.zeros((len(usz), 1))], axis=1)
+    om = np.stack([O.omega_tokens(d, ppm, "bf16", Bs) for Bs in usz])
+    for lam in (0.0, 2.0, 17.0, 1e9):
+        m, _, _ = B.route(dm, T, E.reshape(-1, H, 2), lam=lam)
+        np.testing.assert_array_equal(m.ravel(), O.route(E3, om, lam))
+
+
+def test_tokens_validation(lib):
+    n = ctypes.c_int32(0)
+    for ppm in (-1, 1000001):
+        bad = B.dims(4, 2, 4, 64, 0, "bf16", B.PAIRS, B.RES_TOKENS, ppm)
+        assert lib.fdkv_blocks(ctypes.byref(bad), ctypes.byref(n), None, None) == -1
+    bad = B.dims(4, 2, 4, 64, 0, "bf16", B.PAIRS, 2, 0)
+    assert lib.fdkv_blocks(ctypes.byref(bad), ctypes.byref(n), None, None) == -1

@@ -1,0 +1,180 @@
+"""Token-level residual sets on the GPU through the C ABI, against the oracle.
+
+The score s_t (max over probe rows of |q . (K_t - K^S_t)|) and its sum of
+squares come from MFMA sums in fp32 over bf16 deviations that the oracle
+reproduces exactly, so they agree to fp32 rounding (relative 1e-4 written
+here). Which tokens enter the set is an integer decision taken from those
+sums: tokens whose oracle score clears the n-th largest by a relative 1e-4
+must be in, those below it by as much must be out, and the set has exactly
+n tokens. Everything after the selection is checked against the oracle
+given the GPU's set: the routing losses within 5e-4 relative (the bf16
+deviations), stored rows within 1 ulp (fp32 blocks of four: within 2^-21 of
+the channel's largest input), decode within relative L2 1e-2 (bf16) / 1e-5
+(fp32)."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from synth import WORKLOADS, gen, scaled
+
+from gpu_cases import BYTES, TYPES, _pad, block_of, compare_units, rel_l2, sharpened_queries, ulp_distance, values
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2607_06519_amd import binding
+    binding.load()
+    return torch
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _tok(w, **over):
+    return scaled(w, topk=0, residual=1, **over)
+
+
+CASES = {
+    "pairs_bf16": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(1500,), n_probe=48,
+                       res_ppm=50000),
+    "quads_bf16_ragged": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(1111,),
+                              n_probe=32, res_ppm=80000, schedule=2),
+    "mixed_e4m3_d64_g2": _tok(WORKLOADS["prefill8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, head_dim=64,
+                              seq_lens=(700,), n_probe=20, res_ppm=100000, schedule=1, dtype="bf16_e4m3",
+                              needle_channels=8),
+    "quads_f32_g1": _tok(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=2, seq_lens=(600,), n_probe=24,
+                         res_ppm=70000, schedule=2),
+    # degenerate sets: none (r = 0), and a handful of tokens in a sequence shorter than one chunk
+    "pairs_f32_empty": _tok(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, seq_lens=(200,), n_probe=16,
+                            res_ppm=0),
+    "pairs_bf16_short": _tok(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, seq_lens=(37,),
+                             n_probe=8, res_ppm=30000, n_needles=1),
+}
+
+
+def unpack_tok_unit(buf, off, mode, T, d, ppm, dtype, B):
+    """A token-level residual segment read back (the layout of include/fdkv.h)."""
+    ti, tc = TYPES[dtype]
+    e, c = BYTES[ti], BYTES[tc]
+    if mode != O.RESIDUAL:
+        from gpu_cases import unpack_unit
+        return unpack_unit(buf, off, mode, T, d, 0, dtype, B), None
+    coef = _pad(T * d * c)
+    n = O.n_residual_tokens(T, ppm)
+    mo = 2 * coef
+    co = mo + _pad(-(-T // 32) * 4)
+    hk = co + _pad((-(-T // 128) + 1) * 4)
+    hv = hk + _pad(n * (B - 1) * d * c)
+
+    def plane(o, rows, width, kind):
+        return values(buf[off + o: off + o + rows * width * BYTES[kind]].copy(), kind).reshape(rows, width)
+
+    words = buf[off + mo: off + mo + (-(-T // 32)) * 4].copy().view("<u4")
+    bits = ((words[:, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(-1)[:T]
+    counts = buf[off + co: off + co + ((-(-T // 128)) + 1) * 4].copy().view("<u4").astype(np.int64)
+    u = {"MK": plane(0, T, d, tc), "MV": plane(coef, T, d, tc), "TS": np.nonzero(bits)[0].astype(np.int64),
+         "HK": plane(hk, n, (B - 1) * d, tc).reshape(n, B - 1, d), "HV": plane(hv, n, (B - 1) * d, tc).reshape(n, B - 1, d)}
+    return u, counts
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_token_residual_parity(torch_dev, name):
+    torch = torch_dev
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, probe, to_device
+    w = CASES[name]
+    T, P, G, d, H = w.seq_lens[0], w.n_probe, w.group, w.head_dim, w.n_kv_heads
+    ppm = w.res_ppm
+    n = O.n_residual_tokens(T, ppm)
+    log(f"[case] token residual {name}: T={T} blocks {w.block_sizes} d={d} G={G} r={ppm / 1e6} (n={n}) {w.dtype}")
+    K, V = gen.layer_cache(w, 0)
+    Q = gen.probe_queries(w, 0)
+    Kd, Vd, Qd = to_device(K, w.dtype), to_device(V, w.dtype), to_device(Q, w.dtype)
+    dm = Bn.dims(**w.dims())
+    kl, vl, ql = ([X[l] for l in range(w.n_layers)] for X in (Kd, Vd, Qd))
+    err, scores = probe(dm, T, kl, ql, P)
+    got_err = err.cpu().numpy().astype(np.float64)
+    got_s = scores.cpu().numpy().astype(np.float64)
+
+    # scores against the oracle's, unit by unit
+    ref_s = np.zeros((w.n_blocks, H, T))
+    for b, (f, B) in enumerate(w.blocks):
+        for h in range(H):
+            s, _ = O.token_scores(K[f:f + B, h], Q[f:f + B, h * G:(h + 1) * G])
+            ref_s[b, h] = s
+    rel = np.abs(got_s - ref_s) / np.maximum(ref_s, 1e-30)
+    log(f"  scores: max rel error {rel.max():.2e}")
+    assert rel.max() <= 1e-4
+
+    # modes: every unit residual except a few, so the compressed sets get checked everywhere
+    modes = np.full((w.n_blocks, H), O.RESIDUAL, np.uint8)
+    modes[0, 0] = O.SHARED
+    modes[-1, -1] = O.EXACT
+    cache = CompressedCache(dm, w.seq_lens, modes[None])
+    cache.compress(0, kl, vl, token_scores=scores)
+    torch.cuda.synchronize()
+    buf = cache.host_bytes()
+    units = {}
+    for b, (f, B) in enumerate(w.blocks):
+        for h in range(H):
+            m = int(modes[b, h])
+            got, counts = unpack_tok_unit(buf, int(cache.offsets_host[0, b, h]), m, T, d, ppm, w.dtype, B)
+            if m == O.RESIDUAL:
+                S = got["TS"]
+                assert S.size == n, (b, h, S.size, n)
+                tau = np.sort(ref_s[b, h])[::-1][n - 1] if n else np.inf
+                inside = np.zeros(T, bool)
+                inside[S] = True
+                assert not np.any((ref_s[b, h] > tau * (1 + 1e-4)) & ~inside)
+                assert not np.any((ref_s[b, h] < tau * (1 - 1e-4)) & inside)
+                chunk_starts = np.arange(0, T, 128)
+                np.testing.assert_array_equal(counts[:-1], np.searchsorted(S, chunk_starts))
+                assert counts[-1] == n
+                ref = O.compress_unit_tokens(K[f:f + B, h], V[f:f + B, h], m, S, w.dtype)
+                for key in ("MK", "MV"):
+                    compare_units({key: got[key]}, {key: ref[key]}, w.dtype,
+                                  inputs=(K[f:f + B, h], V[f:f + B, h]) if B == 4 else None)
+                for key, X in (("HK", K), ("HV", V)):
+                    if B == 4 and w.dtype == "f32":
+                        mag = np.abs(X[f:f + B, h][:, S]).max(axis=0)[:, None, :]
+                        assert np.all(np.abs(got[key] - ref[key]) <= 2.0 ** -21 * mag + np.abs(ref[key]) * 2.0 ** -23)
+                    else:
+                        assert ulp_distance(got[key], ref[key], TYPES[w.dtype][1]).max(initial=0) <= 1, key
+                # routing losses, given the GPU's set
+                E = O.routing_errors_tokens(K[f:f + B, h], Q[f:f + B, h * G:(h + 1) * G], 0)   # E_S (S empty)
+                Ks = O.candidate_keys(K[f:f + B, h], O.SHARED, 0)
+                Qh = Q[f:f + B, h * G:(h + 1) * G].astype(np.float64)
+                contrib = sum(np.sum((Qh[l].reshape(-1, d) @ (Ks[l, S] - K[f + l, h, S]).T) ** 2) / (P * d)
+                              for l in range(B)) / (B * G)
+                want = np.array([E[O.SHARED], E[O.SHARED] - contrib])
+                relE = np.abs(got_err[b, h] - want) / np.abs(want)
+                assert relE.max() <= 5e-4, (b, h, got_err[b, h], want)
+                units[(b, h)] = ref
+            else:
+                units[(b, h)] = O.compress_unit_tokens(K[f:f + B, h], V[f:f + B, h], m, None, w.dtype)
+    log(f"  compress ok: every set has {n} tokens, rows within 1 ulp, losses within 5e-4")
+
+    tol = 1e-5 if w.dtype == "f32" else 1e-2
+    worst = 0.0
+    for qi, qs in enumerate(sharpened_queries(w, 0, K)):
+        for layer in range(w.n_layers):
+            out = cache.decode(layer, to_device(qs[layer], w.dtype)).float().cpu().numpy()[0]
+            bi, f, B = block_of(w, layer)
+            for h in range(H):
+                want = O.decode_unit_tokens(units[(bi, h)], int(modes[bi, h]), layer,
+                                            qs[layer][0, h * G:(h + 1) * G].astype(np.float64), 1.0 / math.sqrt(d), d, B)
+                for g in range(G):
+                    e = rel_l2(out[h * G + g], want[g])
+                    worst = max(worst, e)
+                    assert e <= tol, (name, qi, layer, h, g, e)
+    log(f"  decode ok; worst rel-L2 {worst:.3e} (tol {tol})")
