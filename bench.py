@@ -73,6 +73,19 @@ def bytes_per_token(mode, d, k, e, c, B=2):
     return 2 * d * c if mode == 0 else 2 * d * c + 2 * k * ((1 if B == 2 else 2) + c)
 
 
+def unit_read_bytes(w, mode, T, B):
+    """Algorithmic bytes one decode layer reads from one (block, KV head) unit of T
+    tokens.  With token-level residual sets a residual unit is read as its two
+    shared planes, the token mask (one bit per token), the running counts (one
+    word per 128 tokens, plus the total) and every high-frequency row of its n
+    tokens (B - 1 rows of K and of V each)."""
+    d, e, c = w.head_dim, w.elem_bytes, w.coef_bytes
+    if w.residual != 1 or mode != 1:
+        return T * bytes_per_token(mode, d, w.topk, e, c, B)
+    n = (T * w.res_ppm + 999999) // 1000000
+    return T * 2 * d * c + -(-T // 32) * 4 + (-(-T // 128) + 1) * 4 + n * 2 * (B - 1) * d * c
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for name in ("decode.hip", "decode_stream.hip", "fdkv_common.h", "fdkv_kernels.h"):
@@ -211,7 +224,13 @@ def main():
     modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
     cache = CompressedCache(dm, w.seq_lens, modes)
     for s in range(w.batch):
-        cache.compress(s, [Ks[s][l] for l in range(L)], [Vs[s][l] for l in range(L)])
+        scores = None
+        if w.residual == 1:                     # token-level sets need the probe's token scores
+            qp = [torch.from_numpy(gen.probe_queries(w, s, layers=[l])[0]).to(dev).to(tdt) for l in range(L)]
+            _, scores = probe(dm, w.seq_lens[s], [Ks[s][l] for l in range(L)], qp, w.n_probe)
+            del qp
+        cache.compress(s, [Ks[s][l] for l in range(L)], [Vs[s][l] for l in range(L)], token_scores=scores)
+        del scores
     torch.cuda.synchronize()
     log(f"[bench] compressed cache: {cache.total_bytes / 1e9:.3f} GB, mix {np.bincount(modes.ravel(), minlength=3).tolist()}")
 
@@ -220,7 +239,7 @@ def main():
     bytes_layer = []
     for layer in range(L):
         b, _, nb = block_of[layer]
-        bytes_layer.append(sum(w.seq_lens[s] * bytes_per_token(int(modes[s, b, h]), d, k, e, w.coef_bytes, nb)
+        bytes_layer.append(sum(unit_read_bytes(w, int(modes[s, b, h]), w.seq_lens[s], nb)
                                for s in range(w.batch) for h in range(H)))
     bytes_step = sum(bytes_layer)
 
@@ -306,6 +325,7 @@ def main():
         nbk = w.n_blocks
         ws = torch.empty(B.probe_workspace(dm, T, P), dtype=torch.uint8, device=dev)
         err = torch.empty((nbk, H, 2), dtype=torch.float32, device=dev)
+        tscores = torch.empty((nbk, H, T), dtype=torch.float32, device=dev) if w.residual == 1 else None
         _, all_exact = B.layout(dm, [T], np.full((1, nbk, H), 2, np.uint8))
         pcache_buf = torch.empty(all_exact, dtype=torch.uint8, device=dev)
         offs_dev = torch.empty((nbk, H), dtype=torch.int64, device=dev)
@@ -317,7 +337,7 @@ def main():
             a0, a1, c0, c1 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
             tw0 = time.perf_counter()
             a0.record()
-            B.probe(dm, T, kl, ql, P, err, ws)
+            B.probe(dm, T, kl, ql, P, err, ws, None, tscores)
             a1.record()
             eh = err.cpu().numpy()                      # sync point
             tr0 = time.perf_counter()
@@ -327,7 +347,7 @@ def main():
             modes_dev.copy_(torch.from_numpy(pmodes))
             offs_dev.copy_(torch.from_numpy(offs[0].astype(np.int64)))
             c0.record()
-            B.compress(dm, T, kl, vl, modes_dev, offs_dev, pcache_buf)
+            B.compress(dm, T, kl, vl, modes_dev, offs_dev, pcache_buf, None, tscores)
             c1.record()
             torch.cuda.synchronize()
             tw1 = time.perf_counter()
@@ -341,7 +361,7 @@ def main():
         units = nbk * H
         usz = [nb for nb in w.block_sizes for _ in range(H)]
         cmp_read = T * 2 * d * e * L * H                                             # K and V of every layer
-        cmp_write = sum(T * bytes_per_token(int(m), d, k, e, w.coef_bytes, nb) * (nb if m == 2 else 1)
+        cmp_write = sum(unit_read_bytes(w, int(m), T, nb) * (nb if m == 2 else 1)
                         for m, nb in zip(pmodes.ravel(), usz))                # exact heads copy all nb layers
         # upper 32x32 tiles of the deviation Gram matrices: 2 per pair, 8 per block of four
         mfma_flops = sum(T * (d // 32) * (d // 32 + 1) // 2 * (2 if nb == 2 else 8) * (32 * 32 * 2) for nb in usz)
@@ -362,7 +382,7 @@ def main():
         }
         log(f"[bench] prefill: probe {tp * 1e3:.2f} ms, route {trt * 1e3:.2f} ms, compress {tc * 1e3:.2f} ms "
             f"({prefill['compress_gbs']:.0f} GB/s), mix {prefill['probe_mode_mix']}")
-        del Qp, ws, pcache_buf
+        del Qp, ws, pcache_buf, tscores
 
     # ------------------------------------------------------------ generation: append + spans + tail, refresh
     generation = None
@@ -438,6 +458,9 @@ def main():
            "mode_mix": np.bincount(modes.ravel(), minlength=3).tolist(),
            "layer_order": args.order, "graph": graph is not None, "cache_gb": cache.total_bytes / 1e9,
            "bytes_per_step": bytes_step}
+    if w.residual == 1:
+        cfg["residual"] = "token set"
+        cfg["residual_fraction"] = w.res_ppm / 1e6
     res = {
         "metric": "compressed-KV decode attn tokens/s + achieved HBM GB/s vs 8 TB/s, 32k ctx",
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -480,13 +503,24 @@ def cpu_baseline(w, modes):
     for (b, h) in pick:
         K, V, _ = gen.block_segment(w, 0, b, h)
         f, nb = w.blocks[b]
-        unit = O.compress_unit(K, V, int(modes[b, h]), w.topk, w.dtype)
+        m = int(modes[b, h])
+        if w.residual == 1:
+            tokens = None
+            if m == 1:                  # the set the probe picks (selection is prefill work, not timed)
+                QB = gen.probe_queries(w, 0, layers=list(range(f, f + nb)))[:, h * G:(h + 1) * G]
+                sc, _ = O.token_scores(K, QB)
+                tokens = O.residual_tokens(sc, O.n_residual_tokens(K.shape[1], w.res_ppm))
+            unit = O.compress_unit_tokens(K, V, m, tokens, w.dtype)
+            dec = O.decode_unit_tokens
+        else:
+            unit = O.compress_unit(K, V, m, w.topk, w.dtype)
+            dec = O.decode_unit
         for s in range(n_steps):
             q = gen.decode_queries(w, s)
             for layer in range(f, f + nb):
                 qq = q[layer][0, h * G:(h + 1) * G].astype(np.float64)
                 t0 = time.perf_counter()
-                O.decode_unit(unit, int(modes[b, h]), layer, qq, 1.0 / math.sqrt(d), d, nb)
+                dec(unit, m, layer, qq, 1.0 / math.sqrt(d), d, nb)
                 elapsed += time.perf_counter() - t0
                 n_calls += 1
     per_unit_layer = elapsed / n_calls
