@@ -365,6 +365,9 @@ def main():
                         for m, nb in zip(pmodes.ravel(), usz))                # exact heads copy all nb layers
         # upper 32x32 tiles of the deviation Gram matrices: 2 per pair, 8 per block of four
         mfma_flops = sum(T * (d // 32) * (d // 32 + 1) // 2 * (2 if nb == 2 else 8) * (32 * 32 * 2) for nb in usz)
+        if w.residual == 1:
+            # token scores: every probe row of the block's layers against every token's deviation
+            mfma_flops = sum(2 * nb * (Hq // H) * P * d * T for nb in usz)
         G = Hq // H
         eq2_flops = T * L * H * G * P * d * 2 * 2 * 2                                # literal Eq. 2, 2 modes
         prefill = {
