@@ -458,11 +458,22 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       }
       __syncthreads();  // the whole workgroup shares one unit, hence one flavour
     }
-    for (int t = 0; t < ntiles; t += NB) {
+    if constexpr (RES == 0) {
+      // dense heads: the wave's tiles unrolled at compile time, so every wait
+      // is for exactly the tile computed next
+      constexpr int NT = CW / TILE;
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        load(t + j + PD, buf[(j + PD) % NB]);
-        if (j == 0 || t + j < ntiles) compute(t + j, buf[j]);
+      for (int t = 0; t < NT; ++t) {
+        if (t + PD < NT) load(t + PD, buf[(t + PD) % NB]);
+        if (t < ntiles) compute(t, buf[t % NB]);
+      }
+    } else {
+      for (int t = 0; t < ntiles; t += NB) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          load(t + j + PD, buf[(j + PD) % NB]);
+          if (j == 0 || t + j < ntiles) compute(t + j, buf[j]);
+        }
       }
     }
 
