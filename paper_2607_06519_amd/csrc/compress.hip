@@ -5,10 +5,10 @@
 //    shared/residual heads write the block mean M (the per-layer image of
 //    the low-frequency DCT coefficient, the same for every layer of the
 //    block) for K and V; exact heads copy the input rows.
-//  * residual_select (B = 2) - one lane per token: the top-k channels of
-//    |fl32(x[2b] - x[2b+1])| by a register comparator network (topk_net.h),
-//    written as ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at
-//    those channels.
+//  * residual_select_reg (B = 2, k <= 16) and residual_select (B = 2, any
+//    k) - one lane per token: the top-k channels of |fl32(x[2b] - x[2b+1])|
+//    by a register comparator network (topk_net.h), written as ascending
+//    uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those channels.
 //  * residual_select4 (B = 4) - one lane per token: the top-k of the 3d
 //    high-frequency coefficients Z_j[c] (j = 1..3) of the DCT-II(4), ranked
 //    by |Z| as the fp32 butterfly gives them, written as ascending uint16
@@ -273,6 +273,152 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   }
 }
 
+// ---------------------------------------------------------------- residual select, k <= 16
+// One lane per token with every key in registers: the lane loads its own
+// rows of both layers (16-byte pieces), forms the fp32 differences, keeps
+// their magnitudes as keys and, when a cache is written, puts the rounded
+// half differences into an LDS table (16-byte pieces rotated by the lane).
+// The threshold comes from the running sorted list of kth_largest_keep,
+// which leaves the keys for the selection mask, so nothing goes through LDS
+// on the way to the threshold and a workgroup needs only the value table:
+// two waves fit on a SIMD instead of one.
+template <int D, bool BF16>
+__device__ __forceinline__ int vtab_slot(int lane, int piece) {  // 16-byte slot of a value piece
+  constexpr int NPV = D * (BF16 ? 2 : 4) / 16;
+  return lane * NPV + (piece ^ (lane & (NPV - 1)));
+}
+
+template <int D, bool BF16, int RS>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void residual_select_reg_kernel(
+    SelectParams P) {
+  constexpr int E = BF16 ? 2 : 4;
+  constexpr int NPC = D * E / 16;       // 16-byte pieces per input row
+  constexpr int CPP = 16 / E;           // channels per piece
+  constexpr int NW = D / 32;
+  // value table: per lane D values of E bytes (bf16 bits, an E4M3 code in
+  // the low byte, or fp32), piece p of the row holding channels p*CPP ...
+  __shared__ uint4 vtab[64 * NPC];
+
+  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
+  const int first = P.bl.first[bi];
+  const int unit = P.bl.block[bi] * P.hkv + head;
+  const int tensor = blockIdx.z;        // 0: K, 1: V
+  if (P.modes && P.modes[unit] != kResidual) return;
+  const int T = P.seq_len, k = P.topk;
+  const int lane = threadIdx.x;
+  const int t = blockIdx.x * 64 + lane;
+  const uint64_t row_bytes = (uint64_t)D * E;
+  const void* const* src = tensor ? P.v : P.k;
+  const uint64_t row = (uint64_t)head * T + (uint64_t)min(t, T - 1);
+  const uint4* xa = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first]) + row * row_bytes);
+  const uint4* xb = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first + 1]) + row * row_bytes);
+  const bool values = P.modes != nullptr;
+  const bool c8 = BF16 && P.coef8;
+
+  uint32_t key[D];
+#pragma unroll
+  for (int p = 0; p < NPC; ++p) {
+    const uint4 a = xa[p], b = xb[p];
+    const uint32_t pa[4] = {a.x, a.y, a.z, a.w}, pb[4] = {b.x, b.y, b.z, b.w};
+    float d[CPP];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if constexpr (BF16) {
+        d[2 * w] = bf16_lo(pa[w]) - bf16_lo(pb[w]);
+        d[2 * w + 1] = bf16_hi(pa[w]) - bf16_hi(pb[w]);
+      } else {
+        d[w] = as_f32(pa[w]) - as_f32(pb[w]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < CPP; ++i) key[p * CPP + i] = as_u32(d[i]) & 0x7FFFFFFFu;
+    if (values) {
+      uint32_t vw[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (BF16) {
+          const float h0 = d[2 * w] * 0.5f, h1 = d[2 * w + 1] * 0.5f;
+          vw[w] = c8 ? ((uint32_t)f32_to_e4m3(h0) | ((uint32_t)f32_to_e4m3(h1) << 16)) : pack_bf16x2(h0, h1);
+        } else {
+          vw[w] = as_u32(d[w] * 0.5f);
+        }
+      }
+      vtab[vtab_slot<D, BF16>(lane, p)] = make_uint4(vw[0], vw[1], vw[2], vw[3]);
+    }
+  }
+  const uint32_t tau = net::kth_largest_keep<D, RS>(key, k);
+  uint32_t mask[NW];
+  net::select_mask<D>(key, tau, k, mask);
+  if (t >= T) return;
+
+  // ascending channels, packed stores
+  const int CE = c8 ? 1 : E;            // bytes per stored value
+  uint8_t* out_idx;
+  uint8_t* out_val = nullptr;
+  if (values) {
+    uint8_t* seg = P.cache + P.seg_off[unit];
+    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 2);
+    out_idx = seg + (tensor ? L.iv : L.ik) + (uint64_t)t * k;
+    out_val = seg + (tensor ? L.vv : L.vk) + (uint64_t)t * k * CE;
+  } else {
+    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k) + (uint64_t)t * k;
+  }
+  const uint8_t* vt = reinterpret_cast<const uint8_t*>(vtab);
+  auto value_bits = [&](int c) -> uint32_t {  // stored value of channel c
+    const uint8_t* pc = vt + vtab_slot<D, BF16>(lane, c / CPP) * 16 + (c % CPP) * E;
+    if constexpr (BF16) return *reinterpret_cast<const uint16_t*>(pc) & (c8 ? 0xFFu : 0xFFFFu);
+    else return *reinterpret_cast<const uint32_t*>(pc);
+  };
+  if ((k & 3) == 0) {
+    uint32_t iw[RS / 4];
+    uint32_t vw[RS * 4 / 4];
+#pragma unroll
+    for (int s = 0; s < RS; ++s) {
+      if (s < k) {
+        const int c = net::pop_lowest<D>(mask);
+        if (s % 4 == 0) iw[s / 4] = 0;
+        iw[s / 4] |= (uint32_t)c << (8 * (s % 4));
+        if (values) {
+          const uint32_t v = value_bits(c);
+          if (CE == 1) {
+            if (s % 4 == 0) vw[s / 4] = 0;
+            vw[s / 4] |= v << (8 * (s % 4));
+          } else if (CE == 2) {
+            if (s % 2 == 0) vw[s / 2] = 0;
+            vw[s / 2] |= v << (16 * (s % 2));
+          } else {
+            vw[s] = v;
+          }
+        }
+      }
+    }
+    uint32_t* oi = reinterpret_cast<uint32_t*>(out_idx);
+#pragma unroll
+    for (int w = 0; w < RS / 4; ++w)
+      if (4 * w < k) oi[w] = iw[w];
+    if (values) {
+      uint32_t* ov = reinterpret_cast<uint32_t*>(out_val);
+#pragma unroll
+      for (int w = 0; w < RS; ++w)
+        if (w < k * CE / 4) ov[w] = vw[w];
+    }
+  } else {
+    for (int s = 0; s < k; ++s) {
+      const int c = net::pop_lowest<D>(mask);
+      out_idx[s] = (uint8_t)c;
+      if (values) {
+        const uint32_t v = value_bits(c);
+        if (CE == 1)
+          out_val[s] = (uint8_t)v;
+        else if (CE == 2)
+          reinterpret_cast<uint16_t*>(out_val)[s] = (uint16_t)v;
+        else
+          reinterpret_cast<uint32_t*>(out_val)[s] = v;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- residual select, blocks of four
 // The coefficients of the token's block come 16 channels at a time: the
 // wave loads those channels of its 64 tokens from the four layers
@@ -473,10 +619,17 @@ static hipError_t launch_select_t(const SelectParams& P, int tensors, hipStream_
   return hipGetLastError();
 }
 
+template <int D, bool BF16, int RS>
+static hipError_t launch_select_reg_t(const SelectParams& P, int tensors, hipStream_t s) {
+  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
+  hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS>), grid, dim3(64), 0, s, P);
+  return hipGetLastError();
+}
+
 template <int D, bool BF16>
 static hipError_t launch_select_d(const SelectParams& P, int tensors, hipStream_t s) {
-  if (P.topk <= 8) return launch_select_t<D, BF16, 8>(P, tensors, s);
-  if (P.topk <= 16) return launch_select_t<D, BF16, 16>(P, tensors, s);
+  if (P.topk <= 8) return launch_select_reg_t<D, BF16, 8>(P, tensors, s);
+  if (P.topk <= 16) return launch_select_reg_t<D, BF16, 16>(P, tensors, s);
   return launch_select_t<D, BF16, D>(P, tensors, s);
 }
 

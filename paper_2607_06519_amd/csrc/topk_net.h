@@ -93,6 +93,36 @@ FDKV_NET_HD uint32_t kth_largest(uint32_t* a, int k) {
   return tau;
 }
 
+// k-th largest of key[0..D) with multiplicity, 1 <= k <= RS, leaving the keys
+// as they are (the selection mask reads them again).  A list R of the RS
+// largest keys seen so far, sorted descending, absorbs one sorted group of RS
+// keys at a time: the elementwise max of R against the group reversed is
+// bitonic and holds the RS largest of both, and the half-cleaner cascade
+// sorts it again.  The first group becomes R as it is.
+template <int D, int RS>
+FDKV_NET_HD uint32_t kth_largest_keep(const uint32_t* key, int k) {
+  static_assert((RS & (RS - 1)) == 0 && RS <= D && D % RS == 0, "list size");
+  uint32_t R[RS];
+#pragma unroll
+  for (int i = 0; i < RS; ++i) R[i] = key[i];
+  sort_desc<RS>(R);
+#pragma unroll
+  for (int g = 1; g < D / RS; ++g) {
+    uint32_t x[RS];
+#pragma unroll
+    for (int i = 0; i < RS; ++i) x[i] = key[g * RS + i];
+    sort_desc<RS>(x);
+#pragma unroll
+    for (int i = 0; i < RS; ++i) R[i] = R[i] > x[RS - 1 - i] ? R[i] : x[RS - 1 - i];
+    merge_bitonic_desc<RS>(R);
+  }
+  uint32_t tau = R[0];
+#pragma unroll
+  for (int i = 1; i < RS; ++i)
+    if (i == k - 1) tau = R[i];
+  return tau;
+}
+
 // Streaming form (blocks of four, 3D keys per token): a list R of the RS
 // largest keys seen so far, sorted descending and starting at zero, absorbs
 // a group of 16 keys (destroyed).  The elementwise max of R's last 16

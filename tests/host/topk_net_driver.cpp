@@ -6,8 +6,10 @@
 #include <vector>
 #include "../../paper_2607_06519_amd/csrc/topk_net.h"
 
+// keep = 0: kth_largest (destroys its copy of the keys); keep = 1:
+// kth_largest_keep (leaves the keys, list size GS)
 template <int D, int GS>
-static void run_rows(int k, int n) {
+static void run_rows(int k, int n, int keep) {
   std::vector<uint32_t> key(D), work(D);
   for (int r = 0; r < n; ++r) {
     for (int c = 0; c < D; ++c) {
@@ -16,7 +18,8 @@ static void run_rows(int k, int n) {
       key[c] = v;
       work[c] = v;
     }
-    const uint32_t tau = fdkv::net::kth_largest<D, GS>(work.data(), k);
+    const uint32_t tau = keep ? fdkv::net::kth_largest_keep<D, GS>(key.data(), k)
+                              : fdkv::net::kth_largest<D, GS>(work.data(), k);
     uint32_t mask[D / 32];
     fdkv::net::select_mask<D>(key.data(), tau, k, mask);
     for (int s = 0; s < k; ++s) printf("%d ", fdkv::net::pop_lowest<D>(mask));
@@ -25,14 +28,14 @@ static void run_rows(int k, int n) {
 }
 
 int main() {
-  int D, GS, k, n;
-  if (scanf("%d %d %d %d", &D, &GS, &k, &n) != 4) return 2;
-  if (D == 64 && GS == 8) run_rows<64, 8>(k, n);
-  else if (D == 64 && GS == 16) run_rows<64, 16>(k, n);
-  else if (D == 64 && GS == 64) run_rows<64, 64>(k, n);
-  else if (D == 128 && GS == 8) run_rows<128, 8>(k, n);
-  else if (D == 128 && GS == 16) run_rows<128, 16>(k, n);
-  else if (D == 128 && GS == 128) run_rows<128, 128>(k, n);
+  int D, GS, k, n, keep;
+  if (scanf("%d %d %d %d %d", &D, &GS, &k, &n, &keep) != 5) return 2;
+  if (D == 64 && GS == 8) run_rows<64, 8>(k, n, keep);
+  else if (D == 64 && GS == 16) run_rows<64, 16>(k, n, keep);
+  else if (D == 64 && GS == 64) run_rows<64, 64>(k, n, keep);
+  else if (D == 128 && GS == 8) run_rows<128, 8>(k, n, keep);
+  else if (D == 128 && GS == 16) run_rows<128, 16>(k, n, keep);
+  else if (D == 128 && GS == 128) run_rows<128, 128>(k, n, keep);
   else return 3;
   return 0;
 }

@@ -27,10 +27,13 @@ def _expected(keys, k):
     return np.sort(order[:, :k], axis=-1)
 
 
-@pytest.mark.parametrize("D,GS,k", [(64, 8, 8), (64, 8, 3), (64, 16, 16), (64, 16, 9), (64, 64, 64),
-                                    (64, 64, 40), (128, 16, 16), (128, 16, 11), (128, 8, 1),
-                                    (128, 128, 128), (128, 128, 77)])
-def test_network_matches_sort(driver, D, GS, k):
+@pytest.mark.parametrize("D,GS,k,keep", [(64, 8, 8, 0), (64, 8, 3, 0), (64, 16, 16, 0), (64, 16, 9, 0),
+                                         (64, 64, 64, 0), (64, 64, 40, 0), (128, 16, 16, 0), (128, 16, 11, 0),
+                                         (128, 8, 1, 0), (128, 128, 128, 0), (128, 128, 77, 0),
+                                         (64, 8, 8, 1), (64, 8, 1, 1), (64, 16, 16, 1), (64, 16, 9, 1),
+                                         (128, 8, 8, 1), (128, 8, 5, 1), (128, 16, 16, 1), (128, 16, 13, 1)])
+def test_network_matches_sort(driver, D, GS, k, keep):
+    """keep = 1: the threshold that leaves the keys in place (a running sorted list of GS keys)."""
     rng = np.random.default_rng(D * 1000 + GS * 10 + k)
     rows = []
     # float-like keys: |a - b| bit patterns of bf16-valued differences
@@ -42,7 +45,7 @@ def test_network_matches_sort(driver, D, GS, k):
     rows.append(np.zeros((3, D), np.uint32))
     rows.append(np.full((3, D), 0x7F7FFFFF, np.uint32))
     keys = np.concatenate(rows)
-    inp = f"{D} {GS} {k} {keys.shape[0]}\n" + "\n".join(" ".join(map(str, r)) for r in keys.tolist())
+    inp = f"{D} {GS} {k} {keys.shape[0]} {keep}\n" + "\n".join(" ".join(map(str, r)) for r in keys.tolist())
     out = subprocess.run([driver], input=inp, capture_output=True, text=True, check=True).stdout
     got = np.array([[int(x) for x in line.split()] for line in out.strip().splitlines()])
     np.testing.assert_array_equal(got, _expected(keys, k))
