@@ -500,8 +500,8 @@ def cpu_baseline(w, modes):
     pick = []
     for m in (0, 1, 2):
         cand = [u for u in flat if modes[u] == m]
-        pick += [cand[i] for i in rng.choice(len(cand), size=min(2, len(cand)), replace=False)]
-    n_steps = 3
+        pick += [cand[i] for i in rng.choice(len(cand), size=min(4, len(cand)), replace=False)]
+    n_steps = 14                        # about 10 s of oracle work on the 8B shape
     elapsed, n_calls = 0.0, 0
     for (b, h) in pick:
         K, V, _ = gen.block_segment(w, 0, b, h)

@@ -104,12 +104,14 @@ template <int D, int G>
 struct SS {
   static constexpr int NP = D / 8;                 // lanes per row, one 16-byte piece each
   static constexpr int RPL = 64 / NP;              // rows per load instruction
-  static constexpr int TILE = 16;
+  // eight query heads at d = 128: 8-row tiles, so the per-row logits and
+  // tile buffers leave room for two waves per SIMD
+  static constexpr int TILE = (G >= 8 && D == 128) ? 8 : 16;
   static constexpr int NL = TILE / RPL;            // rows of a tile per lane
   static constexpr int CW = kDecodeChunk;          // tokens per wave
   static constexpr int W = kDecodeWaves;
   static constexpr int RS = D + 4;
-  static constexpr int PD0 = G >= 8 ? 1 : 2;       // tiles in flight behind the current one (dense heads)
+  static constexpr int PD0 = 2;                    // tiles in flight behind the current one (dense heads)
   static constexpr int SP = W * RPL * G * D;       // residual V accumulators (floats)
   static constexpr int MG = W * G * (D + 2);       // per-wave (acc, m, l) for the workgroup merge
   static constexpr int LDSF = SP > MG ? SP : MG;
