@@ -80,7 +80,12 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const bool tail = part == P.tail_part;
   const int T = P.part[part].lens[seq];
   const int wg_tok0 = wgc * kDecodeWgTokens;
-  if (wg_tok0 >= T) return;  // uniform over the workgroup
+  if (wg_tok0 >= T) {  // uniform over the workgroup
+    // an empty record (m = -inf, l = 0, acc = 0): the merge reads every slot
+    float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
+    for (int i = threadIdx.x; i < G * S::RS; i += 256) rec[i] = i % S::RS == D ? -INFINITY : 0.f;
+    return;
+  }
 
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   const bool q4 = P.bsize == 4;

@@ -166,7 +166,13 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   }
   const int mode = (int)(mode_word & 0xFFu);
   const int wg_tok0 = wgc * kDecodeWgTokens;
-  if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) return;
+  if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) {
+    // no tokens here (or a unit left alone): an empty record, m = -inf,
+    // l = 0, acc = 0, since the merge reads every slot
+    float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
+    for (int i = threadIdx.x; i < G * S::RS; i += 256) rec[i] = i % S::RS == D ? -INFINITY : 0.f;
+    return;
+  }
 
   const int k = P.topk;
   // residual heads hold either per-token channel entries or a token-level set
@@ -708,7 +714,8 @@ __device__ __forceinline__ float wave_sum_dpp(float x) {
 }
 
 // Log-sum-exp merge of the workgroup records of one (sequence, query head),
-// over every part of the call (compressed spans, then the exact tail):
+// over every slot of the call (compressed spans, then the exact tail; a slot
+// with no tokens holds an empty record, so no lengths are read first):
 //   M = max_i m_i,  l = sum_i l_i 2^(m_i - M),  o = sum_i acc_i 2^(m_i - M) / l.
 // One workgroup of four waves per query head, records taken in blocks of 64.
 // Within a block every wave loads the (m, l) pairs (record i in lane i) and
@@ -732,12 +739,11 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
   float M = -INFINITY, lsum = 0.f, o[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) o[c] = 0.f;
-  int total = 0;
-  for (int part = 0; part < P.n_parts; ++part) {
-    const int Tp = P.part[part].lens[seq];
-    const int nch = min((Tp + kDecodeWgTokens - 1) / kDecodeWgTokens, P.part[part].chunks);
-    const float* base = head_base + (uint64_t)P.part[part].base * stride;
-    total += nch;
+  // every slot of every part holds a record (empty ones have m = -inf), so
+  // the slots are merged as one range without reading the lengths first
+  {
+    const int nch = P.n_chunks_total;
+    const float* base = head_base;
   for (int b0 = 0; b0 < nch; b0 += 64) {
     const int last = nch - 1;  // loads past the end repeat the last record and get weight 0
     const int il = b0 + lane;
@@ -753,7 +759,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
     const float Mb = wave_max_dpp(mi);
     const float Mn = fmaxf(M, Mb);
     const float fo = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
-    const float w = il < nch ? __builtin_amdgcn_exp2f(mi - Mn) : 0.f;
+    const float w = (il < nch && mi != -INFINITY) ? __builtin_amdgcn_exp2f(mi - Mn) : 0.f;
     lsum = lsum * fo + wave_sum_dpp(w * ml.y);
 #pragma unroll
     for (int c = 0; c < CPL; ++c) o[c] *= fo;
@@ -774,7 +780,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams P) {
     for (int c = 0; c < CPL; ++c) {
       const int ch = lane * CPL + c;
       const float s = (part[0][ch] + part[1][ch]) + (part[2][ch] + part[3][ch]);
-      const float res = total > 0 ? s / lsum : 0.f;
+      const float res = lsum > 0.f ? s / lsum : 0.f;
       const uint64_t oi = ((uint64_t)seq * P.hq + qh) * D + ch;
       if constexpr (BF16)
         reinterpret_cast<uint16_t*>(P.out)[oi] = (uint16_t)f32_to_bf16_bits(res);
