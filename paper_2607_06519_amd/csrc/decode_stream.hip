@@ -2,8 +2,9 @@
 // reconstruction of Eq. 3 fused into the attention).
 //
 // One workgroup = 4 waves = 512 tokens of one (sequence, KV head); a wave
-// walks its 128 tokens in 16-row tiles with an online softmax, keeping the
-// next tiles' loads in flight while it computes the current one.
+// walks its 128 tokens in 8-row tiles (d = 128; 16 rows at d = 64) with an
+// online softmax, keeping the next tiles' loads in flight while it computes
+// the current one.
 //
 // One lane layout serves the K pass, the softmax and the V pass: NP = d/8
 // lanes per token row, each holding one 16-byte piece (8 channels), so one
@@ -104,9 +105,11 @@ template <int D, int G>
 struct SS {
   static constexpr int NP = D / 8;                 // lanes per row, one 16-byte piece each
   static constexpr int RPL = 64 / NP;              // rows per load instruction
-  // eight query heads at d = 128: 8-row tiles, so the per-row logits and
-  // tile buffers leave room for two waves per SIMD
-  static constexpr int TILE = (G >= 8 && D == 128) ? 8 : 16;
+  // d = 128: 8-row tiles (two rows per lane).  Each wait is for 4 KB of K
+  // and V instead of 8 KB, and with eight query heads the per-row logits and
+  // tile buffers leave room for two waves per SIMD; d = 64 keeps 16 rows
+  // (two rows per lane there too)
+  static constexpr int TILE = D == 128 ? 8 : 16;
   static constexpr int NL = TILE / RPL;            // rows of a tile per lane
   static constexpr int CW = kDecodeChunk;          // tokens per wave
   static constexpr int W = kDecodeWaves;
