@@ -288,7 +288,18 @@ __device__ __forceinline__ int vtab_slot(int lane, int piece) {  // 16-byte slot
   return lane * NPV + (piece ^ (lane & (NPV - 1)));
 }
 
-template <int D, bool BF16, int RS>
+// Two fp32 values as a bf16 pair, round to nearest even (the gfx950
+// conversion instruction: one per pair; finite inputs round as f32_to_bf16_bits).
+__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const f32x2v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+}
+
+// C8: residual values stored as FP8 E4M3 (a compile-time flavour, so the
+// bf16 path carries none of the encoder)
+template <int D, bool BF16, int RS, bool C8>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void residual_select_reg_kernel(
     SelectParams P) {
   constexpr int E = BF16 ? 2 : 4;
@@ -313,7 +324,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void re
   const uint4* xa = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first]) + row * row_bytes);
   const uint4* xb = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first + 1]) + row * row_bytes);
   const bool values = P.modes != nullptr;
-  const bool c8 = BF16 && P.coef8;
+  constexpr bool c8 = BF16 && C8;
 
   uint32_t key[D];
 #pragma unroll
@@ -338,7 +349,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void re
       for (int w = 0; w < 4; ++w) {
         if constexpr (BF16) {
           const float h0 = d[2 * w] * 0.5f, h1 = d[2 * w + 1] * 0.5f;
-          vw[w] = c8 ? ((uint32_t)f32_to_e4m3(h0) | ((uint32_t)f32_to_e4m3(h1) << 16)) : pack_bf16x2(h0, h1);
+          if constexpr (c8)
+            vw[w] = (uint32_t)f32_to_e4m3(h0) | ((uint32_t)f32_to_e4m3(h1) << 16);
+          else
+            vw[w] = cvt_bf16x2(h0, h1);
         } else {
           vw[w] = as_u32(d[w] * 0.5f);
         }
@@ -352,7 +366,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void re
   if (t >= T) return;
 
   // ascending channels, packed stores
-  const int CE = c8 ? 1 : E;            // bytes per stored value
+  constexpr int CE = c8 ? 1 : E;        // bytes per stored value
   uint8_t* out_idx;
   uint8_t* out_val = nullptr;
   if (values) {
@@ -622,7 +636,10 @@ static hipError_t launch_select_t(const SelectParams& P, int tensors, hipStream_
 template <int D, bool BF16, int RS>
 static hipError_t launch_select_reg_t(const SelectParams& P, int tensors, hipStream_t s) {
   const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
-  hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS>), grid, dim3(64), 0, s, P);
+  if (BF16 && P.coef8)
+    hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS, true>), grid, dim3(64), 0, s, P);
+  else
+    hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS, false>), grid, dim3(64), 0, s, P);
   return hipGetLastError();
 }
 
