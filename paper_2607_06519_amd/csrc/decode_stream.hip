@@ -9,7 +9,7 @@
 // One lane layout serves the K pass, the softmax and the V pass: NP = d/8
 // lanes per token row, each holding one 16-byte piece (8 channels), so one
 // load instruction covers RPL = 64/NP consecutive rows and a lane owns
-// NL = 16/RPL rows of a tile.  The NP lanes of a row form a DPP row (d = 128)
+// NL = TILE/RPL rows of a tile (two).  The NP lanes of a row form a DPP row (d = 128)
 // or half row (d = 64).
 //  K   - bf16 dot2 of the lane's piece with its piece of every query (held in
 //        registers); residual heads add the lane's residual entry
