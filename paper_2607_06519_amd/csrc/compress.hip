@@ -478,26 +478,39 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
 #pragma unroll
   for (int n = 0; n < 4; ++n) x[n] = static_cast<const uint8_t*>(src[first + n]) + head_off;
 
-  auto stage = [&](int ch) {  // Z of channels 16 ch .. 16 ch + 15 into LDS
-    __syncthreads();
+  // The workgroup is one wave, so the staging needs only wave-scope ordering
+  // (LDS operations of a wave complete in order): no workgroup barrier, which
+  // would also wait for the next chunk's loads already in flight.
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+  uint4 vin[PPC][4];  // the next chunk's input pieces, loaded ahead of its use
+  auto load = [&](int ch) {
 #pragma unroll
     for (int i = 0; i < PPC; ++i) {
       const int r = lane / PPC + (64 / PPC) * i, pc = lane % PPC;
       const int t = min(tok0 + r, T - 1);
       const uint64_t off = (uint64_t)t * row_bytes + (uint64_t)(ch * PPC + pc) * 16;
-      uint4 v[4];
 #pragma unroll
-      for (int n = 0; n < 4; ++n) v[n] = *reinterpret_cast<const uint4*>(x[n] + off);
+      for (int n = 0; n < 4; ++n) vin[i][n] = *reinterpret_cast<const uint4*>(x[n] + off);
+    }
+  };
+  auto stage = [&]() {  // Z of the loaded chunk's 16 channels into LDS
+    wave_sync();        // the previous chunk's rows are read
+#pragma unroll
+    for (int i = 0; i < PPC; ++i) {
+      const int r = lane / PPC + (64 / PPC) * i, pc = lane % PPC;
       float z[3 * CPP];
 #pragma unroll
       for (int c = 0; c < CPP; ++c)
-        dct4_high(chan<BF16>(v[0], c), chan<BF16>(v[1], c), chan<BF16>(v[2], c), chan<BF16>(v[3], c), z[3 * c],
-                  z[3 * c + 1], z[3 * c + 2]);
+        dct4_high(chan<BF16>(vin[i][0], c), chan<BF16>(vin[i][1], c), chan<BF16>(vin[i][2], c),
+                  chan<BF16>(vin[i][3], c), z[3 * c], z[3 * c + 1], z[3 * c + 2]);
 #pragma unroll
       for (int q = 0; q < 3 * CPP / 4; ++q)
         zs[z4_slot(r, pc * (3 * CPP / 4) + q)] = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
     }
-    __syncthreads();
+    wave_sync();
   };
   auto row = [&](float (&zr)[48]) {
 #pragma unroll
@@ -514,8 +527,10 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
   uint32_t R[RS];
 #pragma unroll
   for (int i = 0; i < RS; ++i) R[i] = 0u;
+  load(0);
   for (int ch = 0; ch < NC; ++ch) {
-    stage(ch);
+    stage();
+    load(ch + 1 < NC ? ch + 1 : 0);  // the last one starts pass 2
     float zr[48];
     row(zr);
 #pragma unroll
@@ -533,7 +548,8 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
   uint2* my = slot + lane * (RS + 1);
   int s = 0, eq = 0;
   for (int ch = 0; ch < NC; ++ch) {
-    stage(ch);
+    stage();
+    if (ch + 1 < NC) load(ch + 1);
     float zr[48];
     row(zr);
 #pragma unroll
