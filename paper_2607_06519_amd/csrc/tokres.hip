@@ -145,24 +145,38 @@ __global__ __launch_bounds__(256) void token_score_kernel(TokenParams P) {
     for (int ly = 0; ly < nlay; ++ly) {
       const int layer = first + (NB == 2 ? ly : pass);
       const auto qr = make_rsrc(static_cast<const uint8_t*>(P.qp[layer]) + (uint64_t)head * qspan, qspan);
+      // 32 probe rows per round; the next round's rows are loaded into
+      // registers while this round's MFMAs run
+      constexpr int PER = (32 * NPQ + 255) / 256;  // 8-channel pieces per thread and round
+      float qn[PER][8];
+      auto fetch = [&](int r0) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          const int i = tid + 256 * j, row = i / NPQ, pc = i % NPQ;
+          load8<BF16>(qr, (uint32_t)((r0 + row) * RB + pc * 8 * E), i < 32 * NPQ && r0 + row < GP, qn[j]);
+        }
+      };
+      fetch(0);
       for (int r0 = 0; r0 < GP; r0 += 32) {
-        __syncthreads();
-        for (int i = tid; i < 32 * NPQ; i += 256) {
-          const int row = i / NPQ, pc = i % NPQ;
-          float q[8];
-          load8<BF16>(qr, (uint32_t)((r0 + row) * RB + pc * 8 * E), r0 + row < GP, q);
+        __syncthreads();  // the previous round's rows are read
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          const int i = tid + 256 * j, row = i / NPQ, pc = i % NPQ;
+          if (i >= 32 * NPQ) continue;
+          const float* q = qn[j];
           uint32_t hi[4], lo[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            hi[j] = pack_bf16x2(q[2 * j], q[2 * j + 1]);
+          for (int jj = 0; jj < 4; ++jj) {
+            hi[jj] = pack_bf16x2(q[2 * jj], q[2 * jj + 1]);
             if constexpr (NH == 2)
-              lo[j] = pack_bf16x2(q[2 * j] - bf16_lo(hi[j]), q[2 * j + 1] - bf16_hi(hi[j]));
+              lo[jj] = pack_bf16x2(q[2 * jj] - bf16_lo(hi[jj]), q[2 * jj + 1] - bf16_hi(hi[jj]));
           }
           *reinterpret_cast<uint4*>(&qs[0][row * LDR + pc * 8]) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
           if constexpr (NH == 2)
             *reinterpret_cast<uint4*>(&qs[NH - 1][row * LDR + pc * 8]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
         }
         __syncthreads();
+        if (r0 + 32 < GP) fetch(r0 + 32);
         f32x16_t acc[2];
 #pragma unroll
         for (int st = 0; st < 2; ++st)
