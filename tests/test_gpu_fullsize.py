@@ -96,7 +96,7 @@ def _samples_by_mode(modes_b, per_mode=1, seqs=None):
     return out
 
 
-@pytest.mark.parametrize("name,per_mode", [("llama8b", 2), ("long70b", 1), ("llama8b_quads", 2)])
+@pytest.mark.parametrize("name,per_mode", [("llama8b", 2), ("long70b", 1), ("llama8b_quads", 2), ("llama8b_e4m3", 2)])
 def test_fullsize_single_sequence(torch_mod, name, per_mode):
     if name == "llama8b_quads":    # one block of four layers at the full 8B shape
         w = scaled(WORKLOADS["llama8b_mixed"], n_layers=4, schedule=2)
