@@ -144,3 +144,69 @@ def test_fullsize_probe(torch_mod, nl, sched):
         rel = np.abs(got[h] - ref[:2]) / ref[:2]
         log(f"  head {h}: E_S {got[h, 0]:.6g} vs {ref[0]:.6g}, E_R {got[h, 1]:.6g} vs {ref[1]:.6g}, rel {rel.max():.2e}")
         assert rel.max() <= 1e-4
+
+
+def test_fullsize_token_residual(torch_mod):
+    """Token-level residual sets at the 8B shape (T = 32768, 8 KV heads, 32 query
+    heads, P = 256, r = 5%): probe scores, sets, stored rows and decode of sampled
+    units against the oracle, with the rules of the small token-level cases."""
+    torch = torch_mod
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, probe, to_device
+    from test_gpu_tokres import unpack_tok_unit
+    from gpu_cases import TYPES, ulp_distance
+    w = scaled(WORKLOADS["llama8b_tokres"], n_layers=2)
+    T, G, d, H, ppm = w.seq_lens[0], w.group, w.head_dim, w.n_kv_heads, w.res_ppm
+    n = O.n_residual_tokens(T, ppm)
+    log(f"[case] full-size token residual: T={T} Hkv={H} Hq={w.n_q_heads} P={w.n_probe} r={ppm / 1e6} (n={n})")
+    K, V = gen.layer_cache(w, 0, threads=16)
+    Q = gen.probe_queries(w, 0)
+    Kd, Vd, Qd = to_device(K, w.dtype), to_device(V, w.dtype), to_device(Q, w.dtype)
+    dm = Bn.dims(**w.dims())
+    kl, vl, ql = ([X[l] for l in range(w.n_layers)] for X in (Kd, Vd, Qd))
+    _, scores = probe(dm, T, kl, ql, w.n_probe)
+    got_s = scores.cpu().numpy().astype(np.float64)
+    modes = np.full((1, H), O.RESIDUAL, np.uint8)
+    modes[0, 0] = O.SHARED
+    modes[0, H - 1] = O.EXACT
+    cache = CompressedCache(dm, w.seq_lens, modes[None])
+    cache.compress(0, kl, vl, token_scores=scores)
+    torch.cuda.synchronize()
+    del Kd, Vd, Qd
+    buf = cache.host_bytes()
+    q = gen.decode_queries(w, 0, scale=8.0)
+    outs = [cache.decode(layer, to_device(q[layer], w.dtype)).float().cpu().numpy()[0] for layer in range(w.n_layers)]
+    worst = 0.0
+    for h in (0, 1, 4, H - 1):
+        m = int(modes[0, h])
+        got, counts = unpack_tok_unit(buf, int(cache.offsets_host[0, 0, h]), m, T, d, ppm, w.dtype, 2)
+        if m == O.RESIDUAL:
+            ref_s, _ = O.token_scores(K[0:2, h], Q[0:2, h * G:(h + 1) * G])
+            rel = np.abs(got_s[0, h] - ref_s) / np.maximum(ref_s, 1e-30)
+            assert rel.max() <= 1e-4, (h, rel.max())
+            S = got["TS"]
+            assert S.size == n, (h, S.size, n)
+            tau = np.sort(ref_s)[::-1][n - 1]
+            inside = np.zeros(T, bool)
+            inside[S] = True
+            assert not np.any((ref_s > tau * (1 + 1e-4)) & ~inside)
+            assert not np.any((ref_s < tau * (1 - 1e-4)) & inside)
+            np.testing.assert_array_equal(counts[:-1], np.searchsorted(S, np.arange(0, T, 128)))
+            assert counts[-1] == n
+            ref = O.compress_unit_tokens(K[0:2, h], V[0:2, h], m, S, w.dtype)
+            for key in ("MK", "MV"):
+                compare_units({key: got[key]}, {key: ref[key]}, w.dtype)
+            for key in ("HK", "HV"):
+                assert ulp_distance(got[key], ref[key], TYPES[w.dtype][1]).max(initial=0) <= 1, key
+        else:
+            ref = O.compress_unit_tokens(K[0:2, h], V[0:2, h], m, None, w.dtype)
+            compare_units(got, ref, w.dtype)
+        for layer in range(2):
+            want = O.decode_unit_tokens(ref, m, layer, q[layer][0, h * G:(h + 1) * G].astype(np.float64),
+                                        1.0 / math.sqrt(d), d, 2)
+            for g in range(G):
+                e = rel_l2(outs[layer][h * G + g], want[g])
+                worst = max(worst, e)
+                assert e <= 1e-2, (h, layer, g, e)
+        log(f"  unit head={h} mode={m} ok")
+    log(f"  worst rel-L2 {worst:.3e}")
