@@ -210,3 +210,84 @@ def test_fullsize_token_residual(torch_mod):
                 assert e <= 1e-2, (h, layer, g, e)
         log(f"  unit head={h} mode={m} ok")
     log(f"  worst rel-L2 {worst:.3e}")
+
+
+def test_fullsize_generation(torch_mod):
+    """Generation over a 32768-token prefix at the 8B head shape: appends into a
+    40-row exact tail, decode over the compressed span plus the tail (the
+    several-part launch), one refresh; refreshed modes and spans checked for
+    every head, decode outputs for sampled heads of every mode at every step."""
+    torch = torch_mod
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, Generation, to_device
+    from test_gpu_generation import _new_token
+    w = scaled(WORKLOADS["llama8b"], n_layers=2)
+    T, H, G, d, k, L = w.seq_lens[0], w.n_kv_heads, w.group, w.head_dim, w.topk, w.n_layers
+    cap, P, steps = 40, 16, 45
+    heads = (0, 1, 2, 5)
+    log(f"[case] full-size generation: prefix {T}, Hkv={H} Hq={w.n_q_heads}, tail {cap}, {steps} steps")
+    dm = Bn.dims(**w.dims())
+    modes0 = gen.fixed_modes(w)[None].copy()
+    modes0[0, 0, :3] = [0, 1, 2]
+    cache = CompressedCache(dm, w.seq_lens, modes0)
+    K, V = gen.layer_cache(w, 0, threads=16)
+    Kd, Vd = to_device(K, w.dtype), to_device(V, w.dtype)
+    cache.compress(0, [Kd[l] for l in range(L)], [Vd[l] for l in range(L)])
+    torch.cuda.synchronize()
+    del Kd, Vd
+    spans = [{h: (O.compress_unit(K[0:2, h], V[0:2, h], int(modes0[0, 0, h]), k, w.dtype), int(modes0[0, 0, h]), 2)
+              for h in heads}]
+    del K, V
+    g = Generation(dm, cache, cap)
+    rng = np.random.default_rng(11)
+    tailK = [[] for _ in range(L)]
+    tailV = [[] for _ in range(L)]
+    recent = [[] for _ in range(L)]
+    worst, refreshes = 0.0, 0
+    for step in range(steps):
+        if g.full:
+            Qr = [np.stack(recent[l][-P:], axis=2) for l in range(L)]           # [1][Hq][P][d]
+            Kt = np.array([np.stack([r[0] for r in tailK[l]], axis=1) for l in range(L)])  # [L][H][n][d]
+            Vt = np.array([np.stack([r[0] for r in tailV[l]], axis=1) for l in range(L)])
+            E = np.stack([O.routing_errors(Kt[:, h], np.stack(Qr)[:, 0, h * G:(h + 1) * G], k) for h in range(H)])
+            lam = float(np.median(E[:, 0])) * 2.0
+            modes = g.refresh([to_device(Qr[l], w.dtype) for l in range(L)], P, lam=lam)
+            refreshes += 1
+            om = np.stack([O.omega(d, k, w.dtype, 2) for _ in range(H)])
+            want = O.route(E, om, lam)
+            cost = E + lam * om
+            srt = np.sort(cost, axis=1)
+            ok = (srt[:, 1] - srt[:, 0]) / np.maximum(srt[:, 0], 1e-30) >= 1e-3
+            np.testing.assert_array_equal(modes[0, 0][ok], want[ok])
+            buf = g.spans[-1].host_bytes()
+            span = {}
+            for h in range(H):
+                m = int(modes[0, 0, h])
+                unit = O.compress_unit(Kt[:, h], Vt[:, h], m, k, w.dtype)
+                compare_units(unpack_unit(buf, int(g.spans[-1].offsets_host[0, 0, h]), m, cap, d, k, w.dtype, 2),
+                              unit, w.dtype)
+                span[h] = (unit, m, 2)
+            spans.append(span)
+            tailK = [[] for _ in range(L)]
+            tailV = [[] for _ in range(L)]
+            log(f"  refresh: modes {np.bincount(modes.ravel(), minlength=3).tolist()}, {int(ok.sum())} checked")
+        kn, vn = _new_token(w, rng)
+        qs = gen.decode_queries(w, step, scale=4.0)
+        for layer in range(L):
+            g.append(layer, to_device(kn[layer], w.dtype), to_device(vn[layer], w.dtype))
+            out = g.decode(layer, to_device(qs[layer], w.dtype)).float().cpu().numpy()
+            tailK[layer].append(kn[layer])
+            tailV[layer].append(vn[layer])
+            for h in heads:
+                tk = np.stack([r[0, h] for r in tailK[layer]])
+                tv = np.stack([r[0, h] for r in tailV[layer]])
+                want = O.decode_spans([sp[h] for sp in spans], tk, tv, layer,
+                                      qs[layer][0, h * G:(h + 1) * G].astype(np.float64), 1.0 / math.sqrt(d), d)
+                for gg in range(G):
+                    e = rel_l2(out[0, h * G + gg], want[gg])
+                    worst = max(worst, e)
+                    assert e <= 1e-2, (step, layer, h, gg, e)
+            recent[layer].append(qs[layer])
+        g.advance()
+    assert refreshes == 1 and len(g.spans) == 2
+    log(f"  {steps} steps ok; worst rel-L2 {worst:.3e}")
