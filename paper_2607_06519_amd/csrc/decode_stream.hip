@@ -61,6 +61,14 @@ __device__ __forceinline__ uint4 ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+// The K and V tile loads: every byte of a plane is read once per decode
+// step, so they carry the non-temporal cache hint (cache policy NT).
+__device__ __forceinline__ uint4 ld128_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  constexpr int kNonTemporal = 2;
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 __device__ __forceinline__ uint32_t word(const uint4& v, int w) {
   return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
 }
@@ -276,7 +284,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? row * D + pc * 8 : kOob, 0, 0);
           b.k[i] = make_uint4(w2[0], w2[1], 0u, 0u);
         } else {
-          b.k[i] = ld128(kr, ok ? row * RB + pc * 16 : kOob);
+          b.k[i] = ld128_stream(kr, ok ? row * RB + pc * 16 : kOob);
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
@@ -293,7 +301,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? row * D + pc * 8 : kOob, 0, 0);
           b.v[i] = make_uint4(w2[0], w2[1], 0u, 0u);
         } else {
-          b.v[i] = ld128(vr, ok ? row * RB + pc * 16 : kOob);
+          b.v[i] = ld128_stream(vr, ok ? row * RB + pc * 16 : kOob);
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
