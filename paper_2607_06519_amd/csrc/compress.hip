@@ -66,6 +66,18 @@ __device__ __forceinline__ uint2 mean_piece_e4m3(const uint4* x) {
   return make_uint2(w[0], w[1]);
 }
 
+// The dense pass reads every input row once and writes every plane once:
+// 16-byte loads and stores with the non-temporal cache hint.
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store_stream(uint8_t* p, const uint4& x) {
+  const u32x4v v = {x.x, x.y, x.z, x.w};
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4v*>(p));
+}
+
 template <int D, bool BF16, int NB>
 __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   constexpr int E = BF16 ? 2 : 4;
@@ -98,22 +110,22 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
     uint4 ka[NB], va[NB];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
-      ka[n] = *reinterpret_cast<const uint4*>(kx[n] + off);
-      va[n] = *reinterpret_cast<const uint4*>(vx[n] + off);
+      ka[n] = load_stream(kx[n] + off);
+      va[n] = load_stream(vx[n] + off);
     }
     if (mode == kExact) {
 #pragma unroll
       for (int n = 0; n < NB; ++n) {
-        *reinterpret_cast<uint4*>(seg + L.ek[n] + off) = ka[n];
-        *reinterpret_cast<uint4*>(seg + L.ev[n] + off) = va[n];
+        store_stream(seg + L.ek[n] + off, ka[n]);
+        store_stream(seg + L.ev[n] + off, va[n]);
       }
     } else if (c8) {
       const uint64_t o8 = (uint64_t)t * D + piece * 8;
       *reinterpret_cast<uint2*>(seg + L.mk + o8) = mean_piece_e4m3<NB>(ka);
       *reinterpret_cast<uint2*>(seg + L.mv + o8) = mean_piece_e4m3<NB>(va);
     } else {
-      *reinterpret_cast<uint4*>(seg + L.mk + off) = mean_piece<BF16, NB>(ka);
-      *reinterpret_cast<uint4*>(seg + L.mv + off) = mean_piece<BF16, NB>(va);
+      store_stream(seg + L.mk + off, mean_piece<BF16, NB>(ka));
+      store_stream(seg + L.mv + off, mean_piece<BF16, NB>(va));
     }
   }
 }
