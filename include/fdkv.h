@@ -215,9 +215,13 @@ fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t 
  *   seq_lens     device int32 [batch], 0 <= T_i <= max_seq_len (T_i = 0 gives o = 0)
  *   max_seq_len  host, sizes the launch; max_seq_len * d * elem_bytes < 2^31
  *                (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets)
- *   modes        device [batch][n_blocks][Hkv], 4-byte aligned (read in aligned
- *                4-byte words; bytes past the array inside its last word are ignored)
+ *   modes        device [batch][n_blocks][Hkv], 4-byte aligned and allocated to a
+ *                multiple of 4 bytes (read in aligned 4-byte words; the padding
+ *                bytes are ignored)
  *   seg_offsets  device [batch][n_blocks][Hkv]
+ *                A unit whose mode is above FDKV_EXACT or whose offset is not a
+ *                multiple of 256 is not read: the outputs of its query heads
+ *                come out NaN, so a corrupt mode table cannot pass unnoticed.
  *   layer        0 <= layer < L
  *   q            device [batch][Hq][d]
  *   out          device [batch][Hq][d]
@@ -243,7 +247,7 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
 typedef struct {
   const int32_t* seq_lens;      /* device [batch]: tokens of each sequence in this span */
   int32_t max_seq_len;          /* host: the largest entry of seq_lens (sizes the launch) */
-  const uint8_t* modes;         /* device [batch][n_blocks][Hkv], 4-byte aligned */
+  const uint8_t* modes;         /* device [batch][n_blocks][Hkv], 4-byte aligned, padded to 4 bytes */
   const uint64_t* seg_offsets;  /* device [batch][n_blocks][Hkv] */
   const void* cache;            /* device, 256-byte aligned */
 } fdkv_span;

@@ -45,9 +45,9 @@ Readings of the paper adopted here (the paper leaves these open):
   decimal arithmetic so that stored values are correctly rounded;
 * in a B = 4 block the residual of a token keeps the ``k`` largest of its
   ``3 d`` high-frequency coefficients ``|Z_j[c]|`` (j = 1..3; by Parseval this
-  minimises the block's squared reconstruction error), ranked in float32 as
-  the DCT-II(4) butterfly evaluates them on the stored inputs
-  (``residual_keys_dct4``), ties to the lower code ``4 c + j``; what is stored
+  minimises the block's squared reconstruction error), ranked by their
+  float64 values (``residual_keys_dct4``), ties to the lower code
+  ``4 c + j``; what is stored
   is the code (uint16, ascending) and the orthonormal coefficient ``Z_j[c]``
   itself, and layer ``p`` of the block adds ``F_4[j, p] Z_j[c]``; the shared
   plane is the image of ``Z_0``, the four-layer mean;
@@ -60,12 +60,11 @@ Readings of the paper adopted here (the paper leaves these open):
 * the budget rule takes the smallest ``lambda`` among 0, the per-head
   breakpoints and +inf whose footprint fits the budget;
 * decode scales logits by ``1/sqrt(d)`` and attends over the cached tokens;
-* the token score is taken at the kernel's precision: the deviations
-  ``x_l - M`` in fp32 on the stored inputs, rounded to bf16 (exact products,
-  the sum in fp64 here); its maximum runs over the probe rows of every layer
-  of the block and every query head of the group; ``r`` is one fraction per
-  cache (parts per million), ``n = ceil(r T)``, ties to the lower token; the
-  stored rows are the unrounded coefficients rounded to the coefficient type;
+* the token score is computed in float64 from the stored inputs; its
+  maximum runs over the probe rows of every layer of the block and every
+  query head of the group; ``r`` is one fraction per cache (parts per
+  million), ``n = ceil(r T)``, ties to the lower token; the stored rows are
+  the unrounded coefficients rounded to the coefficient type;
 * a refresh re-decides routing only for the tokens it compresses (earlier
   spans keep their modes: a shared head's dropped coefficients cannot be
   recovered), and a span's probe rows are the last decode queries;
@@ -364,24 +363,14 @@ def residual_channels(x_even, x_odd, k: int) -> np.ndarray:
 
 
 def residual_keys_dct4(X) -> np.ndarray:
-    """Ranking keys ``|Z_j[c]|``, j = 1..3, of a B = 4 block, ``[..., d, 3]``, in float32.
+    """Ranking keys ``|Z_j[c]|``, j = 1..3, of a B = 4 block, ``[..., d, 3]``.
 
-    ``X``: ``[4][..., d]`` stored inputs of the block's layers.  The
-    coefficients ``Z = F_4 X`` are evaluated by the DCT-II(4) butterfly in
-    float32, every product and sum rounded on its own:
-    ``Z_1 = a (x0 - x3) + b (x1 - x2)``, ``Z_2 = ((x0 + x3) - (x1 + x2)) / 2``,
-    ``Z_3 = b (x0 - x3) - a (x1 - x2)`` with ``a = F_4[1, 0]`` and
-    ``b = F_4[1, 1]`` rounded to float32.
+    ``X``: ``[4][..., d]`` stored inputs of the block's layers.  The keys are the
+    magnitudes of the high-frequency coefficients ``Z = F_4 X`` of Eq. (1), in
+    float64 (``depth_factorize``).
     """
-    x0, x1, x2, x3 = (np.asarray(X[n], dtype=np.float32) for n in range(4))
-    F = dct_matrix(4)
-    a, b = np.float32(F[1, 0]), np.float32(F[1, 1])
-    d03, d12 = x0 - x3, x1 - x2
-    s03, s12 = x0 + x3, x1 + x2
-    z1 = a * d03 + b * d12
-    z2 = (s03 - s12) * np.float32(0.5)
-    z3 = b * d03 - a * d12
-    return np.abs(np.stack([z1, z2, z3], axis=-1))
+    Z = depth_factorize(np.asarray(X, dtype=np.float64))
+    return np.abs(np.moveaxis(Z[1:], 0, -1))
 
 
 def residual_codes_dct4(X, k: int) -> np.ndarray:
@@ -493,25 +482,17 @@ def decode_unit(unit, mode: int, layer: int, q, scale: float, d: int, B: int = 2
 # the largest logit change the token's removal would cause at a probe row
 # ----------------------------------------------------------------------------
 def token_deviations(KB) -> np.ndarray:
-    """Deviations of each layer's keys from the shared reconstruction, ``[B][T][d]``,
-    at the precision the token score is taken in: fp32 arithmetic on the
-    stored inputs, rounded to bf16.  Pairs: ``x0 - M = (x0 - x1) / 2`` and its
-    negation; fours: ``x_l - M`` with ``M = ((x0 + x3) + (x1 + x2)) / 4``."""
-    X = [np.asarray(x, dtype=np.float32) for x in KB]
-    B = len(X)
-    if B == 2:
-        D = (X[0] - X[1]) * np.float32(0.5)
-        dev = np.stack([D, -D])
-    else:
-        M = ((X[0] + X[3]) + (X[1] + X[2])) * np.float32(0.25)
-        dev = np.stack([x - M for x in X])
-    return round_bf16(dev.astype(np.float64))
+    """Deviations ``K_t - K^S_t`` of each layer's keys from the shared
+    reconstruction, ``[B][T][d]``, in float64 on the stored inputs: ``x_l - M``
+    with ``M`` the block mean (pairs: ``(x0 - x1) / 2`` and its negation)."""
+    X = np.asarray(KB, dtype=np.float64)
+    return X - coefficient_image(X, 0, 0)[None]
 
 
 def token_scores(KB, QB) -> Tuple[np.ndarray, np.ndarray]:
     """``(s, e)`` per token: ``s_t = max |q . dev_{l,t}|`` over the probe rows q of every
     layer l of the block and every query head of the group, and ``e_t`` the sum of
-    the squares of those dot products (fp64 on the bf16 deviations)."""
+    the squares of those dot products (float64)."""
     dev = token_deviations(KB)
     QB = np.asarray(QB, dtype=np.float64)
     s = np.zeros(dev.shape[1])
@@ -785,13 +766,45 @@ def cache_bytes(seq_lens, modes, d: int, k: int, dtype: str, sizes=None) -> int:
     return tot
 
 
+def _breakpoint(Ea: float, Eb: float, oa: float, ob: float) -> float:
+    """The lambda at which mode a (the cheaper, ``oa < ob``) and mode b cost the same:
+    ``Ea + lam oa = Eb + lam ob``."""
+    return (Ea - Eb) / (ob - oa)
+
+
+def _prefer(Ea: float, Eb: float, oa: float, ob: float, lam: float) -> bool:
+    """Whether mode a wins against mode b at ``lam``, a being the cheaper one
+    (``oa < ob``, or equal cost and the lower mode): a costs no more than b,
+    ``Ea + lam oa <= Eb + lam ob``, i.e. ``lam >= breakpoint`` (ties go to the
+    cheaper mode).  Deciding against the breakpoint itself, not against the two
+    costs evaluated in floating point, makes a tie at a breakpoint exact: at
+    ``lam`` equal to the breakpoint value the two costs are equal by definition,
+    whereas ``Ea + lam oa`` and ``Eb + lam ob`` may round apart."""
+    if oa == ob:
+        return Ea <= Eb
+    return lam >= _breakpoint(Ea, Eb, oa, ob)
+
+
+def _cheaper_first(m1: int, m2: int, om) -> Tuple[int, int]:
+    return (m1, m2) if (om[m1], m1) <= (om[m2], m2) else (m2, m1)
+
+
 def route(E, om, lam: float) -> np.ndarray:
-    """argmin_m E[u, m] + lam * Omega(m), ties to the cheaper (lower) mode."""
-    E = np.asarray(E, dtype=np.float64)
-    cost = E + lam * np.asarray(om, dtype=np.float64)
-    if np.isinf(lam):
-        cost = np.where(np.isnan(cost), np.inf, cost)
-    return np.argmin(cost, axis=-1).astype(np.uint8)
+    """argmin_m E[u, m] + lam * Omega(m) (Eq. 3), ties to the cheaper mode.
+
+    ``om`` is ``[3]`` or ``[units][3]``.  The three modes are compared in turn,
+    each pair through ``_prefer``.
+    """
+    E = np.asarray(E, dtype=np.float64).reshape(-1, 3)
+    om = np.broadcast_to(np.asarray(om, dtype=np.float64), E.shape)
+    out = np.zeros(E.shape[0], dtype=np.uint8)
+    for u in range(E.shape[0]):
+        best = 0
+        for m in (1, 2):
+            a, b = _cheaper_first(best, m, om[u])
+            best = a if _prefer(E[u, a], E[u, b], om[u, a], om[u, b], lam) else b
+        out[u] = best
+    return out
 
 
 def route_budget(E, T: int, d: int, k: int, dtype: str, budget: int,
@@ -811,9 +824,10 @@ def route_budget(E, T: int, d: int, k: int, dtype: str, budget: int,
     for u in range(n):
         for i in range(3):
             for j in range(i + 1, 3):
-                if not om[u, j] > om[u, i]:
+                a, b = _cheaper_first(i, j, om[u])
+                if not om[u, b] > om[u, a]:
                     continue
-                lam = (E[u, i] - E[u, j]) / (om[u, j] - om[u, i])
+                lam = _breakpoint(E[u, a], E[u, b], om[u, a], om[u, b])
                 if lam > 0 and np.isfinite(lam):
                     cands.add(float(lam))
     order = sorted(cands) + [math.inf]

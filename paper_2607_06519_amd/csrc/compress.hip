@@ -300,15 +300,6 @@ __device__ __forceinline__ int vtab_slot(int lane, int piece) {  // 16-byte slot
   return lane * NPV + (piece ^ (lane & (NPV - 1)));
 }
 
-// Two fp32 values as a bf16 pair, round to nearest even (the gfx950
-// conversion instruction: one per pair; finite inputs round as f32_to_bf16_bits).
-__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
-  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
-  typedef float f32x2v __attribute__((ext_vector_type(2)));
-  const f32x2v v = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
-}
-
 // C8: residual values stored as FP8 E4M3 (a compile-time flavour, so the
 // bf16 path carries none of the encoder)
 template <int D, bool BF16, int RS, bool C8>

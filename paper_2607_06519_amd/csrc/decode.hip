@@ -80,20 +80,28 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const bool tail = part == P.tail_part;
   const int T = P.part[part].lens[seq];
   const int wg_tok0 = wgc * kDecodeWgTokens;
-  if (wg_tok0 >= T) {  // uniform over the workgroup
-    // an empty record (m = -inf, l = 0, acc = 0): the merge reads every slot
+  const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
+  // the exact tail of a generation has no unit arrays
+  const int mode = tail ? kExact : P.part[part].modes[unit];
+  const uint64_t seg_off = tail ? 0 : P.part[part].seg_off[unit];
+  const bool bad_unit = mode > kExact || (seg_off & 255) != 0;
+  if (wg_tok0 >= T || bad_unit) {  // uniform over the workgroup
+    // an empty record (m = -inf, l = 0, acc = 0): the merge reads every slot;
+    // an invalid unit (mode above exact or a misaligned segment) writes
+    // m = 0, l = 1, acc = NaN, which turns its query heads' outputs into NaN
     float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
-    for (int i = threadIdx.x; i < G * S::RS; i += 256) rec[i] = i % S::RS == D ? -INFINITY : 0.f;
+    for (int i = threadIdx.x; i < G * S::RS; i += 256) {
+      const int c = i % S::RS;
+      rec[i] = bad_unit ? (c == D ? 0.f : c == D + 1 ? 1.f : __builtin_nanf("")) : (c == D ? -INFINITY : 0.f);
+    }
     return;
   }
 
-  const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   const bool q4 = P.bsize == 4;
-  const int mode = tail ? kExact : P.part[part].modes[unit];   // the exact tail of a generation has no unit arrays
   const int k = P.topk;
   const bool resid = !P.tokres && (mode == kResidual) && k > 0;
   const bool tokres = P.tokres && mode == kResidual;   // token-level residual set
-  const uint8_t* seg = tail ? static_cast<const uint8_t*>(P.tail_k) : P.part[part].cache + P.part[part].seg_off[unit];
+  const uint8_t* seg = tail ? static_cast<const uint8_t*>(P.tail_k) : P.part[part].cache + seg_off;
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, E, E, P.bsize);
   const uint64_t xplane = plane_bytes((uint64_t)T * D * E);  // exact planes: K_p at p * xplane, V_p at (B + p) * xplane
   const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * D * E;

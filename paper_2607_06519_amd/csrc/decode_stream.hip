@@ -162,11 +162,12 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const bool tail = MULTI && part == P.tail_part;
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   // The three per-unit values are fetched together, as scalar loads (the
-  // mode byte through its aligned dword; the array is 4-byte aligned), and
-  // the exit test below reads all of them: the start-up costs one round trip
-  // that does not queue behind other waves' tile loads.  (A segment offset is
-  // a multiple of 256 and a mode is at most kExact; a unit that breaks either
-  // is left alone.)
+  // mode byte through its aligned dword; the array is 4-byte aligned and
+  // padded to a multiple of 4 bytes), and the exit test below reads all of
+  // them: the start-up costs one round trip that does not queue behind other
+  // waves' tile loads.  A segment offset is a multiple of 256 and a mode is at
+  // most kExact; a unit that breaks either reads nothing and writes a record
+  // that turns its query heads' outputs into NaN.
   // (The exact tail of a generation has no unit arrays: its rows are exact.)
   const int T = P.part[part].lens[seq];
   uint32_t mode_word = (uint32_t)kExact;
@@ -177,11 +178,16 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   }
   const int mode = (int)(mode_word & 0xFFu);
   const int wg_tok0 = wgc * kDecodeWgTokens;
-  if (wg_tok0 >= T || mode > kExact || (seg_off & 255) != 0) {
-    // no tokens here (or a unit left alone): an empty record, m = -inf,
-    // l = 0, acc = 0, since the merge reads every slot
+  const bool bad_unit = mode > kExact || (seg_off & 255) != 0;
+  if (wg_tok0 >= T || bad_unit) {
+    // no tokens here: an empty record, m = -inf, l = 0, acc = 0, since the
+    // merge reads every slot; an invalid unit: m = 0, l = 1, acc = NaN, which
+    // the merge carries into every output channel of the KV head's queries
     float* rec = P.ws + ((uint64_t)sh * P.n_chunks_total + slot) * G * S::RS;
-    for (int i = threadIdx.x; i < G * S::RS; i += 256) rec[i] = i % S::RS == D ? -INFINITY : 0.f;
+    for (int i = threadIdx.x; i < G * S::RS; i += 256) {
+      const int c = i % S::RS;
+      rec[i] = bad_unit ? (c == D ? 0.f : c == D + 1 ? 1.f : __builtin_nanf("")) : (c == D ? -INFINITY : 0.f);
+    }
     return;
   }
 
@@ -394,7 +400,13 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       for (int i = 0; i < NL; ++i)
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-          p[i][g] = __builtin_amdgcn_exp2f(s[i][g] - m[g]);  // masked rows: exp2(-inf) = 0
+          // masked rows: exp2(-inf) = 0; a token-level set can mask every
+          // row of a tile before any logit has set the reference max, and
+          // exp2(-inf - -inf) would be NaN
+          if constexpr (RES == 3)
+            p[i][g] = s[i][g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i][g] - m[g]);
+          else
+            p[i][g] = __builtin_amdgcn_exp2f(s[i][g] - m[g]);
           l[g] += p[i][g];
         }
       // P V over the dense plane: the lane's rows 2pr and 2pr + 1 share one dot2

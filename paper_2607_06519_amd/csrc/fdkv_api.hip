@@ -231,20 +231,31 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
     }
   }
   auto quad = [&](int u) { return sch.size[u / dims->n_kv_heads] == 4 ? 1 : 0; };
+  // Of two modes, the cheaper one first (equal cost: the lower mode).
+  auto order = [](const double* om, int m1, int m2, int& a, int& b) {
+    const bool first = om[m1] < om[m2] || (om[m1] == om[m2] && m1 < m2);
+    a = first ? m1 : m2;
+    b = first ? m2 : m1;
+  };
+  // The lambda at which the cheaper mode a and mode b cost the same.
+  auto breakpoint = [](const double* E, const double* om, int a, int b) { return (E[a] - E[b]) / (om[b] - om[a]); };
 
+  // m = argmin E_m + lambda Omega_m, ties to the cheaper mode.  Two modes are
+  // compared through their breakpoint: the cheaper wins iff lambda >= it.  At
+  // a candidate lambda equal to a unit's breakpoint its two modes tie exactly
+  // (the same expression gives both numbers), where the two costs evaluated
+  // in floating point might round apart.
   auto decide = [&](double lam, uint8_t* out) {
     uint64_t fp = 0;
     for (int u = 0; u < units; ++u) {
       const double* om = omB[quad(u)];
       const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
       int best = 0;
-      double bc = E[0] + lam * om[0];
       for (int m = 1; m < 3; ++m) {
-        const double c = E[m] + lam * om[m];
-        if (c < bc) {
-          bc = c;
-          best = m;
-        }
+        int a, b;
+        order(om, best, m, a, b);
+        const bool cheaper_wins = om[a] == om[b] ? E[a] <= E[b] : lam >= breakpoint(E, om, a, b);
+        best = cheaper_wins ? a : b;
       }
       out[u] = (uint8_t)best;
       fp += segB[quad(u)][best];
@@ -264,8 +275,10 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
     const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
     for (int i = 0; i < 3; ++i)
       for (int j = i + 1; j < 3; ++j) {
-        if (!(om[j] > om[i])) continue;
-        const double lam = (E[i] - E[j]) / (om[j] - om[i]);
+        int a, b;
+        order(om, i, j, a, b);
+        if (!(om[b] > om[a])) continue;
+        const double lam = breakpoint(E, om, a, b);
         if (lam > 0.0 && isfinite(lam)) cands.push_back(lam);
       }
   }

@@ -112,6 +112,28 @@ FDKV_HD uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
 }
 
+#ifdef __HIPCC__
+// Two fp32 values as a bf16 pair, round to nearest even (the gfx950
+// conversion instruction: one per pair; finite inputs round as f32_to_bf16_bits).
+__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const f32x2v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+}
+
+// Two fp32 values as a sum of two bf16 pairs, hi = bf16(x) and
+// lo = bf16(x - hi) (x - hi is exact in fp32): hi + lo is x to within
+// 2^-18 |x|.  Products of bf16 values are exact in the fp32 MFMA, so the
+// Gram matrix of x taken as H H^T + H L^T + L H^T carries only that error
+// (plus the dropped L L^T, 2^-18 relative), where H H^T alone would carry
+// the bf16 rounding of x (2^-9 relative per element).
+__device__ __forceinline__ void split_bf16x2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  hi = cvt_bf16x2(x0, x1);
+  lo = cvt_bf16x2(x0 - bf16_lo(hi), x1 - bf16_hi(hi));
+}
+#endif
+
 // ---------------------------------------------------------------- wavefront helpers
 // DPP lane permutations within rows of 16 lanes (gfx9 encodings).
 template <int CTRL>

@@ -257,12 +257,13 @@ __global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
   }
 }
 
-// Gram matrices of bf16(D) and bf16(Dbar) over one chunk of kProbeChunk
-// tokens of a unit, contracted with S_u.  64 tokens per step: each thread
-// turns its 16-byte pieces of the two layers into bf16 half differences,
-// zeroes the channels that are among its token's top-k (for Dbar), and
-// writes both rows to LDS; waves 0-1 accumulate the blocks of D, waves 2-3
-// those of Dbar.  The next step's loads are in flight during the MFMAs.
+// Gram matrices of D and Dbar over one chunk of kProbeChunk tokens of a
+// unit, contracted with S_u.  64 tokens per step: each thread turns its
+// 16-byte pieces of the two layers into fp32 half differences, splits each
+// into bf16 hi + lo (split_bf16x2), zeroes the channels that are among its
+// token's top-k (for Dbar), and writes the four rows to LDS; waves 0-1
+// accumulate the blocks of D D^T ~ H H^T + H L^T + L H^T, waves 2-3 those
+// of Dbar.  The next step's loads are in flight during the MFMAs.
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   constexpr int E = BF16 ? 2 : 4;
@@ -273,7 +274,8 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   constexpr int R = kGramRows, LDR = D + 16;
   constexpr int LPT = R * NPc / 256;             // loads per thread per layer per step
   constexpr TriTiles<NB> tri{};
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][R * LDR];  // [D, Dbar][token][channel]
+  // [D hi, D lo, Dbar hi, Dbar lo][token][channel]
+  __shared__ __attribute__((aligned(16))) uint16_t tile[4][R * LDR];
   __shared__ float red[4];
 
   const int chunk = blockIdx.x;
@@ -317,19 +319,19 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
       const int i = tid + 256 * j, row = i / NPc, pc = i % NPc, t = t0 + row;
       const uint32_t* pa = reinterpret_cast<const uint32_t*>(&ra[j]);
       const uint32_t* pb = reinterpret_cast<const uint32_t*>(&rb[j]);
-      uint16_t h[CPP];
+      float dv[CPP];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         if constexpr (BF16) {
-          h[2 * w] = (uint16_t)f32_to_bf16_bits((bf16_lo(pa[w]) - bf16_lo(pb[w])) * 0.5f);
-          h[2 * w + 1] = (uint16_t)f32_to_bf16_bits((bf16_hi(pa[w]) - bf16_hi(pb[w])) * 0.5f);
+          dv[2 * w] = (bf16_lo(pa[w]) - bf16_lo(pb[w])) * 0.5f;
+          dv[2 * w + 1] = (bf16_hi(pa[w]) - bf16_hi(pb[w])) * 0.5f;
         } else {
-          h[w] = (uint16_t)f32_to_bf16_bits((as_f32(pa[w]) - as_f32(pb[w])) * 0.5f);
+          dv[w] = (as_f32(pa[w]) - as_f32(pb[w])) * 0.5f;
         }
       }
-      uint32_t wd[CPP / 2], wr[CPP / 2];
+      uint32_t wd[CPP / 2], wl[CPP / 2], wr[CPP / 2], wrl[CPP / 2];
 #pragma unroll
-      for (int c = 0; c < CPP / 2; ++c) wd[c] = (uint32_t)h[2 * c] | ((uint32_t)h[2 * c + 1] << 16);
+      for (int c = 0; c < CPP / 2; ++c) split_bf16x2(dv[2 * c], dv[2 * c + 1], wd[c], wl[c]);
       // Dbar: drop the channels of this piece that are among the token's top-k
       uint32_t keep = (1u << CPP) - 1;
       if (k16) {
@@ -346,28 +348,39 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
         }
       }
 #pragma unroll
-      for (int c = 0; c < CPP / 2; ++c)
-        wr[c] = (((keep >> (2 * c)) & 1) ? (wd[c] & 0xFFFFu) : 0u) | (((keep >> (2 * c + 1)) & 1) ? (wd[c] & 0xFFFF0000u) : 0u);
-      uint16_t* d0 = &tile[0][row * LDR + pc * CPP];
-      uint16_t* d1 = &tile[1][row * LDR + pc * CPP];
-      if constexpr (CPP == 8) {
-        *reinterpret_cast<uint4*>(d0) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
-        *reinterpret_cast<uint4*>(d1) = make_uint4(wr[0], wr[1], wr[2], wr[3]);
-      } else {
-        *reinterpret_cast<uint2*>(d0) = make_uint2(wd[0], wd[1]);
-        *reinterpret_cast<uint2*>(d1) = make_uint2(wr[0], wr[1]);
+      for (int c = 0; c < CPP / 2; ++c) {
+        const uint32_t km = (((keep >> (2 * c)) & 1) ? 0xFFFFu : 0u) | (((keep >> (2 * c + 1)) & 1) ? 0xFFFF0000u : 0u);
+        wr[c] = wd[c] & km;
+        wrl[c] = wl[c] & km;
+      }
+      const uint32_t* src[4] = {wd, wl, wr, wrl};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        uint16_t* dst = &tile[m][row * LDR + pc * CPP];
+        if constexpr (CPP == 8)
+          *reinterpret_cast<uint4*>(dst) = make_uint4(src[m][0], src[m][1], src[m][2], src[m][3]);
+        else
+          *reinterpret_cast<uint2*>(dst) = make_uint2(src[m][0], src[m][1]);
       }
     }
     load(t0 + R);
     __syncthreads();
 #pragma unroll
     for (int kk = 0; kk < R / 16; ++kk) {
-      bf16x8_t op[NB];
+      bf16x8_t oh[NB], ol[NB];
 #pragma unroll
-      for (int I = 0; I < NB; ++I) op[I] = gram_operand<LDR>(tile[mat], kk, I, lane);
+      for (int I = 0; I < NB; ++I) {
+        oh[I] = gram_operand<LDR>(tile[2 * mat], kk, I, lane);
+        ol[I] = gram_operand<LDR>(tile[2 * mat + 1], kk, I, lane);
+      }
 #pragma unroll
       for (int t = 0; t < NT; ++t)  // block t belongs to wave t / TPW of the pair (indices stay compile-time)
-        if (t / TPW == (wave & 1)) acc[t % TPW] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[tri.i[t]], op[tri.j[t]], acc[t % TPW], 0, 0, 0);
+        if (t / TPW == (wave & 1)) {
+          const int bi_ = tri.i[t], bj_ = tri.j[t];
+          f32x16_t a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[bi_], oh[bj_], acc[t % TPW], 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[bi_], ol[bj_], a, 0, 0, 0);
+          acc[t % TPW] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ol[bi_], oh[bj_], a, 0, 0, 0);
+        }
     }
     __syncthreads();
   }
@@ -398,19 +411,23 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
 // one or two 16-byte pieces of a token row from all four layers, forms the
 // block mean, the layer deviations, the coefficients Z_1..Z_3 (the same fp32
 // butterfly as residual_select4) and the images of the token's kept
-// coefficients, and writes the eight bf16 rows to LDS; wave w accumulates
-// layer w / 2, shared (w even) or residual (w odd).
+// coefficients, and writes the eight deviation rows to LDS as bf16 hi + lo
+// pairs (split_bf16x2); wave w accumulates layer w / 2, shared (w even) or
+// residual (w odd), as H H^T + H L^T + L H^T.
 template <int D, bool BF16>
 __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NPc = D * E / 16;                // 16-byte input pieces per row
   constexpr int CPP = 16 / E;                    // channels per piece
   constexpr int NB = D / 32, NT = NB * (NB + 1) / 2;
-  constexpr int R = 512 / NPc > 32 ? 512 / NPc : 32, LDR = D + 16;
+  // LDS rows padded by 16 channels (8 at d = 64, where 16 tiles of 64 rows
+  // would pass the 160 KB of a workgroup)
+  constexpr int R = 512 / NPc > 32 ? 512 / NPc : 32, LDR = D == 64 ? D + 8 : D + 16;
   constexpr int LPT = R * NPc / 512;             // pieces per thread per step
   constexpr TriTiles<NB> tri{};
   static_assert(LPT >= 1 && R % 16 == 0, "shape");
-  __shared__ __attribute__((aligned(16))) uint16_t tile[8][R * LDR];  // [layer * 2 + residual][token][channel]
+  // [layer * 2 + residual][hi, lo][token][channel]
+  __shared__ __attribute__((aligned(16))) uint16_t tile[16][R * LDR];
   __shared__ float red[8];
 
   const int chunk = blockIdx.x;
@@ -472,34 +489,35 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
           if (c < (uint32_t)CPP && (code & 3u) != 0u) kept |= 1u << (3 * c + (code & 3u) - 1);
         }
       }
-      uint32_t hw[8][CPP / 2];
+      // deviations of the eight matrices, channel pairs at a time, split into bf16 hi + lo
+      uint32_t hw[16][CPP / 2];
 #pragma unroll
-      for (int c = 0; c < CPP; ++c) {
-        float x[4];
+      for (int c2 = 0; c2 < CPP; c2 += 2) {
+        float dv[8][2];
 #pragma unroll
-        for (int n = 0; n < 4; ++n) x[n] = chan_of<BF16>(rx[j][n], c);
-        float z1, z2, z3;
-        dct4_high(x[0], x[1], x[2], x[3], z1, z2, z3);
-        const float m = ((x[0] + x[3]) + (x[1] + x[2])) * 0.25f;
-        const float k1 = (kept >> (3 * c)) & 1u ? z1 : 0.f;
-        const float k2 = (kept >> (3 * c + 1)) & 1u ? z2 : 0.f;
-        const float k3 = (kept >> (3 * c + 2)) & 1u ? z3 : 0.f;
+        for (int e = 0; e < 2; ++e) {
+          const int c = c2 + e;
+          float x[4];
 #pragma unroll
-        for (int n = 0; n < 4; ++n) {
-          const float dev = m - x[n];
-          const float dres = dev + (F1[n] * k1 + F2[n] * k2 + F3[n] * k3);
-          const uint32_t hs = f32_to_bf16_bits(dev), hr = f32_to_bf16_bits(dres);
-          if (c & 1) {
-            hw[2 * n][c >> 1] |= hs << 16;
-            hw[2 * n + 1][c >> 1] |= hr << 16;
-          } else {
-            hw[2 * n][c >> 1] = hs;
-            hw[2 * n + 1][c >> 1] = hr;
+          for (int n = 0; n < 4; ++n) x[n] = chan_of<BF16>(rx[j][n], c);
+          float z1, z2, z3;
+          dct4_high(x[0], x[1], x[2], x[3], z1, z2, z3);
+          const float m = ((x[0] + x[3]) + (x[1] + x[2])) * 0.25f;
+          const float k1 = (kept >> (3 * c)) & 1u ? z1 : 0.f;
+          const float k2 = (kept >> (3 * c + 1)) & 1u ? z2 : 0.f;
+          const float k3 = (kept >> (3 * c + 2)) & 1u ? z3 : 0.f;
+#pragma unroll
+          for (int n = 0; n < 4; ++n) {
+            const float dev = m - x[n];
+            dv[2 * n][e] = dev;
+            dv[2 * n + 1][e] = dev + (F1[n] * k1 + F2[n] * k2 + F3[n] * k3);
           }
         }
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) split_bf16x2(dv[mt][0], dv[mt][1], hw[2 * mt][c2 >> 1], hw[2 * mt + 1][c2 >> 1]);
       }
 #pragma unroll
-      for (int m = 0; m < 8; ++m) {
+      for (int m = 0; m < 16; ++m) {
         uint16_t* dst = &tile[m][row * LDR + pc * CPP];
         if constexpr (CPP == 8)
           *reinterpret_cast<uint4*>(dst) = make_uint4(hw[m][0], hw[m][1], hw[m][2], hw[m][3]);
@@ -511,12 +529,18 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
     __syncthreads();
 #pragma unroll
     for (int kk = 0; kk < R / 16; ++kk) {
-      bf16x8_t op[NB];
+      bf16x8_t oh[NB], ol[NB];
 #pragma unroll
-      for (int I = 0; I < NB; ++I) op[I] = gram_operand<LDR>(tile[wave], kk, I, lane);
+      for (int I = 0; I < NB; ++I) {
+        oh[I] = gram_operand<LDR>(tile[2 * wave], kk, I, lane);
+        ol[I] = gram_operand<LDR>(tile[2 * wave + 1], kk, I, lane);
+      }
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[tri.i[t]], op[tri.j[t]], acc[t], 0, 0, 0);
+      for (int t = 0; t < NT; ++t) {
+        f32x16_t a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[tri.i[t]], oh[tri.j[t]], acc[t], 0, 0, 0);
+        a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[tri.i[t]], ol[tri.j[t]], a, 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ol[tri.i[t]], oh[tri.j[t]], a, 0, 0, 0);
+      }
     }
     __syncthreads();
   }

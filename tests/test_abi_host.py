@@ -78,6 +78,23 @@ def test_route_lambda_matches_oracle(lib, dtype, d, k):
         np.testing.assert_array_equal(modes.ravel(), O.route(E3, om, lam))
 
 
+def test_route_at_breakpoints_matches_oracle(lib):
+    """At every unit's own breakpoints the C rule and the oracle give the same
+    modes (the tie goes to the cheaper mode on both sides)."""
+    rng = np.random.default_rng(9)
+    d, k = 128, 16
+    dm = B.dims(32, 8, 32, d, k, "bf16")
+    E = _rand_errors(rng, 128)
+    E3 = np.concatenate([E.astype(np.float64), np.zeros((128, 1))], axis=1)
+    om = O.omega(d, k, "bf16")
+    for u in range(0, 128, 9):
+        for a, b in ((0, 1), (1, 2), (0, 2)):
+            lam = (E3[u, a] - E3[u, b]) / (om[b] - om[a])
+            modes, _, st = B.route(dm, 32768, E.reshape(16, 8, 2), lam=float(lam))
+            assert st == 0
+            np.testing.assert_array_equal(modes.ravel(), O.route(E3, om, lam))
+
+
 @pytest.mark.parametrize("frac", [0.0, 0.15, 0.5, 0.85, 1.0])
 def test_route_budget_matches_oracle(lib, frac):
     rng = np.random.default_rng(6)

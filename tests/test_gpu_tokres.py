@@ -1,16 +1,21 @@
 """Token-level residual sets on the GPU through the C ABI, against the oracle.
 
-The score s_t (max over probe rows of |q . (K_t - K^S_t)|) and its sum of
-squares come from MFMA sums in fp32 over bf16 deviations that the oracle
-reproduces exactly, so they agree to fp32 rounding (relative 1e-4 written
-here). Which tokens enter the set is an integer decision taken from those
-sums: tokens whose oracle score clears the n-th largest by a relative 1e-4
-must be in, those below it by as much must be out, and the set has exactly
-n tokens. Everything after the selection is checked against the oracle
-given the GPU's set: the routing losses within 5e-4 relative (the bf16
-deviations), stored rows within 1 ulp (fp32 blocks of four: within 2^-21 of
-the channel's largest input), decode within relative L2 1e-2 (bf16) / 1e-5
-(fp32)."""
+The oracle's score s_t (max over probe rows of |q . (K_t - K^S_t)|) is float64.
+The kernel multiplies the probe rows by the deviations rounded to bf16 (MFMA,
+exact products, fp32 sums), so its score is within
+    bound_t = (2^-9 + 2^-16) max_q sum_c |q_c| |dev_c|
+of the oracle's (the bf16 rounding moves each deviation by at most 2^-9 of
+itself; the fp32 sum of d = 128 products adds at most d 2^-24).  Which tokens
+enter the set is an integer decision on those scores: the kernel's set is
+exactly the top n of its own scores (ties to the lower token), tokens whose
+oracle score clears the n-th largest by more than twice the largest bound are
+in, those below it by as much are out, and the number of tokens whose
+membership differs from the oracle's set inside that band is reported.
+Everything after the selection is checked against the oracle given the GPU's
+set: the routing losses within 5e-4 relative (the bf16 deviations), stored
+rows within 1 ulp (blocks of four: the fp32 butterfly's 2^-21 of the
+channel's largest input plus one spacing of the storage type), decode within
+relative L2 1e-2 (bf16) / 1e-5 (fp32)."""
 import math
 import sys
 
@@ -20,7 +25,8 @@ import pytest
 import oracle as O
 from synth import WORKLOADS, gen, scaled
 
-from gpu_cases import BYTES, TYPES, _pad, block_of, compare_units, rel_l2, sharpened_queries, ulp_distance, values
+from gpu_cases import (BYTES, TYPES, _pad, block_of, compare_units, quad_value_tol, rel_l2, sharpened_queries,
+                       ulp_distance, values)
 
 pytestmark = pytest.mark.gpu
 
@@ -60,6 +66,40 @@ CASES = {
     "pairs_bf16_short": _tok(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, seq_lens=(37,),
                              n_probe=8, res_ppm=30000, n_needles=1),
 }
+
+
+def score_bound(KB, QB) -> np.ndarray:
+    """Per token, the largest |kernel score - float64 score| the bf16 deviations and
+    fp32 sums allow: (2^-9 + 2^-16) max over probe rows of sum_c |q_c| |dev_c|."""
+    dev = np.abs(O.token_deviations(KB))                     # [B][T][d]
+    QB = np.abs(np.asarray(QB, np.float64))
+    out = np.zeros(dev.shape[1])
+    for l in range(dev.shape[0]):
+        out = np.maximum(out, (QB[l].reshape(-1, QB.shape[-1]) @ dev[l].T).max(axis=0))
+    return (2.0 ** -9 + 2.0 ** -16) * out
+
+
+def check_token_set(S, got_s, ref_s, bound, n, what) -> int:
+    """A kernel token set against the oracle's scores: exactly n tokens, ascending, the top
+    n of the kernel's own scores (ties to the lower token); tokens whose oracle score
+    clears the n-th largest by more than twice the largest bound are in, those below it
+    by as much out.  Returns how many tokens differ from the oracle's own set."""
+    S = np.asarray(S, np.int64)
+    T = len(ref_s)
+    assert S.size == n, (what, S.size, n)
+    assert np.all(np.diff(S) > 0), what
+    np.testing.assert_array_equal(S, O.residual_tokens(got_s, n), err_msg=str(what))
+    if n == 0:
+        return 0
+    inside = np.zeros(T, bool)
+    inside[S] = True
+    tau = np.sort(ref_s)[::-1][n - 1]
+    band = 2.0 * bound.max()
+    assert not np.any((ref_s > tau + band) & ~inside), what
+    assert not np.any((ref_s < tau - band) & inside), what
+    want = np.zeros(T, bool)
+    want[O.residual_tokens(ref_s, n)] = True
+    return int((inside != want).sum())
 
 
 def unpack_tok_unit(buf, off, mode, T, d, ppm, dtype, B):
@@ -106,15 +146,18 @@ def test_token_residual_parity(torch_dev, name):
     got_err = err.cpu().numpy().astype(np.float64)
     got_s = scores.cpu().numpy().astype(np.float64)
 
-    # scores against the oracle's, unit by unit
+    # scores against the oracle's, unit by unit, within the bf16-deviation bound
     ref_s = np.zeros((w.n_blocks, H, T))
+    bound = np.zeros((w.n_blocks, H, T))
     for b, (f, B) in enumerate(w.blocks):
         for h in range(H):
-            s, _ = O.token_scores(K[f:f + B, h], Q[f:f + B, h * G:(h + 1) * G])
-            ref_s[b, h] = s
-    rel = np.abs(got_s - ref_s) / np.maximum(ref_s, 1e-30)
-    log(f"  scores: max rel error {rel.max():.2e}")
-    assert rel.max() <= 1e-4
+            QB = Q[f:f + B, h * G:(h + 1) * G]
+            ref_s[b, h], _ = O.token_scores(K[f:f + B, h], QB)
+            bound[b, h] = score_bound(K[f:f + B, h], QB)
+    err = np.abs(got_s - ref_s)
+    log(f"  scores: max error / bound {(err / np.maximum(bound, 1e-30)).max():.3f}, "
+        f"max rel error {(err / np.maximum(ref_s, 1e-30)).max():.2e}")
+    assert np.all(err <= bound)
 
     # modes: every unit residual except a few, so the compressed sets get checked everywhere
     modes = np.full((w.n_blocks, H), O.RESIDUAL, np.uint8)
@@ -125,18 +168,14 @@ def test_token_residual_parity(torch_dev, name):
     torch.cuda.synchronize()
     buf = cache.host_bytes()
     units = {}
+    band_diff = 0
     for b, (f, B) in enumerate(w.blocks):
         for h in range(H):
             m = int(modes[b, h])
             got, counts = unpack_tok_unit(buf, int(cache.offsets_host[0, b, h]), m, T, d, ppm, w.dtype, B)
             if m == O.RESIDUAL:
                 S = got["TS"]
-                assert S.size == n, (b, h, S.size, n)
-                tau = np.sort(ref_s[b, h])[::-1][n - 1] if n else np.inf
-                inside = np.zeros(T, bool)
-                inside[S] = True
-                assert not np.any((ref_s[b, h] > tau * (1 + 1e-4)) & ~inside)
-                assert not np.any((ref_s[b, h] < tau * (1 - 1e-4)) & inside)
+                band_diff += check_token_set(S, got_s[b, h], ref_s[b, h], bound[b, h], n, (b, h))
                 chunk_starts = np.arange(0, T, 128)
                 np.testing.assert_array_equal(counts[:-1], np.searchsorted(S, chunk_starts))
                 assert counts[-1] == n
@@ -145,9 +184,9 @@ def test_token_residual_parity(torch_dev, name):
                     compare_units({key: got[key]}, {key: ref[key]}, w.dtype,
                                   inputs=(K[f:f + B, h], V[f:f + B, h]) if B == 4 else None)
                 for key, X in (("HK", K), ("HV", V)):
-                    if B == 4 and w.dtype == "f32":
+                    if B == 4:
                         mag = np.abs(X[f:f + B, h][:, S]).max(axis=0)[:, None, :]
-                        assert np.all(np.abs(got[key] - ref[key]) <= 2.0 ** -21 * mag + np.abs(ref[key]) * 2.0 ** -23)
+                        assert np.all(np.abs(got[key] - ref[key]) <= quad_value_tol(ref[key], mag, TYPES[w.dtype][1]))
                     else:
                         assert ulp_distance(got[key], ref[key], TYPES[w.dtype][1]).max(initial=0) <= 1, key
                 # routing losses, given the GPU's set
@@ -162,7 +201,8 @@ def test_token_residual_parity(torch_dev, name):
                 units[(b, h)] = ref
             else:
                 units[(b, h)] = O.compress_unit_tokens(K[f:f + B, h], V[f:f + B, h], m, None, w.dtype)
-    log(f"  compress ok: every set has {n} tokens, rows within 1 ulp, losses within 5e-4")
+    log(f"  compress ok: every set has {n} tokens ({band_diff} tokens differ from the oracle's sets, all inside "
+        f"the bound), rows within 1 ulp, losses within 5e-4")
 
     tol = 1e-5 if w.dtype == "f32" else 1e-2
     worst = 0.0

@@ -361,6 +361,32 @@ def test_route_limits():
     assert (O.route(E, om, 1e30) == O.SHARED).all()
 
 
+def test_route_breakpoint_ties_go_to_the_cheaper_mode():
+    """At lambda equal to a unit's breakpoint its two modes cost the same, and the
+    tie rule gives the cheaper one, even where E_a + lam O_a and E_b + lam O_b
+    evaluated in floating point round apart (cases searched for below)."""
+    rng = np.random.default_rng(151)
+    om = O.omega(128, 16, "bf16")
+    rounded_apart = 0
+    for _ in range(4000):
+        E = np.array([rng.uniform(1, 100), 0.0, 0.0])
+        E[1] = E[0] * rng.uniform(0.2, 0.8)
+        for a, b in ((0, 1), (1, 2), (0, 2)):
+            lam = (E[a] - E[b]) / (om[b] - om[a])
+            if not lam > 0:
+                continue
+            ca, cb = E[a] + lam * om[a], E[b] + lam * om[b]
+            rounded_apart += ca != cb
+            # with only modes a and b competing (the third priced out), the tie goes to a
+            E2 = E.copy()
+            third = 3 - a - b
+            E2[third] = 1e300
+            assert int(O.route(E2[None], om, lam)[0]) == a, (E, a, b, lam)
+            # a hair below the breakpoint the costlier, more accurate mode wins
+            assert int(O.route(E2[None], om, np.nextafter(lam, 0.0))[0]) == b
+    assert rounded_apart > 0          # the floating-point costs do break some of these ties
+
+
 def test_route_budget_minimal_lambda_brute_force():
     rng = np.random.default_rng(16)
     T, d, k = 1000, 64, 8
@@ -488,14 +514,14 @@ def test_block_schedules():
 
 
 def test_dct4_keys_are_coefficient_magnitudes():
-    # the float32 butterfly agrees with scipy's orthonormal DCT-II to float32 rounding
+    # the keys are |Z_j| of scipy's orthonormal DCT-II along the layer axis, to float64 rounding
     rng = np.random.default_rng(21)
     X = O.round_bf16(rng.standard_normal((4, 50, 16)) * 3.0)
     key = O.residual_keys_dct4(X)
-    assert key.dtype == np.float32 and key.shape == (50, 16, 3)
+    assert key.dtype == np.float64 and key.shape == (50, 16, 3)
     ref = np.abs(np.moveaxis(scipy.fft.dct(X, type=2, norm="ortho", axis=0)[1:], 0, -1))
-    bound = 1e-6 * np.abs(X).max(axis=0)[..., None]
-    assert np.all(np.abs(key.astype(np.float64) - ref) <= bound)
+    bound = 1e-14 * np.abs(X).max(axis=0)[..., None]
+    assert np.all(np.abs(key - ref) <= bound)
 
 
 def test_dct4_codes_brute_force():
@@ -718,6 +744,31 @@ def test_tail_is_exact_attention():
     assert np.all(O.decode_spans([], np.zeros((0, d)), np.zeros((0, d)), 0, q, 0.3, d) == 0.0)
 
 
+def test_refresh_routes_a_hand_worked_span():
+    """One token, d = 4, k = 1, a probe row of ones in both layers: x0 = (2, 1, 0, 0),
+    x1 = 0.  D = (1, 1/2, 0, 0); the shared reconstruction misses -+D, so each
+    layer's logit error is (1 + 1/2) / sqrt(4) = 3/4 and E_S = 9/16; the residual
+    keeps channel 0 and misses -+(0, 1/2, 0, 0): E_R = (1/4)^2 = 1/16.  bf16,
+    d = 4, k = 1: Omega = (16, 16 + 2 (1 + 2), 32) / 32 = (1/2, 11/16, 1).
+    Breakpoints: R|E at (1/16) / (5/16) = 1/5, S|R at (1/2) / (3/16) = 8/3, so
+    exact below 1/5, residual up to 8/3, shared above (ties to the cheaper)."""
+    K = np.zeros((2, 1, 4))
+    K[0, 0] = [2.0, 1.0, 0.0, 0.0]
+    Q = np.ones((2, 1, 1, 4))
+    np.testing.assert_allclose(O.routing_errors(K, Q, 1), [9 / 16, 1 / 16, 0.0], rtol=0, atol=1e-15)
+    np.testing.assert_array_equal(O.omega(4, 1, "bf16"), [0.5, 11 / 16, 1.0])
+    om = O.omega(4, 1, "bf16")
+    lam_re = (1 / 16 - 0.0) / (om[2] - om[1])
+    lam_sr = (9 / 16 - 1 / 16) / (om[1] - om[0])
+    want = [(0.0, O.EXACT), (0.1, O.EXACT), (lam_re, O.RESIDUAL), (1.0, O.RESIDUAL), (2.5, O.RESIDUAL),
+            (lam_sr, O.SHARED), (3.0, O.SHARED), (math.inf, O.SHARED)]
+    for lam, m in want:
+        assert O.refresh_modes(K, Q, 1, "bf16", lam) == m, (lam, m)
+    # a block of four with the same deviations in its four layers' halves routes by Omega of B = 4
+    om4 = O.omega(4, 1, "bf16", 4)
+    np.testing.assert_array_equal(om4, [16 / 64, (16 + 2 * (2 + 2)) / 64, 1.0])
+
+
 def test_refresh_routes_the_span():
     rng = np.random.default_rng(45)
     X = rng.standard_normal((9, 16))
@@ -733,8 +784,8 @@ def test_refresh_routes_the_span():
 # ---------------------------------------------------------------- token-level residual set
 @pytest.mark.parametrize("B", [2, 4])
 def test_token_score_is_the_shared_logit_change(B):
-    """s_t = max over probe rows of |q . (K_t - K^S_t)| (the paper's score), up to the bf16
-    rounding of the deviations; e_t sums the squares, so sum_t e_t / (B G P d) is E_S."""
+    """s_t = max over probe rows of |q . (K_t - K^S_t)| (the paper's score); e_t sums the
+    squares, so sum_t e_t / (B G P d) is E_S."""
     rng = np.random.default_rng(50 + B)
     T, d, G, P = 40, 16, 2, 3
     K = O.round_bf16(rng.standard_normal((B, T, d)))
@@ -750,22 +801,20 @@ def test_token_score_is_the_shared_logit_change(B):
                     v = sum(Q[l, g, p, c] * (K[l, t, c] - Ks[l, t, c]) for c in range(d))
                     brute_s[t] = max(brute_s[t], abs(v))
                     brute_e[t] += v * v
-    np.testing.assert_allclose(s, brute_s, rtol=2 ** -7, atol=1e-12)
-    np.testing.assert_allclose(e, brute_e, rtol=2 ** -6, atol=1e-12)
+    np.testing.assert_allclose(s, brute_s, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(e, brute_e, rtol=1e-12, atol=1e-12)
     E = O.routing_errors(K, Q, 0)
-    np.testing.assert_allclose(e.sum() / (B * G * P * d), E[O.SHARED], rtol=2 ** -6)
+    np.testing.assert_allclose(e.sum() / (B * G * P * d), E[O.SHARED], rtol=1e-12)
 
 
-def test_token_deviation_precision():
-    # pairs: bf16(fl32(x0 - x1) * 0.5); fours: bf16(fl32(x_l - fl32(((x0+x3)+(x1+x2)) * 0.25)))
-    x = np.array([[1.0, 3.0], [1.0 + 2 ** -7, -5.0]], np.float32)[:, None, :]     # [2][1][2]
+def test_token_deviations_are_exact_differences():
+    # pairs: x0 - M = (x0 - x1) / 2 and its negation; fours: x_l minus the four-layer mean, exactly
+    x = np.array([[1.0, 3.0], [1.0 + 2 ** -7, -5.0]])[:, None, :]     # [2][1][2]
     dev = O.token_deviations(x)
-    want = O.round_bf16(np.float64((np.float32(1.0) - np.float32(1.0 + 2 ** -7)) * np.float32(0.5)))
-    assert dev[0, 0, 0] == want and dev[1, 0, 0] == -want and dev[0, 0, 1] == 4.0
-    X4 = np.array([1.0, 2.0, 4.0, 1.0 + 2 ** -20], np.float32)[:, None, None]
-    x4 = X4[:, 0, 0]
-    M = np.float32((np.float32(x4[0] + x4[3]) + np.float32(x4[1] + x4[2])) * np.float32(0.25))
-    np.testing.assert_array_equal(O.token_deviations(X4)[:, 0, 0], O.round_bf16((x4 - M).astype(np.float64)))
+    assert dev[0, 0, 0] == -2 ** -8 and dev[1, 0, 0] == 2 ** -8 and dev[0, 0, 1] == 4.0 and dev[1, 0, 1] == -4.0
+    X4 = np.array([1.0, 2.0, 4.0, 1.0 + 2 ** -20])[:, None, None]
+    M = (8.0 + 2 ** -20) / 4
+    np.testing.assert_array_equal(O.token_deviations(X4)[:, 0, 0], X4[:, 0, 0] - M)
 
 
 def test_residual_tokens_brute_force():
