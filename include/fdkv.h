@@ -124,7 +124,8 @@ typedef struct {
 /* Message for a status code (static storage). */
 const char* fdkv_status_string(int32_t status);
 
-/* Text of the last FDKV_E_HIP failure in the calling thread ("" if none). */
+/* Text of the last failure in the calling thread that carries a message (every
+ * FDKV_E_HIP, and FDKV_E_WORKSPACE from fdkv_decode_attn_static); "" if none. */
 const char* fdkv_last_error(void);
 
 /*
@@ -232,6 +233,30 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
                              int32_t max_seq_len, const uint8_t* modes, const uint64_t* seg_offsets,
                              const void* cache, int32_t layer, const void* q, void* out,
                              float sm_scale, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * fdkv_decode_attn_static - device.  fdkv_decode_attn for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same computation and arguments
+ * without the workspace.  Its split-K records live in a static device array
+ * of the library, fdkv_decode_static_scratch_bytes() bytes (16 MiB), one per
+ * GPU, held until the process ends; the call itself allocates nothing.
+ *   Returns FDKV_E_WORKSPACE (message in fdkv_last_error) when the call needs
+ *   more than that, i.e. fdkv_decode_workspace(dims, batch, max_seq_len) >
+ *   fdkv_decode_static_scratch_bytes(): batch x Hkv x ceil(max_seq_len / 512) x
+ *   G x (d + 4) x 4 bytes (the 8B shape at 32k tokens needs 1 MiB, the 70B shape
+ *   at 131k tokens 8.3 MiB).
+ * Every call on one GPU shares that GPU's array (the current device's), which
+ * keeps the last call's records: calls that overlap on one GPU (on different
+ * streams, or from different host threads without ordering) race and must
+ * not be issued.  Nothing in the array needs clearing between calls: each
+ * call writes every record it reads.
+ */
+size_t fdkv_decode_static_scratch_bytes(void);
+fdkv_status fdkv_decode_attn_static(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens,
+                                    int32_t max_seq_len, const uint8_t* modes, const uint64_t* seg_offsets,
+                                    const void* cache, int32_t layer, const void* q, void* out, float sm_scale,
+                                    void* stream);
 
 /*
  * Generation (the end of Section 3's method): routing is decided once after

@@ -24,7 +24,8 @@ STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: 
 
 SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
            "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
-           "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans")
+           "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans", "fdkv_decode_static_scratch_bytes",
+           "fdkv_decode_attn_static")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 RES_CHANNELS, RES_TOKENS = 0, 1  # residual kinds (fdkv_residual)
 
@@ -33,7 +34,7 @@ class FdkvError(RuntimeError):
     def __init__(self, status: int, where: str):
         lib = load()
         msg = lib.fdkv_status_string(status).decode()
-        if status == -5:
+        if status == -5 or (status == -3 and "static" in where):
             msg += ": " + lib.fdkv_last_error().decode()
         super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
         self.status = status
@@ -89,6 +90,10 @@ def load():
     lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_decode_attn.restype = I32
     lib.fdkv_decode_attn.argtypes = [DP, I32, P, I32, P, P, P, I32, P, P, ctypes.c_float, P, SZ, P]
+    lib.fdkv_decode_static_scratch_bytes.restype = SZ
+    lib.fdkv_decode_static_scratch_bytes.argtypes = []
+    lib.fdkv_decode_attn_static.restype = I32
+    lib.fdkv_decode_attn_static.argtypes = [DP, I32, P, I32, P, P, P, I32, P, P, ctypes.c_float, P]
     lib.fdkv_append.restype = I32
     lib.fdkv_append.argtypes = [DP, I32, P, I32, P, P, P, P, P]
     lib.fdkv_decode_spans_workspace.restype = I32
@@ -202,6 +207,19 @@ def decode_attn(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offs
                                    _dev(seg_offsets), _dev(cache), int(layer), _dev(q), _dev(out),
                                    ctypes.c_float(sm_scale), _dev(ws), int(ws.numel() * ws.element_size()),
                                    _stream(stream)), "fdkv_decode_attn")
+
+
+def decode_static_scratch_bytes() -> int:
+    """Bytes of the static device scratch behind fdkv_decode_attn_static."""
+    return int(load().fdkv_decode_static_scratch_bytes())
+
+
+def decode_attn_static(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offsets, cache, layer: int, q,
+                       out, sm_scale: float, stream=None):
+    """Queue fdkv_decode_attn_static for one layer (no workspace: the library's static scratch)."""
+    _check(load().fdkv_decode_attn_static(ctypes.byref(d), int(batch), _dev(seq_lens), int(max_seq_len), _dev(modes),
+                                          _dev(seg_offsets), _dev(cache), int(layer), _dev(q), _dev(out),
+                                          ctypes.c_float(sm_scale), _stream(stream)), "fdkv_decode_attn_static")
 
 
 def decode_attn_raw(d: Dims, batch: int, seq_lens_ptr: int, max_seq_len: int, modes_ptr: int, offs_ptr: int,

@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -153,6 +154,42 @@ ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
 }
 
 uint64_t decode_chunks(int max_T) { return (uint64_t)(max_T + kDecodeWgTokens - 1) / kDecodeWgTokens; }
+
+// The split-K records of fdkv_decode_attn_static live in this file-scope
+// device array, one copy per GPU, held until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is only a
+// stand-in for the symbol): each device's address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kStaticScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+fdkv_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    g_last_error = std::string("hipGetDevice: ") + hipGetErrorString(e);
+    return FDKV_E_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    g_last_error = "fdkv_decode_attn_static: device index beyond the static scratch table";
+    return FDKV_E_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      g_last_error = std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e);
+      return FDKV_E_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FDKV_OK;
+}
 
 }  // namespace
 
@@ -603,6 +640,30 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
   if (max_seq_len < 0) return FDKV_E_INVALID_ARG;
   fdkv_span sp{seq_lens, max_seq_len, modes, seg_offsets, cache};
   return fdkv_decode_spans(dims, batch, 1, &sp, nullptr, layer, q, out, sm_scale, ws, ws_bytes, stream);
+}
+
+size_t fdkv_decode_static_scratch_bytes(void) { return kStaticScratchBytes; }
+
+fdkv_status fdkv_decode_attn_static(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens,
+                                    int32_t max_seq_len, const uint8_t* modes, const uint64_t* seg_offsets,
+                                    const void* cache, int32_t layer, const void* q, void* out, float sm_scale,
+                                    void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (max_seq_len < 0) return FDKV_E_INVALID_ARG;
+  size_t need = 0;
+  st = fdkv_decode_workspace(dims, batch, max_seq_len, &need);
+  if (st != FDKV_OK) return st;
+  if (need > kStaticScratchBytes) {
+    g_last_error = "fdkv_decode_attn_static: this call needs " + std::to_string(need) +
+                   " bytes of split-K records; the static scratch holds " + std::to_string(kStaticScratchBytes);
+    return FDKV_E_WORKSPACE;
+  }
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
+  if (st != FDKV_OK) return st;
+  return fdkv_decode_attn(dims, batch, seq_lens, max_seq_len, modes, seg_offsets, cache, layer, q, out, sm_scale, ws,
+                          kStaticScratchBytes, stream);
 }
 
 }  // extern "C"

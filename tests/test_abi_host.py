@@ -276,3 +276,19 @@ def test_tokens_validation(lib):
         assert lib.fdkv_blocks(ctypes.byref(bad), ctypes.byref(n), None, None) == -1
     bad = B.dims(4, 2, 4, 64, 0, "bf16", B.PAIRS, 2, 0)
     assert lib.fdkv_blocks(ctypes.byref(bad), ctypes.byref(n), None, None) == -1
+
+
+def test_static_decode_checks_its_scratch_on_the_host(lib):
+    """fdkv_decode_attn_static refuses a call whose split-K records exceed its static
+    scratch, and bad dimensions, before any HIP call (the fake pointers are never used)."""
+    fake = ctypes.c_void_p(1 << 20)
+    big = B.dims(2, 8, 64, 128, 16, "bf16")
+    need = ctypes.c_size_t(0)
+    assert lib.fdkv_decode_workspace(ctypes.byref(big), 4, 131072, ctypes.byref(need)) == 0
+    assert need.value > lib.fdkv_decode_static_scratch_bytes() == 16 << 20
+    st = lib.fdkv_decode_attn_static(ctypes.byref(big), 4, fake, 131072, fake, fake, fake, 0, fake, fake,
+                                     ctypes.c_float(0.1), None)
+    assert st == -3 and b"static scratch" in lib.fdkv_last_error()
+    bad = B.dims(2, 8, 64, 96, 16, "bf16")
+    assert lib.fdkv_decode_attn_static(ctypes.byref(bad), 1, fake, 100, fake, fake, fake, 0, fake, fake,
+                                       ctypes.c_float(0.1), None) == -2
