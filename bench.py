@@ -162,16 +162,21 @@ def main():
         if args.traffic_json and args.calibrate_copy_mib > 0 and cal_f:
             n = args.calibrate_copy_mib << 20
             fs, ws_ = n / cal_f, n / cal_w
-            dec = [k for k in fetch if "decode" in k]
-            fb = sum(sum(v for v, _ in fetch[k]) / len(fetch[k]) for k in dec) * fs
-            wb = sum(sum(v for v, _ in write[k]) / len(write[k]) for k in dec if k in write) * ws_
+            def per_dispatch(names):
+                fb = sum(sum(v for v, _ in fetch[k]) / len(fetch[k]) for k in names) * fs
+                wb = sum(sum(v for v, _ in write[k]) / len(write[k]) for k in names if k in write) * ws_
+                return fb, wb
+            dec = [k for k in fetch if "decode_stream" in k or "decode_splitk" in k]   # the split-K launch
+            mrg = [k for k in fetch if "decode_merge" in k]
+            fb, wb = per_dispatch(dec)
+            mf, mw = per_dispatch(mrg)
             rec = {"source_hash": kernel_source_hash(), "bytes_per_launch": fb + wb, "fetch_bytes": fb,
-                   "write_bytes": wb, "kernels": dec, "fetch_scale": fs, "write_scale": ws_,
-                   "calibration_bytes": n}
+                   "write_bytes": wb, "kernels": dec, "combine_bytes": mf + mw, "fetch_scale": fs,
+                   "write_scale": ws_, "calibration_bytes": n}
             with open(args.traffic_json, "w") as f:
                 json.dump(rec, f, indent=1)
-            print(f"decode launch traffic: fetch {fb / 1e6:.2f} MB + write {wb / 1e6:.2f} MB per layer call "
-                  f"(scales {fs:.4f}, {ws_:.4f})")
+            print(f"split-K launch traffic: fetch {fb / 1e6:.2f} MB + write {wb / 1e6:.2f} MB per layer; combine "
+                  f"{(mf + mw) / 1e6:.3f} MB (scales {fs:.4f}, {ws_:.4f})")
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the compressed-KV path here has no multi-GPU leg "
@@ -290,25 +295,61 @@ def main():
         torch.cuda.synchronize()
         step_ms = ev0.elapsed_time(ev1) / args.steps
 
-        # per-launch timing of the layer call, HIP events on the launch stream
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in order]
+        # per-launch timing with HIP events on the launch stream, each phase replayed as a graph of
+        # the step's L launches in cold layer order (every layer's split-K records come from HBM, as
+        # in the step): the split-K launch alone (fdkv_decode_partial: decode_stream_kernel, the
+        # dominant kernel), the combine launch alone (fdkv_decode_combine: decode_merge_kernel);
+        # per launch = the replays' time / (replays x L).  The one-call layer decode is timed eagerly
+        # with events around each call.
+        n_chunks = -(-cache.max_seq_len // 512)
+
+        def split_phase():
+            for layer in order:
+                B.decode_partial(dm, w.batch, cache.seq_lens, cache.max_seq_len, cache.modes, cache.offsets,
+                                 cache.buf, layer, q_static[layer], scale, cache.ws, stream)
+
+        def combine_phase():
+            for layer in order:
+                B.decode_combine(dm, w.batch, n_chunks, out_static[layer], cache.ws, stream)
+
         n_rep = max(3, min(args.steps, 20))
-        launch_ms = np.zeros(L)
+        phase_ms = []
+        for fn in (split_phase, combine_phase):
+            fn()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                fn()
+            for _ in range(2):
+                g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(n_rep):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            phase_ms.append(e0.elapsed_time(e1) / (n_rep * L))
+            del g
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in order]
+        call_ms = np.zeros(L)
         for rep in range(n_rep):
             q_static.copy_(qs[args.warmup + rep % args.steps])
             for j, layer in enumerate(order):
-                evs[j][0].record(stream)
+                ev[j][0].record(stream)
                 cache.decode(layer, q_static[layer], out_static[layer], scale)
-                evs[j][1].record(stream)
+                ev[j][1].record(stream)
             torch.cuda.synchronize()
             for j, layer in enumerate(order):
-                launch_ms[layer] += evs[j][0].elapsed_time(evs[j][1]) / n_rep
-    launch_avg_ms = float(launch_ms.mean())
-    achieved = (bytes_step / L) / (launch_avg_ms * 1e-3) / 1e9
+                call_ms[layer] += ev[j][0].elapsed_time(ev[j][1]) / n_rep
+    split_avg_ms, merge_avg_ms = phase_ms
+    call_avg_ms = float(call_ms.mean())
+    achieved = (bytes_step / L) / (split_avg_ms * 1e-3) / 1e9
     step_gbs = bytes_step / (step_ms * 1e-3) / 1e9
     tokens_per_s = w.batch / (step_ms * 1e-3)
     log(f"[bench] decode step {step_ms * 1e3:.1f} us -> {tokens_per_s:.1f} tok/s, {step_gbs:.0f} GB/s over the step; "
-        f"layer launch {launch_avg_ms * 1e3:.2f} us -> {achieved:.0f} GB/s")
+        f"split-K launch {split_avg_ms * 1e3:.2f} us -> {achieved:.0f} GB/s, combine {merge_avg_ms * 1e3:.2f} us, "
+        f"one-call layer decode {call_avg_ms * 1e3:.2f} us")
 
     # ------------------------------------------------------------ prefill: probe + route + compress
     prefill = None
@@ -363,13 +404,12 @@ def main():
         cmp_read = T * 2 * d * e * L * H                                             # K and V of every layer
         cmp_write = sum(unit_read_bytes(w, int(m), T, nb) * (nb if m == 2 else 1)
                         for m, nb in zip(pmodes.ravel(), usz))                # exact heads copy all nb layers
-        # upper 32x32 tiles of the deviation Gram matrices: 2 per pair, 8 per block of four
-        mfma_flops = sum(T * (d // 32) * (d // 32 + 1) // 2 * (2 if nb == 2 else 8) * (32 * 32 * 2) for nb in usz)
+        # executed MFMA work of the deviation Gram kernels: per 16 tokens, 3 MFMAs (H H^T + H L^T + L H^T of
+        # the bf16 hi/lo split) on each upper 32x32 tile of each matrix, 2 matrices per pair, 8 per block of four
+        mfma_flops = sum(T * (d // 32) * (d // 32 + 1) // 2 * (2 if nb == 2 else 8) * 3 * (32 * 32 * 2) for nb in usz)
         if w.residual == 1:
             # token scores: every probe row of the block's layers against every token's deviation
             mfma_flops = sum(2 * nb * (Hq // H) * P * d * T for nb in usz)
-        G = Hq // H
-        eq2_flops = T * L * H * G * P * d * 2 * 2 * 2                                # literal Eq. 2, 2 modes
         prefill = {
             "workload": "prefill8b" if w.name == "llama8b" else w.name,
             "probe_ms": tp * 1e3, "route_ms": trt * 1e3, "compress_ms": tc * 1e3,
@@ -379,10 +419,12 @@ def main():
             "compress_frac_hbm": (cmp_read + cmp_write) / tc / 1e9 / HBM_PEAK_GBS,
             "probe_read_gbs": L * H * T * d * e / tp / 1e9,
             "probe_mfma_util": mfma_flops / tp / (MFMA_BF16_PEAK_TFLOPS * 1e12),
-            "probe_eq2_equiv_tflops": eq2_flops / tp / 1e12,
+            "probe_mfma_tflop": mfma_flops / 1e12,
             "probe_mode_mix": np.bincount(pmodes.ravel(), minlength=3).tolist(),
             "budget_bytes": int(budget), "lambda": lam,
         }
+        if not args.no_cpu_baseline:
+            prefill["cpu_baseline"] = cpu_baseline_prefill(w, pmodes.reshape(nbk, H), budget)
         log(f"[bench] prefill: probe {tp * 1e3:.2f} ms, route {trt * 1e3:.2f} ms, compress {tc * 1e3:.2f} ms "
             f"({prefill['compress_gbs']:.0f} GB/s), mix {prefill['probe_mode_mix']}")
         del Qp, ws, pcache_buf, tscores
@@ -473,13 +515,60 @@ def main():
         "step_hbm_gbs": step_gbs,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "decode layer launch (decode_stream_kernel + decode_merge_kernel)",
-                     "bytes_per_launch": bytes_step / L, "launch_us": launch_avg_ms * 1e3},
+                     "kernel": "decode_stream_kernel (the split-K launch of a layer, fdkv_decode_partial)",
+                     "bytes_per_launch": bytes_step / L, "launch_us": split_avg_ms * 1e3,
+                     "combine_us": merge_avg_ms * 1e3, "layer_call_us": call_avg_ms * 1e3,
+                     "layer_call_frac": (bytes_step / L) / (call_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "step_frac": step_gbs / HBM_PEAK_GBS},
         "cpu_baseline": cpu,
         "prefill": prefill,
         "generation": generation,
     }
     print(json.dumps(res), flush=True)
+
+
+def cpu_baseline_prefill(w, pmodes, budget):
+    """The oracle's prefill (Eq. 2 probe in its literal form, budget route, compress) timed on a
+    bounded sample of (block, KV head) units and scaled to the whole workload."""
+    import numpy as np
+
+    import oracle as O
+    from synth import gen
+    cores = len(os.sched_getaffinity(0))
+    T, d, k, G = w.seq_lens[0], w.head_dim, w.topk, w.group
+    units = [(b, h) for b in range(w.n_blocks) for h in range(w.n_kv_heads)]
+    pick = []
+    for m in (1, 0, 2):                       # up to three units of each mode the probe chose
+        cand = [u for u in units if pmodes[u] == m]
+        pick += cand[:3]
+    probe_s, comp_s, E = [], {0: [], 1: [], 2: []}, []
+    for (b, h) in pick:
+        K, V, _ = gen.block_segment(w, 0, b, h)
+        f, nb = w.blocks[b]
+        Q = gen.probe_queries(w, 0, layers=list(range(f, f + nb)))[:, h * G:(h + 1) * G]
+        t0 = time.perf_counter()
+        E.append(O.routing_errors(K, Q, k))
+        probe_s.append(time.perf_counter() - t0)
+        m = int(pmodes[b, h])
+        t0 = time.perf_counter()
+        O.compress_unit(K, V, m, k, w.dtype)
+        comp_s[m].append(time.perf_counter() - t0)
+    # the budget search over every unit: the sampled losses, spread by seeded factors
+    rng = np.random.default_rng(0)
+    Eall = np.array([E[i % len(E)] for i in range(len(units))]) * rng.uniform(0.5, 1.5, (len(units), 1))
+    t0 = time.perf_counter()
+    O.route_budget(Eall, T, d, k, w.dtype, budget, [nb for nb in w.block_sizes for _ in range(w.n_kv_heads)])
+    route_s = time.perf_counter() - t0
+    counts = np.bincount(pmodes.ravel(), minlength=3)
+    t_probe = float(np.mean(probe_s)) * len(units)
+    t_comp = float(sum(counts[m] * np.mean(comp_s[m]) for m in comp_s if comp_s[m]))
+    total = t_probe + route_s + t_comp
+    return {"value": T / total, "unit": "compressed tokens/s", "cores": cores, "kind": "oracle",
+            "probe_s": t_probe, "route_s": route_s, "compress_s": t_comp,
+            "sample": f"oracle Eq. 2 (literal logit matrices, fp64) on {len(pick)} (block, KV head) units "
+                      f"({sum(probe_s):.1f}s) scaled to {len(units)}; compress of the same units "
+                      f"({sum(sum(v) for v in comp_s.values()):.1f}s) scaled by the routed mix {counts.tolist()}; budget route "
+                      f"over {len(units)} units ({route_s:.2f}s)"}
 
 
 def cpu_baseline(w, modes):

@@ -235,6 +235,33 @@ fdkv_status fdkv_decode_attn(const fdkv_dims* dims, int32_t batch, const int32_t
                              float sm_scale, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * fdkv_decode_partial / fdkv_decode_combine - device.  The two phases of
+ * fdkv_decode_attn, for callers that merge partial attention results
+ * themselves: a sequence split over several devices runs the partial phase
+ * on each device's tokens, gathers the records and combines them once (the
+ * log-sum-exp merge is associative and order-free).
+ * fdkv_decode_partial takes the arguments of fdkv_decode_attn minus `out`
+ * and writes the split-K records into ws: for every (sequence, KV head,
+ * 512-token chunk) slot and every query head g of the KV head's group, d + 4
+ * floats
+ *   acc[0..d) = sum_t 2^(z_t - m) V~_t,  m = a reference max of z_t,
+ *   l         = sum_t 2^(z_t - m),      then 2 floats of padding,
+ * with z_t = (q . K~_t) sm_scale log2(e) over the chunk's tokens; records are
+ * laid out [batch][Hkv][n_chunks][G][d + 4], n_chunks = ceil(max_seq_len / 512),
+ * and a slot with no tokens holds m = -inf, l = 0, acc = 0.
+ * fdkv_decode_combine merges, per (sequence, query head), the n_chunks records
+ * of ws (the same layout, any n_chunks >= 1):
+ *   o = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i,  M = max_i m_i,
+ * and writes o in the cache type (o = 0 when no slot holds a token).
+ *   ws_bytes >= batch x Hkv x n_chunks x G x (d + 4) x 4 (FDKV_E_WORKSPACE otherwise)
+ */
+fdkv_status fdkv_decode_partial(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, int32_t max_seq_len,
+                                const uint8_t* modes, const uint64_t* seg_offsets, const void* cache, int32_t layer,
+                                const void* q, float sm_scale, void* ws, size_t ws_bytes, void* stream);
+fdkv_status fdkv_decode_combine(const fdkv_dims* dims, int32_t batch, int32_t n_chunks, void* out, const void* ws,
+                                size_t ws_bytes, void* stream);
+
+/*
  * fdkv_decode_attn_static - device.  fdkv_decode_attn for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc): the same computation and arguments

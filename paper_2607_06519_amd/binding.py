@@ -25,7 +25,7 @@ STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: 
 SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
            "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
            "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans", "fdkv_decode_static_scratch_bytes",
-           "fdkv_decode_attn_static")
+           "fdkv_decode_attn_static", "fdkv_decode_partial", "fdkv_decode_combine")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 RES_CHANNELS, RES_TOKENS = 0, 1  # residual kinds (fdkv_residual)
 
@@ -94,6 +94,10 @@ def load():
     lib.fdkv_decode_static_scratch_bytes.argtypes = []
     lib.fdkv_decode_attn_static.restype = I32
     lib.fdkv_decode_attn_static.argtypes = [DP, I32, P, I32, P, P, P, I32, P, P, ctypes.c_float, P]
+    lib.fdkv_decode_partial.restype = I32
+    lib.fdkv_decode_partial.argtypes = [DP, I32, P, I32, P, P, P, I32, P, ctypes.c_float, P, SZ, P]
+    lib.fdkv_decode_combine.restype = I32
+    lib.fdkv_decode_combine.argtypes = [DP, I32, I32, P, P, SZ, P]
     lib.fdkv_append.restype = I32
     lib.fdkv_append.argtypes = [DP, I32, P, I32, P, P, P, P, P]
     lib.fdkv_decode_spans_workspace.restype = I32
@@ -207,6 +211,21 @@ def decode_attn(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offs
                                    _dev(seg_offsets), _dev(cache), int(layer), _dev(q), _dev(out),
                                    ctypes.c_float(sm_scale), _dev(ws), int(ws.numel() * ws.element_size()),
                                    _stream(stream)), "fdkv_decode_attn")
+
+
+def decode_partial(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offsets, cache, layer: int, q,
+                   sm_scale: float, ws, stream=None):
+    """Queue fdkv_decode_partial: the split-K records of one layer into ``ws``."""
+    _check(load().fdkv_decode_partial(ctypes.byref(d), int(batch), _dev(seq_lens), int(max_seq_len), _dev(modes),
+                                      _dev(seg_offsets), _dev(cache), int(layer), _dev(q), ctypes.c_float(sm_scale),
+                                      _dev(ws), int(ws.numel() * ws.element_size()), _stream(stream)),
+           "fdkv_decode_partial")
+
+
+def decode_combine(d: Dims, batch: int, n_chunks: int, out, ws, stream=None):
+    """Queue fdkv_decode_combine: merge ``n_chunks`` records per (sequence, query head) of ``ws`` into ``out``."""
+    _check(load().fdkv_decode_combine(ctypes.byref(d), int(batch), int(n_chunks), _dev(out), _dev(ws),
+                                      int(ws.numel() * ws.element_size()), _stream(stream)), "fdkv_decode_combine")
 
 
 def decode_static_scratch_bytes() -> int:

@@ -61,10 +61,11 @@ __device__ __forceinline__ uint4 ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-// The K and V tile loads: every byte of a plane is read once per decode
-// step, so they carry the non-temporal cache hint (cache policy NT).
+// The K and V tile loads and the residual entries: every byte of a plane is
+// read once per decode step, so they carry the non-temporal cache hint
+// (cache policy NT).
+constexpr int kNonTemporal = 2;
 __device__ __forceinline__ uint4 ld128_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  constexpr int kNonTemporal = 2;
   const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
@@ -155,27 +156,60 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int slot = blockIdx.x % P.n_chunks_total;
-  const int sh = blockIdx.x / P.n_chunks_total;
-  const int head = sh % P.hkv, seq = sh / P.hkv;
+  const int seq = blockIdx.x / P.n_chunks_total / P.hkv;
+  const int rank = blockIdx.x / P.n_chunks_total % P.hkv;
   const int part = MULTI ? decode_part(P, slot) : 0;
   const int wgc = MULTI ? slot - P.part[part].base : slot;
   const bool tail = MULTI && part == P.tail_part;
-  const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
-  // The three per-unit values are fetched together, as scalar loads (the
-  // mode byte through its aligned dword; the array is 4-byte aligned and
-  // padded to a multiple of 4 bytes), and the exit test below reads all of
-  // them: the start-up costs one round trip that does not queue behind other
-  // waves' tile loads.  A segment offset is a multiple of 256 and a mode is at
-  // most kExact; a unit that breaks either reads nothing and writes a record
-  // that turns its query heads' outputs into NaN.
-  // (The exact tail of a generation has no unit arrays: its rows are exact.)
+  // Workgroups are dispatched in index order, and the older of the waves
+  // sharing a SIMD are served first, so the heads of a sequence are taken
+  // in cost order: residual heads (the most bytes per token) first, then
+  // the others, each group in head order.  The per-unit values are fetched
+  // together, as scalar loads, before the exit test reads them: the mode
+  // bytes of the sequence's heads through their aligned words (the array is
+  // 4-byte aligned and padded to a multiple of 4 bytes), every head's
+  // segment offset, and the length; the start-up costs one round trip that
+  // does not queue behind other waves' tile loads.  A segment offset is a
+  // multiple of 256 and a mode is at most kExact; a unit that breaks either
+  // reads nothing and writes a record that turns its query heads' outputs
+  // into NaN.  (The exact tail of a generation has no unit arrays: its rows
+  // are exact.  More than 8 KV heads keep the head order.)
   const int T = P.part[part].lens[seq];
+  int head = rank;
   uint32_t mode_word = (uint32_t)kExact;
   uint64_t seg_off = 0;
   if (!tail) {
-    mode_word = reinterpret_cast<const uint32_t*>(P.part[part].modes)[unit >> 2] >> (8 * (unit & 3));
-    seg_off = P.part[part].seg_off[unit];
+    const uint64_t u0 = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv;
+    const uint32_t* mw = reinterpret_cast<const uint32_t*>(P.part[part].modes);
+    const uint64_t* so = P.part[part].seg_off + u0;
+    if (P.hkv <= 8) {
+      const uint64_t w0 = u0 >> 2, w1 = (u0 + P.hkv - 1) >> 2;
+      const uint32_t a = mw[w0];
+      const uint32_t b = w1 > w0 ? mw[w0 + 1] : 0u;
+      const uint32_t c = w1 > w0 + 1 ? mw[w0 + 2] : 0u;
+      uint64_t offs[8];
+#pragma unroll
+      for (int h = 0; h < 8; ++h) offs[h] = h < P.hkv ? so[h] : 0ull;
+      const int sft = 8 * (int)(u0 & 3);
+      const uint64_t lo = (uint64_t)a | ((uint64_t)b << 32);
+      const uint64_t bytes = sft ? (lo >> sft) | ((uint64_t)c << (64 - sft)) : lo;  // mode of head h at bits 8h
+      uint32_t rmask = 0;
+#pragma unroll
+      for (int h = 0; h < 8; ++h) rmask |= (h < P.hkv && ((bytes >> (8 * h)) & 0xFFu) == (uint64_t)kResidual) << h;
+      const int nr = __builtin_popcount(rmask);
+      uint32_t sel = rank < nr ? rmask : ~rmask & ((1u << P.hkv) - 1u);
+      for (int i = rank < nr ? rank : rank - nr; i > 0; --i) sel &= sel - 1u;  // drop the lower set bits
+      head = __builtin_ctz(sel);
+      mode_word = (uint32_t)(bytes >> (8 * head));
+#pragma unroll
+      for (int h = 0; h < 8; ++h) seg_off = h == head ? offs[h] : seg_off;
+    } else {
+      const uint64_t unit = u0 + head;
+      mode_word = mw[unit >> 2] >> (8 * (unit & 3));
+      seg_off = so[head];
+    }
   }
+  const int sh = seq * P.hkv + head;   // the (sequence, KV head) of the record slots
   const int mode = (int)(mode_word & 0xFFu);
   const int wg_tok0 = wgc * kDecodeWgTokens;
   const bool bad_unit = mode > kExact || (seg_off & 255) != 0;
@@ -294,10 +328,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
-          b.ki[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ikr, ok ? e * 2 : kOob, 0, 0)
-                       : __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, 0);
-          b.kv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vkr, ok ? e : kOob, 0, 0)
-                       : __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, 0);
+          b.ki[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ikr, ok ? e * 2 : kOob, 0, kNonTemporal)
+                       : __builtin_amdgcn_raw_buffer_load_b8(ikr, ok ? e : kOob, 0, kNonTemporal);
+          b.kv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vkr, ok ? e : kOob, 0, kNonTemporal)
+                       : __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, kNonTemporal);
         }
       }
 #pragma unroll
@@ -311,10 +345,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         }
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
-          b.vi[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, ok ? e * 2 : kOob, 0, 0)
-                       : __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, 0);
-          b.vv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vvr, ok ? e : kOob, 0, 0)
-                       : __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, 0);
+          b.vi[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, ok ? e * 2 : kOob, 0, kNonTemporal)
+                       : __builtin_amdgcn_raw_buffer_load_b8(ivr, ok ? e : kOob, 0, kNonTemporal);
+          b.vv[i] = C8 ? __builtin_amdgcn_raw_buffer_load_b8(vvr, ok ? e : kOob, 0, kNonTemporal)
+                       : __builtin_amdgcn_raw_buffer_load_b16(vvr, ok ? e * 2 : kOob, 0, kNonTemporal);
         }
       }
     };

@@ -545,16 +545,24 @@ fdkv_status fdkv_append(const fdkv_dims* dims, int32_t batch, const int32_t* pos
   return FDKV_OK;
 }
 
-fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_spans, const fdkv_span* spans,
-                              const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale,
-                              void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Decode phases: the split-K pass that writes the records, the merge of the records into the outputs.
+enum : int { kPhaseSplit = 1, kPhaseMerge = 2 };
+
+fdkv_status decode_impl(const fdkv_dims* dims, int32_t batch, int32_t n_spans, const fdkv_span* spans,
+                        const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale, void* ws,
+                        size_t ws_bytes, void* stream, int phases) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   const int n_parts = n_spans + (tail ? 1 : 0);
   if (batch < 1 || n_spans < 0 || n_parts > kMaxParts || (n_spans > 0 && !spans) || layer < 0 ||
       layer >= dims->n_layers)
     return FDKV_E_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(out, 16) || !aligned(ws, 16) || !isfinite(sm_scale)) return FDKV_E_INVALID_ARG;
+  if (!aligned(q, 16) || ((phases & kPhaseMerge) && !aligned(out, 16)) || !aligned(ws, 16) || !isfinite(sm_scale))
+    return FDKV_E_INVALID_ARG;
   const uint64_t row = (uint64_t)dims->head_dim * elem_bytes(dims);
   int32_t maxes[kMaxParts];
   for (int i = 0; i < n_spans; ++i) {
@@ -623,11 +631,56 @@ fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_sp
     p.tail_cap = tail->cap;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (total > 0) {
+  if (total > 0 && (phases & kPhaseSplit)) {
     const hipError_t e = launch_decode(p, s);
     if (e != hipSuccess) return hip_fail(e, "decode");
   }
-  const hipError_t e = launch_decode_merge(p, s);
+  if (phases & kPhaseMerge) {
+    const hipError_t e = launch_decode_merge(p, s);
+    if (e != hipSuccess) return hip_fail(e, "decode_merge");
+  }
+  return FDKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_spans, const fdkv_span* spans,
+                              const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale,
+                              void* ws, size_t ws_bytes, void* stream) {
+  return decode_impl(dims, batch, n_spans, spans, tail, layer, q, out, sm_scale, ws, ws_bytes, stream,
+                     kPhaseSplit | kPhaseMerge);
+}
+
+fdkv_status fdkv_decode_partial(const fdkv_dims* dims, int32_t batch, const int32_t* seq_lens, int32_t max_seq_len,
+                                const uint8_t* modes, const uint64_t* seg_offsets, const void* cache, int32_t layer,
+                                const void* q, float sm_scale, void* ws, size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (max_seq_len < 0) return FDKV_E_INVALID_ARG;
+  fdkv_span sp{seq_lens, max_seq_len, modes, seg_offsets, cache};
+  return decode_impl(dims, batch, 1, &sp, nullptr, layer, q, nullptr, sm_scale, ws, ws_bytes, stream, kPhaseSplit);
+}
+
+fdkv_status fdkv_decode_combine(const fdkv_dims* dims, int32_t batch, int32_t n_chunks, void* out, const void* ws,
+                                size_t ws_bytes, void* stream) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (batch < 1 || n_chunks < 1 || !aligned(out, 16) || !aligned(ws, 16)) return FDKV_E_INVALID_ARG;
+  const uint64_t G = dims->n_q_heads / dims->n_kv_heads;
+  const uint64_t need = (uint64_t)batch * dims->n_kv_heads * n_chunks * G * (dims->head_dim + 4) * 4;
+  if (ws_bytes < need) return FDKV_E_WORKSPACE;
+  DecodeParams p{};
+  p.out = out;
+  p.ws = static_cast<float*>(const_cast<void*>(ws));
+  p.hkv = dims->n_kv_heads;
+  p.hq = dims->n_q_heads;
+  p.d = dims->head_dim;
+  p.batch = batch;
+  p.bf16 = dims->dtype != FDKV_F32;
+  p.n_chunks_total = n_chunks;
+  const hipError_t e = launch_decode_merge(p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_merge");
   return FDKV_OK;
 }

@@ -45,9 +45,9 @@ def test_trace_summary_means(tmp_path):
 
 def test_pmc_summary_scales_by_the_calibration_copy(tmp_path):
     # The calibration copy of 1 MiB reads 512 KiB and writes 1024 KiB by the counters: the
-    # fetch scale is 2 and the write scale 1.  Per layer call the decode kernels fetch
-    # 1000 + 10 KiB and write 5 KiB (counter units), so the call moves
-    # (1010 * 2 + 5) * 1024 bytes.
+    # fetch scale is 2 and the write scale 1.  Per layer the split-K kernel fetches 1000 KiB
+    # and writes 5 KiB (counter units), so its launch moves (1000 * 2 + 5) * 1024 bytes; the
+    # combine kernel's 10 KiB are recorded apart.
     f, w, out = tmp_path / "f.csv", tmp_path / "w.csv", tmp_path / "traffic.json"
     _write_counters(f, "FETCH_SIZE", [("__amd_rocclr_copyBuffer", 512.0), ("decode_stream_kernel", 1000.0),
                                       ("decode_stream_kernel", 1000.0), ("decode_merge_kernel", 10.0)])
@@ -57,5 +57,6 @@ def test_pmc_summary_scales_by_the_calibration_copy(tmp_path):
     assert r.returncode == 0, r.stderr
     rec = json.loads(out.read_text())
     assert rec["fetch_scale"] == 2.0 and rec["write_scale"] == 1.0
-    assert rec["bytes_per_launch"] == (1010 * 2 + 5) * 1024
-    assert sorted(rec["kernels"]) == ["decode_merge_kernel", "decode_stream_kernel"]
+    assert rec["bytes_per_launch"] == (1000 * 2 + 5) * 1024
+    assert rec["combine_bytes"] == 10 * 2 * 1024
+    assert rec["kernels"] == ["decode_stream_kernel"]

@@ -302,3 +302,107 @@ def test_probe_deterministic(torch_dev):
     a, _ = probe(dm, w.seq_lens[0], kl, ql, w.n_probe)
     b, _ = probe(dm, w.seq_lens[0], kl, ql, w.n_probe)
     assert torch_dev.equal(a, b)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_invalid_unit_gives_nan(torch_dev, dtype):
+    """A unit whose mode is above exact or whose segment offset is not a multiple of 256
+    is not read: its query heads' outputs come out NaN, every other head is unaffected."""
+    torch = torch_dev
+    from paper_2607_06519_amd.cache import to_device
+    w = scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=4, n_q_heads=8, seq_lens=(600,), n_needles=2, dtype=dtype)
+    K, V = gen.layer_cache(w, 0)
+    modes = np.array([[0, 1, 2, 1]], np.uint8)
+    cache, keep = _run_compress(w, modes[None], [K], [V])
+    ref = _oracle_units(w, K, V, modes)
+    q = gen.decode_queries(w, 0, scale=8.0)
+    tol = 1e-5 if dtype == "f32" else 1e-2
+    good_modes, good_offs = cache.modes.clone(), cache.offsets.clone()
+    for bad in ("mode", "offset"):
+        cache.modes.copy_(good_modes)
+        cache.offsets.copy_(good_offs)
+        if bad == "mode":
+            cache.modes[0, 0, 1] = 3
+        else:
+            cache.offsets[0, 0, 2] += 16
+        for layer in range(2):
+            out = cache.decode(layer, to_device(q[layer], dtype)).float().cpu().numpy()[0]
+            want = oracle_decode_layer(ref, modes, layer, q[layer][0].astype(np.float64), w)
+            badh = 1 if bad == "mode" else 2
+            for hq in range(w.n_q_heads):
+                if hq // w.group == badh:
+                    assert np.all(np.isnan(out[hq])), (bad, layer, hq)
+                else:
+                    assert rel_l2(out[hq], want[hq]) <= tol, (bad, layer, hq)
+    cache.modes.copy_(good_modes)
+    cache.offsets.copy_(good_offs)
+    log("  invalid units give NaN, the other heads match the oracle")
+
+
+def test_partial_and_combine(torch_dev):
+    """fdkv_decode_partial followed by fdkv_decode_combine equals fdkv_decode_attn bit for bit;
+    and a sequence split in two token ranges, each compressed on its own and run through the
+    partial phase separately (as two devices would), combines from the concatenated records into
+    the oracle's attention over the whole sequence (the sequence-split merge of the records)."""
+    torch = torch_dev
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache, to_device
+    w = scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=4, n_q_heads=16, seq_lens=(1300, 900), n_needles=3)
+    H, G, d = w.n_kv_heads, w.group, w.head_dim
+    scale = 1.0 / math.sqrt(d)
+    modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
+    modes[:, 0, :3] = [0, 1, 2]
+    Ks, Vs = [], []
+    for s, T in enumerate(w.seq_lens):
+        K, V = gen.layer_cache(scaled(w, seq_lens=(T,)), 0)
+        Ks.append(K)
+        Vs.append(V)
+    whole, keep = _run_compress(w, modes, Ks, Vs)
+    qs = gen.decode_queries(w, 2, scale=8.0)
+    # the two phases against the one call
+    for layer in range(2):
+        q = to_device(qs[layer], w.dtype)
+        want = whole.decode(layer, q).clone()
+        ws = torch.zeros_like(whole.ws)
+        B.decode_partial(whole.dims, whole.batch, whole.seq_lens, whole.max_seq_len, whole.modes, whole.offsets,
+                         whole.buf, layer, q, scale, ws)
+        got = torch.empty_like(want)
+        B.decode_combine(whole.dims, whole.batch, -(-whole.max_seq_len // 512), got, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(got, want), layer
+    # a sequence split at token 700 / 500: two caches of the token ranges, records concatenated per head
+    cut = (700, 500)
+    parts = []
+    for lo_hi in ((0, cut), (cut, None)):
+        lens = tuple((c if lo_hi[0] == 0 else T - c) for T, c in zip(w.seq_lens, cut))
+        sub = [(K[:, :, :c] if lo_hi[0] == 0 else K[:, :, c:], V[:, :, :c] if lo_hi[0] == 0 else V[:, :, c:])
+               for K, V, c in zip(Ks, Vs, cut)]
+        wp = scaled(w, seq_lens=lens)
+        cache, kp = _run_compress(wp, modes, [a for a, _ in sub], [b for _, b in sub])
+        parts.append((wp, cache, kp, sub))
+    for layer in range(2):
+        q = to_device(qs[layer], w.dtype)
+        recs = []
+        for wp, cache, _, _ in parts:
+            n = -(-wp.max_seq_len // 512)
+            ws = torch.zeros(w.batch * H * n * G * (d + 4), dtype=torch.float32, device="cuda")
+            B.decode_partial(cache.dims, cache.batch, cache.seq_lens, cache.max_seq_len, cache.modes,
+                             cache.offsets, cache.buf, layer, q, scale, ws)
+            recs.append(ws.view(w.batch, H, n, G * (d + 4)))
+        cat = torch.cat(recs, dim=2).contiguous()
+        out = torch.empty((w.batch, w.n_q_heads, d), dtype=torch.bfloat16, device="cuda")
+        B.decode_combine(B.dims(**w.dims()), w.batch, cat.shape[2], out, cat.view(-1))
+        got = out.float().cpu().numpy()
+        for s in range(w.batch):
+            for h in range(H):
+                spans = []
+                for wp, _, _, sub in parts:
+                    Kp, Vp = sub[s]
+                    m = int(modes[s, 0, h])
+                    spans.append((O.compress_unit(Kp[0:2, h], Vp[0:2, h], m, w.topk, w.dtype), m, 2))
+                ref = O.decode_spans(spans, np.zeros((0, d)), np.zeros((0, d)), layer,
+                                     qs[layer][s, h * G:(h + 1) * G].astype(np.float64), scale, d)
+                for g in range(G):
+                    e = rel_l2(got[s, h * G + g], ref[g])
+                    assert e <= 1e-2, (layer, s, h, g, e)
+    log("  partial + combine equal the one call; a sequence split in two ranges combines to the oracle")

@@ -61,10 +61,16 @@ CASES = {
     "quads_f32_g1": _tok(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=2, seq_lens=(600,), n_probe=24,
                          res_ppm=70000, schedule=2),
     # degenerate sets: none (r = 0), and a handful of tokens in a sequence shorter than one chunk
-    "pairs_f32_empty": _tok(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, seq_lens=(200,), n_probe=16,
+    "pairs_f32_empty": _tok(WORKLOADS["tiny"], n_layers=2, n_kv_heads=3, n_q_heads=6, seq_lens=(200,), n_probe=16,
                             res_ppm=0),
-    "pairs_bf16_short": _tok(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, seq_lens=(37,),
+    "pairs_bf16_short": _tok(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=3, n_q_heads=6, seq_lens=(37,),
                              n_probe=8, res_ppm=30000, n_needles=1),
+    # every token in the set (each tile of the streaming pass fully masked before any logit),
+    # and a one-token sequence whose only token is in the set
+    "pairs_bf16_all": _tok(WORKLOADS["prefill8b"], n_layers=2, n_kv_heads=3, n_q_heads=6, seq_lens=(300,),
+                           n_probe=8, res_ppm=1000000, n_needles=1),
+    "quads_e4m3_t1": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=3, n_q_heads=12, seq_lens=(1,),
+                          n_probe=8, res_ppm=50000, n_needles=1, schedule=2, dtype="bf16_e4m3"),
 }
 
 
@@ -196,7 +202,8 @@ def test_token_residual_parity(torch_dev, name):
                 contrib = sum(np.sum((Qh[l].reshape(-1, d) @ (Ks[l, S] - K[f + l, h, S]).T) ** 2) / (P * d)
                               for l in range(B)) / (B * G)
                 want = np.array([E[O.SHARED], E[O.SHARED] - contrib])
-                relE = np.abs(got_err[b, h] - want) / np.abs(want)
+                # a set of every token leaves E_R = 0: compare it on the scale of E_S
+                relE = np.abs(got_err[b, h] - want) / np.maximum(np.abs(want), 1e-6 * abs(want[0]) + 1e-30)
                 assert relE.max() <= 5e-4, (b, h, got_err[b, h], want)
                 units[(b, h)] = ref
             else:
