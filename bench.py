@@ -73,6 +73,11 @@ def bytes_per_token(mode, d, k, e, c, B=2):
     return 2 * d * c if mode == 0 else 2 * d * c + 2 * k * ((1 if B == 2 else 2) + c)
 
 
+def unit_ppm(w, byte):
+    """The token-level set's fraction (ppm) of a unit with mode byte ``byte``."""
+    return w.res_rates[(int(byte) >> 2) & 7] if w.res_rates else w.res_ppm
+
+
 def unit_read_bytes(w, mode, T, B):
     """Algorithmic bytes one decode layer reads from one (block, KV head) unit of T
     tokens.  With token-level residual sets a residual unit is read as its two
@@ -80,9 +85,11 @@ def unit_read_bytes(w, mode, T, B):
     word per 128 tokens, plus the total) and every high-frequency row of its n
     tokens (B - 1 rows of K and of V each)."""
     d, e, c = w.head_dim, w.elem_bytes, w.coef_bytes
+    ppm = unit_ppm(w, mode)
+    mode &= 3                                    # bits 2-4 of a mode byte: the routed fraction
     if w.residual != 1 or mode != 1:
         return T * bytes_per_token(mode, d, w.topk, e, c, B)
-    n = (T * w.res_ppm + 999999) // 1000000
+    n = (T * ppm + 999999) // 1000000
     return T * 2 * d * c + -(-T // 32) * 4 + (-(-T // 128) + 1) * 4 + n * 2 * (B - 1) * d * c
 
 
@@ -227,17 +234,27 @@ def main():
         del src, dst
 
     modes = np.stack([gen.fixed_modes(w, s) for s in range(w.batch)])
+    all_scores = []
+    if w.residual == 1:                         # token-level sets need the probe's token scores
+        for s in range(w.batch):
+            qp = [torch.from_numpy(gen.probe_queries(w, s, layers=[l])[0]).to(dev).to(tdt) for l in range(L)]
+            errs, scores = probe(dm, w.seq_lens[s], [Ks[s][l] for l in range(L)], qp, w.n_probe)
+            if w.res_rates:
+                # fractions routed per residual head: the probe's losses under the budget of the seeded mix
+                # with every residual head at the middle candidate fraction
+                mid = np.where(modes[s] == 1, 1 | ((len(w.res_rates) // 2) << 2), modes[s]).astype(np.uint8)
+                _, budget = B.layout(dm, [w.seq_lens[s]], mid[None])
+                modes[s], _, _ = B.route(dm, w.seq_lens[s], errs.cpu().numpy(), budget_bytes=budget,
+                                         allow_infeasible=True)
+            all_scores.append(scores)
+            del qp
     cache = CompressedCache(dm, w.seq_lens, modes)
     for s in range(w.batch):
-        scores = None
-        if w.residual == 1:                     # token-level sets need the probe's token scores
-            qp = [torch.from_numpy(gen.probe_queries(w, s, layers=[l])[0]).to(dev).to(tdt) for l in range(L)]
-            _, scores = probe(dm, w.seq_lens[s], [Ks[s][l] for l in range(L)], qp, w.n_probe)
-            del qp
+        scores = all_scores[s] if all_scores else None
         cache.compress(s, [Ks[s][l] for l in range(L)], [Vs[s][l] for l in range(L)], token_scores=scores)
-        del scores
+    del all_scores
     torch.cuda.synchronize()
-    log(f"[bench] compressed cache: {cache.total_bytes / 1e9:.3f} GB, mix {np.bincount(modes.ravel(), minlength=3).tolist()}")
+    log(f"[bench] compressed cache: {cache.total_bytes / 1e9:.3f} GB, mix {np.bincount(modes.ravel() & 3, minlength=3).tolist()}")
 
     # algorithmic bytes per layer launch: sum over (seq, KV head) of T * bytes per token of the head's mode
     block_of = {l: (b, l - f, nb) for b, (f, nb) in enumerate(w.blocks) for l in range(f, f + nb)}
@@ -365,7 +382,7 @@ def main():
         _, budget = B.layout(dm, [T], gen.fixed_modes(w, 0)[None])   # footprint of the 50/35/15 mix
         nbk = w.n_blocks
         ws = torch.empty(B.probe_workspace(dm, T, P), dtype=torch.uint8, device=dev)
-        err = torch.empty((nbk, H, 2), dtype=torch.float32, device=dev)
+        err = torch.empty((nbk, H, dm.n_err), dtype=torch.float32, device=dev)
         tscores = torch.empty((nbk, H, T), dtype=torch.float32, device=dev) if w.residual == 1 else None
         _, all_exact = B.layout(dm, [T], np.full((1, nbk, H), 2, np.uint8))
         pcache_buf = torch.empty(all_exact, dtype=torch.uint8, device=dev)
@@ -402,7 +419,7 @@ def main():
         units = nbk * H
         usz = [nb for nb in w.block_sizes for _ in range(H)]
         cmp_read = T * 2 * d * e * L * H                                             # K and V of every layer
-        cmp_write = sum(unit_read_bytes(w, int(m), T, nb) * (nb if m == 2 else 1)
+        cmp_write = sum(unit_read_bytes(w, int(m), T, nb) * (nb if (m & 3) == 2 else 1)
                         for m, nb in zip(pmodes.ravel(), usz))                # exact heads copy all nb layers
         # executed MFMA work of the deviation Gram kernels: per 16 tokens, 3 MFMAs (H H^T + H L^T + L H^T of
         # the bf16 hi/lo split) on each upper 32x32 tile of each matrix, 2 matrices per pair, 8 per block of four
@@ -420,7 +437,7 @@ def main():
             "probe_read_gbs": L * H * T * d * e / tp / 1e9,
             "probe_mfma_util": mfma_flops / tp / (MFMA_BF16_PEAK_TFLOPS * 1e12),
             "probe_mfma_tflop": mfma_flops / 1e12,
-            "probe_mode_mix": np.bincount(pmodes.ravel(), minlength=3).tolist(),
+            "probe_mode_mix": np.bincount(pmodes.ravel() & 3, minlength=3).tolist(),
             "budget_bytes": int(budget), "lambda": lam,
         }
         if not args.no_cpu_baseline:
@@ -500,12 +517,17 @@ def main():
     traffic = load_traffic(w.name)
     cfg = {"workload": w.name, "n_layers": L, "n_kv_heads": H, "n_q_heads": Hq, "head_dim": d, "topk": k,
            "batch": w.batch, "seq_len": w.max_seq_len, "block_sizes": list(w.block_sizes),
-           "mode_mix": np.bincount(modes.ravel(), minlength=3).tolist(),
+           "mode_mix": np.bincount(modes.ravel() & 3, minlength=3).tolist(),
            "layer_order": args.order, "graph": graph is not None, "cache_gb": cache.total_bytes / 1e9,
            "bytes_per_step": bytes_step}
     if w.residual == 1:
         cfg["residual"] = "token set"
-        cfg["residual_fraction"] = w.res_ppm / 1e6
+        if w.res_rates:
+            rb = modes.ravel()[(modes.ravel() & 3) == 1] >> 2
+            cfg["residual_fractions"] = [r / 1e6 for r in w.res_rates]
+            cfg["residual_fraction_mix"] = np.bincount(rb, minlength=len(w.res_rates)).tolist()
+        else:
+            cfg["residual_fraction"] = w.res_ppm / 1e6
     res = {
         "metric": "compressed-KV decode attn tokens/s + achieved HBM GB/s vs 8 TB/s, 32k ctx",
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -539,7 +561,7 @@ def cpu_baseline_prefill(w, pmodes, budget):
     units = [(b, h) for b in range(w.n_blocks) for h in range(w.n_kv_heads)]
     pick = []
     for m in (1, 0, 2):                       # up to three units of each mode the probe chose
-        cand = [u for u in units if pmodes[u] == m]
+        cand = [u for u in units if (int(pmodes[u]) & 3) == m]
         pick += cand[:3]
     probe_s, comp_s, E = [], {0: [], 1: [], 2: []}, []
     for (b, h) in pick:
@@ -549,7 +571,7 @@ def cpu_baseline_prefill(w, pmodes, budget):
         t0 = time.perf_counter()
         E.append(O.routing_errors(K, Q, k))
         probe_s.append(time.perf_counter() - t0)
-        m = int(pmodes[b, h])
+        m = int(pmodes[b, h]) & 3
         t0 = time.perf_counter()
         O.compress_unit(K, V, m, k, w.dtype)
         comp_s[m].append(time.perf_counter() - t0)
@@ -559,7 +581,7 @@ def cpu_baseline_prefill(w, pmodes, budget):
     t0 = time.perf_counter()
     O.route_budget(Eall, T, d, k, w.dtype, budget, [nb for nb in w.block_sizes for _ in range(w.n_kv_heads)])
     route_s = time.perf_counter() - t0
-    counts = np.bincount(pmodes.ravel(), minlength=3)
+    counts = np.bincount(pmodes.ravel() & 3, minlength=3)
     t_probe = float(np.mean(probe_s)) * len(units)
     t_comp = float(sum(counts[m] * np.mean(comp_s[m]) for m in comp_s if comp_s[m]))
     total = t_probe + route_s + t_comp
@@ -588,20 +610,20 @@ def cpu_baseline(w, modes):
     flat = [(b, h) for b in range(w.n_blocks) for h in range(w.n_kv_heads)]
     pick = []
     for m in (0, 1, 2):
-        cand = [u for u in flat if modes[u] == m]
+        cand = [u for u in flat if (int(modes[u]) & 3) == m]
         pick += [cand[i] for i in rng.choice(len(cand), size=min(4, len(cand)), replace=False)]
     n_steps = 14                        # about 10 s of oracle work on the 8B shape
     elapsed, n_calls = 0.0, 0
     for (b, h) in pick:
         K, V, _ = gen.block_segment(w, 0, b, h)
         f, nb = w.blocks[b]
-        m = int(modes[b, h])
+        m = int(modes[b, h]) & 3
         if w.residual == 1:
             tokens = None
             if m == 1:                  # the set the probe picks (selection is prefill work, not timed)
                 QB = gen.probe_queries(w, 0, layers=list(range(f, f + nb)))[:, h * G:(h + 1) * G]
                 sc, _ = O.token_scores(K, QB)
-                tokens = O.residual_tokens(sc, O.n_residual_tokens(K.shape[1], w.res_ppm))
+                tokens = O.residual_tokens(sc, O.n_residual_tokens(K.shape[1], unit_ppm(w, modes[b, h])))
             unit = O.compress_unit_tokens(K, V, m, tokens, w.dtype)
             dec = O.decode_unit_tokens
         else:

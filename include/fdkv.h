@@ -36,7 +36,8 @@
  *  - dims.residual = FDKV_RES_TOKENS switches residual heads to the
  *    paper's token-level set (Section 3, after Eq. 2): every high-frequency
  *    coefficient (pairs: D; fours: Z_1..Z_3) of the n = ceil(r T) tokens,
- *    r = res_ppm / 10^6, with the largest score
+ *    r = res_ppm / 10^6 (or, with dims.n_rates > 0, the unit's own fraction
+ *    r_j = rates_ppm[j] / 10^6, j given by its mode byte), with the largest score
  *      s_t = max over the probe rows q of every layer of the block and every
  *            query head of the group of |q . (K_t - K^S_t)|,
  *    K - K^S computed in fp32 on the stored inputs and rounded to bf16 (pairs:
@@ -87,7 +88,11 @@ typedef enum {
   FDKV_E_HIP = -5          /* a HIP runtime call failed (see fdkv_last_error) */
 } fdkv_status;
 
-/* Head modes, in increasing memory cost; ties in routing go to the lower value. */
+/* Head modes, in increasing memory cost; ties in routing go to the lower value.
+ * A unit's mode byte holds the mode in bits 0-1; with token-level sets whose
+ * fraction is routed per unit (dims.n_rates > 0) a residual unit's byte also
+ * holds, in bits 2-4, the index j of its fraction rates_ppm[j].  Every other
+ * byte is invalid. */
 typedef enum { FDKV_SHARED = 0, FDKV_RESIDUAL = 1, FDKV_EXACT = 2 } fdkv_mode;
 
 /*
@@ -119,6 +124,9 @@ typedef struct {
   int32_t schedule;   /* fdkv_schedule */
   int32_t residual;   /* fdkv_residual */
   int32_t res_ppm;    /* FDKV_RES_TOKENS: the set's fraction of tokens, 0..10^6 parts per million */
+  int32_t n_rates;    /* FDKV_RES_TOKENS: 0, every residual head keeps res_ppm of its tokens; 1..8, each
+                         residual head keeps one of rates_ppm[0..n_rates), chosen by fdkv_route */
+  int32_t rates_ppm[8]; /* the candidate fractions, strictly increasing, 0..10^6 */
 } fdkv_dims;
 
 /* Message for a status code (static storage). */
@@ -151,18 +159,23 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
 /*
  * fdkv_route - host only.  Mode choice of Eq. (3), m = argmin E_m + lambda * Omega(m)
  * with Eq. (2)'s loss, and the budget rule that raises lambda until the cache
- * fits (end of Section 3).
+ * fits (end of Section 3).  With routed fractions (dims.n_rates = J > 0) the
+ * residual mode at each fraction r_j is a candidate of its own (loss E_R(r_j),
+ * Omega of its bytes), so each residual unit also gets its fraction (Section
+ * 3: r_{b,h} chosen by the routing loss budget).
  *   seq_len      tokens of the sequence (for the footprint)
  *   errors       host [n_blocks][Hkv][2]   E_shared, E_residual per unit
- *                                          (E_exact = 0), as written by fdkv_probe
+ *                                          (E_exact = 0), as written by fdkv_probe;
+ *                with routed fractions [n_blocks][Hkv][1 + J]: E_shared, E_residual(r_0..r_{J-1})
  *   lambda       penalty used when budget_bytes == 0
  *   budget_bytes 0: route with `lambda`.  Otherwise: the smallest lambda among
  *                0, the per-unit breakpoints (E_i - E_j)/(Omega_j - Omega_i)
  *                and +inf whose fdkv_layout footprint is <= budget_bytes.
- *   modes_out    host [n_blocks][Hkv]   out
+ *   modes_out    host [n_blocks][Hkv]   out: mode bytes
  *   lambda_out   host, may be NULL out: lambda used (+inf when infeasible)
  * Omega(m) = bytes per token of mode m / bytes per token of EXACT, for the
- * unit's block size.  Ties go to the cheaper mode.  Returns FDKV_E_BUDGET (modes all SHARED) when even
+ * unit's block size.  Ties go to the cheaper candidate; two candidates are
+ * compared through their breakpoint, so at a lambda equal to it the tie is exact.  Returns FDKV_E_BUDGET (modes all SHARED) when even
  * all-shared exceeds the budget.
  */
 fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* errors, double lambda,
@@ -181,7 +194,8 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
  *   k_layers   host array of L device pointers, layer l holds K_l [Hkv][T][d]
  *   qp_layers  host array of L device pointers, layer l holds Q_l [Hq][P][d]
  *   n_probe    P >= 1 probe rows per query head
- *   errors_out device float [n_blocks][Hkv][2]
+ *   errors_out device float [n_blocks][Hkv][2], or [n_blocks][Hkv][1 + J] with J = dims.n_rates > 0
+ *              routed fractions (E_residual at each)
  *   token_scores_out  FDKV_RES_TOKENS: device float [n_blocks][Hkv][T], out: s_t
  *                     (the residual loss then keeps the top ceil(r T) tokens); else unused
  *   ws         device workspace of >= fdkv_probe_workspace() bytes

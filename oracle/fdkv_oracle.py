@@ -65,6 +65,10 @@ Readings of the paper adopted here (the paper leaves these open):
   query head of the group; ``r`` is one fraction per cache (parts per
   million), ``n = ceil(r T)``, ties to the lower token; the stored rows are
   the unrounded coefficients rounded to the coefficient type;
+* with several candidate fractions, each residual (block, head) takes its own
+  fraction: every fraction is one more candidate of Eq. (3)'s argmin (its
+  loss E_R(r) and its Omega), and the budget rule runs over all candidates
+  (``route_token_rates``);
 * a refresh re-decides routing only for the tokens it compresses (earlier
   spans keep their modes: a shared head's dropped coefficients cannot be
   recovered), and a span's probe rows are the last decode queries;
@@ -595,6 +599,53 @@ def routing_errors_tokens(KB, QB, ppm: int) -> np.ndarray:
     return out
 
 
+def routing_errors_token_rates(KB, QB, rates_ppm) -> np.ndarray:
+    """Eq. (2) for the shared mode and for the residual mode at every candidate
+    fraction ``r_j`` of tokens: ``[E_S, E_R(r_0), ..., E_R(r_{J-1})]`` (E_E = 0).
+    The paper chooses the fraction of each (block, head) by the routing loss
+    budget (Section 3, after Eq. 2); here each fraction is one more candidate
+    of the argmin of Eq. (3)."""
+    out = [routing_errors_tokens(KB, QB, 0)[SHARED]]
+    for r in rates_ppm:
+        out.append(routing_errors_tokens(KB, QB, int(r))[RESIDUAL])
+    return np.array(out)
+
+
+def token_rate_candidates(d: int, rates_ppm, dtype: str, B: int = 2):
+    """Omega of the candidates ``[shared, residual at r_0 .. r_{J-1}, exact]`` and the
+    mode and fraction index of each (fraction index 0 for shared and exact)."""
+    full = bytes_per_token_tokens(EXACT, d, 0, dtype, B)
+    om = [bytes_per_token_tokens(SHARED, d, 0, dtype, B) / full]
+    om += [bytes_per_token_tokens(RESIDUAL, d, int(r), dtype, B) / full for r in rates_ppm]
+    om.append(1.0)
+    modes = [SHARED] + [RESIDUAL] * len(rates_ppm) + [EXACT]
+    idx = [0] + list(range(len(rates_ppm))) + [0]
+    return np.array(om), modes, idx
+
+
+def route_token_rates(E, T: int, d: int, rates_ppm, dtype: str, lam=None, budget=None, unit_sizes=None):
+    """Routing with the residual fraction chosen per unit (Section 3: r_{b,h} by the
+    routing loss budget): each unit takes the argmin of Eq. (3) over shared, exact and
+    the residual mode at every candidate fraction, at ``lam``, or under the budget rule
+    with ``budget`` bytes.  ``E``: ``[units][1 + J]`` from ``routing_errors_token_rates``.
+    Returns ``(modes, rate_index, lambda, feasible)``."""
+    E = np.asarray(E, dtype=np.float64)
+    n, J = E.shape[0], len(rates_ppm)
+    sizes = [2] * n if unit_sizes is None else [int(B) for B in unit_sizes]
+    Ec = np.concatenate([E, np.zeros((n, 1))], axis=1)                  # exact costs nothing in Eq. 2
+    cands = {B: token_rate_candidates(d, rates_ppm, dtype, B) for B in set(sizes)}
+    om = np.stack([cands[B][0] for B in sizes])
+    if budget is None:
+        ch, lam_used, ok = route(Ec, om, lam), lam, True
+    else:
+        cb = np.array([[unit_bytes_tokens(cands[B][1][c], T, d, int(rates_ppm[cands[B][2][c]]) if c not in (0, J + 1)
+                                          else 0, dtype, B) for c in range(J + 2)] for B in sizes])
+        ch, lam_used, ok = route_budget_candidates(Ec, om, cb, budget)
+    modes = np.array([cands[B][1][c] for B, c in zip(sizes, ch)], dtype=np.uint8)
+    ridx = np.array([cands[B][2][c] for B, c in zip(sizes, ch)], dtype=np.uint8)
+    return modes, ridx, lam_used, ok
+
+
 _TOKEN_MASK_BYTES_PER_TOKEN = 1.0 / 8 + 4.0 / 128   # 1-bit token mask + a uint32 count per 128 tokens
 
 
@@ -792,19 +843,56 @@ def _cheaper_first(m1: int, m2: int, om) -> Tuple[int, int]:
 def route(E, om, lam: float) -> np.ndarray:
     """argmin_m E[u, m] + lam * Omega(m) (Eq. 3), ties to the cheaper mode.
 
-    ``om`` is ``[3]`` or ``[units][3]``.  The three modes are compared in turn,
-    each pair through ``_prefer``.
+    ``E`` is ``[units][C]`` and ``om`` is ``[C]`` or ``[units][C]``: C = 3 for the
+    three modes, or more candidates (the residual mode at several fractions of
+    tokens, ``route_token_rates``).  The candidates are compared in turn, each
+    pair through ``_prefer``; the answer is a candidate index.
     """
-    E = np.asarray(E, dtype=np.float64).reshape(-1, 3)
-    om = np.broadcast_to(np.asarray(om, dtype=np.float64), E.shape)
+    om = np.asarray(om, dtype=np.float64)
+    C = om.shape[-1]
+    E = np.asarray(E, dtype=np.float64).reshape(-1, C)
+    om = np.broadcast_to(om, E.shape)
     out = np.zeros(E.shape[0], dtype=np.uint8)
     for u in range(E.shape[0]):
         best = 0
-        for m in (1, 2):
+        for m in range(1, C):
             a, b = _cheaper_first(best, m, om[u])
             best = a if _prefer(E[u, a], E[u, b], om[u, a], om[u, b], lam) else b
         out[u] = best
     return out
+
+
+def breakpoint_candidates(E, om) -> list:
+    """Every positive finite breakpoint of every unit, between each pair of its candidates."""
+    E = np.asarray(E, dtype=np.float64)
+    om = np.broadcast_to(np.asarray(om, dtype=np.float64), E.shape)
+    C = E.shape[-1]
+    out = set()
+    for u in range(E.shape[0]):
+        for i in range(C):
+            for j in range(i + 1, C):
+                a, b = _cheaper_first(i, j, om[u])
+                if not om[u, b] > om[u, a]:
+                    continue
+                lam = _breakpoint(E[u, a], E[u, b], om[u, a], om[u, b])
+                if lam > 0 and np.isfinite(lam):
+                    out.add(float(lam))
+    return sorted(out)
+
+
+def route_budget_candidates(E, om, cand_bytes, budget: int) -> Tuple[np.ndarray, float, bool]:
+    """The budget rule over any candidate set: the smallest lambda among 0, every
+    breakpoint and +inf whose footprint (the sum of each unit's chosen candidate's
+    bytes, ``cand_bytes`` ``[units][C]``) is within ``budget``.  Returns
+    ``(choices, lambda, feasible)``; infeasible gives each unit's cheapest candidate."""
+    E = np.asarray(E, dtype=np.float64)
+    om = np.broadcast_to(np.asarray(om, dtype=np.float64), E.shape)
+    cand_bytes = np.asarray(cand_bytes)
+    for lam in [0.0] + breakpoint_candidates(E, om) + [math.inf]:
+        ch = route(E, om, lam)
+        if sum(int(cand_bytes[u, c]) for u, c in enumerate(ch)) <= budget:
+            return ch, lam, True
+    return route(E, om, math.inf), math.inf, False
 
 
 def route_budget(E, T: int, d: int, k: int, dtype: str, budget: int,

@@ -43,7 +43,13 @@ class FdkvError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("schedule", ctypes.c_int32), ("residual", ctypes.c_int32), ("res_ppm", ctypes.c_int32)]
+                ("schedule", ctypes.c_int32), ("residual", ctypes.c_int32), ("res_ppm", ctypes.c_int32),
+                ("n_rates", ctypes.c_int32), ("rates_ppm", ctypes.c_int32 * 8)]
+
+    @property
+    def n_err(self) -> int:
+        """Columns of the probe's loss array: E_S, then E_R at each candidate fraction."""
+        return 1 + (self.n_rates if self.residual == RES_TOKENS and self.n_rates else 1)
 
 
 class Span(ctypes.Structure):
@@ -56,9 +62,12 @@ class Tail(ctypes.Structure):
 
 
 def dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dtype, schedule=PAIRS, residual=RES_CHANNELS,
-         res_ppm=0) -> Dims:
+         res_ppm=0, res_rates=()) -> Dims:
+    """``res_rates``: routed candidate fractions (ppm) of token-level sets, at most 8."""
     dt = {"f32": F32, "bf16": BF16, "bf16_e4m3": BF16_E4M3}.get(dtype, dtype)
-    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt, schedule, residual, res_ppm)
+    rates = list(res_rates) + [0] * (8 - len(res_rates))
+    return Dims(n_layers, n_kv_heads, n_q_heads, head_dim, topk, dt, schedule, residual, res_ppm, len(res_rates),
+                (ctypes.c_int32 * 8)(*rates))
 
 
 def load():
@@ -159,7 +168,8 @@ def layout(d: Dims, seq_lens, modes):
 
 
 def route(d: Dims, seq_len: int, errors, lam: float = 0.0, budget_bytes: int = 0, allow_infeasible=False):
-    """``(modes [n_blocks][Hkv] uint8, lambda_used, status)`` from host ``errors [n_blocks][Hkv][2]``."""
+    """``(modes [n_blocks][Hkv] uint8, lambda_used, status)`` from host ``errors [n_blocks][Hkv][n_err]``
+    (the mode bytes carry the routed fraction index of residual units in bits 2-4)."""
     lib = load()
     e = np.ascontiguousarray(errors, dtype=np.float32)
     modes = np.zeros(e.shape[:-1], dtype=np.uint8)

@@ -74,14 +74,14 @@ class CompressedCache:
 
 
 def probe(dims: B.Dims, seq_len: int, k_layers, qp_layers, n_probe: int, stream=None):
-    """Queue fdkv_probe and return the device tensor of errors ``[n_blocks][Hkv][2]`` and the
+    """Queue fdkv_probe and return the device tensor of errors ``[n_blocks][Hkv][n_err]`` and the
     workspace, or, for a token-level residual set, the errors and the token scores
     ``[n_blocks][Hkv][T]``."""
     torch = _torch()
     dev = k_layers[0].device
     ws = torch.empty(B.probe_workspace(dims, seq_len, n_probe), dtype=torch.uint8, device=dev)
     nb = len(B.blocks(dims)[0])
-    err = torch.empty((nb, dims.n_kv_heads, 2), dtype=torch.float32, device=dev)
+    err = torch.empty((nb, dims.n_kv_heads, dims.n_err), dtype=torch.float32, device=dev)
     scores = None
     if dims.residual == B.RES_TOKENS:
         scores = torch.empty((nb, dims.n_kv_heads, seq_len), dtype=torch.float32, device=dev)

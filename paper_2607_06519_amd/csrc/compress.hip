@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
-  const int mode = P.modes[unit];
+  const int mode = mode_of(P.modes[unit]);
   const int T = P.seq_len;
   const uint64_t row_bytes = (uint64_t)D * E;
   const uint64_t head_off = (uint64_t)head * T * row_bytes;
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
   const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && P.modes[unit] != kResidual) return;
+  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
   const int T = P.seq_len, k = P.topk;
   const int lane = threadIdx.x;
   const int tok0 = blockIdx.x * 64;
@@ -317,7 +317,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void re
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
   const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && P.modes[unit] != kResidual) return;
+  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
   const int T = P.seq_len, k = P.topk;
   const int lane = threadIdx.x;
   const int t = blockIdx.x * 64 + lane;
@@ -470,7 +470,7 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
   const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && P.modes[unit] != kResidual) return;
+  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
   const int T = P.seq_len, k = P.topk;
   const int lane = threadIdx.x;
   const int tok0 = blockIdx.x * 64;

@@ -82,9 +82,10 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const int wg_tok0 = wgc * kDecodeWgTokens;
   const uint64_t unit = ((uint64_t)seq * P.n_blocks + P.block) * P.hkv + head;
   // the exact tail of a generation has no unit arrays
-  const int mode = tail ? kExact : P.part[part].modes[unit];
+  const uint32_t mbyte = tail ? (uint32_t)kExact : P.part[part].modes[unit];
+  const int mode = mode_of(mbyte);
   const uint64_t seg_off = tail ? 0 : P.part[part].seg_off[unit];
-  const bool bad_unit = mode > kExact || (seg_off & 255) != 0;
+  const bool bad_unit = !unit_byte_ok(mbyte, P.tokres ? P.n_rates : 0) || (seg_off & 255) != 0;
   if (wg_tok0 >= T || bad_unit) {  // uniform over the workgroup
     // an empty record (m = -inf, l = 0, acc = 0): the merge reads every slot;
     // an invalid unit (mode above exact or a misaligned segment) writes
@@ -206,7 +207,8 @@ __global__ __launch_bounds__(256) void decode_splitk_kernel(DecodeParams P) {
   const uint8_t* hvp = nullptr;
   const uint32_t* tmask = nullptr;
   if (tokres) {
-    const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, P.res_ppm, E, E, P.bsize);
+    const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, unit_ppm(P.res_ppm, P.n_rates, P.rates_ppm, mbyte), E, E,
+                                    P.bsize);
     tmask = reinterpret_cast<const uint32_t*>(seg + Lt.mask);
     tbase = reinterpret_cast<const uint32_t*>(seg + Lt.count)[wtok0 / kTokChunk];
     hkp = seg + Lt.hk;

@@ -195,7 +195,7 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
       const uint64_t bytes = sft ? (lo >> sft) | ((uint64_t)c << (64 - sft)) : lo;  // mode of head h at bits 8h
       uint32_t rmask = 0;
 #pragma unroll
-      for (int h = 0; h < 8; ++h) rmask |= (h < P.hkv && ((bytes >> (8 * h)) & 0xFFu) == (uint64_t)kResidual) << h;
+      for (int h = 0; h < 8; ++h) rmask |= (h < P.hkv && ((bytes >> (8 * h)) & 0xE3u) == (uint64_t)kResidual) << h;
       const int nr = __builtin_popcount(rmask);
       uint32_t sel = rank < nr ? rmask : ~rmask & ((1u << P.hkv) - 1u);
       for (int i = rank < nr ? rank : rank - nr; i > 0; --i) sel &= sel - 1u;  // drop the lower set bits
@@ -210,9 +210,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     }
   }
   const int sh = seq * P.hkv + head;   // the (sequence, KV head) of the record slots
-  const int mode = (int)(mode_word & 0xFFu);
+  const uint32_t mbyte = mode_word & 0xFFu;
+  const int mode = mode_of(mbyte);
   const int wg_tok0 = wgc * kDecodeWgTokens;
-  const bool bad_unit = mode > kExact || (seg_off & 255) != 0;
+  const bool bad_unit = !unit_byte_ok(mbyte, P.tokres ? P.n_rates : 0) || (seg_off & 255) != 0;
   if (wg_tok0 >= T || bad_unit) {
     // no tokens here: an empty record, m = -inf, l = 0, acc = 0, since the
     // merge reads every slot; an invalid unit: m = 0, l = 1, acc = NaN, which
@@ -249,8 +250,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const auto vvr = rsrc(seg + L.vv, (uint64_t)T * k * ce);
   const float w1 = P.wres[0], w2 = P.wres[1], w3 = P.wres[2];
   // token-level residual set: token mask, running counts, rows of the set's tokens
-  const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, P.res_ppm, 2, ce, nb);
-  const uint64_t ntok = residual_token_count((uint64_t)T, P.res_ppm);
+  const int ppm = unit_ppm(P.res_ppm, P.n_rates, P.rates_ppm, mbyte);
+  const TokLayout Lt = tok_layout(mode, (uint64_t)T, D, ppm, 2, ce, nb);
+  const uint64_t ntok = residual_token_count((uint64_t)T, ppm);
   const auto tmr = rsrc(seg + Lt.mask, (uint64_t)(T + 31) / 32 * 4);
   const auto tcr = rsrc(seg + Lt.count, ((uint64_t)(T + kTokChunk - 1) / kTokChunk + 1) * 4);
   const auto hkr = rsrc(seg + Lt.hk, ntok * (uint64_t)(nb - 1) * D * ce);

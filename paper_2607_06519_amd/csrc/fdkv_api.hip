@@ -91,6 +91,11 @@ fdkv_status check_dims(const fdkv_dims* d) {
   if (d->dtype != FDKV_F32 && d->dtype != FDKV_BF16 && d->dtype != FDKV_BF16_E4M3) return FDKV_E_INVALID_ARG;
   if (d->residual != FDKV_RES_CHANNELS && d->residual != FDKV_RES_TOKENS) return FDKV_E_INVALID_ARG;
   if (d->residual == FDKV_RES_TOKENS && (d->res_ppm < 0 || d->res_ppm > 1000000)) return FDKV_E_INVALID_ARG;
+  if (d->n_rates < 0 || d->n_rates > kMaxRates || (d->n_rates > 0 && d->residual != FDKV_RES_TOKENS))
+    return FDKV_E_INVALID_ARG;
+  for (int j = 0; j < d->n_rates; ++j)
+    if (d->rates_ppm[j] < 0 || d->rates_ppm[j] > 1000000 || (j > 0 && d->rates_ppm[j] <= d->rates_ppm[j - 1]))
+      return FDKV_E_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return FDKV_E_UNSUPPORTED;
   const int G = d->n_q_heads / d->n_kv_heads;
   if (G != 1 && G != 2 && G != 4 && G != 8) return FDKV_E_UNSUPPORTED;
@@ -110,21 +115,28 @@ uint64_t bytes_per_token(int mode, int d, int k, int e, int c, int B) {
 
 bool tokens_mode(const fdkv_dims* d) { return d->residual == FDKV_RES_TOKENS; }
 
+// The fraction of tokens of a residual unit's set, from its mode byte.
+int ppm_of(const fdkv_dims* dm, uint32_t byte) { return unit_ppm(dm->res_ppm, dm->n_rates, dm->rates_ppm, byte); }
+
 // Average bytes per token of a mode for Omega: the token-level residual pays
 // r of the (B - 1) high-frequency rows of K and V plus its 1-bit mask and a
 // uint32 count per 128 tokens.
-double omega_bytes(const fdkv_dims* dm, int mode, int B) {
+double omega_bytes(const fdkv_dims* dm, int mode, int B, int ppm) {
   const int d = dm->head_dim, e = elem_bytes(dm), c = coef_bytes(dm);
   if (tokens_mode(dm) && mode == kResidual)
-    return 2.0 * d * c + 2.0 * (B - 1) * d * c * (dm->res_ppm / 1e6) + 1.0 / 8 + 4.0 / kTokChunk;
+    return 2.0 * d * c + 2.0 * (B - 1) * d * c * (ppm / 1e6) + 1.0 / 8 + 4.0 / kTokChunk;
   return (double)bytes_per_token(mode, d, dm->topk, e, c, B);
 }
 
-uint64_t segment_bytes(const fdkv_dims* dm, int mode, uint64_t T, int B) {
+// Bytes of a segment of the unit with mode byte `byte`.
+uint64_t segment_bytes(const fdkv_dims* dm, uint32_t byte, uint64_t T, int B) {
   const int e = elem_bytes(dm), c = coef_bytes(dm);
-  if (tokens_mode(dm)) return tok_layout(mode, T, dm->head_dim, dm->res_ppm, e, c, B).total;
-  return seg_layout(mode, T, dm->head_dim, dm->topk, e, c, B).total;
+  if (tokens_mode(dm)) return tok_layout(mode_of(byte), T, dm->head_dim, ppm_of(dm, byte), e, c, B).total;
+  return seg_layout(mode_of(byte), T, dm->head_dim, dm->topk, e, c, B).total;
 }
+
+// Largest fraction a set of this cache can keep.
+int max_ppm(const fdkv_dims* dm) { return dm->n_rates ? dm->rates_ppm[dm->n_rates - 1] : dm->res_ppm; }
 
 Sched sched_of(const fdkv_dims* d) {
   Sched s{};
@@ -232,7 +244,7 @@ fdkv_status fdkv_layout(const fdkv_dims* dims, int32_t batch, const int32_t* seq
   for (int b = 0; b < batch; ++b) {
     if (seq_lens[b] < 0) return FDKV_E_INVALID_ARG;
     for (int u = 0; u < units; ++u)
-      if (modes[(size_t)b * units + u] > FDKV_EXACT) return FDKV_E_INVALID_ARG;
+      if (!unit_byte_ok(modes[(size_t)b * units + u], tokens_mode(dims) ? dims->n_rates : 0)) return FDKV_E_INVALID_ARG;
   }
   const int e = elem_bytes(dims), c = coef_bytes(dims);
   uint64_t off = 0;
@@ -255,47 +267,56 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   if (budget_bytes == 0 && !(lambda >= 0.0)) return FDKV_E_INVALID_ARG;
   const Sched sch = sched_of(dims);
   const int units = sch.n * dims->n_kv_heads;
-  const int d = dims->head_dim, k = dims->topk, e = elem_bytes(dims), c = coef_bytes(dims);
-  // Omega and segment bytes per block size (index 0: pairs, 1: blocks of four)
-  double omB[2][3];
-  uint64_t segB[2][3];
+  // Candidates of a unit: shared, the residual mode (at every routed fraction,
+  // or at its one fraction), exact.  Per block size: Omega, segment bytes,
+  // mode byte and the column of the errors array that holds the loss (-1: 0).
+  const int J = tokens_mode(dims) && dims->n_rates ? dims->n_rates : 1;
+  const int C = J + 2, stride = 1 + J;
+  double om[2][kMaxRates + 2];
+  uint64_t seg[2][kMaxRates + 2];
+  uint8_t byte[kMaxRates + 2];
+  int col[kMaxRates + 2];
+  for (int c = 0; c < C; ++c) {
+    byte[c] = (uint8_t)(c == 0 ? kShared : c == C - 1 ? kExact : (kResidual | ((J > 1 || dims->n_rates ? c - 1 : 0) << 2)));
+    col[c] = c == C - 1 ? -1 : c;
+  }
   for (int bi = 0; bi < 2; ++bi) {
     const int B = bi ? 4 : 2;
-    const double full = omega_bytes(dims, kExact, B);
-    for (int m = 0; m < 3; ++m) {
-      omB[bi][m] = omega_bytes(dims, m, B) / full;
-      segB[bi][m] = segment_bytes(dims, m, (uint64_t)seq_len, B);
+    const double full = omega_bytes(dims, kExact, B, 0);
+    for (int c = 0; c < C; ++c) {
+      om[bi][c] = omega_bytes(dims, mode_of(byte[c]), B, ppm_of(dims, byte[c])) / full;
+      seg[bi][c] = segment_bytes(dims, byte[c], (uint64_t)seq_len, B);
     }
   }
   auto quad = [&](int u) { return sch.size[u / dims->n_kv_heads] == 4 ? 1 : 0; };
-  // Of two modes, the cheaper one first (equal cost: the lower mode).
-  auto order = [](const double* om, int m1, int m2, int& a, int& b) {
-    const bool first = om[m1] < om[m2] || (om[m1] == om[m2] && m1 < m2);
+  auto loss = [&](int u, int c) { return col[c] < 0 ? 0.0 : (double)errors[(size_t)u * stride + col[c]]; };
+  // Of two candidates, the cheaper one first (equal cost: the lower candidate).
+  auto order = [](const double* o, int m1, int m2, int& a, int& b) {
+    const bool first = o[m1] < o[m2] || (o[m1] == o[m2] && m1 < m2);
     a = first ? m1 : m2;
     b = first ? m2 : m1;
   };
-  // The lambda at which the cheaper mode a and mode b cost the same.
-  auto breakpoint = [](const double* E, const double* om, int a, int b) { return (E[a] - E[b]) / (om[b] - om[a]); };
 
-  // m = argmin E_m + lambda Omega_m, ties to the cheaper mode.  Two modes are
-  // compared through their breakpoint: the cheaper wins iff lambda >= it.  At
-  // a candidate lambda equal to a unit's breakpoint its two modes tie exactly
-  // (the same expression gives both numbers), where the two costs evaluated
-  // in floating point might round apart.
+  // argmin of E_c + lambda Omega_c, ties to the cheaper candidate.  Two
+  // candidates are compared through their breakpoint (E_a - E_b) / (Omega_b -
+  // Omega_a): the cheaper wins iff lambda >= it.  At a candidate lambda equal
+  // to a unit's breakpoint its two candidates tie exactly (the same expression
+  // gives both numbers), where the two costs evaluated in floating point might
+  // round apart.
   auto decide = [&](double lam, uint8_t* out) {
     uint64_t fp = 0;
     for (int u = 0; u < units; ++u) {
-      const double* om = omB[quad(u)];
-      const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
+      const double* o = om[quad(u)];
       int best = 0;
-      for (int m = 1; m < 3; ++m) {
+      for (int c = 1; c < C; ++c) {
         int a, b;
-        order(om, best, m, a, b);
-        const bool cheaper_wins = om[a] == om[b] ? E[a] <= E[b] : lam >= breakpoint(E, om, a, b);
+        order(o, best, c, a, b);
+        const double Ea = loss(u, a), Eb = loss(u, b);
+        const bool cheaper_wins = o[a] == o[b] ? Ea <= Eb : lam >= (Ea - Eb) / (o[b] - o[a]);
         best = cheaper_wins ? a : b;
       }
-      out[u] = (uint8_t)best;
-      fp += segB[quad(u)][best];
+      out[u] = byte[best];
+      fp += seg[quad(u)][best];
     }
     return fp;
   };
@@ -308,14 +329,13 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
   std::vector<double> cands;
   cands.push_back(0.0);
   for (int u = 0; u < units; ++u) {
-    const double* om = omB[quad(u)];
-    const double E[3] = {(double)errors[2 * u], (double)errors[2 * u + 1], 0.0};
-    for (int i = 0; i < 3; ++i)
-      for (int j = i + 1; j < 3; ++j) {
+    const double* o = om[quad(u)];
+    for (int i = 0; i < C; ++i)
+      for (int j = i + 1; j < C; ++j) {
         int a, b;
-        order(om, i, j, a, b);
-        if (!(om[b] > om[a])) continue;
-        const double lam = breakpoint(E, om, a, b);
+        order(o, i, j, a, b);
+        if (!(o[b] > o[a])) continue;
+        const double lam = (loss(u, a) - loss(u, b)) / (o[b] - o[a]);
         if (lam > 0.0 && isfinite(lam)) cands.push_back(lam);
       }
   }
@@ -381,6 +401,8 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
     tp.d = dims->head_dim;
     tp.n_probe = n_probe;
     tp.res_ppm = dims->res_ppm;
+    tp.n_rates = dims->n_rates;
+    for (int j = 0; j < dims->n_rates; ++j) tp.rates_ppm[j] = dims->rates_ppm[j];
     tp.bf16 = dims->dtype != FDKV_F32;
     for (int B = 2; B <= 4; B += 2) {
       tp.bl = blocks_of_size(sch, B);
@@ -480,6 +502,8 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   tp.hq = dims->n_q_heads;
   tp.d = cp.d;
   tp.res_ppm = dims->res_ppm;
+  tp.n_rates = dims->n_rates;
+  for (int j = 0; j < dims->n_rates; ++j) tp.rates_ppm[j] = dims->rates_ppm[j];
   tp.bf16 = cp.bf16;
   tp.coef8 = cp.coef8;
   for (int B = 2; B <= 4; B += 2) {
@@ -572,7 +596,7 @@ fdkv_status decode_impl(const fdkv_dims* dims, int32_t batch, int32_t n_spans, c
       return FDKV_E_INVALID_ARG;
     if ((uint64_t)sp.max_seq_len * row >= (1ull << 31)) return FDKV_E_UNSUPPORTED;
     // the rows of a token-level residual set are addressed with 32-bit offsets too
-    if (tokens_mode(dims) && residual_token_count((uint64_t)sp.max_seq_len, dims->res_ppm) * 3 * row >= (1ull << 31))
+    if (tokens_mode(dims) && residual_token_count((uint64_t)sp.max_seq_len, max_ppm(dims)) * 3 * row >= (1ull << 31))
       return FDKV_E_UNSUPPORTED;
     maxes[i] = sp.max_seq_len;
   }
@@ -608,6 +632,8 @@ fdkv_status decode_impl(const fdkv_dims* dims, int32_t batch, int32_t n_spans, c
   p.coef8 = dims->dtype == FDKV_BF16_E4M3;
   p.tokres = tokens_mode(dims);
   p.res_ppm = dims->res_ppm;
+  p.n_rates = dims->n_rates;
+  for (int j = 0; j < dims->n_rates; ++j) p.rates_ppm[j] = dims->rates_ppm[j];
   // record slots: every part's chunks, spans first, then the tail
   int total = 0;
   for (int i = 0; i < n_parts; ++i) {

@@ -16,6 +16,19 @@ constexpr int kMaxLayers = 256;
 
 enum : int { kShared = 0, kResidual = 1, kExact = 2 };
 
+// A unit's mode byte: bits 0-1 hold the mode; with token-level sets whose
+// fraction is routed per unit, bits 2-4 hold the index of the residual
+// head's fraction among the cache's candidate fractions (0 otherwise).
+constexpr int kMaxRates = 8;
+FDKV_HD int mode_of(uint32_t byte) { return (int)(byte & 3u); }
+FDKV_HD int rate_of(uint32_t byte) { return (int)((byte >> 2) & 7u); }
+// The byte names a mode and, on a residual unit of a cache with n_rates
+// routed fractions, one of them; every other byte is invalid.
+FDKV_HD bool unit_byte_ok(uint32_t byte, int n_rates) {
+  const uint32_t m = byte & 3u, r = byte >> 2;
+  return m <= (uint32_t)kExact && (r == 0 || (m == (uint32_t)kResidual && r < (uint32_t)n_rates));
+}
+
 FDKV_HD float as_f32(uint32_t u) { return __builtin_bit_cast(float, u); }
 FDKV_HD uint32_t as_u32(float f) { return __builtin_bit_cast(uint32_t, f); }
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fdkv_common.h"
+
 namespace fdkv {
 
 constexpr int kMaxPtrLayers = 128;  // layer pointers carried in kernel arguments
@@ -46,8 +48,15 @@ struct TokenParams {
   float* errors;               // [blocks][hkv][2] (probe)
   BlockList bl;
   int seq_len, bsize, hkv, hq, d, n_probe, res_ppm;
+  int n_rates;                 // routed fractions (0: every residual unit keeps res_ppm)
+  int rates_ppm[kMaxRates];
   bool bf16, coef8;
 };
+
+// The fraction of tokens (parts per million) a residual unit's set keeps.
+__host__ __device__ __forceinline__ int unit_ppm(int res_ppm, int n_rates, const int* rates, uint32_t byte) {
+  return n_rates ? rates[rate_of(byte)] : res_ppm;
+}
 
 struct SelectParams {
   const void* k[kMaxPtrLayers];
@@ -82,6 +91,8 @@ struct DecodeParams {
   const void* q;               // [batch][hq][d]
   bool tokres;                 // residual heads hold a token-level residual set
   int res_ppm;
+  int n_rates;                 // routed fractions of the sets (0: every set keeps res_ppm)
+  int rates_ppm[kMaxRates];
   void* out;                   // [batch][hq][d]
   float* ws;                   // records [batch][hkv][n_chunks_total][G][d + 4]
   int block, pos, bsize;       // the layer's block, its position in it, the block size

@@ -253,6 +253,11 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t x, uint32_t* lds16, uint
 
 }  // namespace
 
+// Probe (P.modes null): for every candidate fraction of the cache (res_ppm,
+// or each of the n_rates routed ones) the set's share of the loss, written as
+// errors [unit][1 + J] = E_S, E_R(r_0), ..., E_R(r_{J-1}).  Compress: the set of
+// the unit's own fraction (its mode byte), as the token mask and the running
+// counts.
 __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t scan16[kSelThreads / 64];
@@ -260,10 +265,14 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
   __shared__ double red[kSelThreads / 64][2];
   const int bi = blockIdx.x / P.hkv, head = blockIdx.x % P.hkv;
   const int unit = P.bl.block[bi] * P.hkv + head;
-  if (P.modes && P.modes[unit] != kResidual) return;
+  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
   const int T = P.seq_len, tid = threadIdx.x;
   const uint32_t* key = reinterpret_cast<const uint32_t*>(P.scores + (uint64_t)unit * T);
-  const uint32_t n = (uint32_t)min<uint64_t>(residual_token_count((uint64_t)T, P.res_ppm), (uint64_t)T);
+  const int J = P.modes ? 1 : (P.n_rates ? P.n_rates : 1);
+  for (int jr = 0; jr < J; ++jr) {
+  const int ppm = P.modes ? unit_ppm(P.res_ppm, P.n_rates, P.rates_ppm, P.modes[unit])
+                          : (P.n_rates ? P.rates_ppm[jr] : P.res_ppm);
+  const uint32_t n = (uint32_t)min<uint64_t>(residual_token_count((uint64_t)T, ppm), (uint64_t)T);
 
   // 1. tau = the n-th largest key, need = how many keys equal to tau are taken
   uint32_t prefix = 0, pmask = 0, need = n;
@@ -312,7 +321,7 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
   uint32_t* count_out = nullptr;
   if (P.modes) {
     uint8_t* seg = P.cache + P.seg_off[unit];
-    const TokLayout L = tok_layout(kResidual, (uint64_t)T, P.d, P.res_ppm, P.bf16 ? 2 : 4,
+    const TokLayout L = tok_layout(kResidual, (uint64_t)T, P.d, ppm, P.bf16 ? 2 : 4,
                                    P.bf16 ? (P.coef8 ? 1 : 2) : 4, P.bsize);
     mask_out = reinterpret_cast<uint32_t*>(seg + L.mask);
     count_out = reinterpret_cast<uint32_t*>(seg + L.count);
@@ -365,13 +374,15 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
       red[wave][1] = b;
     }
     __syncthreads();
-    if (tid < 2) {
+    if (tid < 2 && (tid == 1 || jr == 0)) {
       double s = 0.0;
       for (int w = 0; w < kSelThreads / 64; ++w) s += red[w][tid];
       const double norm = (double)P.bsize * (P.hq / P.hkv) * (double)P.n_probe * (double)P.d;
-      P.errors[(uint64_t)unit * 2 + tid] = (float)(s / norm);
+      P.errors[(uint64_t)unit * (1 + J) + (tid ? 1 + jr : 0)] = (float)(s / norm);
     }
+    __syncthreads();  // red, hist and pick are reused by the next fraction
   }
+  }  // fractions
 }
 
 // ---------------------------------------------------------------- rows
@@ -385,12 +396,13 @@ __global__ __launch_bounds__(256) void token_rows_kernel(TokenParams P) {
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
-  if (P.modes[unit] != kResidual) return;
+  if (mode_of(P.modes[unit]) != kResidual) return;
   const int T = P.seq_len, tid = threadIdx.x;
   const bool c8 = BF16 && P.coef8;
   const int CE = c8 ? 1 : E;
   uint8_t* seg = P.cache + P.seg_off[unit];
-  const TokLayout L = tok_layout(kResidual, (uint64_t)T, D, P.res_ppm, E, CE, NB);
+  const TokLayout L = tok_layout(kResidual, (uint64_t)T, D, unit_ppm(P.res_ppm, P.n_rates, P.rates_ppm, P.modes[unit]),
+                                 E, CE, NB);
   const uint32_t* mask = reinterpret_cast<const uint32_t*>(seg + L.mask);
   const uint32_t base = reinterpret_cast<const uint32_t*>(seg + L.count)[chunk];
   const int t0 = chunk * kTokChunk;

@@ -55,6 +55,7 @@ class Workload:
     schedule: int = 0              # layer blocks: 0 pairs, 1 pairs-fours-pairs (first / last four layers in pairs), 2 fours
     residual: int = 0              # residual heads: 0 per-token channel top-k, 1 token-level set
     res_ppm: int = 0               # the token-level set's fraction of tokens (parts per million)
+    res_rates: Tuple[int, ...] = ()  # candidate fractions routed per residual head (ppm), at most 8
     notes: str = field(default="", compare=False)
 
     @property
@@ -109,7 +110,7 @@ class Workload:
         return dict(n_layers=self.n_layers, n_kv_heads=self.n_kv_heads,
                     n_q_heads=self.n_q_heads, head_dim=self.head_dim,
                     topk=self.topk, dtype=self.dtype, schedule=self.schedule,
-                    residual=self.residual, res_ppm=self.res_ppm)
+                    residual=self.residual, res_ppm=self.res_ppm, res_rates=tuple(self.res_rates))
 
 
 def _ragged_lengths(seed: int, cfg_id: int, batch: int, lo: int, hi: int) -> Tuple[int, ...]:
@@ -179,5 +180,11 @@ LLAMA8B_TOKRES = dataclasses.replace(
     LLAMA8B, name="llama8b_tokres", topk=0, residual=1, res_ppm=50000,
     notes="llama8b with token-level residual sets (5% of tokens per residual head)")
 
+# the token-level sets with the fraction chosen per residual head by the routing budget among
+# five candidates (Section 3: r_{b,h} by the routing loss budget)
+LLAMA8B_TOKRATES = dataclasses.replace(
+    LLAMA8B, name="llama8b_tokrates", topk=0, residual=1, res_ppm=0, res_rates=(10000, 25000, 50000, 100000, 200000),
+    notes="llama8b with token-level residual sets whose fraction (1% .. 20%) is routed per residual head")
+
 WORKLOADS = {w.name: w for w in (TINY, LLAMA8B, BATCHED8B, LONG70B, PREFILL8B, LLAMA8B_E4M3, LLAMA8B_MIXED,
-                                 LLAMA8B_TOKRES)}
+                                 LLAMA8B_TOKRES, LLAMA8B_TOKRATES)}

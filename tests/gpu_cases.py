@@ -233,30 +233,25 @@ def cost_margins(E3: np.ndarray, om: np.ndarray, lam: float):
     """The oracle's modes at ``lam`` and each unit's relative cost margin: the
     smallest (cost of another mode - cost of the chosen one) / cost of the chosen
     one (inf when the chosen cost is 0)."""
-    E3 = np.asarray(E3, np.float64).reshape(-1, 3)
-    om = np.broadcast_to(np.asarray(om, np.float64), E3.shape)
+    om = np.asarray(om, np.float64)
+    C = om.shape[-1]
+    E3 = np.asarray(E3, np.float64).reshape(-1, C)
+    om = np.broadcast_to(om, E3.shape)
     modes = O.route(E3, om, lam)
     cost = E3 + lam * om if np.isfinite(lam) else np.where(om == om.min(axis=1, keepdims=True), 0.0, np.inf)
     marg = np.empty(len(E3))
     for u, m in enumerate(modes):
         c = cost[u, m]
-        other = min(cost[u, j] for j in range(3) if j != m)
+        other = min(cost[u, j] for j in range(C) if j != m)
         marg[u] = other / c - 1.0 if c > 0 else np.inf
     return modes, marg
 
 
 def breakpoints(E3: np.ndarray, om: np.ndarray) -> np.ndarray:
-    """Every positive breakpoint (E_a - E_b) / (O_b - O_a), a the cheaper mode, sorted."""
-    E3 = np.asarray(E3, np.float64).reshape(-1, 3)
-    om = np.broadcast_to(np.asarray(om, np.float64), E3.shape)
-    out = []
-    for u in range(len(E3)):
-        for a, b in ((0, 1), (1, 2), (0, 2)):
-            if om[u, b] > om[u, a]:
-                x = (E3[u, a] - E3[u, b]) / (om[u, b] - om[u, a])
-                if x > 0 and np.isfinite(x):
-                    out.append(x)
-    return np.unique(out)
+    """Every positive breakpoint (E_a - E_b) / (O_b - O_a), a the cheaper candidate, sorted."""
+    om = np.asarray(om, np.float64)
+    E3 = np.asarray(E3, np.float64).reshape(-1, om.shape[-1])
+    return np.array(O.breakpoint_candidates(E3, np.broadcast_to(om, E3.shape)))
 
 
 def separated_lambdas(E3: np.ndarray, om: np.ndarray, n: int = 3) -> list:
@@ -270,7 +265,7 @@ def separated_lambdas(E3: np.ndarray, om: np.ndarray, n: int = 3) -> list:
     return [float(0.5 * (bp[i] + bp[i + 1])) for i in idx]
 
 
-def check_modes(got_modes, E3, om, lam: float, what: str = "", exclude=()) -> int:
+def check_modes(got_modes, E3, om, lam: float, what: str = "", exclude=(), near: float = NEAR_TIE) -> int:
     """Head modes bit-exact against the oracle's at ``lam``; units whose oracle
     cost margin is below NEAR_TIE are near-ties, reported and required to be
     absent (``exclude`` lists units tied by construction, e.g. the unit whose
@@ -279,7 +274,8 @@ def check_modes(got_modes, E3, om, lam: float, what: str = "", exclude=()) -> in
     got = np.asarray(got_modes).ravel()
     mask = np.ones(len(want), bool)
     mask[list(exclude)] = False
-    near = np.nonzero(mask & (marg < NEAR_TIE))[0]
+    tie = near
+    near = np.nonzero(mask & (marg < tie))[0]
     print(f"    modes {what} at lambda {lam:.6g}: {int(mask.sum())} units, near-ties {near.tolist()}, "
           f"smallest margin {marg[mask].min(initial=np.inf):.3g}", flush=True)
     assert near.size == 0, (what, lam, near, marg[near])
@@ -288,12 +284,16 @@ def check_modes(got_modes, E3, om, lam: float, what: str = "", exclude=()) -> in
 
 
 def budget_defining_units(E3, om, lam: float) -> list:
-    """Units whose breakpoint equals ``lam`` (their two modes tie there)."""
-    E3 = np.asarray(E3, np.float64).reshape(-1, 3)
-    om = np.broadcast_to(np.asarray(om, np.float64), E3.shape)
+    """Units with a breakpoint equal to ``lam`` (two of their candidates tie there)."""
+    om = np.asarray(om, np.float64)
+    C = om.shape[-1]
+    E3 = np.asarray(E3, np.float64).reshape(-1, C)
+    om = np.broadcast_to(om, E3.shape)
     out = []
     for u in range(len(E3)):
-        for a, b in ((0, 1), (1, 2), (0, 2)):
-            if om[u, b] > om[u, a] and (E3[u, a] - E3[u, b]) / (om[u, b] - om[u, a]) == lam:
-                out.append(u)
+        for i in range(C):
+            for j in range(i + 1, C):
+                a, b = (i, j) if om[u, i] <= om[u, j] else (j, i)
+                if om[u, b] > om[u, a] and (E3[u, a] - E3[u, b]) / (om[u, b] - om[u, a]) == lam:
+                    out.append(u)
     return sorted(set(out))

@@ -292,3 +292,58 @@ def test_static_decode_checks_its_scratch_on_the_host(lib):
     bad = B.dims(2, 8, 64, 96, 16, "bf16")
     assert lib.fdkv_decode_attn_static(ctypes.byref(bad), 1, fake, 100, fake, fake, fake, 0, fake, fake,
                                        ctypes.c_float(0.1), None) == -2
+
+
+def test_route_with_routed_fractions_matches_oracle(lib):
+    """Token-level sets with per-unit fractions: fdkv_route over (mode, fraction) candidates
+    equals the oracle's route_token_rates at several lambdas and under budgets, and
+    fdkv_layout prices each unit at its own fraction."""
+    rng = np.random.default_rng(13)
+    rates = (10000, 50000, 200000)
+    J, T, d = len(rates), 4096, 128
+    dm = B.dims(8, 2, 8, d, 0, "bf16", residual=B.RES_TOKENS, res_rates=rates)
+    n = 4 * 2
+    ES = np.abs(rng.standard_normal(n)).astype(np.float32) * 20
+    ER = (ES[:, None] * np.sort(rng.uniform(0.05, 0.95, (n, J)), axis=1)[:, ::-1]).astype(np.float32)
+    E = np.concatenate([ES[:, None], ER], axis=1)                          # [units][1 + J]
+    for lam in (0.0, 1.0, 5.0, 30.0, 1e9):
+        modes, _, st = B.route(dm, T, E.reshape(4, 2, 1 + J), lam=lam)
+        assert st == 0
+        om_m, om_r, _, _ = O.route_token_rates(E.astype(np.float64), T, d, rates, "bf16", lam=lam)
+        np.testing.assert_array_equal(modes.ravel() & 3, om_m)
+        np.testing.assert_array_equal((modes.ravel() >> 2)[om_m == 1], om_r[om_m == 1])
+        assert np.all((modes.ravel() >> 2)[om_m != 1] == 0)
+    lo = n * O.unit_bytes_tokens(O.SHARED, T, d, 0, "bf16")
+    hi = n * O.unit_bytes_tokens(O.EXACT, T, d, 0, "bf16")
+    for frac in (0.1, 0.3, 0.6):
+        budget = int(lo + frac * (hi - lo))
+        modes, lam, st = B.route(dm, T, E.reshape(4, 2, 1 + J), budget_bytes=budget)
+        om_m, om_r, om_lam, ok = O.route_token_rates(E.astype(np.float64), T, d, rates, "bf16", budget=budget)
+        assert st == 0 and ok and lam == om_lam
+        np.testing.assert_array_equal(modes.ravel() & 3, om_m)
+        np.testing.assert_array_equal((modes.ravel() >> 2)[om_m == 1], om_r[om_m == 1])
+        offs, total = B.layout(dm, [T], modes[None])
+        want = sum(O.unit_bytes_tokens(int(m), T, d, rates[int(r)] if m == 1 else 0, "bf16")
+                   for m, r in zip(om_m, om_r))
+        assert total == want <= budget
+
+
+def test_mode_bytes_are_validated(lib):
+    """A fraction index only on a residual unit of a cache with that many routed fractions."""
+    good = B.dims(2, 1, 1, 64, 0, "bf16", residual=B.RES_TOKENS, res_rates=(10000, 20000))
+    plain = B.dims(2, 1, 1, 64, 4, "bf16")
+    assert B.layout(good, [100], np.array([[[1 | (1 << 2)]]], np.uint8))[1] > 0
+    for dm, byte in ((good, 1 | (2 << 2)), (good, 2 | (1 << 2)), (good, 0 | (1 << 2)), (good, 3),
+                     (plain, 1 | (1 << 2)), (good, 1 | (1 << 5))):
+        total = ctypes.c_uint64(0)
+        modes = np.array([byte], np.uint8)
+        lens = np.array([100], np.int32)
+        st = lib.fdkv_layout(ctypes.byref(dm), 1, lens.ctypes.data_as(ctypes.c_void_p),
+                             modes.ctypes.data_as(ctypes.c_void_p), None, ctypes.byref(total))
+        assert st == -1, byte
+    # routed fractions need token-level sets, increasing and within 0..10^6
+    for dm in (B.dims(2, 1, 1, 64, 4, "bf16", res_rates=(1000,)),
+               B.dims(2, 1, 1, 64, 0, "bf16", residual=B.RES_TOKENS, res_rates=(2000, 1000)),
+               B.dims(2, 1, 1, 64, 0, "bf16", residual=B.RES_TOKENS, res_rates=(2000, 2000000))):
+        n = ctypes.c_int32(0)
+        assert lib.fdkv_blocks(ctypes.byref(dm), ctypes.byref(n), None, None) == -1

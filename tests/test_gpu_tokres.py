@@ -225,3 +225,126 @@ def test_token_residual_parity(torch_dev, name):
                     worst = max(worst, e)
                     assert e <= tol, (name, qi, layer, h, g, e)
     log(f"  decode ok; worst rel-L2 {worst:.3e} (tol {tol})")
+
+
+RATE_CASES = {
+    "pairs_bf16_rates": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=4, n_q_heads=8, seq_lens=(1200,),
+                             n_probe=32, res_ppm=0, res_rates=(20000, 50000, 150000)),
+    "mixed_bf16_rates": _tok(WORKLOADS["prefill8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, head_dim=64,
+                             seq_lens=(700,), n_probe=20, res_ppm=0, res_rates=(10000, 40000, 100000, 300000),
+                             schedule=1, needle_channels=8),
+}
+# byte budgets, as a fraction of the way from all-shared to all-exact, at which the seeded
+# cases route with every other unit at least 2e-3 from a tie (checked in the test)
+RATE_BUDGET = {"pairs_bf16_rates": 0.35, "mixed_bf16_rates": 0.4}
+
+
+@pytest.mark.parametrize("name", list(RATE_CASES))
+def test_token_rates_routed_per_unit(torch_dev, name):
+    """Token-level sets whose fraction is routed per residual head (Section 3: r_{b,h} by the
+    routing loss budget): the probe's E_S and E_R at every candidate fraction against the
+    oracle (given the kernel's sets: the top n_j of its own scores), the budget routing over
+    (mode, fraction) against the oracle's on its own float64 losses (units within 1e-3 of a
+    tie would be near-ties at the bf16-deviation precision of these losses, and must be
+    absent), then compress and decode with each unit's own fraction."""
+    torch = torch_dev
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, probe, to_device
+    from gpu_cases import check_modes
+    w = RATE_CASES[name]
+    T, P, G, d, H = w.seq_lens[0], w.n_probe, w.group, w.head_dim, w.n_kv_heads
+    rates = list(w.res_rates)
+    J = len(rates)
+    log(f"[case] routed fractions {name}: T={T} blocks {w.block_sizes} rates {rates}")
+    K, V = gen.layer_cache(w, 0)
+    Q = gen.probe_queries(w, 0)
+    Kd, Vd, Qd = to_device(K, w.dtype), to_device(V, w.dtype), to_device(Q, w.dtype)
+    dm = Bn.dims(**w.dims())
+    kl, vl, ql = ([X[l] for l in range(w.n_layers)] for X in (Kd, Vd, Qd))
+    err, scores = probe(dm, T, kl, ql, P)
+    got_err = err.cpu().numpy().astype(np.float64)                 # [nb][H][1 + J]
+    got_s = scores.cpu().numpy().astype(np.float64)
+    assert got_err.shape == (w.n_blocks, H, 1 + J)
+    E_or = np.zeros((w.n_blocks, H, 1 + J))
+    worst = 0.0
+    for b, (f, B) in enumerate(w.blocks):
+        for h in range(H):
+            QB = Q[f:f + B, h * G:(h + 1) * G]
+            E_or[b, h] = O.routing_errors_token_rates(K[f:f + B, h], QB, rates)
+            Ks = O.candidate_keys(K[f:f + B, h], O.SHARED, 0)
+            want = [E_or[b, h, 0]]
+            for r in rates:
+                S = O.residual_tokens(got_s[b, h], O.n_residual_tokens(T, r))
+                contrib = sum(np.sum((QB[l].astype(np.float64).reshape(-1, d) @ (Ks[l, S] - K[f + l, h, S]).T) ** 2)
+                              / (P * d) for l in range(B)) / (B * G)
+                want.append(E_or[b, h, 0] - contrib)
+            want = np.array(want)
+            rel = np.abs(got_err[b, h] - want) / np.maximum(np.abs(want), 1e-6 * want[0])
+            worst = max(worst, rel.max())
+            assert rel.max() <= 5e-4, (b, h, got_err[b, h], want)
+    log(f"  losses at {J} fractions within {worst:.2e} of the oracle given the kernel's sets")
+    # the byte budget: a set fraction of the way from all-shared to all-exact
+    sizes = [B for B in w.block_sizes for _ in range(H)]
+    lo = sum(O.unit_bytes_tokens(O.SHARED, T, d, 0, w.dtype, B) for B in sizes)
+    hi = sum(O.unit_bytes_tokens(O.EXACT, T, d, 0, w.dtype, B) for B in sizes)
+    budget = int(lo + RATE_BUDGET[name] * (hi - lo))
+    modes, lam, st = Bn.route(dm, T, got_err.astype(np.float32), budget_bytes=budget)
+    assert st == 0
+    om_modes, om_r, om_lam, ok = O.route_token_rates(E_or.reshape(-1, 1 + J), T, d, rates, w.dtype,
+                                                      budget=budget, unit_sizes=sizes)
+    assert ok
+    cand = [O.token_rate_candidates(d, rates, w.dtype, B) for B in sizes]
+    om = np.stack([c[0] for c in cand])
+    Ec = np.concatenate([E_or.reshape(-1, 1 + J), np.zeros((len(sizes), 1))], axis=1)
+    # compare the choices as candidate indices (shared 0, residual at r_j 1 + j, exact J + 1)
+    def to_cand(byte):
+        m = int(byte) & 3
+        return 0 if m == 0 else J + 1 if m == 2 else 1 + (int(byte) >> 2)
+    got_c = np.array([to_cand(x) for x in modes.ravel()])
+    from gpu_cases import budget_defining_units
+    tied = budget_defining_units(Ec, om, om_lam)
+    gEc = np.concatenate([got_err.reshape(-1, 1 + J).astype(np.float32).astype(np.float64),
+                          np.zeros((len(sizes), 1))], axis=1)
+    assert budget_defining_units(gEc, om, lam) == tied, (tied, budget_defining_units(gEc, om, lam))
+    assert abs(lam / om_lam - 1.0) <= 2e-3, (lam, om_lam)
+    check_modes(got_c, Ec, om, om_lam, f"{name} (mode, fraction)", exclude=tied, near=1e-3)
+    want_c = O.route(Ec, om, om_lam)
+    np.testing.assert_array_equal(got_c[tied], want_c[tied])
+    log(f"  routed: lambda {lam:.5g} (oracle {om_lam:.5g}), modes {np.bincount(modes.ravel() & 3, minlength=3).tolist()}, "
+        f"fractions of residual heads {np.bincount(modes.ravel()[(modes.ravel() & 3) == 1] >> 2, minlength=J).tolist()}")
+    # compress and decode with each unit's own fraction
+    cache = CompressedCache(dm, w.seq_lens, modes[None])
+    cache.compress(0, kl, vl, token_scores=scores)
+    torch.cuda.synchronize()
+    buf = cache.host_bytes()
+    units = {}
+    for b, (f, B) in enumerate(w.blocks):
+        for h in range(H):
+            byte = int(modes[b, h])
+            m = byte & 3
+            ppm = rates[byte >> 2] if m == 1 else 0
+            n = O.n_residual_tokens(T, ppm)
+            got, counts = unpack_tok_unit(buf, int(cache.offsets_host[0, b, h]), m, T, d, ppm, w.dtype, B)
+            if m == O.RESIDUAL:
+                S = got["TS"]
+                QB = Q[f:f + B, h * G:(h + 1) * G]
+                check_token_set(S, got_s[b, h], O.token_scores(K[f:f + B, h], QB)[0], score_bound(K[f:f + B, h], QB),
+                                n, (b, h))
+                np.testing.assert_array_equal(counts[:-1], np.searchsorted(S, np.arange(0, T, 128)))
+                assert counts[-1] == n
+                units[(b, h)] = O.compress_unit_tokens(K[f:f + B, h], V[f:f + B, h], m, S, w.dtype)
+            else:
+                units[(b, h)] = O.compress_unit_tokens(K[f:f + B, h], V[f:f + B, h], m, None, w.dtype)
+    worst = 0.0
+    for qs in sharpened_queries(w, 0, K):
+        for layer in range(w.n_layers):
+            out = cache.decode(layer, to_device(qs[layer], w.dtype)).float().cpu().numpy()[0]
+            bi, f, B = block_of(w, layer)
+            for h in range(H):
+                want = O.decode_unit_tokens(units[(bi, h)], int(modes[bi, h]) & 3, layer,
+                                            qs[layer][0, h * G:(h + 1) * G].astype(np.float64), 1.0 / math.sqrt(d), d, B)
+                for g in range(G):
+                    e = rel_l2(out[h * G + g], want[g])
+                    worst = max(worst, e)
+                    assert e <= 1e-2, (name, layer, h, g, e)
+    log(f"  compress and decode with per-unit fractions ok; worst rel-L2 {worst:.3e}")

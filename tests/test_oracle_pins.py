@@ -885,3 +885,57 @@ def test_token_bytes_closed_form():
     assert O.unit_bytes_tokens(O.SHARED, 1000, 64, 50000, "bf16", 4) == O.unit_bytes(O.SHARED, 1000, 64, 0, "bf16", 4)
     np.testing.assert_allclose(O.omega_tokens(128, 50000, "bf16", 2),
                                [0.5, (512 + 2 * 256 * 0.05 + 5 / 32) / 1024, 1.0])
+
+
+# ---------------------------------------------------------------- token-level sets with per-unit fractions
+def test_token_rate_losses_and_costs():
+    """E_R(r) at every candidate fraction: E_R(0) = E_S, E_R(1) = 0, non-increasing in r, and
+    each equal to the single-fraction loss; Omega of the candidates in closed form."""
+    rng = np.random.default_rng(71)
+    K = O.round_bf16(rng.standard_normal((2, 60, 16)))
+    K[1] = O.round_bf16(0.8 * K[0] + 0.6 * rng.standard_normal((60, 16)))
+    Q = O.round_bf16(rng.standard_normal((2, 2, 5, 16)) / 4)
+    rates = [0, 20000, 100000, 250000, 1000000]
+    E = O.routing_errors_token_rates(K, Q, rates)
+    assert E[1] == E[0] and abs(E[-1]) <= 1e-12 * E[0]
+    assert np.all(np.diff(E[1:]) <= 1e-15 * E[0])
+    for j, r in enumerate(rates):
+        assert E[1 + j] == O.routing_errors_tokens(K, Q, r)[O.RESIDUAL]
+    om, modes, idx = O.token_rate_candidates(128, [50000, 100000], "bf16", 2)
+    np.testing.assert_allclose(om, [512 / 1024, (512 + 25.6 + 1 / 8 + 4 / 128) / 1024,
+                                    (512 + 51.2 + 1 / 8 + 4 / 128) / 1024, 1.0], rtol=1e-15)
+    assert modes == [O.SHARED, O.RESIDUAL, O.RESIDUAL, O.EXACT] and idx == [0, 0, 1, 0]
+
+
+def test_token_rate_routing_brute_force():
+    """Each unit's (mode, fraction) is the argmin of Eq. (3) over shared, exact and the
+    residual mode at every candidate fraction (brute force over the candidates), and the
+    budget rule's lambda is the smallest that fits (dense lambda grid), footprint monotone."""
+    rng = np.random.default_rng(72)
+    T, d, rates = 4000, 64, [10000, 50000, 200000]
+    n = 10
+    ES = np.abs(rng.standard_normal(n)) * 10
+    ER = ES[:, None] * np.sort(rng.uniform(0.05, 0.95, (n, 3)), axis=1)[:, ::-1]    # more tokens, less error
+    E = np.concatenate([ES[:, None], ER], axis=1)
+    om, cmodes, cidx = O.token_rate_candidates(d, rates, "bf16", 2)
+    Ec = np.concatenate([E, np.zeros((n, 1))], axis=1)
+    for lam in (0.0, 0.5, 2.0, 5.0, 20.0, 200.0):
+        modes, ridx, _, _ = O.route_token_rates(E, T, d, rates, "bf16", lam=lam)
+        cost = Ec + lam * om
+        best = [min(range(5), key=lambda c: (cost[u, c], om[c])) for u in range(n)]
+        np.testing.assert_array_equal(modes, [cmodes[c] for c in best])
+        np.testing.assert_array_equal(ridx, [cidx[c] for c in best])
+
+    def fp(lam):
+        m, r, _, _ = O.route_token_rates(E, T, d, rates, "bf16", lam=lam)
+        return sum(O.unit_bytes_tokens(int(mm), T, d, rates[int(rr)] if mm == O.RESIDUAL else 0, "bf16")
+                   for mm, rr in zip(m, r))
+    lo, hi = fp(math.inf), fp(0.0)
+    for frac in (0.2, 0.5, 0.8):
+        budget = int(lo + frac * (hi - lo))
+        modes, ridx, lam, ok = O.route_token_rates(E, T, d, rates, "bf16", budget=budget)
+        assert ok and fp(lam) <= budget
+        assert all(fp(x) > budget for x in np.linspace(0, lam, 1500, endpoint=False))
+        lams = np.linspace(0, 3 * lam + 1, 300)
+        fps = [fp(x) for x in lams]
+        assert all(a >= b for a, b in zip(fps, fps[1:]))
