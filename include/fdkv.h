@@ -300,9 +300,9 @@ fdkv_status fdkv_decode_attn_static(const fdkv_dims* dims, int32_t batch, const 
                                     void* stream);
 
 /*
- * Generation (the end of Section 3's method): routing is decided once after
- * prefill and reused while decoding, with an optional refresh every fixed
- * number of generated tokens.  Here a cache is a list of compressed spans
+ * Generation (the end of Section 3's method): one routing after prefill
+ * serves the whole decode, optionally re-decided at a fixed period of
+ * generated tokens.  Here a cache is a list of compressed spans
  * (prefill is span 0; each refresh compresses the tokens generated since
  * the last one into a new span, routed by fdkv_probe / fdkv_route on those
  * tokens' own keys) followed by an exact tail that holds the tokens not yet

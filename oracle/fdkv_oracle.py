@@ -678,8 +678,8 @@ def unit_bytes_tokens(mode: int, T: int, d: int, ppm: int, dtype: str, B: int = 
 
 # ----------------------------------------------------------------------------
 # generation: appended tokens and refreshed routing (Section 3, last
-# paragraph of the method: routing is decided after prefill and reused while
-# decoding, with an optional refresh every fixed number of generated tokens)
+# paragraph of the method: one routing after prefill serves the whole
+# decode, optionally re-decided at a fixed period of generated tokens)
 # ----------------------------------------------------------------------------
 def decode_spans(spans, tail_K, tail_V, layer: int, q, scale: float, d: int) -> np.ndarray:
     """Decode over a cache made of compressed spans followed by an exact tail.
