@@ -4,20 +4,20 @@
 //  * compress_dense - coalesced streaming pass over every (block, KV head):
 //    shared/residual heads write the block mean M (the per-layer image of
 //    the low-frequency DCT coefficient, the same for every layer of the
-//    block) for K and V; exact heads copy the input rows.
-//  * residual_select_reg (B = 2, k <= 16) and residual_select (B = 2, any
-//    k) - one lane per token: the top-k channels of |fl32(x[2b] - x[2b+1])|
-//    by a register comparator network (topk_net.h), written as ascending
-//    uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those channels.
+//    block) for K and V; exact heads copy the input rows.  Residual heads of
+//    pairs also take, from the same rows, each token's top-k channels of
+//    |fl32(x[2b] - x[2b+1])| (row_topk_mask, rowtopk.h), written as
+//    ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those
+//    channels.
 //  * residual_select4 (B = 4) - one lane per token: the top-k of the 3d
 //    high-frequency coefficients Z_j[c] (j = 1..3) of the DCT-II(4), ranked
 //    by |Z| as the fp32 butterfly gives them, written as ascending uint16
-//    codes 4c + j plus Z_j[c].
-// The select kernels serve residual heads (K and V independently) and the
-// probe (K indices only, into its workspace).
+//    codes 4c + j plus Z_j[c].  It serves residual heads (K and V
+//    independently) and the probe (K codes only, into its workspace).
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 #include "fp8.h"
+#include "rowtopk.h"
 #include "topk_net.h"
 
 namespace fdkv {
@@ -78,11 +78,91 @@ __device__ __forceinline__ void store_stream(uint8_t* p, const uint4& x) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4v*>(p));
 }
 
+// Residual entries of pairs, from the rows the dense pass holds: the lanes
+// of a token row find its top-k channels of |fl32(a - b)| (row_topk_mask),
+// each lane puts its selected channels and their half differences D at
+// their slots (the row's selected channels in ascending order: the lanes'
+// counts before it, then its own order) into the wave's LDS staging, and the
+// wave writes its rows' index and value runs with 4-byte stores (bytes where
+// a run does not start on a 4-byte boundary, and for its last partial word).
+template <int D, bool BF16, bool C8>
+__device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b, int k, int row_in_wave, int t0w,
+                                                 int T, uint8_t* idx_plane, uint8_t* val_plane, uint8_t* stage) {
+  constexpr int E = BF16 ? 2 : 4;
+  constexpr int NP = D * E / 16, CPP = 16 / E, RPW = 64 / NP;
+  constexpr int VB = C8 ? 1 : E;                       // bytes per stored value
+  const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
+  const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
+  uint32_t key[CPP];
+  float dv[CPP];
+#pragma unroll
+  for (int c = 0; c < CPP; ++c) {
+    float x, y;
+    if constexpr (BF16) {
+      x = (c & 1) ? bf16_hi(pa[c >> 1]) : bf16_lo(pa[c >> 1]);
+      y = (c & 1) ? bf16_hi(pb[c >> 1]) : bf16_lo(pb[c >> 1]);
+    } else {
+      x = as_f32(pa[c]);
+      y = as_f32(pb[c]);
+    }
+    const float df = x - y;
+    key[c] = as_u32(df) & 0x7FFFFFFFu;
+    dv[c] = df * 0.5f;
+  }
+  const uint32_t sel = row_topk_mask<NP, CPP>(key, k);
+  const uint32_t mine = (uint32_t)__builtin_popcount(sel);
+  uint32_t incl = mine;
+  const int lr = (int)(threadIdx.x & (NP - 1));
+#pragma unroll
+  for (int o = 1; o < NP; o <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)incl, o, NP);
+    incl += lr >= o ? y : 0u;
+  }
+  // staging of the wave: RPW rows x k index bytes, then RPW rows x k values
+  uint8_t* si = stage;
+  uint8_t* sv = stage + ((RPW * k + 3) & ~3);
+  uint32_t slot = incl - mine;
+#pragma unroll
+  for (int c = 0; c < CPP; ++c) {
+    if ((sel >> c) & 1u) {
+      const int e = row_in_wave * k + (int)slot;
+      si[e] = (uint8_t)(lr * CPP + c);
+      if constexpr (C8)
+        sv[e] = f32_to_e4m3(dv[c]);
+      else if constexpr (BF16)
+        reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)f32_to_bf16_bits(dv[c]);
+      else
+        reinterpret_cast<float*>(sv)[e] = dv[c];
+      ++slot;
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int lane = (int)(threadIdx.x & 63);
+  const int rows = max(0, min(RPW, T - t0w));
+  auto copy = [&](const uint8_t* src, uint8_t* dst, int nbytes) {
+    // 4-byte stores where the run starts on a 4-byte boundary, bytes otherwise
+    const int nw = (reinterpret_cast<uintptr_t>(dst) & 3) == 0 ? nbytes >> 2 : 0;
+    for (int i = lane; i < nw; i += 64)
+      *reinterpret_cast<uint32_t*>(dst + 4 * i) = *reinterpret_cast<const uint32_t*>(src + 4 * i);
+    for (int i = 4 * nw + lane; i < nbytes; i += 64) dst[i] = src[i];
+  };
+  copy(si, idx_plane + (uint64_t)t0w * k, rows * k);
+  copy(sv, val_plane + (uint64_t)t0w * k * VB, rows * k * VB);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();  // the staging is free for the next rows
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int D, bool BF16, int NB>
 __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NP = D * E / 16;        // 16-byte pieces per row
   constexpr int RPP = 256 / NP;         // rows per pass
+  constexpr int RPW = 64 / NP;          // rows of a pass per wave
+  // per wave: RPW rows x (k index bytes + k values of up to 4 bytes)
+  __shared__ __attribute__((aligned(16))) uint8_t stage[4][RPW * D * 5 + 16];
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
@@ -102,18 +182,26 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E, NB);
   const int piece = threadIdx.x % NP;
   const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
+  // pairs with per-token channel residuals take the residual entries in this pass too
+  const bool resid = NB == 2 && mode == kResidual && !P.tokres && P.topk > 0;
 #pragma unroll 2
   for (int r = 0; r < kCompressTile; r += RPP) {
     const int t = row0 + r;
-    if (t >= T) break;
+    // rows past the end: the residual pass needs every lane of a wave, so a
+    // workgroup with residual rows runs the pass to the end on zeros and
+    // stores nothing for them
+    if (!resid && t >= T) break;
+    if (resid && blockIdx.x * kCompressTile + r >= T) break;
+    const bool live = t < T;
     const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
     uint4 ka[NB], va[NB];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
-      ka[n] = load_stream(kx[n] + off);
-      va[n] = load_stream(vx[n] + off);
+      ka[n] = live ? load_stream(kx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
+      va[n] = live ? load_stream(vx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
     }
-    if (mode == kExact) {
+    if (!live) {
+    } else if (mode == kExact) {
 #pragma unroll
       for (int n = 0; n < NB; ++n) {
         store_stream(seg + L.ek[n] + off, ka[n]);
@@ -127,310 +215,21 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
       store_stream(seg + L.mk + off, mean_piece<BF16, NB>(ka));
       store_stream(seg + L.mv + off, mean_piece<BF16, NB>(va));
     }
-  }
-}
-
-// ---------------------------------------------------------------- residual select
-// LDS holds fp32 differences of 64 tokens, [token][D] in float4 units whose
-// index is XOR-swizzled with the token so that one-row-per-lane reads are
-// free of bank conflicts.
-template <int D>
-__device__ __forceinline__ int diff_slot(int t, int j) {  // float4 index
-  return t * (D / 4) + (j ^ (t & 15));
-}
-
-template <int D, bool BF16, int GS>
-__global__ __launch_bounds__(64) void residual_select_kernel(SelectParams P) {
-  constexpr int E = BF16 ? 2 : 4;
-  constexpr int NP = D * E / 16;
-  constexpr int CPP = 16 / E;           // channels per input piece
-  constexpr int RPI = 64 / NP;          // rows per load instruction
-  constexpr int NW = D / 32;
-  __shared__ float4 diff[64 * D / 4];
-
-  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
-  const int first = P.bl.first[bi];
-  const int unit = P.bl.block[bi] * P.hkv + head;
-  const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
-  const int T = P.seq_len, k = P.topk;
-  const int lane = threadIdx.x;
-  const int tok0 = blockIdx.x * 64;
-  const uint64_t row_bytes = (uint64_t)D * E;
-  const void* const* src = tensor ? P.v : P.k;
-  const uint64_t head_off = (uint64_t)head * T * row_bytes;
-  const uint8_t* xa = static_cast<const uint8_t*>(src[first]) + head_off;
-  const uint8_t* xb = static_cast<const uint8_t*>(src[first + 1]) + head_off;
-
-  // 1. coalesced load of 64 rows, differences into LDS
-  {
-    const int piece = lane % NP;
-#pragma unroll 4
-    for (int r = lane / NP; r < 64; r += RPI) {
-      const int t = min(tok0 + r, T - 1);
-      const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
-      const uint4 a = *reinterpret_cast<const uint4*>(xa + off);
-      const uint4 b = *reinterpret_cast<const uint4*>(xb + off);
-      const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
-      const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
-      float d[CPP];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        if constexpr (BF16) {
-          d[2 * w] = bf16_lo(pa[w]) - bf16_lo(pb[w]);
-          d[2 * w + 1] = bf16_hi(pa[w]) - bf16_hi(pb[w]);
+    if constexpr (NB == 2) {
+      if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
+        const int wave = threadIdx.x >> 6;
+        const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
+        if (c8) {
+          residual_entries<D, BF16, true>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
+                                          seg + L.vk, stage[wave]);
+          residual_entries<D, BF16, true>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
+                                          seg + L.vv, stage[wave]);
         } else {
-          d[w] = as_f32(pa[w]) - as_f32(pb[w]);
+          residual_entries<D, BF16, false>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
+                                           seg + L.vk, stage[wave]);
+          residual_entries<D, BF16, false>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
+                                           seg + L.vv, stage[wave]);
         }
-      }
-#pragma unroll
-      for (int q = 0; q < CPP / 4; ++q) {
-        const int j = piece * (CPP / 4) + q;  // float4 index within the row
-        diff[diff_slot<D>(r, j)] = make_float4(d[4 * q], d[4 * q + 1], d[4 * q + 2], d[4 * q + 3]);
-      }
-    }
-  }
-  __syncthreads();
-
-  // 2. one lane per token: threshold by the comparator network, then the mask
-  const int t = tok0 + lane;
-  uint32_t mask[NW];
-  {
-    uint32_t key[D];
-#pragma unroll
-    for (int j = 0; j < D / 4; ++j) {
-      const float4 v = diff[diff_slot<D>(lane, j)];
-      key[4 * j + 0] = as_u32(v.x) & 0x7FFFFFFFu;
-      key[4 * j + 1] = as_u32(v.y) & 0x7FFFFFFFu;
-      key[4 * j + 2] = as_u32(v.z) & 0x7FFFFFFFu;
-      key[4 * j + 3] = as_u32(v.w) & 0x7FFFFFFFu;
-    }
-    const uint32_t tau = net::kth_largest<D, GS>(key, k);
-#pragma unroll
-    for (int j = 0; j < D / 4; ++j) {
-      const float4 v = diff[diff_slot<D>(lane, j)];
-      key[4 * j + 0] = as_u32(v.x) & 0x7FFFFFFFu;
-      key[4 * j + 1] = as_u32(v.y) & 0x7FFFFFFFu;
-      key[4 * j + 2] = as_u32(v.z) & 0x7FFFFFFFu;
-      key[4 * j + 3] = as_u32(v.w) & 0x7FFFFFFFu;
-    }
-    net::select_mask<D>(key, tau, k, mask);
-  }
-  if (t >= T) return;
-
-  // 3. ascending channels, half differences, packed stores
-  uint8_t* out_idx;
-  uint8_t* out_val;
-  const bool c8 = BF16 && P.coef8;      // residual values in FP8 E4M3
-  const int CE = c8 ? 1 : E;            // bytes per stored value
-  if (P.modes) {
-    uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 2);
-    out_idx = seg + (tensor ? L.iv : L.ik);
-    out_val = seg + (tensor ? L.vv : L.vk);
-  } else {
-    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
-    out_val = nullptr;
-  }
-  out_idx += (uint64_t)t * k;
-  if (out_val) out_val += (uint64_t)t * k * CE;
-  const float* drow = reinterpret_cast<const float*>(diff);
-  if ((k & 3) == 0 && k <= GS) {
-    uint32_t iw[GS / 4];
-    uint32_t vw[GS * E / 4];
-#pragma unroll
-    for (int s = 0; s < GS; ++s) {
-      if (s < k) {
-        const int c = net::pop_lowest<D>(mask);
-        const float dv = drow[diff_slot<D>(lane, c >> 2) * 4 + (c & 3)] * 0.5f;
-        if (s % 4 == 0) iw[s / 4] = 0;
-        iw[s / 4] |= (uint32_t)c << (8 * (s % 4));
-        if constexpr (BF16) {
-          if (c8) {
-            if (s % 4 == 0) vw[s / 4] = 0;
-            vw[s / 4] |= (uint32_t)f32_to_e4m3(dv) << (8 * (s % 4));
-          } else {
-            if (s % 2 == 0) vw[s / 2] = 0;
-            vw[s / 2] |= f32_to_bf16_bits(dv) << (16 * (s % 2));
-          }
-        } else {
-          vw[s] = as_u32(dv);
-        }
-      }
-    }
-    uint32_t* oi = reinterpret_cast<uint32_t*>(out_idx);
-#pragma unroll
-    for (int w = 0; w < GS / 4; ++w)
-      if (4 * w < k) oi[w] = iw[w];
-    if (out_val) {
-      uint32_t* ov = reinterpret_cast<uint32_t*>(out_val);
-#pragma unroll
-      for (int w = 0; w < GS * E / 4; ++w)
-        if (w < k * CE / 4) ov[w] = vw[w];
-    }
-  } else {
-    for (int s = 0; s < k; ++s) {
-      const int c = net::pop_lowest<D>(mask);
-      out_idx[s] = (uint8_t)c;
-      if (out_val) {
-        const float dv = drow[diff_slot<D>(lane, c >> 2) * 4 + (c & 3)] * 0.5f;
-        if (c8)
-          out_val[s] = f32_to_e4m3(dv);
-        else if constexpr (BF16)
-          reinterpret_cast<uint16_t*>(out_val)[s] = (uint16_t)f32_to_bf16_bits(dv);
-        else
-          reinterpret_cast<float*>(out_val)[s] = dv;
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------- residual select, k <= 16
-// One lane per token with every key in registers: the lane loads its own
-// rows of both layers (16-byte pieces), forms the fp32 differences, keeps
-// their magnitudes as keys and, when a cache is written, puts the rounded
-// half differences into an LDS table (16-byte pieces rotated by the lane).
-// The threshold comes from the running sorted list of kth_largest_keep,
-// which leaves the keys for the selection mask, so nothing goes through LDS
-// on the way to the threshold and a workgroup needs only the value table:
-// two waves fit on a SIMD instead of one.
-template <int D, bool BF16>
-__device__ __forceinline__ int vtab_slot(int lane, int piece) {  // 16-byte slot of a value piece
-  constexpr int NPV = D * (BF16 ? 2 : 4) / 16;
-  return lane * NPV + (piece ^ (lane & (NPV - 1)));
-}
-
-// C8: residual values stored as FP8 E4M3 (a compile-time flavour, so the
-// bf16 path carries none of the encoder)
-template <int D, bool BF16, int RS, bool C8>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void residual_select_reg_kernel(
-    SelectParams P) {
-  constexpr int E = BF16 ? 2 : 4;
-  constexpr int NPC = D * E / 16;       // 16-byte pieces per input row
-  constexpr int CPP = 16 / E;           // channels per piece
-  constexpr int NW = D / 32;
-  // value table: per lane D values of E bytes (bf16 bits, an E4M3 code in
-  // the low byte, or fp32), piece p of the row holding channels p*CPP ...
-  __shared__ uint4 vtab[64 * NPC];
-
-  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
-  const int first = P.bl.first[bi];
-  const int unit = P.bl.block[bi] * P.hkv + head;
-  const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
-  const int T = P.seq_len, k = P.topk;
-  const int lane = threadIdx.x;
-  const int t = blockIdx.x * 64 + lane;
-  const uint64_t row_bytes = (uint64_t)D * E;
-  const void* const* src = tensor ? P.v : P.k;
-  const uint64_t row = (uint64_t)head * T + (uint64_t)min(t, T - 1);
-  const uint4* xa = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first]) + row * row_bytes);
-  const uint4* xb = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(src[first + 1]) + row * row_bytes);
-  const bool values = P.modes != nullptr;
-  constexpr bool c8 = BF16 && C8;
-
-  uint32_t key[D];
-#pragma unroll
-  for (int p = 0; p < NPC; ++p) {
-    const uint4 a = xa[p], b = xb[p];
-    const uint32_t pa[4] = {a.x, a.y, a.z, a.w}, pb[4] = {b.x, b.y, b.z, b.w};
-    float d[CPP];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if constexpr (BF16) {
-        d[2 * w] = bf16_lo(pa[w]) - bf16_lo(pb[w]);
-        d[2 * w + 1] = bf16_hi(pa[w]) - bf16_hi(pb[w]);
-      } else {
-        d[w] = as_f32(pa[w]) - as_f32(pb[w]);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < CPP; ++i) key[p * CPP + i] = as_u32(d[i]) & 0x7FFFFFFFu;
-    if (values) {
-      uint32_t vw[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        if constexpr (BF16) {
-          const float h0 = d[2 * w] * 0.5f, h1 = d[2 * w + 1] * 0.5f;
-          if constexpr (c8)
-            vw[w] = (uint32_t)f32_to_e4m3(h0) | ((uint32_t)f32_to_e4m3(h1) << 16);
-          else
-            vw[w] = cvt_bf16x2(h0, h1);
-        } else {
-          vw[w] = as_u32(d[w] * 0.5f);
-        }
-      }
-      vtab[vtab_slot<D, BF16>(lane, p)] = make_uint4(vw[0], vw[1], vw[2], vw[3]);
-    }
-  }
-  const uint32_t tau = net::kth_largest_keep<D, RS>(key, k);
-  uint32_t mask[NW];
-  net::select_mask<D>(key, tau, k, mask);
-  if (t >= T) return;
-
-  // ascending channels, packed stores
-  constexpr int CE = c8 ? 1 : E;        // bytes per stored value
-  uint8_t* out_idx;
-  uint8_t* out_val = nullptr;
-  if (values) {
-    uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 2);
-    out_idx = seg + (tensor ? L.iv : L.ik) + (uint64_t)t * k;
-    out_val = seg + (tensor ? L.vv : L.vk) + (uint64_t)t * k * CE;
-  } else {
-    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k) + (uint64_t)t * k;
-  }
-  const uint8_t* vt = reinterpret_cast<const uint8_t*>(vtab);
-  auto value_bits = [&](int c) -> uint32_t {  // stored value of channel c
-    const uint8_t* pc = vt + vtab_slot<D, BF16>(lane, c / CPP) * 16 + (c % CPP) * E;
-    if constexpr (BF16) return *reinterpret_cast<const uint16_t*>(pc) & (c8 ? 0xFFu : 0xFFFFu);
-    else return *reinterpret_cast<const uint32_t*>(pc);
-  };
-  if ((k & 3) == 0) {
-    uint32_t iw[RS / 4];
-    uint32_t vw[RS * 4 / 4];
-#pragma unroll
-    for (int s = 0; s < RS; ++s) {
-      if (s < k) {
-        const int c = net::pop_lowest<D>(mask);
-        if (s % 4 == 0) iw[s / 4] = 0;
-        iw[s / 4] |= (uint32_t)c << (8 * (s % 4));
-        if (values) {
-          const uint32_t v = value_bits(c);
-          if (CE == 1) {
-            if (s % 4 == 0) vw[s / 4] = 0;
-            vw[s / 4] |= v << (8 * (s % 4));
-          } else if (CE == 2) {
-            if (s % 2 == 0) vw[s / 2] = 0;
-            vw[s / 2] |= v << (16 * (s % 2));
-          } else {
-            vw[s] = v;
-          }
-        }
-      }
-    }
-    uint32_t* oi = reinterpret_cast<uint32_t*>(out_idx);
-#pragma unroll
-    for (int w = 0; w < RS / 4; ++w)
-      if (4 * w < k) oi[w] = iw[w];
-    if (values) {
-      uint32_t* ov = reinterpret_cast<uint32_t*>(out_val);
-#pragma unroll
-      for (int w = 0; w < RS; ++w)
-        if (w < k * CE / 4) ov[w] = vw[w];
-    }
-  } else {
-    for (int s = 0; s < k; ++s) {
-      const int c = net::pop_lowest<D>(mask);
-      out_idx[s] = (uint8_t)c;
-      if (values) {
-        const uint32_t v = value_bits(c);
-        if (CE == 1)
-          out_val[s] = (uint8_t)v;
-        else if (CE == 2)
-          reinterpret_cast<uint16_t*>(out_val)[s] = (uint16_t)v;
-        else
-          reinterpret_cast<uint32_t*>(out_val)[s] = v;
       }
     }
   }
@@ -580,8 +379,8 @@ __global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
     const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 4);
     out_idx = seg + (tensor ? L.iv : L.ik);
     out_val = seg + (tensor ? L.vv : L.vk);
-  } else {
-    out_idx = P.idx_out + (uint64_t)unit * probe_idx_stride(T, k);
+  } else {  // probe workspace: one slot per (block of four in the list, KV head)
+    out_idx = P.idx_out + (uint64_t)blockIdx.y * probe_idx_stride(T, k);
   }
   auto value_bits = [&](int e) -> uint32_t {  // entry e in the coefficient type
     const float z = as_f32(my[e].y);
@@ -645,30 +444,6 @@ hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s) {
   return P.bsize == 4 ? launch_compress_b<4>(P, s) : launch_compress_b<2>(P, s);
 }
 
-template <int D, bool BF16, int GS>
-static hipError_t launch_select_t(const SelectParams& P, int tensors, hipStream_t s) {
-  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
-  hipLaunchKernelGGL((residual_select_kernel<D, BF16, GS>), grid, dim3(64), 0, s, P);
-  return hipGetLastError();
-}
-
-template <int D, bool BF16, int RS>
-static hipError_t launch_select_reg_t(const SelectParams& P, int tensors, hipStream_t s) {
-  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
-  if (BF16 && P.coef8)
-    hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS, true>), grid, dim3(64), 0, s, P);
-  else
-    hipLaunchKernelGGL((residual_select_reg_kernel<D, BF16, RS, false>), grid, dim3(64), 0, s, P);
-  return hipGetLastError();
-}
-
-template <int D, bool BF16>
-static hipError_t launch_select_d(const SelectParams& P, int tensors, hipStream_t s) {
-  if (P.topk <= 8) return launch_select_reg_t<D, BF16, 8>(P, tensors, s);
-  if (P.topk <= 16) return launch_select_reg_t<D, BF16, 16>(P, tensors, s);
-  return launch_select_t<D, BF16, D>(P, tensors, s);
-}
-
 template <int D, bool BF16, int RS>
 static hipError_t launch_select4_t(const SelectParams& P, int tensors, hipStream_t s) {
   const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
@@ -686,12 +461,9 @@ static hipError_t launch_select4_d(const SelectParams& P, int tensors, hipStream
 
 hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s) {
   if (P.topk <= 0 || P.bl.n == 0 || P.seq_len == 0) return hipSuccess;
-  if (P.bsize == 4) {
-    if (P.d == 128) return P.bf16 ? launch_select4_d<128, true>(P, tensors, s) : launch_select4_d<128, false>(P, tensors, s);
-    return P.bf16 ? launch_select4_d<64, true>(P, tensors, s) : launch_select4_d<64, false>(P, tensors, s);
-  }
-  if (P.d == 128) return P.bf16 ? launch_select_d<128, true>(P, tensors, s) : launch_select_d<128, false>(P, tensors, s);
-  return P.bf16 ? launch_select_d<64, true>(P, tensors, s) : launch_select_d<64, false>(P, tensors, s);
+  if (P.bsize != 4) return hipErrorInvalidValue;  // pairs select inside the dense and Gram passes
+  if (P.d == 128) return P.bf16 ? launch_select4_d<128, true>(P, tensors, s) : launch_select4_d<128, false>(P, tensors, s);
+  return P.bf16 ? launch_select4_d<64, true>(P, tensors, s) : launch_select4_d<64, false>(P, tensors, s);
 }
 
 }  // namespace fdkv

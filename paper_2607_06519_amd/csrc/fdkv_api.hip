@@ -146,20 +146,24 @@ Sched sched_of(const fdkv_dims* d) {
 
 uint64_t probe_chunks(int T) { return (uint64_t)(T + kProbeChunk - 1) / kProbeChunk; }
 
-// Probe workspace regions, each aligned to 256 bytes: residual indices per
-// unit, probe Gram matrices per (layer, KV head), per-chunk partials.
+// Probe workspace regions, each aligned to 256 bytes: residual codes per unit
+// of a block of four (pairs find theirs inside the Gram kernel), probe Gram
+// matrices per (layer, KV head), per-chunk partials.
 struct ProbeWs {
   uint64_t idx, gram, part, total;
 };
 ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
-  const uint64_t units = (uint64_t)sched_of(d).n * d->n_kv_heads;
+  const Sched sch = sched_of(d);
+  int quads = 0;
+  for (int i = 0; i < sch.n; ++i) quads += sch.size[i] == 4;
+  const uint64_t units = (uint64_t)sch.n * d->n_kv_heads;
   ProbeWs w{};
   if (tokens_mode(d)) {  // the token scores' sums of squares
     w.total = plane_bytes(units * (uint64_t)T * 4);
     return w;
   }
   w.idx = 0;
-  w.gram = w.idx + units * probe_idx_stride((uint64_t)T, d->topk);
+  w.gram = w.idx + (uint64_t)quads * d->n_kv_heads * probe_idx_stride((uint64_t)T, d->topk);
   w.part = w.gram + plane_bytes((uint64_t)d->n_layers * d->n_kv_heads * d->head_dim * d->head_dim * 4);
   w.total = w.part + plane_bytes(units * probe_chunks(T) * 2 * 4);
   return w;
@@ -448,8 +452,11 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
     sp.bl = pp.bl = blocks_of_size(sch, B);
     sp.bsize = pp.bsize = B;
     if (sp.bl.n == 0) continue;
-    hipError_t e = launch_residual_select(sp, 1, s);
-    if (e != hipSuccess) return hip_fail(e, "residual_select");
+    hipError_t e = hipSuccess;
+    if (B == 4) {  // pairs find their top-k inside the Gram kernel
+      e = launch_residual_select(sp, 1, s);
+      if (e != hipSuccess) return hip_fail(e, "residual_select");
+    }
     e = launch_probe(pp, s);
     if (e != hipSuccess) return hip_fail(e, "probe");
   }
@@ -487,6 +494,7 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   cp.bf16 = sp.bf16 = dims->dtype != FDKV_F32;
   cp.coef8 = sp.coef8 = dims->dtype == FDKV_BF16_E4M3;
   const bool tok = tokens_mode(dims);
+  cp.tokres = tok;
   if (tok && !aligned(token_scores, 4)) return FDKV_E_INVALID_ARG;
   TokenParams tp{};
   for (int l = 0; l < dims->n_layers; ++l) {
@@ -517,7 +525,7 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
       if (e != hipSuccess) return hip_fail(e, "token_select");
       e = launch_token_rows(tp, s);
       if (e != hipSuccess) return hip_fail(e, "token_rows");
-    } else {
+    } else if (B == 4) {  // pairs take their residual entries in the dense pass
       e = launch_residual_select(sp, 2, s);
       if (e != hipSuccess) return hip_fail(e, "residual_select");
     }

@@ -34,6 +34,7 @@
 // order in fp64.
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
+#include "rowtopk.h"
 
 namespace fdkv {
 
@@ -258,25 +259,29 @@ __global__ __launch_bounds__(256) void probe_qgram_mfma_kernel(ProbeParams P) {
 }
 
 // Gram matrices of D and Dbar over one chunk of kProbeChunk tokens of a
-// unit, contracted with S_u.  64 tokens per step: each thread turns its
-// 16-byte pieces of the two layers into fp32 half differences, splits each
-// into bf16 hi + lo (split_bf16x2), zeroes the channels that are among its
-// token's top-k (for Dbar), and writes the four rows to LDS; waves 0-1
-// accumulate the blocks of D D^T ~ H H^T + H L^T + L H^T, waves 2-3 those
-// of Dbar.  The next step's loads are in flight during the MFMAs.
+// unit, contracted with S_u, reading the keys once.  64 tokens per step: the
+// threads holding a token row's 16-byte pieces of the two layers form its
+// fp32 differences, find the token's top-k channels among them
+// (row_topk_mask: a bisection over the row's keys with DPP counts), split
+// each half difference into bf16 hi + lo (split_bf16x2), zero the top-k
+// channels for Dbar, and write the four rows to LDS; waves 0-3 accumulate the
+// blocks of D D^T ~ H H^T + H L^T + L H^T (block t on wave t % 4), waves 4-7
+// those of Dbar.  Eight waves keep the accumulators at three blocks a wave,
+// so four waves fit on a SIMD for the VALU-heavy selection.  The next step's
+// loads are in flight during the MFMAs.
 template <int D, bool BF16>
-__global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
+__global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NPc = D * E / 16;                // 16-byte input pieces per row
   constexpr int CPP = 16 / E;                    // channels per piece
   constexpr int NB = D / 32, NT = NB * (NB + 1) / 2;
-  constexpr int TPW = (NT + 1) / 2;              // blocks per wave (two waves per matrix)
+  constexpr int WPM = 4, TPW = (NT + WPM - 1) / WPM;  // four waves per matrix: block t on wave t % WPM
   constexpr int R = kGramRows, LDR = D + 16;
-  constexpr int LPT = R * NPc / 256;             // loads per thread per layer per step
+  constexpr int LPT = R * NPc / 512;             // loads per thread per layer per step
   constexpr TriTiles<NB> tri{};
   // [D hi, D lo, Dbar hi, Dbar lo][token][channel]
   __shared__ __attribute__((aligned(16))) uint16_t tile[4][R * LDR];
-  __shared__ float red[4];
+  __shared__ float red[8];
 
   const int chunk = blockIdx.x;
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
@@ -288,65 +293,55 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   const uint64_t plane = (uint64_t)T * RB;
   const auto ka = make_rsrc(static_cast<const uint8_t*>(P.k[first]) + (uint64_t)head * plane, plane);
   const auto kb = make_rsrc(static_cast<const uint8_t*>(P.k[first + 1]) + (uint64_t)head * plane, plane);
-  const uint8_t* idx = P.idx + (uint64_t)unit * probe_idx_stride(T, k);
   const int t_begin = chunk * kProbeChunk;
   const int t_end = min(T, t_begin + kProbeChunk);
-  const int mat = wave >> 1;                      // 0: D, 1: Dbar
+  const int mat = wave >> 2;                      // 0: D, 1: Dbar
 
   f32x16_t acc[TPW];
 #pragma unroll
   for (int i = 0; i < TPW; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
-  // k = 16: a token's indices are one 16-byte load, issued with its keys
-  const bool k16 = k == 16;
-  const auto ir = make_rsrc(idx, k16 ? (uint64_t)T * 16 : 0);
-  uint4 ra[LPT], rb[LPT], ri[LPT];
+  uint4 ra[LPT], rb[LPT];
   auto load = [&](int t0) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
-      const int i = tid + 256 * j, t = t0 + i / NPc, pc = i % NPc;
+      const int i = tid + 512 * j, t = t0 + i / NPc, pc = i % NPc;
       const bool ok = t < t_end;
       ra[j] = load16(ka, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
       rb[j] = load16(kb, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
-      ri[j] = load16(ir, ok ? (uint32_t)t * 16 : kOobOff);  // reads 0 unless k = 16
     }
   };
   load(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += R) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
-      const int i = tid + 256 * j, row = i / NPc, pc = i % NPc, t = t0 + row;
+      const int i = tid + 512 * j, row = i / NPc, pc = i % NPc;
       const uint32_t* pa = reinterpret_cast<const uint32_t*>(&ra[j]);
       const uint32_t* pb = reinterpret_cast<const uint32_t*>(&rb[j]);
+      // the half differences, and the token's top-k keys |fl32(a - b)| (the
+      // NPc lanes of the row hold its pieces; rows past the chunk read zeros)
       float dv[CPP];
+      uint32_t key[CPP];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         if constexpr (BF16) {
-          dv[2 * w] = (bf16_lo(pa[w]) - bf16_lo(pb[w])) * 0.5f;
-          dv[2 * w + 1] = (bf16_hi(pa[w]) - bf16_hi(pb[w])) * 0.5f;
+          const float d0 = bf16_lo(pa[w]) - bf16_lo(pb[w]), d1 = bf16_hi(pa[w]) - bf16_hi(pb[w]);
+          key[2 * w] = as_u32(d0) & 0x7FFFFFFFu;
+          key[2 * w + 1] = as_u32(d1) & 0x7FFFFFFFu;
+          dv[2 * w] = d0 * 0.5f;
+          dv[2 * w + 1] = d1 * 0.5f;
         } else {
-          dv[w] = (as_f32(pa[w]) - as_f32(pb[w])) * 0.5f;
+          const float d0 = as_f32(pa[w]) - as_f32(pb[w]);
+          key[w] = as_u32(d0) & 0x7FFFFFFFu;
+          dv[w] = d0 * 0.5f;
         }
       }
+      // Dbar: drop the channels of this piece that are among the token's top-k
+      const uint32_t keep = ~row_topk_mask<NPc, CPP>(key, k) & ((1u << CPP) - 1u);
       uint32_t wd[CPP / 2], wl[CPP / 2], wr[CPP / 2], wrl[CPP / 2];
 #pragma unroll
       for (int c = 0; c < CPP / 2; ++c) split_bf16x2(dv[2 * c], dv[2 * c + 1], wd[c], wl[c]);
-      // Dbar: drop the channels of this piece that are among the token's top-k
-      uint32_t keep = (1u << CPP) - 1;
-      if (k16) {
-        const uint32_t* iw = reinterpret_cast<const uint32_t*>(&ri[j]);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const uint32_t c = ((iw[e >> 2] >> (8 * (e & 3))) & 0xFFu) - (uint32_t)(pc * CPP);
-          keep &= c < (uint32_t)CPP ? ~(1u << c) : ~0u;
-        }
-      } else if (t < t_end) {
-        for (int e = 0; e < k; ++e) {
-          const int c = idx[(uint64_t)t * k + e] - pc * CPP;
-          if (c >= 0 && c < CPP) keep &= ~(1u << c);
-        }
-      }
 #pragma unroll
       for (int c = 0; c < CPP / 2; ++c) {
         const uint32_t km = (((keep >> (2 * c)) & 1) ? 0xFFFFu : 0u) | (((keep >> (2 * c + 1)) & 1) ? 0xFFFF0000u : 0u);
@@ -374,12 +369,12 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
         ol[I] = gram_operand<LDR>(tile[2 * mat + 1], kk, I, lane);
       }
 #pragma unroll
-      for (int t = 0; t < NT; ++t)  // block t belongs to wave t / TPW of the pair (indices stay compile-time)
-        if (t / TPW == (wave & 1)) {
+      for (int t = 0; t < NT; ++t)  // indices stay compile-time
+        if (t % WPM == (wave & 3)) {
           const int bi_ = tri.i[t], bj_ = tri.j[t];
-          f32x16_t a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[bi_], oh[bj_], acc[t % TPW], 0, 0, 0);
+          f32x16_t a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[bi_], oh[bj_], acc[t / WPM], 0, 0, 0);
           a = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oh[bi_], ol[bj_], a, 0, 0, 0);
-          acc[t % TPW] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ol[bi_], oh[bj_], a, 0, 0, 0);
+          acc[t / WPM] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ol[bi_], oh[bj_], a, 0, 0, 0);
         }
     }
     __syncthreads();
@@ -390,19 +385,21 @@ __global__ __launch_bounds__(256) void probe_dgram_kernel(ProbeParams P) {
   float part = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (t / TPW != (wave & 1)) continue;
+    if (t % WPM != (wave & 3)) continue;
     const float wgt = (tri.i[t] == tri.j[t]) ? 1.f : 2.f;
     const int col = 32 * tri.j[t] + (lane & 31);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 32 * tri.i[t] + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      part = fmaf(wgt * acc[t % TPW][r], S[row * D + col], part);
+      part = fmaf(wgt * acc[t / WPM][r], S[row * D + col], part);
     }
   }
   part = wave_sum(part);
   if (lane == 0) red[wave] = part;
   __syncthreads();
-  if (tid < 2) P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + tid] = red[2 * tid] + red[2 * tid + 1];
+  if (tid < 2)
+    P.partial[((uint64_t)unit * P.n_chunks + chunk) * 2 + tid] =
+        (red[4 * tid] + red[4 * tid + 1]) + (red[4 * tid + 2] + red[4 * tid + 3]);
 }
 
 // Blocks of four: Gram matrices of the eight deviation matrices (4 layers x
@@ -441,7 +438,8 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
   __amdgpu_buffer_rsrc_t kr[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) kr[n] = make_rsrc(static_cast<const uint8_t*>(P.k[first + n]) + (uint64_t)head * plane, plane);
-  const uint16_t* codes = reinterpret_cast<const uint16_t*>(P.idx + (uint64_t)unit * probe_idx_stride(T, k));
+  // the residual codes of this (block of four, KV head) in the workspace slot of its list position
+  const uint16_t* codes = reinterpret_cast<const uint16_t*>(P.idx + (uint64_t)blockIdx.y * probe_idx_stride(T, k));
   const bool k16 = k == 16;                       // a token's codes are two 16-byte loads
   const auto ir = make_rsrc(codes, k16 ? (uint64_t)T * 32 : 0);
   const int t_begin = chunk * kProbeChunk;
@@ -590,7 +588,7 @@ static hipError_t launch_probe_t(const ProbeParams& P, hipStream_t s) {
   if (P.bsize == 4)
     hipLaunchKernelGGL((probe_dgram4_kernel<D, BF16>), grid, dim3(512), 0, s, P);
   else
-    hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), grid, dim3(256), 0, s, P);
+    hipLaunchKernelGGL((probe_dgram_kernel<D, BF16>), grid, dim3(512), 0, s, P);
   return hipGetLastError();
 }
 

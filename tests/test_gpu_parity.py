@@ -290,6 +290,59 @@ def test_probe_parity(torch_dev, name):
         np.testing.assert_array_equal(gm.ravel()[tied], want_m[tied])
 
 
+TIE_CASES = {
+    # rows on LPR = 16 lanes (bf16, d = 128), k below and above LPR, k = d
+    "bf16_k8": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=8, seq_lens=(515,),
+                      n_needles=0, fixed_modes=(1, 1)),
+    "bf16_k40": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=40, seq_lens=(131,),
+                       n_needles=0, fixed_modes=(1, 1)),
+    "bf16_k128": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=1, n_q_heads=2, topk=128, seq_lens=(70,),
+                        n_needles=0, fixed_modes=(1,)),
+    # 32 lanes (f32, d = 128), 8 lanes (bf16, d = 64), FP8 values
+    "f32_k16": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=128, topk=16,
+                      seq_lens=(203,), n_needles=0, fixed_modes=(1, 1)),
+    "f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
+                         seq_lens=(97,), n_needles=0, fixed_modes=(1, 1)),
+    "bf16_d64_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=5,
+                          seq_lens=(333,), n_needles=0, fixed_modes=(1, 1)),
+    "e4m3_k12": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=12, seq_lens=(300,),
+                       n_needles=0, fixed_modes=(1, 1), dtype="bf16_e4m3"),
+}
+
+
+def _tie_heavy(K, V, seed: int):
+    """Inputs whose channel differences tie often: values on a coarse grid,
+    every 7th token with equal layers (all keys zero), every 11th with the
+    second layer a constant shift of the first (all keys equal)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for X in (K, V):
+        X = np.round(X * 4.0) / 4.0
+        X += rng.integers(-2, 3, size=X.shape) * 0.25 * (rng.random(X.shape) < 0.3)
+        X = np.clip(X, -4.0, 4.0).astype(np.float32)
+        T = X.shape[2]
+        X[1, :, 0:T:7] = X[0, :, 0:T:7]
+        X[1, :, 0:T:11] = X[0, :, 0:T:11] + np.float32(0.5)
+        out.append(X)
+    return out
+
+
+@pytest.mark.parametrize("name", list(TIE_CASES))
+def test_compress_residual_ties(torch_dev, name):
+    """Residual channel sets under heavy ties: bit-exact indices (ties to the
+    lower channel), values within 1 ulp."""
+    w = TIE_CASES[name]
+    log(f"[case] compress ties {name} T={w.seq_lens} d={w.head_dim} k={w.topk} {w.dtype}")
+    K, V = gen.layer_cache(w, 0)
+    K, V = _tie_heavy(K, V, 7 + len(name))
+    modes = _modes(w)
+    cache, keep = _run_compress(w, modes[None], [K], [V])
+    torch_dev.cuda.synchronize()
+    ref = _oracle_units(w, K, V, modes)
+    nz = _check_compress(w, cache, 0, ref, K, V)
+    log(f"  ties ok; values 1 ulp apart: {nz}")
+
+
 def test_probe_deterministic(torch_dev):
     from paper_2607_06519_amd import binding as B
     from paper_2607_06519_amd.cache import probe, to_device
