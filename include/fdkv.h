@@ -68,6 +68,11 @@
  *    MK, MV, MASK[ceil(T/32)] (u32, bit t%32 of word t/32: token t is in the
  *    set), COUNT[ceil(T/128) + 1] (u32, set tokens before each 128-token
  *    chunk, then n), HK[n][B-1][d] (c), HV[n][B-1][d] (c)  (set tokens ascending)
+ * FP8 shared planes (MK, MV with c = 1) are not row-major: they fill whole
+ * 1 KB blocks of R = 1024/d rows, and the 8 channels 8p .. 8p+7 of row t sit
+ * at byte 1024 (t / R) + 16 ((t % (R/2)) d/8 + p) + 8 ((t % R) / (R/2)), so
+ * rows t and t + R/2 of a block share each 16-byte slot.  Every other plane
+ * is row-major.
  */
 #ifndef FDKV_H
 #define FDKV_H

@@ -671,7 +671,7 @@ def unit_bytes_tokens(mode: int, T: int, d: int, ppm: int, dtype: str, B: int = 
         return unit_bytes(mode, T, d, 0, dtype, B)
     c = coef_bytes(dtype)
     n = n_residual_tokens(T, ppm)
-    coef = _plane(T * d * c)
+    coef = _coef_plane(T, d, c)
     return (2 * coef + _plane(-(-T // 32) * 4) + _plane((-(-T // 128) + 1) * 4)
             + 2 * _plane(n * (B - 1) * d * c))
 
@@ -791,10 +791,23 @@ def _plane(nbytes: int) -> int:
     return -(-nbytes // PLANE_ALIGN) * PLANE_ALIGN
 
 
+FP8_BLOCK = 1024
+
+
+def _coef_plane(T: int, d: int, c: int) -> int:
+    """A shared (M) plane: one-byte FP8 coefficients fill whole 1 KB blocks
+    (a storage choice of the implementation, not of the paper: the decode
+    reads two rows' pieces per 16-byte load), wider ones are padded to 256 B."""
+    if c == 1:
+        return _plane(-(-(T * d) // FP8_BLOCK) * FP8_BLOCK)
+    return _plane(T * d * c)
+
+
 def unit_bytes(mode: int, T: int, d: int, k: int, dtype: str, B: int = 2) -> int:
-    """Bytes of one (sequence, block, KV head) segment; every plane padded to 256 B."""
+    """Bytes of one (sequence, block, KV head) segment; every plane padded to 256 B
+    (FP8 shared planes to 1 KB)."""
     e, c = input_bytes(dtype), coef_bytes(dtype)
-    coef = _plane(T * d * c)
+    coef = _coef_plane(T, d, c)
     if mode == SHARED:
         return 2 * coef
     if mode == RESIDUAL:

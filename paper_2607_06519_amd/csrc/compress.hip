@@ -184,13 +184,21 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
   // pairs with per-token channel residuals take the residual entries in this pass too
   const bool resid = NB == 2 && mode == kResidual && !P.tokres && P.topk > 0;
+  // FP8 shared planes fill whole 1 KB blocks of R8 rows: the rows after the
+  // last token of its block are written as zeros, so that a decode tile (one
+  // block) reads no stale bytes (R8 divides the rows of a pass, so they lie
+  // in the pass of the last token)
+  constexpr int R8 = kC8Block / D;
+  const bool pad8 = c8 && mode != kExact;
+  const int t_end = pad8 ? (T + R8 - 1) / R8 * R8 : T;
+  static_assert(RPP % R8 == 0 || !BF16, "FP8 blocks within a pass");
 #pragma unroll 2
   for (int r = 0; r < kCompressTile; r += RPP) {
     const int t = row0 + r;
     // rows past the end: the residual pass needs every lane of a wave, so a
     // workgroup with residual rows runs the pass to the end on zeros and
-    // stores nothing for them
-    if (!resid && t >= T) break;
+    // stores nothing for them (but the FP8 block padding)
+    if (!resid && t >= t_end) break;
     if (resid && blockIdx.x * kCompressTile + r >= T) break;
     const bool live = t < T;
     const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
@@ -201,6 +209,11 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
       va[n] = live ? load_stream(vx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
     }
     if (!live) {
+      if (pad8 && t < t_end) {
+        const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);
+        *reinterpret_cast<uint2*>(seg + L.mk + o8) = make_uint2(0u, 0u);
+        *reinterpret_cast<uint2*>(seg + L.mv + o8) = make_uint2(0u, 0u);
+      }
     } else if (mode == kExact) {
 #pragma unroll
       for (int n = 0; n < NB; ++n) {
@@ -208,7 +221,7 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
         store_stream(seg + L.ev[n] + off, va[n]);
       }
     } else if (c8) {
-      const uint64_t o8 = (uint64_t)t * D + piece * 8;
+      const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);  // the 1 KB block layout of FP8 planes
       *reinterpret_cast<uint2*>(seg + L.mk + o8) = mean_piece_e4m3<NB>(ka);
       *reinterpret_cast<uint2*>(seg + L.mv + o8) = mean_piece_e4m3<NB>(va);
     } else {

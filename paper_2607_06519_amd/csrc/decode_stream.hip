@@ -237,7 +237,8 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const uint8_t* seg = P.part[part].cache + seg_off;
   const int nb = P.bsize, ib = index_bytes(nb);
   const SegLayout L = seg_layout(mode, (uint64_t)T, D, k, 2, ce, nb);
-  const uint64_t dense = (uint64_t)T * D * ce;
+  // bytes of the plane a tile reads: FP8 shared planes in whole 1 KB blocks
+  const uint64_t dense = c8 ? coef_plane_bytes((uint64_t)T, D, 1) : (uint64_t)T * D * ce;
   const uint64_t xplane = plane_bytes(dense);  // exact planes: K of layer p at p * xplane, V at (B + p) * xplane
   const uint64_t tail_off = ((uint64_t)seq * P.hkv + head) * (uint64_t)P.tail_cap * RB;
   const auto kr = rsrc(tail ? static_cast<const uint8_t*>(P.tail_k) + tail_off
@@ -315,19 +316,22 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
 
     constexpr int PD = (RES == 0 || RES == 3) ? S::PD0 : 1, NB = PD + 1;
 
+    // FP8 planes: a tile is one 1 KB block, and the lane's 16-byte slot of it
+    // holds its piece of both of its rows (rows rg and rg + RPL)
+    static_assert(!C8 || (TILE * D == kC8Block && NL == 2 && RPL * 2 == TILE), "FP8 tile = one block");
     auto load = [&](int t, TileBuf<D, G>& b) {
       const bool ok = t < ntiles;
       const uint32_t r0 = (uint32_t)(wtok0 + t * TILE);
       if constexpr (RES == 3) b.tm = __builtin_amdgcn_raw_buffer_load_b32(tmr, ok ? (r0 >> 5) * 4 : kOob, 0, 0);
+      if constexpr (C8) {
+        const uint4 w = ld128_stream(kr, ok ? r0 * D + lane * 16 : kOob);
+        b.k[0] = make_uint4(w.x, w.y, 0u, 0u);
+        b.k[1] = make_uint4(w.z, w.w, 0u, 0u);
+      }
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const uint32_t row = r0 + i * RPL + rg;
-        if constexpr (C8) {
-          const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? row * D + pc * 8 : kOob, 0, 0);
-          b.k[i] = make_uint4(w2[0], w2[1], 0u, 0u);
-        } else {
-          b.k[i] = ld128_stream(kr, ok ? row * RB + pc * 16 : kOob);
-        }
+        if constexpr (!C8) b.k[i] = ld128_stream(kr, ok ? row * RB + pc * 16 : kOob);
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
           b.ki[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ikr, ok ? e * 2 : kOob, 0, kNonTemporal)
@@ -336,15 +340,15 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
                        : __builtin_amdgcn_raw_buffer_load_b16(vkr, ok ? e * 2 : kOob, 0, kNonTemporal);
         }
       }
+      if constexpr (C8) {
+        const uint4 w = ld128_stream(vr, ok ? r0 * D + lane * 16 : kOob);
+        b.v[0] = make_uint4(w.x, w.y, 0u, 0u);
+        b.v[1] = make_uint4(w.z, w.w, 0u, 0u);
+      }
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const uint32_t row = r0 + i * RPL + rg;
-        if constexpr (C8) {
-          const auto w2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? row * D + pc * 8 : kOob, 0, 0);
-          b.v[i] = make_uint4(w2[0], w2[1], 0u, 0u);
-        } else {
-          b.v[i] = ld128_stream(vr, ok ? row * RB + pc * 16 : kOob);
-        }
+        if constexpr (!C8) b.v[i] = ld128_stream(vr, ok ? row * RB + pc * 16 : kOob);
         if constexpr (RES == 1) {
           const uint32_t e = row * NP + pc;
           b.vi[i] = Q4 ? __builtin_amdgcn_raw_buffer_load_b16(ivr, ok ? e * 2 : kOob, 0, kNonTemporal)
@@ -574,8 +578,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
         const uint32_t hrow = (base + (uint32_t)j) * NF * D;  // element index of the token's first row
         uint4 mk, mv, hk[NF], hv[NF];
         if constexpr (C8) {
-          const auto a = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? row * D + pc * 8 : kOob, 0, 0);
-          const auto b2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? row * D + pc * 8 : kOob, 0, 0);
+          const uint32_t o8 = (uint32_t)c8_piece_offset(row, pc, D);
+          const auto a = __builtin_amdgcn_raw_buffer_load_b64(kr, ok ? o8 : kOob, 0, 0);
+          const auto b2 = __builtin_amdgcn_raw_buffer_load_b64(vr, ok ? o8 : kOob, 0, 0);
           mk = widen_e4m3(make_uint4(a[0], a[1], 0u, 0u));
           mv = widen_e4m3(make_uint4(b2[0], b2[1], 0u, 0u));
 #pragma unroll

@@ -34,6 +34,24 @@ FDKV_HD uint32_t as_u32(float f) { return __builtin_bit_cast(uint32_t, f); }
 
 FDKV_HD uint64_t plane_bytes(uint64_t n) { return (n + kPlaneAlign - 1) / kPlaneAlign * kPlaneAlign; }
 
+// FP8 coefficient planes (the shared planes of an FP8 cache, one byte per
+// channel) are stored in 1 KB blocks of R = 1024 / d token rows, so that a
+// decode lane reads both of its rows' 8-channel pieces with one 16-byte
+// load: piece p (channels 8p .. 8p + 7) of row t sits at
+//   1024 * (t / R) + 16 * ((t % (R/2)) * (d/8) + p) + 8 * ((t % R) / (R/2)),
+// i.e. rows t and t + R/2 of a block share a 16-byte slot.  The plane is
+// padded to whole blocks.
+constexpr int kC8Block = 1024;
+FDKV_HD uint64_t c8_piece_offset(uint64_t t, int p, int d) {
+  const uint64_t R = (uint64_t)(kC8Block / d), half = R / 2;
+  const uint64_t r = t % R;
+  return (t / R) * kC8Block + 16 * ((r % half) * (uint64_t)(d / 8) + (uint64_t)p) + 8 * (r / half);
+}
+FDKV_HD uint64_t coef_plane_bytes(uint64_t T, int d, int c) {
+  const uint64_t n = T * (uint64_t)d * (uint64_t)c;
+  return c == 1 ? plane_bytes((n + kC8Block - 1) / kC8Block * kC8Block) : plane_bytes(n);
+}
+
 // Byte offsets of the planes of one (sequence, block, KV head) segment of a
 // block of B = 2 or 4 layers.
 // Shared:   MK, MV.  Residual: MK, MV, IK, VK, IV, VV.
@@ -52,7 +70,7 @@ FDKV_HD int index_bytes(int B) { return B == 2 ? 1 : 2; }
 FDKV_HD SegLayout seg_layout(int mode, uint64_t T, int d, int k, int e, int c, int B) {
   SegLayout s{};
   const uint64_t dense = plane_bytes(T * (uint64_t)d * e);
-  const uint64_t coef = plane_bytes(T * (uint64_t)d * c);
+  const uint64_t coef = coef_plane_bytes(T, d, c);
   const uint64_t ip = plane_bytes(T * (uint64_t)k * index_bytes(B));
   const uint64_t vp = plane_bytes(T * (uint64_t)k * c);
   if (mode == kExact) {
@@ -91,7 +109,7 @@ FDKV_HD uint64_t residual_token_count(uint64_t T, int ppm) { return (T * (uint64
 
 FDKV_HD TokLayout tok_layout(int mode, uint64_t T, int d, int ppm, int e, int c, int B) {
   TokLayout s{};
-  const uint64_t coef = plane_bytes(T * (uint64_t)d * c);
+  const uint64_t coef = coef_plane_bytes(T, d, c);
   if (mode == kExact) {
     s.total = 2 * B * plane_bytes(T * (uint64_t)d * e);
     return s;

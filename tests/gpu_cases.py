@@ -40,15 +40,41 @@ def values(raw: np.ndarray, kind: str) -> np.ndarray:
     return raw.view(np.float32).astype(np.float64)
 
 
+def coef_plane_bytes(T: int, d: int, c: int) -> int:
+    """A shared plane's bytes: FP8 planes fill whole 1 KB blocks."""
+    return _pad(-(-(T * d) // 1024) * 1024) if c == 1 else _pad(T * d * c)
+
+
+def shared_plane(buf: np.ndarray, o: int, T: int, d: int, dtype: str) -> np.ndarray:
+    """A shared (M) plane ``[T][d]`` read back from byte ``o``.  FP8 planes (the
+    layout of include/fdkv.h): 1 KB blocks of R = 1024 / d rows; rows t and
+    t + R/2 of a block share each 16-byte slot, slot (t % (R/2)) * d/8 + p
+    holding channels 8p .. 8p + 7 of the first row, then of the second."""
+    tc = TYPES[dtype][1]
+    if BYTES[tc] != 1:
+        return values(buf[o: o + T * d * BYTES[tc]].copy(), tc).reshape(T, d)
+    R, npc = 1024 // d, d // 8
+    t = np.arange(T)[:, None]
+    p = np.arange(npc)[None, :]
+    at = (t // R) * 1024 + 16 * ((t % (R // 2)) * npc + p) + 8 * ((t % R) // (R // 2))
+    raw = buf[o + at[..., None] + np.arange(8)]
+    return values(raw.reshape(-1).copy(), tc).reshape(T, d)
+
+
 def unpack_unit(buf: np.ndarray, off: int, mode: int, T: int, d: int, k: int, dtype: str, B: int = 2) -> dict:
     ti, tc = TYPES[dtype]
     e, c = BYTES[ti], BYTES[tc]
     ib = 1 if B == 2 else 2                       # channel bytes (pairs) or uint16 codes 4c + j (fours)
-    dense, coef = _pad(T * d * e), _pad(T * d * c)
+    fp8 = c == 1
+    dense = _pad(T * d * e)
+    coef = coef_plane_bytes(T, d, c)
     ip, vp = _pad(T * k * ib), _pad(T * k * c)
 
     def plane(o, width, kind):
         return values(buf[off + o: off + o + T * width * BYTES[kind]].copy(), kind).reshape(T, width)
+
+    def block_plane(o):
+        return shared_plane(buf, off + o, T, d, dtype)
 
     def index(o):
         raw = buf[off + o: off + o + T * k * ib].copy()
@@ -60,7 +86,7 @@ def unpack_unit(buf: np.ndarray, off: int, mode: int, T: int, d: int, k: int, dt
             u[f"K{n}"] = plane(n * dense, d, ti)
             u[f"V{n}"] = plane((B + n) * dense, d, ti)
         return u
-    u = {"MK": plane(0, d, tc), "MV": plane(coef, d, tc)}
+    u = {"MK": block_plane(0), "MV": block_plane(coef)} if fp8 else {"MK": plane(0, d, tc), "MV": plane(coef, d, tc)}
     if mode == O.RESIDUAL:
         o = 2 * coef
         u["IK"] = index(o)

@@ -25,8 +25,8 @@ import pytest
 import oracle as O
 from synth import WORKLOADS, gen, scaled
 
-from gpu_cases import (BYTES, TYPES, _pad, block_of, compare_units, quad_value_tol, rel_l2, sharpened_queries,
-                       ulp_distance, values)
+from gpu_cases import (BYTES, TYPES, _pad, block_of, coef_plane_bytes, compare_units, quad_value_tol, rel_l2,
+                       shared_plane, sharpened_queries, ulp_distance, values)
 
 pytestmark = pytest.mark.gpu
 
@@ -115,7 +115,7 @@ def unpack_tok_unit(buf, off, mode, T, d, ppm, dtype, B):
     if mode != O.RESIDUAL:
         from gpu_cases import unpack_unit
         return unpack_unit(buf, off, mode, T, d, 0, dtype, B), None
-    coef = _pad(T * d * c)
+    coef = coef_plane_bytes(T, d, c)
     n = O.n_residual_tokens(T, ppm)
     mo = 2 * coef
     co = mo + _pad(-(-T // 32) * 4)
@@ -128,7 +128,8 @@ def unpack_tok_unit(buf, off, mode, T, d, ppm, dtype, B):
     words = buf[off + mo: off + mo + (-(-T // 32)) * 4].copy().view("<u4")
     bits = ((words[:, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(-1)[:T]
     counts = buf[off + co: off + co + ((-(-T // 128)) + 1) * 4].copy().view("<u4").astype(np.int64)
-    u = {"MK": plane(0, T, d, tc), "MV": plane(coef, T, d, tc), "TS": np.nonzero(bits)[0].astype(np.int64),
+    u = {"MK": shared_plane(buf, off, T, d, dtype), "MV": shared_plane(buf, off + coef, T, d, dtype),
+         "TS": np.nonzero(bits)[0].astype(np.int64),
          "HK": plane(hk, n, (B - 1) * d, tc).reshape(n, B - 1, d), "HV": plane(hv, n, (B - 1) * d, tc).reshape(n, B - 1, d)}
     return u, counts
 
