@@ -109,31 +109,32 @@ __device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b,
     key[c] = as_u32(df) & 0x7FFFFFFFu;
     dv[c] = df * 0.5f;
   }
+  // bf16 values: every channel's rounded half difference, one conversion per pair
+  uint32_t hv[CPP / 2];
+  if constexpr (BF16 && !C8) {
+#pragma unroll
+    for (int c = 0; c < CPP / 2; ++c) hv[c] = cvt_bf16x2(dv[2 * c], dv[2 * c + 1]);
+  }
   const uint32_t sel = row_topk_mask<NP, CPP>(key, k);
   const uint32_t mine = (uint32_t)__builtin_popcount(sel);
-  uint32_t incl = mine;
+  const uint32_t incl = row_prefix_u32<NP>(mine);
   const int lr = (int)(threadIdx.x & (NP - 1));
-#pragma unroll
-  for (int o = 1; o < NP; o <<= 1) {
-    const uint32_t y = (uint32_t)__shfl_up((int)incl, o, NP);
-    incl += lr >= o ? y : 0u;
-  }
   // staging of the wave: RPW rows x k index bytes, then RPW rows x k values
   uint8_t* si = stage;
   uint8_t* sv = stage + ((RPW * k + 3) & ~3);
-  uint32_t slot = incl - mine;
+  // the lane's selected channels go to consecutive slots from its first one
+  const int e0 = row_in_wave * k + (int)(incl - mine);
 #pragma unroll
   for (int c = 0; c < CPP; ++c) {
     if ((sel >> c) & 1u) {
-      const int e = row_in_wave * k + (int)slot;
+      const int e = e0 + __builtin_popcount(sel & ((1u << c) - 1u));
       si[e] = (uint8_t)(lr * CPP + c);
       if constexpr (C8)
         sv[e] = f32_to_e4m3(dv[c]);
       else if constexpr (BF16)
-        reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)f32_to_bf16_bits(dv[c]);
+        reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)(hv[c >> 1] >> (16 * (c & 1)));
       else
         reinterpret_cast<float*>(sv)[e] = dv[c];
-      ++slot;
     }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

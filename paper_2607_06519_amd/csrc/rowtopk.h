@@ -49,6 +49,24 @@ __device__ __forceinline__ uint32_t row_ext_u32(uint32_t x) {
   return x;
 }
 
+// Inclusive prefix sum over the row's lanes, in lane order (DPP row shifts
+// inside each 16-lane DPP row; a row of 32 lanes adds the lower half's total
+// through row_bcast:15; a row of 8 lanes masks the shifts at its boundary).
+template <int LPR>
+__device__ __forceinline__ uint32_t row_prefix_u32(uint32_t x) {
+  static_assert(LPR == 8 || LPR == 16 || LPR == 32, "row width");
+  const int lr = (int)(threadIdx.x & (LPR - 1));
+  uint32_t y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (LPR != 8 || lr >= 1) ? y : 0u;
+  y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);           // row_shr:2
+  x += (LPR != 8 || lr >= 2) ? y : 0u;
+  y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);           // row_shr:4
+  x += (LPR != 8 || lr >= 4) ? y : 0u;
+  if constexpr (LPR >= 16) x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  if constexpr (LPR == 32) x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  return x;
+}
+
 // Keys of this lane's CPL channels >= x, summed over the row.
 template <int LPR, int CPL>
 __device__ __forceinline__ uint32_t row_count_ge(const uint32_t (&key)[CPL], uint32_t x) {
@@ -93,23 +111,21 @@ __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], in
     const uint32_t need = ku - chi, ns = clo - chi;
     const bool take_max = ns > need && need == 1u;
     const bool drop_min = ns > need && need + 1u == ns && !take_max;
-    uint32_t nlo = lo;
-    if (__ballot(take_max) != 0) {
+    if (__ballot(take_max || drop_min) != 0) {
+      // one max reduction for both: the largest key below hi, or the
+      // complement of the smallest key at or above lo (complements order
+      // the other way round)
       uint32_t m = 0;
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) m = (key[i] < hi && key[i] > m) ? key[i] : m;
+      for (int i = 0; i < CPL; ++i) {
+        const uint32_t x = take_max ? (key[i] < hi ? key[i] : 0u) : (key[i] >= lo ? ~key[i] : 0u);
+        m = x > m ? x : m;
+      }
       m = row_ext_u32<LPR, true>(m);
-      if (take_max) nlo = m;
+      if (take_max) lo = m;
+      if (drop_min) lo = ~m;
+      clo = row_count_ge<LPR, CPL>(key, lo);
     }
-    if (__ballot(drop_min) != 0) {
-      uint32_t m = 0xFFFFFFFFu;
-#pragma unroll
-      for (int i = 0; i < CPL; ++i) m = (key[i] >= lo && key[i] < m) ? key[i] : m;
-      m = row_ext_u32<LPR, false>(m);
-      if (drop_min) nlo = m;
-    }
-    if (__ballot(nlo != lo) != 0) clo = row_count_ge<LPR, CPL>(key, nlo);
-    lo = nlo;
   }
   uint32_t sel = 0;
 #pragma unroll
@@ -123,13 +139,7 @@ __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], in
     for (int i = 0; i < CPL; ++i) eq |= key[i] == lo ? 1u << i : 0u;
     const uint32_t neq = (uint32_t)__builtin_popcount(eq);
     // exclusive prefix of the equal counts over the row's lower lanes
-    uint32_t incl = neq;
-    const int lr = (int)(threadIdx.x & (LPR - 1));
-#pragma unroll
-    for (int o = 1; o < LPR; o <<= 1) {
-      const uint32_t y = (uint32_t)__shfl_up((int)incl, o, LPR);
-      incl += lr >= o ? y : 0u;
-    }
+    const uint32_t incl = row_prefix_u32<LPR>(neq);
     if (tied) {
       const uint32_t need = ku - cgt;
       uint32_t rank = incl - neq;
