@@ -478,6 +478,10 @@ def test_e4m3_cache_bytes_closed_form():
     assert O.unit_bytes(O.RESIDUAL, T, d, k, "bf16_e4m3") == 2 * pad(T * d) + 2 * (pad(T * k) + pad(T * k))
     assert O.unit_bytes(O.EXACT, T, d, k, "bf16_e4m3") == 4 * pad(T * d * 2)
     np.testing.assert_allclose(O.omega(d, k, "bf16_e4m3"), [256 / 1024, (256 + 64) / 1024, 1.0])
+    # FP8 shared planes fill whole 1 KB blocks (1001 rows of 64 channels: 62.56 blocks -> 63)
+    assert O.unit_bytes(O.SHARED, 1001, 64, 8, "bf16_e4m3") == 2 * 63 * 1024
+    assert O.unit_bytes(O.RESIDUAL, 1001, 64, 8, "bf16_e4m3") == 2 * 63 * 1024 + 2 * (pad(1001 * 8) + pad(1001 * 8))
+    assert O.unit_bytes(O.SHARED, 1001, 64, 8, "bf16") == 2 * pad(1001 * 64 * 2)
 
 
 def test_e4m3_unit_stores_rounded_coefficients():
