@@ -13,7 +13,10 @@ bandwidth.  The step is captured once in a HIP graph and replayed.
 Printed: one JSON line with the metric, a roofline object for the decode
 launch (split-K + combine per layer, timed with HIP events on the launch
 stream), the prefill path (probe, route, compress) timed on the same cache,
-and the CPU oracle timed on a bounded sample of the same workload.
+the CPU oracle timed on a bounded sample of the same workload, and (for the
+default workload) the decode lines of the 16-sequence batch and the 70B-shaped
+131k-token cache, each measured by a child process before this one starts
+(`other_workloads`).
 """
 from __future__ import annotations
 
@@ -60,7 +63,35 @@ def parse():
                          "scaled by the calibration copy, and exit")
     ap.add_argument("--traffic-json", metavar="PATH", help="with --summarize-pmc: also write the decode "
                     "traffic record that the bench line reads")
+    ap.add_argument("--legs", default=None,
+                    help="comma-separated further decode workloads measured in child processes before this "
+                         "one and reported under other_workloads (default: batched8b,long70b for the llama8b "
+                         "run, none otherwise; 'none' skips them)")
     return ap.parse_args()
+
+
+def run_legs(names, args):
+    """Decode-only bench lines of further workloads, each a child process of this script started
+    before this process touches the GPU; returns a compact record per workload."""
+    import subprocess
+    out = {}
+    for wl in names:
+        cmd = [sys.executable, os.path.abspath(__file__), "--workload", wl, "--no-prefill", "--no-cpu-baseline",
+               "--gen-tail", "0", "--steps", str(min(args.steps, 20)), "--warmup", str(min(args.warmup, 3)),
+               "--legs", "none"]
+        log(f"[bench] leg {wl}: {' '.join(cmd[1:])}")
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, text=True, timeout=600)
+        if r.returncode != 0:
+            raise RuntimeError(f"bench leg {wl} failed with status {r.returncode}")
+        d = json.loads(r.stdout.strip().splitlines()[-1])
+        rf = d["roofline"]
+        out[wl] = {"value": d["value"], "unit": d["unit"], "ms_per_step": d["ms_per_step"],
+                   "steps": d["steps"], "dtype": d["dtype"],
+                   "launch_us": rf["launch_us"], "frac": rf["frac"], "achieved_gbs": rf["achieved"],
+                   "bytes_per_launch": rf["bytes_per_launch"], "traffic": rf["traffic"],
+                   "config": {k: d["config"][k] for k in ("n_layers", "n_kv_heads", "n_q_heads", "head_dim",
+                                                          "batch", "seq_len", "mode_mix", "cache_gb")}}
+    return out
 
 
 def bytes_per_token(mode, d, k, e, c, B=2):
@@ -189,6 +220,10 @@ def main():
         print(f"bench.py measures one GPU: the compressed-KV path here has no multi-GPU leg "
               f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    legs = args.legs
+    if legs is None:
+        legs = "batched8b,long70b" if args.workload == "llama8b" else "none"
+    other = run_legs([x for x in legs.split(",") if x and x != "none"], args) if legs != "none" else None
 
     import numpy as np
     import torch
@@ -546,6 +581,8 @@ def main():
         "prefill": prefill,
         "generation": generation,
     }
+    if other:
+        res["other_workloads"] = other
     print(json.dumps(res), flush=True)
 
 
