@@ -419,6 +419,9 @@ def main():
         ws = torch.empty(B.probe_workspace(dm, T, P), dtype=torch.uint8, device=dev)
         err = torch.empty((nbk, H, dm.n_err), dtype=torch.float32, device=dev)
         tscores = torch.empty((nbk, H, T), dtype=torch.float32, device=dev) if w.residual == 1 else None
+        # per-token channel residuals: the probe's K selections, which compress reuses
+        ksel = (torch.empty(B.selection_bytes(dm, T), dtype=torch.uint8, device=dev)
+                if w.residual != 1 else None)
         _, all_exact = B.layout(dm, [T], np.full((1, nbk, H), 2, np.uint8))
         pcache_buf = torch.empty(all_exact, dtype=torch.uint8, device=dev)
         offs_dev = torch.empty((nbk, H), dtype=torch.int64, device=dev)
@@ -430,7 +433,7 @@ def main():
             a0, a1, c0, c1 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
             tw0 = time.perf_counter()
             a0.record()
-            B.probe(dm, T, kl, ql, P, err, ws, None, tscores)
+            B.probe(dm, T, kl, ql, P, err, ws, None, tscores, ksel)
             a1.record()
             eh = err.cpu().numpy()                      # sync point
             tr0 = time.perf_counter()
@@ -440,7 +443,7 @@ def main():
             modes_dev.copy_(torch.from_numpy(pmodes))
             offs_dev.copy_(torch.from_numpy(offs[0].astype(np.int64)))
             c0.record()
-            B.compress(dm, T, kl, vl, modes_dev, offs_dev, pcache_buf, None, tscores)
+            B.compress(dm, T, kl, vl, modes_dev, offs_dev, pcache_buf, None, tscores, ksel)
             c1.record()
             torch.cuda.synchronize()
             tw1 = time.perf_counter()
@@ -479,7 +482,7 @@ def main():
             prefill["cpu_baseline"] = cpu_baseline_prefill(w, pmodes.reshape(nbk, H), budget)
         log(f"[bench] prefill: probe {tp * 1e3:.2f} ms, route {trt * 1e3:.2f} ms, compress {tc * 1e3:.2f} ms "
             f"({prefill['compress_gbs']:.0f} GB/s), mix {prefill['probe_mode_mix']}")
-        del Qp, ws, pcache_buf, tscores
+        del Qp, ws, pcache_buf, tscores, ksel
 
     # ------------------------------------------------------------ generation: append + spans + tail, refresh
     generation = None

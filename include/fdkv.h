@@ -189,6 +189,11 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
 /* Device workspace bytes fdkv_probe needs for this shape. */
 fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t n_probe, size_t* bytes);
 
+/* Bytes of the K selection buffer that fdkv_probe may fill and fdkv_compress
+ * may read (the per-token top-k channels of K for every unit of a pair, in an
+ * internal layout of (d * elem_bytes / 16) bytes per unit and token). */
+fdkv_status fdkv_selection_bytes(const fdkv_dims* dims, int32_t seq_len, size_t* bytes);
+
 /*
  * fdkv_probe - device.  Routing loss of Eq. (2) for every (block, KV head):
  *   E_m[b,h] = 1/(B G P) * sum over the B layers l of the block, query heads g
@@ -204,12 +209,17 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
  *   token_scores_out  FDKV_RES_TOKENS: device float [n_blocks][Hkv][T], out: s_t
  *                     (the residual loss then keeps the top ceil(r T) tokens); else unused
  *   ws         device workspace of >= fdkv_probe_workspace() bytes
+ *   k_select_out  device, NULL or fdkv_selection_bytes() bytes, out: the per-token
+ *              top-k channels of K of every pair that the residual loss uses (the
+ *              selection of Eq. 3), for fdkv_compress of the same keys to reuse;
+ *              unused with FDKV_RES_TOKENS and for blocks of four
  * T * d * elem_bytes and P * G * d * elem_bytes must stay below 2^31
  * (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets).
  */
 fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                        const void* const* qp_layers, int32_t n_probe, float* errors_out,
-                       float* token_scores_out, void* ws, size_t ws_bytes, void* stream);
+                       float* token_scores_out, void* ws, size_t ws_bytes, uint8_t* k_select_out,
+                       void* stream);
 
 /*
  * fdkv_compress - device.  Writes one sequence's segments of the compressed
@@ -218,11 +228,16 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
  *   modes        device [n_blocks][Hkv]
  *   seg_offsets  device [n_blocks][Hkv], from fdkv_layout (256-byte multiples)
  *   token_scores FDKV_RES_TOKENS: device float [n_blocks][Hkv][T] from fdkv_probe; else unused
+ *   k_select     device, NULL (residual pairs select their K channels in the pass)
+ *                or the buffer fdkv_probe filled for these k_layers and seq_len
+ *                (the residual pairs then take their K channels from it: the same
+ *                channels, without selecting them again); unused with FDKV_RES_TOKENS
  *   cache        device buffer the offsets index into
  */
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                           const void* const* v_layers, const uint8_t* modes,
-                          const uint64_t* seg_offsets, const float* token_scores, void* cache, void* stream);
+                          const uint64_t* seg_offsets, const float* token_scores, const uint8_t* k_select,
+                          void* cache, void* stream);
 
 /* Device workspace bytes fdkv_decode_attn needs for this batch shape. */
 fdkv_status fdkv_decode_workspace(const fdkv_dims* dims, int32_t batch, int32_t max_seq_len, size_t* bytes);

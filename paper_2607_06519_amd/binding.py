@@ -25,7 +25,7 @@ STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: 
 SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
            "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
            "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans", "fdkv_decode_static_scratch_bytes",
-           "fdkv_decode_attn_static", "fdkv_decode_partial", "fdkv_decode_combine")
+           "fdkv_decode_attn_static", "fdkv_decode_partial", "fdkv_decode_combine", "fdkv_selection_bytes")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 RES_CHANNELS, RES_TOKENS = 0, 1  # residual kinds (fdkv_residual)
 
@@ -92,9 +92,11 @@ def load():
     lib.fdkv_probe_workspace.restype = I32
     lib.fdkv_probe_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_probe.restype = I32
-    lib.fdkv_probe.argtypes = [DP, I32, P, P, I32, P, P, P, SZ, P]
+    lib.fdkv_probe.argtypes = [DP, I32, P, P, I32, P, P, P, SZ, P, P]
     lib.fdkv_compress.restype = I32
-    lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P, P]
+    lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P, P, P]
+    lib.fdkv_selection_bytes.restype = I32
+    lib.fdkv_selection_bytes.argtypes = [DP, I32, P]
     lib.fdkv_decode_workspace.restype = I32
     lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_decode_attn.restype = I32
@@ -188,6 +190,12 @@ def probe_workspace(d: Dims, seq_len: int, n_probe: int) -> int:
     return int(n.value)
 
 
+def selection_bytes(d: Dims, seq_len: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().fdkv_selection_bytes(ctypes.byref(d), int(seq_len), ctypes.byref(n)), "fdkv_selection_bytes")
+    return int(n.value)
+
+
 def decode_workspace(d: Dims, batch: int, max_seq_len: int) -> int:
     n = ctypes.c_size_t(0)
     _check(load().fdkv_decode_workspace(ctypes.byref(d), int(batch), int(max_seq_len), ctypes.byref(n)),
@@ -197,21 +205,23 @@ def decode_workspace(d: Dims, batch: int, max_seq_len: int) -> int:
 
 # ----------------------------------------------------------------- device entry points
 def probe(d: Dims, seq_len: int, k_layers: Sequence, qp_layers: Sequence, n_probe: int, errors_out, ws,
-          stream=None, token_scores=None):
+          stream=None, token_scores=None, k_select=None):
     """Queue fdkv_probe; ``k_layers``/``qp_layers`` are per-layer device tensors;
-    ``token_scores`` (token-level residual set) receives s_t ``[n_blocks][Hkv][T]``."""
+    ``token_scores`` (token-level residual set) receives s_t ``[n_blocks][Hkv][T]``;
+    ``k_select`` (``selection_bytes`` bytes) the K selections for compress to reuse."""
     _check(load().fdkv_probe(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(qp_layers),
                              int(n_probe), _dev(errors_out), _dev(token_scores), _dev(ws),
-                             int(ws.numel() * ws.element_size()), _stream(stream)), "fdkv_probe")
+                             int(ws.numel() * ws.element_size()), _dev(k_select), _stream(stream)), "fdkv_probe")
 
 
 def compress(d: Dims, seq_len: int, k_layers: Sequence, v_layers: Sequence, modes, seg_offsets, cache,
-             stream=None, token_scores=None):
+             stream=None, token_scores=None, k_select=None):
     """Queue fdkv_compress for one sequence (``modes``/``seg_offsets`` device tensors; ``token_scores``
-    from the probe when residual heads hold a token-level set)."""
+    from the probe when residual heads hold a token-level set; ``k_select`` the probe's K selections
+    of the same keys, or None to select in the pass)."""
     _check(load().fdkv_compress(ctypes.byref(d), int(seq_len), _ptr_array(k_layers), _ptr_array(v_layers),
-                                _dev(modes), _dev(seg_offsets), _dev(token_scores), _dev(cache), _stream(stream)),
-           "fdkv_compress")
+                                _dev(modes), _dev(seg_offsets), _dev(token_scores), _dev(k_select), _dev(cache),
+                                _stream(stream)), "fdkv_compress")
 
 
 def decode_attn(d: Dims, batch: int, seq_lens, max_seq_len: int, modes, seg_offsets, cache, layer: int, q, out,

@@ -53,11 +53,12 @@ class CompressedCache:
         self.ws = torch.empty(B.decode_workspace(dims, self.batch, self.max_seq_len) // 4 + 64,
                               dtype=torch.float32, device=device)
 
-    def compress(self, seq: int, k_layers, v_layers, stream=None, token_scores=None):
+    def compress(self, seq: int, k_layers, v_layers, stream=None, token_scores=None, k_select=None):
         """Write sequence ``seq`` from per-layer device tensors ``[Hkv][T][d]`` (``token_scores``
-        from the probe when residual heads hold a token-level set)."""
+        from the probe when residual heads hold a token-level set; ``k_select`` the probe's K
+        selections of the same keys, reused instead of selecting again)."""
         B.compress(self.dims, self.seq_lens_host[seq], k_layers, v_layers, self.modes[seq],
-                   self.offsets[seq], self.buf, stream, token_scores)
+                   self.offsets[seq], self.buf, stream, token_scores, k_select)
 
     def decode(self, layer: int, q, out=None, sm_scale: Optional[float] = None, stream=None):
         """One decode step of ``layer`` for queries ``q [batch][Hq][d]``; returns ``out``."""
@@ -74,19 +75,21 @@ class CompressedCache:
 
 
 def probe(dims: B.Dims, seq_len: int, k_layers, qp_layers, n_probe: int, stream=None):
-    """Queue fdkv_probe and return the device tensor of errors ``[n_blocks][Hkv][n_err]`` and the
-    workspace, or, for a token-level residual set, the errors and the token scores
-    ``[n_blocks][Hkv][T]``."""
+    """Queue fdkv_probe and return the device tensor of errors ``[n_blocks][Hkv][n_err]`` and what
+    compress of the same keys takes from the probe: for a token-level residual set the token
+    scores ``[n_blocks][Hkv][T]``, otherwise the K selections of the pairs."""
     torch = _torch()
     dev = k_layers[0].device
     ws = torch.empty(B.probe_workspace(dims, seq_len, n_probe), dtype=torch.uint8, device=dev)
     nb = len(B.blocks(dims)[0])
     err = torch.empty((nb, dims.n_kv_heads, dims.n_err), dtype=torch.float32, device=dev)
-    scores = None
+    scores, ksel = None, None
     if dims.residual == B.RES_TOKENS:
         scores = torch.empty((nb, dims.n_kv_heads, seq_len), dtype=torch.float32, device=dev)
-    B.probe(dims, seq_len, k_layers, qp_layers, n_probe, err, ws, stream, scores)
-    return err, (scores if scores is not None else ws)
+    else:
+        ksel = torch.empty(max(B.selection_bytes(dims, seq_len), 1), dtype=torch.uint8, device=dev)
+    B.probe(dims, seq_len, k_layers, qp_layers, n_probe, err, ws, stream, scores, ksel)
+    return err, (scores if scores is not None else ksel)
 
 
 class Generation:
@@ -171,14 +174,17 @@ class Generation:
             kl = [t.contiguous() for t in kl]
             ql = [probe_rows[l][s].contiguous() for l in range(self.dims.n_layers)]
             err, extra = probe(self.dims, T, kl, ql, n_probe)
-            scores.append(extra if self.dims.residual == B.RES_TOKENS else None)
+            scores.append(extra)
             modes[s], _, _ = B.route(self.dims, T, err.cpu().numpy(), lam=lam, budget_bytes=budget_bytes,
                                      allow_infeasible=True)
         span = CompressedCache(self.dims, [T] * self.batch, modes, device=self.pos.device)
         for s in range(self.batch):
             kl = [self.tail_k[l][s, :, :T].contiguous() for l in range(self.dims.n_layers)]
             vl = [self.tail_v[l][s, :, :T].contiguous() for l in range(self.dims.n_layers)]
-            span.compress(s, kl, vl, token_scores=scores[s])
+            if self.dims.residual == B.RES_TOKENS:
+                span.compress(s, kl, vl, token_scores=scores[s])
+            else:
+                span.compress(s, kl, vl, k_select=scores[s])
         torch.cuda.synchronize()
         self.spans.append(span)
         self.n_tail = 0

@@ -87,7 +87,8 @@ __device__ __forceinline__ void store_stream(uint8_t* p, const uint4& x) {
 // a run does not start on a 4-byte boundary, and for its last partial word).
 template <int D, bool BF16, bool C8>
 __device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b, int k, int row_in_wave, int t0w,
-                                                 int T, uint8_t* idx_plane, uint8_t* val_plane, uint8_t* stage) {
+                                                 int T, uint8_t* idx_plane, uint8_t* val_plane, uint8_t* stage,
+                                                 int preset = -1) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NP = D * E / 16, CPP = 16 / E, RPW = 64 / NP;
   constexpr int VB = C8 ? 1 : E;                       // bytes per stored value
@@ -115,7 +116,8 @@ __device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b,
 #pragma unroll
     for (int c = 0; c < CPP / 2; ++c) hv[c] = cvt_bf16x2(dv[2 * c], dv[2 * c + 1]);
   }
-  const uint32_t sel = row_topk_mask<NP, CPP>(key, k);
+  // the probe's selection of this row when given (the same keys, so the same channels)
+  const uint32_t sel = preset >= 0 ? (uint32_t)preset : row_topk_mask<NP, CPP>(key, k);
   const uint32_t mine = (uint32_t)__builtin_popcount(sel);
   const uint32_t incl = row_prefix_u32<NP>(mine);
   const int lr = (int)(threadIdx.x & (NP - 1));
@@ -233,14 +235,16 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
       if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
         const int wave = threadIdx.x >> 6;
         const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
+        const int kpre = (P.ksel && live) ? (int)P.ksel[selection_offset(unit, T, t, piece, D, E)]
+                                          : (P.ksel ? 0 : -1);
         if (c8) {
           residual_entries<D, BF16, true>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
-                                          seg + L.vk, stage[wave]);
+                                          seg + L.vk, stage[wave], kpre);
           residual_entries<D, BF16, true>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
                                           seg + L.vv, stage[wave]);
         } else {
           residual_entries<D, BF16, false>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
-                                           seg + L.vk, stage[wave]);
+                                           seg + L.vk, stage[wave], kpre);
           residual_entries<D, BF16, false>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
                                            seg + L.vv, stage[wave]);
         }

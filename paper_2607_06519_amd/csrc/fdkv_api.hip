@@ -368,9 +368,19 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
   return FDKV_OK;
 }
 
+fdkv_status fdkv_selection_bytes(const fdkv_dims* dims, int32_t seq_len, size_t* bytes) {
+  fdkv_status st = check_dims(dims);
+  if (st != FDKV_OK) return st;
+  if (seq_len < 0 || !bytes) return FDKV_E_INVALID_ARG;
+  const Sched sch = sched_of(dims);
+  *bytes = (size_t)((uint64_t)sch.n * dims->n_kv_heads * (uint64_t)seq_len *
+                    selection_row_bytes(dims->head_dim, elem_bytes(dims)));
+  return FDKV_OK;
+}
+
 fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                        const void* const* qp_layers, int32_t n_probe, float* errors_out, float* token_scores_out,
-                       void* ws, size_t ws_bytes, void* stream) {
+                       void* ws, size_t ws_bytes, uint8_t* k_select_out, void* stream) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 1 || n_probe < 1 || !k_layers || !qp_layers) return FDKV_E_INVALID_ARG;
@@ -435,6 +445,7 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
     pp.qp[l] = qp_layers[l];
   }
   pp.idx = base + w.idx;
+  pp.ksel = k_select_out;
   pp.gram_q = reinterpret_cast<float*>(base + w.gram);
   pp.partial = reinterpret_cast<float*>(base + w.part);
   pp.errors = errors_out;
@@ -467,7 +478,7 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
 
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,
                           const void* const* v_layers, const uint8_t* modes, const uint64_t* seg_offsets,
-                          const float* token_scores, void* cache, void* stream) {
+                          const float* token_scores, const uint8_t* k_select, void* cache, void* stream) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 0 || !k_layers || !v_layers || !modes || !aligned(seg_offsets, 8) || !aligned(cache, 256))
@@ -495,6 +506,7 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   cp.coef8 = sp.coef8 = dims->dtype == FDKV_BF16_E4M3;
   const bool tok = tokens_mode(dims);
   cp.tokres = tok;
+  cp.ksel = tok ? nullptr : k_select;
   if (tok && !aligned(token_scores, 4)) return FDKV_E_INVALID_ARG;
   TokenParams tp{};
   for (int l = 0; l < dims->n_layers; ++l) {

@@ -33,7 +33,19 @@ struct CompressParams {
   bool tokres;                 // token-level residual set (else per-token channel top-k)
   int res_ppm;                 // its fraction of tokens, parts per million
   const float* scores;         // token scores [blocks][hkv][T] (token-level residual set)
+  const uint8_t* ksel;         // the probe's K selections of pairs (selection_offset), or null
 };
+
+// The K channel selections of pairs that the probe takes and compress may
+// reuse: unit u's row t holds one byte per 16-byte input piece p (bit i:
+// channel CPP p + i, CPP = 16 / element bytes) at selection_offset(u, t, p).
+__host__ __device__ __forceinline__ uint64_t selection_row_bytes(int d, int elem_bytes) {
+  return (uint64_t)d * elem_bytes / 16;
+}
+__host__ __device__ __forceinline__ uint64_t selection_offset(uint64_t unit, uint64_t T, uint64_t t, int p,
+                                                             int d, int elem_bytes) {
+  return (unit * T + t) * selection_row_bytes(d, elem_bytes) + (uint64_t)p;
+}
 
 // Token-level residual set: score kernel (probe), selection and rows.
 struct TokenParams {
@@ -141,6 +153,7 @@ struct ProbeParams {
   float* gram_q;               // [layers][hkv][d][d]  sums of q q^T over probe rows (see probe.hip)
   float* partial;              // [units][n_chunks][2]
   float* errors;               // [units][2]
+  uint8_t* ksel;               // out: the K selections of pairs (selection_offset), or null
   BlockList bl;                // blocks of size bsize
   int8_t bsizes[kMaxBlocks];   // every block's size (finalize)
   int seq_len, bsize, n_blocks, hkv, hq, d, topk, n_probe, n_chunks;

@@ -338,7 +338,12 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
         }
       }
       // Dbar: drop the channels of this piece that are among the token's top-k
-      const uint32_t keep = ~row_topk_mask<NPc, CPP>(key, k) & ((1u << CPP) - 1u);
+      const uint32_t sel = row_topk_mask<NPc, CPP>(key, k);
+      const uint32_t keep = ~sel & ((1u << CPP) - 1u);
+      if (P.ksel) {  // the selection, for compress to reuse
+        const int t = t0 + row;
+        if (t < t_end) P.ksel[selection_offset(unit, T, t, pc, D, E)] = (uint8_t)sel;
+      }
       uint32_t wd[CPP / 2], wl[CPP / 2], wr[CPP / 2], wrl[CPP / 2];
 #pragma unroll
       for (int c = 0; c < CPP / 2; ++c) split_bf16x2(dv[2 * c], dv[2 * c + 1], wd[c], wl[c]);

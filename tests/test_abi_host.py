@@ -145,12 +145,18 @@ def test_validation_errors_before_any_device_call(lib):
     # planes are addressed with 32-bit offsets: T * d * 2 bytes must stay below 2^31
     assert lib.fdkv_decode_attn(ctypes.byref(good), 1, fake, 1 << 23, fake, fake, fake, 0, fake, fake,
                                 ctypes.c_float(0.1), fake, 1 << 40, None) == -2
-    assert lib.fdkv_compress(ctypes.byref(good), 16, ptrs, None, fake, fake, None, fake, None) == -1
+    assert lib.fdkv_compress(ctypes.byref(good), 16, ptrs, None, fake, fake, None, None, fake, None) == -1
     n = ctypes.c_size_t(0)
     assert lib.fdkv_probe_workspace(ctypes.byref(good), 100, 4, ctypes.byref(n)) == 0 and n.value > 0
-    assert lib.fdkv_probe(ctypes.byref(good), 100, ptrs, ptrs, 4, fake, None, fake, n.value - 1, None) == -3
-    assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, None, fake, n.value, None) == -1
-    assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, None, fake, 1 << 40, None) == -2
+    assert lib.fdkv_probe(ctypes.byref(good), 100, ptrs, ptrs, 4, fake, None, fake, n.value - 1, None, None) == -3
+    assert lib.fdkv_probe(ctypes.byref(good), 0, ptrs, ptrs, 4, fake, None, fake, n.value, None, None) == -1
+    assert lib.fdkv_probe(ctypes.byref(good), 1 << 23, ptrs, ptrs, 4, fake, None, fake, 1 << 40, None, None) == -2
+    # the K selection buffer: one byte per 16-byte input piece of every unit's rows
+    sb = ctypes.c_size_t(0)
+    assert lib.fdkv_selection_bytes(ctypes.byref(good), 100, ctypes.byref(sb)) == 0
+    assert sb.value == (good.n_layers // 2) * good.n_kv_heads * 100 * (good.head_dim * 2 // 16)
+    assert lib.fdkv_selection_bytes(ctypes.byref(good), -1, ctypes.byref(sb)) == -1
+    assert lib.fdkv_selection_bytes(ctypes.byref(good), 100, None) == -1
     assert lib.fdkv_layout(None, 1, None, None, None, None) == -1
 
 

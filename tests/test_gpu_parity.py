@@ -345,6 +345,51 @@ def test_compress_residual_ties(torch_dev, name):
     log(f"  ties ok; values 1 ulp apart: {nz}")
 
 
+REUSE_CASES = {
+    "bf16_k16": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(1000,), n_probe=16,
+                       n_needles=4, fixed_modes=(1, 0, 1, 2)),
+    "f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
+                         seq_lens=(333,), n_probe=8, n_needles=0, fixed_modes=(1, 1)),
+    "e4m3_d64_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=5,
+                          seq_lens=(517,), n_probe=8, n_needles=2, dtype="bf16_e4m3", fixed_modes=(1, 1)),
+    "mixed_bf16": scaled(WORKLOADS["llama8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, seq_lens=(300,), n_probe=8,
+                         n_needles=2, schedule=1, fixed_modes=(1, 1, 0, 1, 1, 2, 1, 0, 1, 1)),
+}
+
+
+@pytest.mark.parametrize("name", list(REUSE_CASES))
+@pytest.mark.parametrize("ties", [False, True])
+def test_compress_reuses_probe_selection(torch_dev, name, ties):
+    """Compress taking the probe's K selections writes exactly the cache that
+    compress selecting in its own pass writes (random and tie-heavy inputs)."""
+    from paper_2607_06519_amd.cache import probe, to_device
+    w = REUSE_CASES[name]
+    log(f"[case] compress with the probe's selections {name} ties={ties}")
+    K, V = gen.layer_cache(w, 0)
+    if ties:
+        for f in range(0, w.n_layers, 2):
+            K[f:f + 2], V[f:f + 2] = _tie_heavy(K[f:f + 2], V[f:f + 2], 3 + f)
+    Q = gen.probe_queries(w, 0)
+    Kd, Vd, Qd = to_device(K, w.dtype), to_device(V, w.dtype), to_device(Q, w.dtype)
+    kl, vl, ql = ([X[l] for l in range(w.n_layers)] for X in (Kd, Vd, Qd))
+    from paper_2607_06519_amd import binding as B
+    from paper_2607_06519_amd.cache import CompressedCache
+    dm = B.dims(**w.dims())
+    _, ksel = probe(dm, w.seq_lens[0], kl, ql, w.n_probe)
+    modes = _modes(w)[None]
+    a = CompressedCache(dm, w.seq_lens, modes)
+    b = CompressedCache(dm, w.seq_lens, modes)
+    a.buf.zero_()
+    b.buf.zero_()
+    a.compress(0, kl, vl)
+    b.compress(0, kl, vl, k_select=ksel)
+    torch_dev.cuda.synchronize()
+    np.testing.assert_array_equal(a.host_bytes(), b.host_bytes())
+    if ties:
+        nz = _check_compress(w, b, 0, _oracle_units(w, K, V, _modes(w)), K, V)
+        log(f"  equal to the oracle; values 1 ulp apart: {nz}")
+
+
 def test_probe_deterministic(torch_dev):
     from paper_2607_06519_amd import binding as B
     from paper_2607_06519_amd.cache import probe, to_device
