@@ -190,8 +190,10 @@ fdkv_status fdkv_route(const fdkv_dims* dims, int32_t seq_len, const float* erro
 fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t n_probe, size_t* bytes);
 
 /* Bytes of the K selection buffer that fdkv_probe may fill and fdkv_compress
- * may read (the per-token top-k channels of K for every unit of a pair, in an
- * internal layout of (d * elem_bytes / 16) bytes per unit and token). */
+ * may read: the per-token residual selection of K of every unit (top-k
+ * channels of a pair, top-k coefficients of a block of four), in an internal
+ * layout of d * elem_bytes / 16 slots per unit and token, a slot being 1 byte,
+ * or 4 when the schedule has blocks of four. */
 fdkv_status fdkv_selection_bytes(const fdkv_dims* dims, int32_t seq_len, size_t* bytes);
 
 /*
@@ -209,10 +211,10 @@ fdkv_status fdkv_selection_bytes(const fdkv_dims* dims, int32_t seq_len, size_t*
  *   token_scores_out  FDKV_RES_TOKENS: device float [n_blocks][Hkv][T], out: s_t
  *                     (the residual loss then keeps the top ceil(r T) tokens); else unused
  *   ws         device workspace of >= fdkv_probe_workspace() bytes
- *   k_select_out  device, NULL or fdkv_selection_bytes() bytes, out: the per-token
- *              top-k channels of K of every pair that the residual loss uses (the
- *              selection of Eq. 3), for fdkv_compress of the same keys to reuse;
- *              unused with FDKV_RES_TOKENS and for blocks of four
+ *   k_select_out  device, NULL or fdkv_selection_bytes() bytes (4-byte aligned), out:
+ *              the per-token residual selection of K that the residual loss uses
+ *              (Eq. 3), for fdkv_compress of the same keys to reuse; unused with
+ *              FDKV_RES_TOKENS
  * T * d * elem_bytes and P * G * d * elem_bytes must stay below 2^31
  * (FDKV_E_UNSUPPORTED otherwise: planes are addressed with 32-bit offsets).
  */
@@ -228,10 +230,10 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
  *   modes        device [n_blocks][Hkv]
  *   seg_offsets  device [n_blocks][Hkv], from fdkv_layout (256-byte multiples)
  *   token_scores FDKV_RES_TOKENS: device float [n_blocks][Hkv][T] from fdkv_probe; else unused
- *   k_select     device, NULL (residual pairs select their K channels in the pass)
+ *   k_select     device, NULL (residual units select their K entries in the pass)
  *                or the buffer fdkv_probe filled for these k_layers and seq_len
- *                (the residual pairs then take their K channels from it: the same
- *                channels, without selecting them again); unused with FDKV_RES_TOKENS
+ *                (residual units then take their K entries' positions from it: the
+ *                same selection, without ranking again); unused with FDKV_RES_TOKENS
  *   cache        device buffer the offsets index into
  */
 fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* const* k_layers,

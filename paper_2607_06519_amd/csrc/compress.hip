@@ -4,21 +4,18 @@
 //  * compress_dense - coalesced streaming pass over every (block, KV head):
 //    shared/residual heads write the block mean M (the per-layer image of
 //    the low-frequency DCT coefficient, the same for every layer of the
-//    block) for K and V; exact heads copy the input rows.  Residual heads of
-//    pairs also take, from the same rows, each token's top-k channels of
-//    |fl32(x[2b] - x[2b+1])| (row_topk_mask, rowtopk.h), written as
-//    ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those
-//    channels.
-//  * residual_select4 (B = 4) - one lane per token: the top-k of the 3d
-//    high-frequency coefficients Z_j[c] (j = 1..3) of the DCT-II(4), ranked
-//    by |Z| as the fp32 butterfly gives them, written as ascending uint16
-//    codes 4c + j plus Z_j[c].  It serves residual heads (K and V
-//    independently) and the probe (K codes only, into its workspace).
+//    block) for K and V; exact heads copy the input rows.  Residual heads
+//    also take their entries from the same rows, K and V independently:
+//    pairs each token's top-k channels of |fl32(x[2b] - x[2b+1])|, written
+//    as ascending uint8 indices plus D = (x[2b] - x[2b+1]) / 2 at those
+//    channels; blocks of four the top-k of the token's 3d high-frequency
+//    coefficients |Z_j[c]| of the DCT-II(4) (the fp32 butterfly of dct4.h),
+//    written as ascending uint16 codes 4c + j plus Z_j[c].  Both rank with
+//    the wavefront top-k of rowtopk.h (ties to the lower channel or code).
 #include "fdkv_common.h"
 #include "fdkv_kernels.h"
 #include "fp8.h"
 #include "rowtopk.h"
-#include "topk_net.h"
 
 namespace fdkv {
 
@@ -158,14 +155,93 @@ __device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b,
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Residual entries of blocks of four, from the rows the dense pass holds: each
+// lane evaluates the fp32 butterfly (dct4.h) of its CPP channels, keys the 3
+// CPP coefficients |Z_j[c]| in code order (bit 3 c + j - 1), finds the row's
+// top-k (row_topk_mask: ties to the lower code), and stages its selected
+// codes 4c + j (uint16) and coefficients at consecutive slots of the wave's
+// LDS area, which the wave then writes with 4-byte stores like the pairs.
+template <int D, bool BF16, bool C8>
+__device__ __forceinline__ void residual_entries4(const uint4 (&x)[4], int k, int row_in_wave, int t0w, int T,
+                                                  uint8_t* idx_plane, uint8_t* val_plane, uint8_t* stage,
+                                                  const uint32_t* preset = nullptr) {
+  constexpr int E = BF16 ? 2 : 4;
+  constexpr int NP = D * E / 16, CPP = 16 / E, NK = 3 * CPP, RPW = 64 / NP;
+  constexpr int VB = C8 ? 1 : E;
+  uint32_t sel;
+  if (preset) {  // the probe's selection of this row (the same keys, so the same coefficients)
+    sel = *preset;
+  } else {
+    uint32_t key[NK];
+#pragma unroll
+    for (int c = 0; c < CPP; ++c) {
+      float z[3];
+      dct4_high(chan<BF16>(x[0], c), chan<BF16>(x[1], c), chan<BF16>(x[2], c), chan<BF16>(x[3], c), z[0], z[1],
+                z[2]);
+#pragma unroll
+      for (int j = 0; j < 3; ++j) key[3 * c + j] = as_u32(z[j]) & 0x7FFFFFFFu;
+    }
+    sel = row_topk_mask<NP, NK>(key, k);
+  }
+  // the staging below evaluates the butterfly again rather than keep its NK
+  // results alive (an empty asm statement that only marks the input pieces
+  // as possibly changed)
+  uint4 y[4] = {x[0], x[1], x[2], x[3]};
+#pragma unroll
+  for (int n = 0; n < 4; ++n) asm volatile("" : "+v"(y[n].x), "+v"(y[n].y), "+v"(y[n].z), "+v"(y[n].w));
+  const uint32_t mine = (uint32_t)__builtin_popcount(sel);
+  const uint32_t incl = row_prefix_u32<NP>(mine);
+  const int lr = (int)(threadIdx.x & (NP - 1));
+  uint16_t* si = reinterpret_cast<uint16_t*>(stage);
+  uint8_t* sv = stage + ((RPW * k * 2 + 3) & ~3);
+  const int e0 = row_in_wave * k + (int)(incl - mine);
+#pragma unroll
+  for (int c = 0; c < CPP; ++c) {
+    if (((sel >> (3 * c)) & 7u) == 0u) continue;
+    float z[3];  // evaluated again (the same rounded operations): fewer live registers
+    dct4_high(chan<BF16>(y[0], c), chan<BF16>(y[1], c), chan<BF16>(y[2], c), chan<BF16>(y[3], c), z[0], z[1],
+              z[2]);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const int b = 3 * c + j;
+      if ((sel >> b) & 1u) {
+        const int e = e0 + __builtin_popcount(sel & ((1u << b) - 1u));
+        si[e] = (uint16_t)(4 * (lr * CPP + c) + j + 1);
+        if constexpr (C8)
+          sv[e] = f32_to_e4m3(z[j]);
+        else if constexpr (BF16)
+          reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)f32_to_bf16_bits(z[j]);
+        else
+          reinterpret_cast<float*>(sv)[e] = z[j];
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int lane = (int)(threadIdx.x & 63);
+  const int rows = max(0, min(RPW, T - t0w));
+  auto copy = [&](const uint8_t* src, uint8_t* dst, int nbytes) {
+    const int nw = (reinterpret_cast<uintptr_t>(dst) & 3) == 0 ? nbytes >> 2 : 0;
+    for (int i = lane; i < nw; i += 64)
+      *reinterpret_cast<uint32_t*>(dst + 4 * i) = *reinterpret_cast<const uint32_t*>(src + 4 * i);
+    for (int i = 4 * nw + lane; i < nbytes; i += 64) dst[i] = src[i];
+  };
+  copy(stage, idx_plane + (uint64_t)t0w * k * 2, rows * k * 2);
+  copy(sv, val_plane + (uint64_t)t0w * k * VB, rows * k * VB);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();  // the staging is free for the next rows
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int D, bool BF16, int NB>
 __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   constexpr int E = BF16 ? 2 : 4;
   constexpr int NP = D * E / 16;        // 16-byte pieces per row
   constexpr int RPP = 256 / NP;         // rows per pass
   constexpr int RPW = 64 / NP;          // rows of a pass per wave
-  // per wave: RPW rows x (k index bytes + k values of up to 4 bytes)
-  __shared__ __attribute__((aligned(16))) uint8_t stage[4][RPW * D * 5 + 16];
+  // per wave: RPW rows x (k indices of up to 2 bytes + k values of up to 4 bytes)
+  __shared__ __attribute__((aligned(16))) uint8_t stage[4][RPW * D * 6 + 16];
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
   const int first = P.bl.first[bi];
   const int unit = P.bl.block[bi] * P.hkv + head;
@@ -185,8 +261,9 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
   const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E, NB);
   const int piece = threadIdx.x % NP;
   const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
-  // pairs with per-token channel residuals take the residual entries in this pass too
-  const bool resid = NB == 2 && mode == kResidual && !P.tokres && P.topk > 0;
+  // residual heads with per-token channel (pairs) or coefficient (fours)
+  // entries take them in this pass too
+  const bool resid = mode == kResidual && !P.tokres && P.topk > 0;
   // FP8 shared planes fill whole 1 KB blocks of R8 rows: the rows after the
   // last token of its block are written as zeros, so that a decode tile (one
   // block) reads no stale bytes (R8 divides the rows of a pass, so they lie
@@ -231,11 +308,30 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
       store_stream(seg + L.mk + off, mean_piece<BF16, NB>(ka));
       store_stream(seg + L.mv + off, mean_piece<BF16, NB>(va));
     }
+    if constexpr (NB == 4) {
+      if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
+        const int wave = threadIdx.x >> 6;
+        const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
+        const int rw = (threadIdx.x & 63) / NP;
+        // the probe's K selection of this row, when given (rows past the end take 0)
+        uint32_t kpre = 0;
+        if (P.ksel && live)
+          kpre = *reinterpret_cast<const uint32_t*>(P.ksel + selection_offset(unit, T, t, piece, D, E, 4));
+        const uint32_t* kp = P.ksel ? &kpre : nullptr;
+        if (c8) {
+          residual_entries4<D, BF16, true>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
+          residual_entries4<D, BF16, true>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+        } else {
+          residual_entries4<D, BF16, false>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
+          residual_entries4<D, BF16, false>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+        }
+      }
+    }
     if constexpr (NB == 2) {
       if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
         const int wave = threadIdx.x >> 6;
         const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
-        const int kpre = (P.ksel && live) ? (int)P.ksel[selection_offset(unit, T, t, piece, D, E)]
+        const int kpre = (P.ksel && live) ? (int)P.ksel[selection_offset(unit, T, t, piece, D, E, P.ksel_bytes)]
                                           : (P.ksel ? 0 : -1);
         if (c8) {
           residual_entries<D, BF16, true>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
@@ -249,196 +345,6 @@ __global__ __launch_bounds__(256) void compress_dense_kernel(CompressParams P) {
                                            seg + L.vv, stage[wave]);
         }
       }
-    }
-  }
-}
-
-// ---------------------------------------------------------------- residual select, blocks of four
-// The coefficients of the token's block come 16 channels at a time: the
-// wave loads those channels of its 64 tokens from the four layers
-// (coalesced), evaluates the DCT-II(4) butterfly in fp32 with every product
-// and sum rounded on its own, and leaves Z_1..Z_3 in LDS, [token][channel][j]
-// (float4 slots rotated by the token so one-row-per-lane reads spread over
-// the banks).  Each lane then reads its token's 48 values.
-//  pass 1 - threshold: a running list of the RS largest keys (sorted
-//           descending) absorbs each sorted group of 16 keys (one frequency
-//           of one chunk) by the bitonic merge of topk_net.h; tau is its
-//           k-th entry and the list holds every key above tau.
-//  pass 2 - selection in code order (channel, then frequency): every key
-//           above tau and the first keys equal to tau until k are taken;
-//           each candidate is written to the lane's LDS slot at its running
-//           count, which advances only when it is taken (the count stops at
-//           k, hence k + 1 slots), and the k slots are then stored as packed
-//           words.
-__device__ __forceinline__ int z4_slot(int t, int q) {  // float4 slot of quarter q (0..11) of token t's row
-  return t * 12 + (q + t) % 12;
-}
-
-template <int D, bool BF16, int RS>
-__global__ __launch_bounds__(64) void residual_select4_kernel(SelectParams P) {
-  constexpr int E = BF16 ? 2 : 4;
-  constexpr int CPP = 16 / E;           // channels per input piece
-  constexpr int PPC = 16 / CPP;         // pieces per chunk of 16 channels
-  constexpr int NC = D / 16;            // chunks
-  __shared__ float4 zs[64 * 12];        // [token][16 channels][3] of one chunk
-  __shared__ uint2 slot[64 * (RS + 1)];  // per lane: (code, value bits) of the taken entries
-
-  const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
-  const int first = P.bl.first[bi];
-  const int unit = P.bl.block[bi] * P.hkv + head;
-  const int tensor = blockIdx.z;        // 0: K, 1: V
-  if (P.modes && mode_of(P.modes[unit]) != kResidual) return;
-  const int T = P.seq_len, k = P.topk;
-  const int lane = threadIdx.x;
-  const int tok0 = blockIdx.x * 64;
-  const uint64_t row_bytes = (uint64_t)D * E;
-  const void* const* src = tensor ? P.v : P.k;
-  const uint64_t head_off = (uint64_t)head * T * row_bytes;
-  const uint8_t* x[4];
-#pragma unroll
-  for (int n = 0; n < 4; ++n) x[n] = static_cast<const uint8_t*>(src[first + n]) + head_off;
-
-  // The workgroup is one wave, so the staging needs only wave-scope ordering
-  // (LDS operations of a wave complete in order): no workgroup barrier, which
-  // would also wait for the next chunk's loads already in flight.
-  auto wave_sync = [] {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-  };
-  uint4 vin[PPC][4];  // the next chunk's input pieces, loaded ahead of its use
-  auto load = [&](int ch) {
-#pragma unroll
-    for (int i = 0; i < PPC; ++i) {
-      const int r = lane / PPC + (64 / PPC) * i, pc = lane % PPC;
-      const int t = min(tok0 + r, T - 1);
-      const uint64_t off = (uint64_t)t * row_bytes + (uint64_t)(ch * PPC + pc) * 16;
-#pragma unroll
-      for (int n = 0; n < 4; ++n) vin[i][n] = *reinterpret_cast<const uint4*>(x[n] + off);
-    }
-  };
-  auto stage = [&]() {  // Z of the loaded chunk's 16 channels into LDS
-    wave_sync();        // the previous chunk's rows are read
-#pragma unroll
-    for (int i = 0; i < PPC; ++i) {
-      const int r = lane / PPC + (64 / PPC) * i, pc = lane % PPC;
-      float z[3 * CPP];
-#pragma unroll
-      for (int c = 0; c < CPP; ++c)
-        dct4_high(chan<BF16>(vin[i][0], c), chan<BF16>(vin[i][1], c), chan<BF16>(vin[i][2], c),
-                  chan<BF16>(vin[i][3], c), z[3 * c], z[3 * c + 1], z[3 * c + 2]);
-#pragma unroll
-      for (int q = 0; q < 3 * CPP / 4; ++q)
-        zs[z4_slot(r, pc * (3 * CPP / 4) + q)] = make_float4(z[4 * q], z[4 * q + 1], z[4 * q + 2], z[4 * q + 3]);
-    }
-    wave_sync();
-  };
-  auto row = [&](float (&zr)[48]) {
-#pragma unroll
-    for (int q = 0; q < 12; ++q) {
-      const float4 v = zs[z4_slot(lane, q)];
-      zr[4 * q] = v.x;
-      zr[4 * q + 1] = v.y;
-      zr[4 * q + 2] = v.z;
-      zr[4 * q + 3] = v.w;
-    }
-  };
-
-  // pass 1: the RS largest keys
-  uint32_t R[RS];
-#pragma unroll
-  for (int i = 0; i < RS; ++i) R[i] = 0u;
-  load(0);
-  for (int ch = 0; ch < NC; ++ch) {
-    stage();
-    load(ch + 1 < NC ? ch + 1 : 0);  // the last one starts pass 2
-    float zr[48];
-    row(zr);
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-      uint32_t g[16];
-#pragma unroll
-      for (int c = 0; c < 16; ++c) g[c] = as_u32(zr[3 * c + j]) & 0x7FFFFFFFu;
-      net::absorb16<RS>(R, g);
-    }
-  }
-  int need_eq;
-  const uint32_t tau = net::list_threshold<RS>(R, k, &need_eq);
-
-  // pass 2: selection in code order into the lane's slots
-  uint2* my = slot + lane * (RS + 1);
-  int s = 0, eq = 0;
-  for (int ch = 0; ch < NC; ++ch) {
-    stage();
-    if (ch + 1 < NC) load(ch + 1);
-    float zr[48];
-    row(zr);
-#pragma unroll
-    for (int c = 0; c < 16; ++c)
-#pragma unroll
-      for (int j = 0; j < 3; ++j) {
-        const float z = zr[3 * c + j];
-        const uint32_t key = as_u32(z) & 0x7FFFFFFFu;
-        const bool take = key > tau || (key == tau && eq < need_eq);
-        eq += key == tau ? 1 : 0;
-        my[s] = make_uint2((uint32_t)(4 * (16 * ch + c) + j + 1), as_u32(z));
-        s += take ? 1 : 0;
-      }
-  }
-
-  // store: codes as uint16, values in the coefficient type, packed in words
-  const int t = tok0 + lane;
-  if (t >= T) return;
-  const bool c8 = BF16 && P.coef8;      // values in FP8 E4M3
-  const int CE = c8 ? 1 : E;
-  uint8_t* out_idx;
-  uint8_t* out_val = nullptr;
-  if (P.modes) {
-    uint8_t* seg = P.cache + P.seg_off[unit];
-    const SegLayout L = seg_layout(kResidual, T, D, k, E, CE, 4);
-    out_idx = seg + (tensor ? L.iv : L.ik);
-    out_val = seg + (tensor ? L.vv : L.vk);
-  } else {  // probe workspace: one slot per (block of four in the list, KV head)
-    out_idx = P.idx_out + (uint64_t)blockIdx.y * probe_idx_stride(T, k);
-  }
-  auto value_bits = [&](int e) -> uint32_t {  // entry e in the coefficient type
-    const float z = as_f32(my[e].y);
-    if (c8) return f32_to_e4m3(z);
-    if constexpr (BF16)
-      return f32_to_bf16_bits(z);
-    else
-      return as_u32(z);
-  };
-  uint32_t* oi = reinterpret_cast<uint32_t*>(out_idx + (uint64_t)t * k * 2);
-  if ((k & 1) == 0) {
-#pragma unroll
-    for (int w = 0; w < RS / 2; ++w)
-      if (2 * w < k) oi[w] = my[2 * w].x | (my[2 * w + 1].x << 16);
-  } else {
-    for (int e = 0; e < k; ++e) reinterpret_cast<uint16_t*>(oi)[e] = (uint16_t)my[e].x;
-  }
-  if (!out_val) return;
-  uint8_t* ov = out_val + (uint64_t)t * k * CE;
-  if (CE == 4) {
-#pragma unroll
-    for (int e = 0; e < RS; ++e)
-      if (e < k) reinterpret_cast<uint32_t*>(ov)[e] = value_bits(e);
-  } else if (CE == 2 && (k & 1) == 0) {
-#pragma unroll
-    for (int w = 0; w < RS / 2; ++w)
-      if (2 * w < k) reinterpret_cast<uint32_t*>(ov)[w] = value_bits(2 * w) | (value_bits(2 * w + 1) << 16);
-  } else if (CE == 1 && (k & 3) == 0) {
-#pragma unroll
-    for (int w = 0; w < RS / 4; ++w)
-      if (4 * w < k)
-        reinterpret_cast<uint32_t*>(ov)[w] = value_bits(4 * w) | (value_bits(4 * w + 1) << 8) |
-                                             (value_bits(4 * w + 2) << 16) | (value_bits(4 * w + 3) << 24);
-  } else {
-    for (int e = 0; e < k; ++e) {
-      const uint32_t v = value_bits(e);
-      if (CE == 1)
-        ov[e] = (uint8_t)v;
-      else
-        reinterpret_cast<uint16_t*>(ov)[e] = (uint16_t)v;
     }
   }
 }
@@ -462,26 +368,5 @@ hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s) {
   return P.bsize == 4 ? launch_compress_b<4>(P, s) : launch_compress_b<2>(P, s);
 }
 
-template <int D, bool BF16, int RS>
-static hipError_t launch_select4_t(const SelectParams& P, int tensors, hipStream_t s) {
-  const dim3 grid((P.seq_len + 63) / 64, P.bl.n * P.hkv, tensors);
-  hipLaunchKernelGGL((residual_select4_kernel<D, BF16, RS>), grid, dim3(64), 0, s, P);
-  return hipGetLastError();
-}
-
-template <int D, bool BF16>
-static hipError_t launch_select4_d(const SelectParams& P, int tensors, hipStream_t s) {
-  if (P.topk <= 16) return launch_select4_t<D, BF16, 16>(P, tensors, s);
-  if (P.topk <= 32) return launch_select4_t<D, BF16, 32>(P, tensors, s);
-  if (P.topk <= 64) return launch_select4_t<D, BF16, 64>(P, tensors, s);
-  return launch_select4_t<D, BF16, 128>(P, tensors, s);
-}
-
-hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s) {
-  if (P.topk <= 0 || P.bl.n == 0 || P.seq_len == 0) return hipSuccess;
-  if (P.bsize != 4) return hipErrorInvalidValue;  // pairs select inside the dense and Gram passes
-  if (P.d == 128) return P.bf16 ? launch_select4_d<128, true>(P, tensors, s) : launch_select4_d<128, false>(P, tensors, s);
-  return P.bf16 ? launch_select4_d<64, true>(P, tensors, s) : launch_select4_d<64, false>(P, tensors, s);
-}
 
 }  // namespace fdkv

@@ -146,24 +146,20 @@ Sched sched_of(const fdkv_dims* d) {
 
 uint64_t probe_chunks(int T) { return (uint64_t)(T + kProbeChunk - 1) / kProbeChunk; }
 
-// Probe workspace regions, each aligned to 256 bytes: residual codes per unit
-// of a block of four (pairs find theirs inside the Gram kernel), probe Gram
-// matrices per (layer, KV head), per-chunk partials.
+// Probe workspace: probe Gram matrices per (layer, KV head) and per-chunk
+// partials (every block finds its top-k inside its Gram kernel).
 struct ProbeWs {
-  uint64_t idx, gram, part, total;
+  uint64_t gram, part, total;
 };
 ProbeWs probe_ws_layout(const fdkv_dims* d, int T) {
   const Sched sch = sched_of(d);
-  int quads = 0;
-  for (int i = 0; i < sch.n; ++i) quads += sch.size[i] == 4;
   const uint64_t units = (uint64_t)sch.n * d->n_kv_heads;
   ProbeWs w{};
   if (tokens_mode(d)) {  // the token scores' sums of squares
     w.total = plane_bytes(units * (uint64_t)T * 4);
     return w;
   }
-  w.idx = 0;
-  w.gram = w.idx + (uint64_t)quads * d->n_kv_heads * probe_idx_stride((uint64_t)T, d->topk);
+  w.gram = 0;
   w.part = w.gram + plane_bytes((uint64_t)d->n_layers * d->n_kv_heads * d->head_dim * d->head_dim * 4);
   w.total = w.part + plane_bytes(units * probe_chunks(T) * 2 * 4);
   return w;
@@ -368,13 +364,21 @@ fdkv_status fdkv_probe_workspace(const fdkv_dims* dims, int32_t seq_len, int32_t
   return FDKV_OK;
 }
 
+// Bytes per input piece of the probe's K selections: a 32-bit mask when the
+// schedule has blocks of four (3 CPP coefficients a piece), else a byte.
+int selection_slot_bytes(const Sched& sch) {
+  for (int i = 0; i < sch.n; ++i)
+    if (sch.size[i] == 4) return 4;
+  return 1;
+}
+
 fdkv_status fdkv_selection_bytes(const fdkv_dims* dims, int32_t seq_len, size_t* bytes) {
   fdkv_status st = check_dims(dims);
   if (st != FDKV_OK) return st;
   if (seq_len < 0 || !bytes) return FDKV_E_INVALID_ARG;
   const Sched sch = sched_of(dims);
   *bytes = (size_t)((uint64_t)sch.n * dims->n_kv_heads * (uint64_t)seq_len *
-                    selection_row_bytes(dims->head_dim, elem_bytes(dims)));
+                    selection_pieces(dims->head_dim, elem_bytes(dims)) * selection_slot_bytes(sch));
   return FDKV_OK;
 }
 
@@ -389,7 +393,8 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   if ((uint64_t)seq_len * row_bytes >= (1ull << 31) ||
       (uint64_t)n_probe * (dims->n_q_heads / dims->n_kv_heads) * row_bytes >= (1ull << 31))
     return FDKV_E_UNSUPPORTED;
-  if (!aligned(errors_out, 4) || !aligned(ws, 256)) return FDKV_E_INVALID_ARG;
+  if (!aligned(errors_out, 4) || !aligned(ws, 256) || (k_select_out && !aligned(k_select_out, 4)))
+    return FDKV_E_INVALID_ARG;
   for (int l = 0; l < dims->n_layers; ++l)
     if (!aligned(k_layers[l], 16) || !aligned(qp_layers[l], 16)) return FDKV_E_INVALID_ARG;
   const ProbeWs w = probe_ws_layout(dims, seq_len);
@@ -429,23 +434,13 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
     }
     return FDKV_OK;
   }
-  SelectParams sp{};
-  for (int l = 0; l < dims->n_layers; ++l) sp.k[l] = sp.v[l] = k_layers[l];
-  sp.modes = nullptr;
-  sp.idx_out = base + w.idx;
-  sp.seq_len = seq_len;
-  sp.hkv = dims->n_kv_heads;
-  sp.d = dims->head_dim;
-  sp.topk = dims->topk;
-  sp.bf16 = dims->dtype != FDKV_F32;
-
   ProbeParams pp{};
   for (int l = 0; l < dims->n_layers; ++l) {
     pp.k[l] = k_layers[l];
     pp.qp[l] = qp_layers[l];
   }
-  pp.idx = base + w.idx;
   pp.ksel = k_select_out;
+  pp.ksel_bytes = selection_slot_bytes(sch);
   pp.gram_q = reinterpret_cast<float*>(base + w.gram);
   pp.partial = reinterpret_cast<float*>(base + w.part);
   pp.errors = errors_out;
@@ -460,15 +455,10 @@ fdkv_status fdkv_probe(const fdkv_dims* dims, int32_t seq_len, const void* const
   pp.n_chunks = (int)probe_chunks(seq_len);
   pp.bf16 = dims->dtype != FDKV_F32;
   for (int B = 2; B <= 4; B += 2) {
-    sp.bl = pp.bl = blocks_of_size(sch, B);
-    sp.bsize = pp.bsize = B;
-    if (sp.bl.n == 0) continue;
-    hipError_t e = hipSuccess;
-    if (B == 4) {  // pairs find their top-k inside the Gram kernel
-      e = launch_residual_select(sp, 1, s);
-      if (e != hipSuccess) return hip_fail(e, "residual_select");
-    }
-    e = launch_probe(pp, s);
+    pp.bl = blocks_of_size(sch, B);
+    pp.bsize = B;
+    if (pp.bl.n == 0) continue;
+    const hipError_t e = launch_probe(pp, s);  // every block takes its top-k inside its Gram kernel
     if (e != hipSuccess) return hip_fail(e, "probe");
   }
   const hipError_t e = launch_probe_finalize(pp, s);
@@ -490,24 +480,25 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
 
   const Sched sch = sched_of(dims);
   CompressParams cp{};
-  SelectParams sp{};
   for (int l = 0; l < dims->n_layers; ++l) {
-    cp.k[l] = sp.k[l] = k_layers[l];
-    cp.v[l] = sp.v[l] = v_layers[l];
+    cp.k[l] = k_layers[l];
+    cp.v[l] = v_layers[l];
   }
-  cp.modes = sp.modes = modes;
-  cp.seg_off = sp.seg_off = seg_offsets;
-  cp.cache = sp.cache = static_cast<uint8_t*>(cache);
-  cp.seq_len = sp.seq_len = seq_len;
-  cp.hkv = sp.hkv = dims->n_kv_heads;
-  cp.d = sp.d = dims->head_dim;
-  cp.topk = sp.topk = dims->topk;
-  cp.bf16 = sp.bf16 = dims->dtype != FDKV_F32;
-  cp.coef8 = sp.coef8 = dims->dtype == FDKV_BF16_E4M3;
+  cp.modes = modes;
+  cp.seg_off = seg_offsets;
+  cp.cache = static_cast<uint8_t*>(cache);
+  cp.seq_len = seq_len;
+  cp.hkv = dims->n_kv_heads;
+  cp.d = dims->head_dim;
+  cp.topk = dims->topk;
+  cp.bf16 = dims->dtype != FDKV_F32;
+  cp.coef8 = dims->dtype == FDKV_BF16_E4M3;
   const bool tok = tokens_mode(dims);
   cp.tokres = tok;
   cp.ksel = tok ? nullptr : k_select;
+  cp.ksel_bytes = selection_slot_bytes(sch);
   if (tok && !aligned(token_scores, 4)) return FDKV_E_INVALID_ARG;
+  if (!tok && k_select && !aligned(k_select, 4)) return FDKV_E_INVALID_ARG;
   TokenParams tp{};
   for (int l = 0; l < dims->n_layers; ++l) {
     tp.k[l] = k_layers[l];
@@ -527,8 +518,8 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
   tp.bf16 = cp.bf16;
   tp.coef8 = cp.coef8;
   for (int B = 2; B <= 4; B += 2) {
-    cp.bl = sp.bl = tp.bl = blocks_of_size(sch, B);
-    cp.bsize = sp.bsize = tp.bsize = B;
+    cp.bl = tp.bl = blocks_of_size(sch, B);
+    cp.bsize = tp.bsize = B;
     if (cp.bl.n == 0) continue;
     hipError_t e = launch_compress_dense(cp, s);
     if (e != hipSuccess) return hip_fail(e, "compress_dense");
@@ -537,10 +528,7 @@ fdkv_status fdkv_compress(const fdkv_dims* dims, int32_t seq_len, const void* co
       if (e != hipSuccess) return hip_fail(e, "token_select");
       e = launch_token_rows(tp, s);
       if (e != hipSuccess) return hip_fail(e, "token_rows");
-    } else if (B == 4) {  // pairs take their residual entries in the dense pass
-      e = launch_residual_select(sp, 2, s);
-      if (e != hipSuccess) return hip_fail(e, "residual_select");
-    }
+    }  // per-token channel residuals: the dense pass takes their entries
   }
   return FDKV_OK;
 }

@@ -33,18 +33,23 @@ struct CompressParams {
   bool tokres;                 // token-level residual set (else per-token channel top-k)
   int res_ppm;                 // its fraction of tokens, parts per million
   const float* scores;         // token scores [blocks][hkv][T] (token-level residual set)
-  const uint8_t* ksel;         // the probe's K selections of pairs (selection_offset), or null
+  const uint8_t* ksel;         // the probe's K selections (selection_offset), or null
+  int ksel_bytes;              // bytes per piece of ksel (1, or 4 with blocks of four)
 };
 
-// The K channel selections of pairs that the probe takes and compress may
-// reuse: unit u's row t holds one byte per 16-byte input piece p (bit i:
-// channel CPP p + i, CPP = 16 / element bytes) at selection_offset(u, t, p).
-__host__ __device__ __forceinline__ uint64_t selection_row_bytes(int d, int elem_bytes) {
+// The K selections that the probe takes and compress may reuse: unit u's
+// row t holds one slot of sb bytes per 16-byte input piece p at
+// selection_offset(u, t, p): a pair's mask of the piece's CPP channels
+// (bit i: channel CPP p + i, CPP = 16 / element bytes) in the slot's first
+// byte, a block of four's mask of the piece's 3 CPP coefficients (bit
+// 3 c + j - 1: Z_j of channel CPP p + c) as a 32-bit word.  sb is 4 when the
+// schedule has blocks of four, else 1.
+__host__ __device__ __forceinline__ uint64_t selection_pieces(int d, int elem_bytes) {
   return (uint64_t)d * elem_bytes / 16;
 }
 __host__ __device__ __forceinline__ uint64_t selection_offset(uint64_t unit, uint64_t T, uint64_t t, int p,
-                                                             int d, int elem_bytes) {
-  return (unit * T + t) * selection_row_bytes(d, elem_bytes) + (uint64_t)p;
+                                                             int d, int elem_bytes, int sb) {
+  return ((unit * T + t) * selection_pieces(d, elem_bytes) + (uint64_t)p) * (uint64_t)sb;
 }
 
 // Token-level residual set: score kernel (probe), selection and rows.
@@ -69,19 +74,6 @@ struct TokenParams {
 __host__ __device__ __forceinline__ int unit_ppm(int res_ppm, int n_rates, const int* rates, uint32_t byte) {
   return n_rates ? rates[rate_of(byte)] : res_ppm;
 }
-
-struct SelectParams {
-  const void* k[kMaxPtrLayers];
-  const void* v[kMaxPtrLayers];
-  const uint8_t* modes;        // null: select every unit (probe); else residual units only
-  const uint64_t* seg_off;
-  uint8_t* cache;
-  uint8_t* idx_out;            // probe: [units] planes of plane_bytes(T*k*index bytes) bytes
-  BlockList bl;                // blocks of size bsize
-  int seq_len, bsize, hkv, d, topk;
-  bool bf16;
-  bool coef8;                  // residual values in FP8 E4M3 (bf16 inputs)
-};
 
 // decode: tokens per wave and waves per workgroup of the split-K kernel
 constexpr int kDecodeChunk = 128;
@@ -149,24 +141,18 @@ constexpr int kProbeChunk = 1024;   // tokens per probe workgroup
 struct ProbeParams {
   const void* k[kMaxPtrLayers];
   const void* qp[kMaxPtrLayers];
-  const uint8_t* idx;          // K residual indices per unit (from residual_select)
   float* gram_q;               // [layers][hkv][d][d]  sums of q q^T over probe rows (see probe.hip)
   float* partial;              // [units][n_chunks][2]
   float* errors;               // [units][2]
-  uint8_t* ksel;               // out: the K selections of pairs (selection_offset), or null
+  uint8_t* ksel;               // out: the K selections (selection_offset), or null
+  int ksel_bytes;              // bytes per piece of ksel (1, or 4 with blocks of four)
   BlockList bl;                // blocks of size bsize
   int8_t bsizes[kMaxBlocks];   // every block's size (finalize)
   int seq_len, bsize, n_blocks, hkv, hq, d, topk, n_probe, n_chunks;
   bool bf16;
 };
 
-// Bytes per unit of the probe's residual-index workspace (room for uint16 codes).
-__host__ __device__ __forceinline__ uint64_t probe_idx_stride(uint64_t T, int k) {
-  return (T * (uint64_t)k * 2 + 255) / 256 * 256;
-}
-
 hipError_t launch_compress_dense(const CompressParams& P, hipStream_t s);
-hipError_t launch_residual_select(const SelectParams& P, int tensors, hipStream_t s);
 hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // split-K over every part (bf16 or fp32)
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records

@@ -20,13 +20,14 @@
 //   E_m = sum_p < C_{p,m}, S_p > / (4 G P d)
 // with one Gram matrix per layer of the deviations and of the probe rows.
 //
-// Kernels: residual_select / residual_select4 (compress.hip) write every
-// unit's K top-k indices; probe_qgram forms the probe Gram matrices (MFMA
+// Kernels: probe_qgram forms the probe Gram matrices (MFMA
 // Gram of the probe rows for bf16 queries, fp32 VALU for fp32 ones) into
 // per-(layer, KV head) slots: a pair's S_u sits in the slot of its first
 // layer, a block of four has one slot per layer; probe_dgram (pairs) and
-// probe_dgram4 (blocks of four) stream the keys and stage the bf16
-// deviations row-major in LDS; all Gram kernels take their
+// probe_dgram4 (blocks of four) stream the keys once, find each token's
+// top-k in the same pass (the wavefront top-k of rowtopk.h, as compress
+// does), and stage the bf16 deviations row-major in LDS; all Gram kernels
+// take their
 // v_mfma_f32_32x32x16_bf16 operands with transposing LDS reads
 // (ds_read_b64_tr_b16) and accumulate the upper-triangular 32x32 blocks.
 // The deviation Gram kernels contract with the probe Gram matrices in their
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
       const uint32_t keep = ~sel & ((1u << CPP) - 1u);
       if (P.ksel) {  // the selection, for compress to reuse
         const int t = t0 + row;
-        if (t < t_end) P.ksel[selection_offset(unit, T, t, pc, D, E)] = (uint8_t)sel;
+        if (t < t_end) P.ksel[selection_offset(unit, T, t, pc, D, E, P.ksel_bytes)] = (uint8_t)sel;
       }
       uint32_t wd[CPP / 2], wl[CPP / 2], wr[CPP / 2], wrl[CPP / 2];
 #pragma unroll
@@ -410,12 +411,14 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
 // Blocks of four: Gram matrices of the eight deviation matrices (4 layers x
 // shared / residual) over one chunk of kProbeChunk tokens, contracted with
 // the layers' probe Gram matrices.  R tokens per step: each thread takes
-// one or two 16-byte pieces of a token row from all four layers, forms the
-// block mean, the layer deviations, the coefficients Z_1..Z_3 (the same fp32
-// butterfly as residual_select4) and the images of the token's kept
-// coefficients, and writes the eight deviation rows to LDS as bf16 hi + lo
-// pairs (split_bf16x2); wave w accumulates layer w / 2, shared (w even) or
-// residual (w odd), as H H^T + H L^T + L H^T.
+// one 16-byte piece of a token row from all four layers, forms the
+// coefficients Z_1..Z_3 (the fp32 butterfly of dct4.h, as compress ranks
+// them), the token's top-k among the row's 3d coefficients with the other
+// lanes of the row (row_topk_mask), the block mean, the layer deviations and
+// the images of the token's kept coefficients, and writes the eight
+// deviation rows to LDS as bf16 hi + lo pairs (split_bf16x2); wave w
+// accumulates layer w / 2, shared (w even) or residual (w odd), as
+// H H^T + H L^T + L H^T.
 template <int D, bool BF16>
 __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
   constexpr int E = BF16 ? 2 : 4;
@@ -443,10 +446,6 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
   __amdgpu_buffer_rsrc_t kr[4];
 #pragma unroll
   for (int n = 0; n < 4; ++n) kr[n] = make_rsrc(static_cast<const uint8_t*>(P.k[first + n]) + (uint64_t)head * plane, plane);
-  // the residual codes of this (block of four, KV head) in the workspace slot of its list position
-  const uint16_t* codes = reinterpret_cast<const uint16_t*>(P.idx + (uint64_t)blockIdx.y * probe_idx_stride(T, k));
-  const bool k16 = k == 16;                       // a token's codes are two 16-byte loads
-  const auto ir = make_rsrc(codes, k16 ? (uint64_t)T * 32 : 0);
   const int t_begin = chunk * kProbeChunk;
   const int t_end = min(T, t_begin + kProbeChunk);
   const float F1[4] = {kDct4A, kDct4B, -kDct4B, -kDct4A};   // F_4[1][p]
@@ -458,7 +457,7 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
   for (int i = 0; i < NT; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
-  uint4 rx[LPT][4], rc[LPT][2];
+  uint4 rx[LPT][4];
   auto load = [&](int t0) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
@@ -466,32 +465,36 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
       const bool ok = t < t_end;
 #pragma unroll
       for (int n = 0; n < 4; ++n) rx[j][n] = load16(kr[n], ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
-      rc[j][0] = load16(ir, ok ? (uint32_t)t * 32 : kOobOff);       // reads 0 unless k = 16
-      rc[j][1] = load16(ir, ok ? (uint32_t)t * 32 + 16 : kOobOff);
     }
   };
   load(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += R) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
-      const int i = tid + 512 * j, row = i / NPc, pc = i % NPc, t = t0 + row;
-      // kept (channel, frequency) pairs of this piece: bit 3 c + j - 1
-      uint32_t kept = 0;
-      if (k16) {
+      const int i = tid + 512 * j, row = i / NPc, pc = i % NPc;
+      // the token's top-k of its 3d coefficients |Z_j[c]|, found by the NPc
+      // lanes of its row (rows past the chunk read zeros and add nothing):
+      // kept (channel, frequency) pairs of this piece, bit 3 c + j - 1
+      uint32_t key[3 * CPP];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const uint32_t w = word16(rc[j][e >> 3], (e >> 1) & 3);
-          const uint32_t code = (e & 1) ? (w >> 16) : (w & 0xFFFFu);
-          const uint32_t c = (code >> 2) - (uint32_t)(pc * CPP);
-          kept |= (c < (uint32_t)CPP && (code & 3u) != 0u) ? 1u << (3 * c + (code & 3u) - 1) : 0u;
-        }
-      } else if (t < t_end) {
-        for (int e = 0; e < k; ++e) {
-          const uint32_t code = codes[(uint64_t)t * k + e];
-          const uint32_t c = (code >> 2) - (uint32_t)(pc * CPP);
-          if (c < (uint32_t)CPP && (code & 3u) != 0u) kept |= 1u << (3 * c + (code & 3u) - 1);
-        }
+      for (int c = 0; c < CPP; ++c) {
+        float z1, z2, z3;
+        dct4_high(chan_of<BF16>(rx[j][0], c), chan_of<BF16>(rx[j][1], c), chan_of<BF16>(rx[j][2], c),
+                  chan_of<BF16>(rx[j][3], c), z1, z2, z3);
+        key[3 * c] = as_u32(z1) & 0x7FFFFFFFu;
+        key[3 * c + 1] = as_u32(z2) & 0x7FFFFFFFu;
+        key[3 * c + 2] = as_u32(z3) & 0x7FFFFFFFu;
       }
+      const uint32_t kept = row_topk_mask<NPc, 3 * CPP>(key, k);
+      if (P.ksel) {  // the selection, for compress to reuse
+        const int t = t0 + row;
+        if (t < t_end) *reinterpret_cast<uint32_t*>(P.ksel + selection_offset(unit, T, t, pc, D, E, 4)) = kept;
+      }
+      // the deviations below evaluate the butterfly again rather than keep
+      // its 3 CPP results alive beside the accumulators (an empty asm
+      // statement that only marks the input pieces as possibly changed)
+#pragma unroll
+      for (int n = 0; n < 4; ++n) asm volatile("" : "+v"(rx[j][n].x), "+v"(rx[j][n].y), "+v"(rx[j][n].z), "+v"(rx[j][n].w));
       // deviations of the eight matrices, channel pairs at a time, split into bf16 hi + lo
       uint32_t hw[16][CPP / 2];
 #pragma unroll
@@ -503,7 +506,7 @@ __global__ __launch_bounds__(512) void probe_dgram4_kernel(ProbeParams P) {
           float x[4];
 #pragma unroll
           for (int n = 0; n < 4; ++n) x[n] = chan_of<BF16>(rx[j][n], c);
-          float z1, z2, z3;
+          float z1, z2, z3;  // evaluated again (the same rounded operations): fewer live registers
           dct4_high(x[0], x[1], x[2], x[3], z1, z2, z3);
           const float m = ((x[0] + x[3]) + (x[1] + x[2])) * 0.25f;
           const float k1 = (kept >> (3 * c)) & 1u ? z1 : 0.f;

@@ -156,6 +156,9 @@ def test_validation_errors_before_any_device_call(lib):
     assert lib.fdkv_selection_bytes(ctypes.byref(good), 100, ctypes.byref(sb)) == 0
     assert sb.value == (good.n_layers // 2) * good.n_kv_heads * 100 * (good.head_dim * 2 // 16)
     assert lib.fdkv_selection_bytes(ctypes.byref(good), -1, ctypes.byref(sb)) == -1
+    mixed = B.dims(12, 2, 8, 128, 16, "bf16", schedule=B.MIXED)     # blocks 2,2,4,2,2: 4-byte slots
+    assert lib.fdkv_selection_bytes(ctypes.byref(mixed), 100, ctypes.byref(sb)) == 0
+    assert sb.value == 5 * 2 * 100 * 16 * 4
     assert lib.fdkv_selection_bytes(ctypes.byref(good), 100, None) == -1
     assert lib.fdkv_layout(None, 1, None, None, None, None) == -1
 

@@ -354,6 +354,10 @@ REUSE_CASES = {
                           seq_lens=(517,), n_probe=8, n_needles=2, dtype="bf16_e4m3", fixed_modes=(1, 1)),
     "mixed_bf16": scaled(WORKLOADS["llama8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, seq_lens=(300,), n_probe=8,
                          n_needles=2, schedule=1, fixed_modes=(1, 1, 0, 1, 1, 2, 1, 0, 1, 1)),
+    "quads_f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
+                               seq_lens=(211,), n_probe=8, n_needles=0, schedule=2, fixed_modes=(1, 1)),
+    "quads_e4m3_k16": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=4, seq_lens=(260,), n_probe=8,
+                             n_needles=2, schedule=2, dtype="bf16_e4m3", fixed_modes=(1, 1)),
 }
 
 
