@@ -8,9 +8,10 @@
 // Kernels:
 //  * token_score - the probe's logits against the deviations K - K^S of
 //    every layer of the block, with v_mfma_f32_32x32x16_bf16: probe rows
-//    (staged in LDS, shared by the workgroup's four waves) times the
+//    (staged in LDS, shared by the workgroup's eight waves) times the
 //    deviations of 64 tokens per wave (built in registers from the inputs:
-//    fp32 arithmetic rounded to bf16, the score's defined precision).  Per
+//    fp32 arithmetic rounded to bf16 for the MFMA, so a score lies within
+//    (2^-9 + 2^-16) max_q sum_c |q_c| |dev_c| of its exact value).  Per
 //    token: the largest |logit| (the score) and the sum of squares (its
 //    share of Eq. 2).  fp32 queries go in as two bf16 halves.
 //  * token_select - one workgroup per unit: the n-th largest score by a
@@ -94,8 +95,14 @@ __device__ __forceinline__ bf16x8_t pack8(const float (&v)[8]) {
 }  // namespace
 
 // ---------------------------------------------------------------- scores
+// Eight waves (512 tokens) per workgroup share each round of probe rows in
+// LDS: half the probe-row traffic of four waves, 2.35 -> 2.25 ms on the 8B
+// token-set probe (sixteen waves, or 64 rows a round, lose occupancy).
+constexpr int kScoreThreads = 512;
+
 template <int D, bool BF16, int NB>
-__global__ __launch_bounds__(256) void token_score_kernel(TokenParams P) {
+__global__ __launch_bounds__(kScoreThreads) void token_score_kernel(TokenParams P) {
+  constexpr int TH = kScoreThreads;
   constexpr int E = BF16 ? 2 : 4;
   constexpr int KS = D / 16;                 // k-steps of the 32x32x16 MFMA
   constexpr int NPQ = D / 8;                 // 8-channel pieces of a probe row
@@ -118,7 +125,7 @@ __global__ __launch_bounds__(256) void token_score_kernel(TokenParams P) {
   const uint64_t qspan = (uint64_t)GP * RB;  // one layer's probe rows of this KV head
 
   const int tl = lane & 31, kh = lane >> 5;
-  const int tok_w = blockIdx.x * 256 + wave * 64;   // the wave's 64 tokens: two sets of 32
+  const int tok_w = blockIdx.x * TH + wave * 64;   // the wave's 64 tokens: two sets of 32
   float mx[2] = {0.f, 0.f}, ss[2] = {0.f, 0.f};
 
   for (int pass = 0; pass < NL; ++pass) {
@@ -147,12 +154,12 @@ __global__ __launch_bounds__(256) void token_score_kernel(TokenParams P) {
       const auto qr = make_rsrc(static_cast<const uint8_t*>(P.qp[layer]) + (uint64_t)head * qspan, qspan);
       // 32 probe rows per round; the next round's rows are loaded into
       // registers while this round's MFMAs run
-      constexpr int PER = (32 * NPQ + 255) / 256;  // 8-channel pieces per thread and round
+      constexpr int PER = (32 * NPQ + TH - 1) / TH;  // 8-channel pieces per thread and round
       float qn[PER][8];
       auto fetch = [&](int r0) {
 #pragma unroll
         for (int j = 0; j < PER; ++j) {
-          const int i = tid + 256 * j, row = i / NPQ, pc = i % NPQ;
+          const int i = tid + TH * j, row = i / NPQ, pc = i % NPQ;
           load8<BF16>(qr, (uint32_t)((r0 + row) * RB + pc * 8 * E), i < 32 * NPQ && r0 + row < GP, qn[j]);
         }
       };
@@ -161,7 +168,7 @@ __global__ __launch_bounds__(256) void token_score_kernel(TokenParams P) {
         __syncthreads();  // the previous round's rows are read
 #pragma unroll
         for (int j = 0; j < PER; ++j) {
-          const int i = tid + 256 * j, row = i / NPQ, pc = i % NPQ;
+          const int i = tid + TH * j, row = i / NPQ, pc = i % NPQ;
           if (i >= 32 * NPQ) continue;
           const float* q = qn[j];
           uint32_t hi[4], lo[4];
@@ -472,8 +479,8 @@ __global__ __launch_bounds__(256) void token_rows_kernel(TokenParams P) {
 // ---------------------------------------------------------------- launchers
 template <int D, bool BF16, int NB>
 static hipError_t launch_scores_t(const TokenParams& P, hipStream_t s) {
-  const dim3 grid((P.seq_len + 255) / 256, P.bl.n * P.hkv);
-  hipLaunchKernelGGL((token_score_kernel<D, BF16, NB>), grid, dim3(256), 0, s, P);
+  const dim3 grid((P.seq_len + kScoreThreads - 1) / kScoreThreads, P.bl.n * P.hkv);
+  hipLaunchKernelGGL((token_score_kernel<D, BF16, NB>), grid, dim3(kScoreThreads), 0, s, P);
   return hipGetLastError();
 }
 
