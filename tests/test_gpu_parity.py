@@ -309,13 +309,24 @@ TIE_CASES = {
                           seq_lens=(333,), n_needles=0, fixed_modes=(1, 1)),
     "e4m3_k12": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, topk=12, seq_lens=(300,),
                        n_needles=0, fixed_modes=(1, 1), dtype="bf16_e4m3"),
+    "bf16_k1": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=1, n_q_heads=2, topk=1, seq_lens=(129,),
+                      n_needles=0, fixed_modes=(1,)),
+    # blocks of four: 3d coefficients per row, 24 keys a lane (bf16) or 12 (fp32)
+    "quads_bf16_k16": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=16, seq_lens=(301,),
+                             n_needles=0, schedule=2, fixed_modes=(1, 1)),
+    "quads_bf16_k1": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=1, n_q_heads=2, topk=1, seq_lens=(77,),
+                            n_needles=0, schedule=2, fixed_modes=(1,)),
+    "quads_bf16_k128": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=1, n_q_heads=2, topk=128, seq_lens=(65,),
+                              n_needles=0, schedule=2, fixed_modes=(1,)),
+    "quads_f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
+                               seq_lens=(99,), n_needles=0, schedule=2, fixed_modes=(1, 1)),
 }
 
 
 def _tie_heavy(K, V, seed: int):
-    """Inputs whose channel differences tie often: values on a coarse grid,
-    every 7th token with equal layers (all keys zero), every 11th with the
-    second layer a constant shift of the first (all keys equal)."""
+    """Inputs whose residual keys tie often: values on a coarse grid, every
+    7th token with equal layers (all keys zero), every 11th with each later
+    layer a constant shift of the first (pairs: all keys equal)."""
     rng = np.random.default_rng(seed)
     out = []
     for X in (K, V):
@@ -323,16 +334,19 @@ def _tie_heavy(K, V, seed: int):
         X += rng.integers(-2, 3, size=X.shape) * 0.25 * (rng.random(X.shape) < 0.3)
         X = np.clip(X, -4.0, 4.0).astype(np.float32)
         T = X.shape[2]
-        X[1, :, 0:T:7] = X[0, :, 0:T:7]
-        X[1, :, 0:T:11] = X[0, :, 0:T:11] + np.float32(0.5)
+        for n in range(1, X.shape[0]):
+            X[n, :, 0:T:7] = X[0, :, 0:T:7]
+            X[n, :, 0:T:11] = X[0, :, 0:T:11] + np.float32(0.5 * n)
         out.append(X)
     return out
 
 
 @pytest.mark.parametrize("name", list(TIE_CASES))
 def test_compress_residual_ties(torch_dev, name):
-    """Residual channel sets under heavy ties: bit-exact indices (ties to the
-    lower channel), values within 1 ulp."""
+    """Residual entries under heavy ties: pairs' indices bit-exact (ties to the
+    lower channel) with values within 1 ulp; blocks of four's codes by the
+    near-tie rule of check_quad_codes (ties to the lower code) with values
+    within the butterfly's bound."""
     w = TIE_CASES[name]
     log(f"[case] compress ties {name} T={w.seq_lens} d={w.head_dim} k={w.topk} {w.dtype}")
     K, V = gen.layer_cache(w, 0)
