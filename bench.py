@@ -346,6 +346,18 @@ def main():
         ev1.record(stream)
         torch.cuda.synchronize()
         step_ms = ev0.elapsed_time(ev1) / args.steps
+        # the per-step spread, after the timed region: the same steps again, each bracketed by its
+        # own events (the mean of these includes the events themselves; `value` does not)
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for i in range(args.steps):
+            sev[i][0].record(stream)
+            run(args.warmup + i)
+            sev[i][1].record(stream)
+        torch.cuda.synchronize()
+        per_step = np.array([a.elapsed_time(b) for a, b in sev])
+        step_stats = {"n": args.steps, "mean": float(per_step.mean()), "p50": float(np.percentile(per_step, 50)),
+                      "p95": float(np.percentile(per_step, 95)), "min": float(per_step.min()),
+                      "max": float(per_step.max())}
 
         # per-launch timing with HIP events on the launch stream, each phase replayed as a graph of
         # the step's L launches in cold layer order (every layer's split-K records come from HBM, as
@@ -569,7 +581,8 @@ def main():
     res = {
         "metric": "compressed-KV decode attn tokens/s + achieved HBM GB/s vs 8 TB/s, 32k ctx",
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "ms_per_step": step_ms, "step_ms_stats": step_stats, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
         "dtype": w.dtype, "data": "synthetic (seeded generator, layers correlated along depth within each block, needles)",
         "config": cfg,
         "step_hbm_gbs": step_gbs,
