@@ -110,6 +110,92 @@ __device__ __forceinline__ float run_sum(int c, float x, int pc, bool valid, boo
   return x + (n1 ? x1 : 0.f) + (n2 ? x2 : 0.f);
 }
 
+// Lane exchange across bit B of a row's lane index (rows of 8 or 16 lanes).
+// Bits 3 and 2 use the mirrors, which also flip the lower bits: that still
+// pairs each lane with one of the other half, and once the lower bits hold
+// equal values (duplicates, or lists already gathered) it is the plain swap.
+template <int B>
+__device__ __forceinline__ uint32_t swap_bit(uint32_t x) {
+  constexpr int kCtrl = B == 3 ? kDppRowMirror : B == 2 ? kDppRowHalfMirror : B == 1 ? kDppQuadXor2 : kDppQuadXor1;
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kCtrl, 0xF, 0xF, false);
+}
+template <int B>
+__device__ __forceinline__ float swap_bit(float x) {
+  return __uint_as_float(swap_bit<B>(__float_as_uint(x)));
+}
+
+// The lane NP/2 further along a row of NP lanes (the lane holding the same
+// head for the other row of a load): row_ror:8 for 16 lanes; for 8 lanes,
+// row_shl:4 into banks 0 and 2 and row_shr:4 into banks 1 and 3.
+template <int NP>
+__device__ __forceinline__ float swap_half(float x) {
+  if constexpr (NP == 16) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
+  } else {
+    static_assert(NP == 8, "row width");
+    int y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x104, 0xF, 0x5, false);
+    y = __builtin_amdgcn_update_dpp(y, __float_as_int(x), 0x114, 0xF, 0xA, false);
+    return __int_as_float(y);
+  }
+}
+
+// One reduce-scatter stage across lane bit B: the lanes with the bit clear
+// keep the list's lower half and add their partner's copy of it, the others
+// the upper half.
+template <int B, int H, int V>
+__device__ __forceinline__ void scatter_stage(float (&a)[V], int lane) {
+  const bool up = (lane >> B) & 1;
+#pragma unroll
+  for (int t = 0; t < H; ++t) {
+    const float keep = up ? a[t + H] : a[t], send = up ? a[t] : a[t + H];
+    a[t] = keep + swap_bit<B>(send);
+  }
+}
+
+// Sum of V values over the 2^NPB lanes of a row, one sum per lane: the
+// stages on the top log2(V) lane bits split the list (lane bits b, from the
+// top, choose the half), butterflies on the lower bits finish the sums, so
+// the lane holds value number (lane % 2^NPB) >> (NPB - log2 V).
+template <int NPB, int V>
+__device__ __forceinline__ float row_reduce_scatter(float (&a)[V], int lane) {
+  constexpr int RB = V == 16 ? 4 : V == 8 ? 3 : V == 4 ? 2 : 1;
+  static_assert((1 << RB) == V && RB <= NPB, "one value per lane at most");
+  scatter_stage<NPB - 1, V / 2>(a, lane);
+  if constexpr (RB >= 2) scatter_stage<NPB - 2, V / 4>(a, lane);
+  if constexpr (RB >= 3) scatter_stage<NPB - 3, V / 8>(a, lane);
+  if constexpr (RB >= 4) scatter_stage<NPB - 4, V / 16>(a, lane);
+  if constexpr (NPB - RB - 1 >= 2) a[0] += swap_bit<2>(a[0]);
+  if constexpr (NPB - RB - 1 >= 1) a[0] += swap_bit<1>(a[0]);
+  if constexpr (NPB - RB - 1 >= 0) a[0] += swap_bit<0>(a[0]);
+  return a[0];
+}
+
+// All-gather stage across lane bit B: the list of N values doubles, the
+// values of lanes with the bit clear first.
+template <int B, int N, int G>
+__device__ __forceinline__ void gather_stage(uint32_t (&y)[G], int lane) {
+  const bool up = (lane >> B) & 1;
+  uint32_t o[N];
+#pragma unroll
+  for (int t = 0; t < N; ++t) o[t] = swap_bit<B>(y[t]);
+#pragma unroll
+  for (int t = 0; t < N; ++t) {
+    const uint32_t mine = y[t];
+    y[t] = up ? o[t] : mine;
+    y[t + N] = up ? mine : o[t];
+  }
+}
+
+// Every lane of a row gets the G values x of head g = (lane >> SH) % G (lanes
+// that differ only below bit SH hold equal values).
+template <int SH, int G>
+__device__ __forceinline__ void row_gather(uint32_t x, uint32_t (&y)[G], int lane) {
+  y[0] = x;
+  if constexpr (G >= 2) gather_stage<SH, 1>(y, lane);
+  if constexpr (G >= 4) gather_stage<SH + 1, 2>(y, lane);
+  if constexpr (G >= 8) gather_stage<SH + 2, 4>(y, lane);
+}
+
 template <int D, int G>
 struct SS {
   static constexpr int NP = D / 8;                 // lanes per row, one 16-byte piece each
@@ -127,7 +213,13 @@ struct SS {
   static constexpr int SP = W * RPL * G * D;       // residual V accumulators (floats)
   static constexpr int MG = W * G * (D + 2);       // per-wave (acc, m, l) for the workgroup merge
   static constexpr int LDSF = SP > MG ? SP : MG;
-  static_assert(NL % 2 == 0 && CW % TILE == 0 && RPL * NP == 64, "shape");
+  static constexpr int NPB = NP == 16 ? 4 : 3;     // log2 NP
+  // the NL x G logits of a lane's rows fit one per lane of the row: the
+  // softmax runs on a reduce-scatter of them (lane v << SH holds row v / G,
+  // head v % G)
+  static constexpr bool SCATTER = NL == 2 && NL * G <= NP;
+  static constexpr int SH = SCATTER ? NPB - (G == 8 ? 4 : G == 4 ? 3 : G == 2 ? 2 : 1) : 0;
+  static_assert(NL == 2 && CW % TILE == 0 && RPL * NP == 64, "shape");
 };
 
 template <int D, int G>
@@ -280,6 +372,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
   const int ntiles = wtok0 < T ? min(CW / TILE, (T - wtok0 + TILE - 1) / TILE) : 0;
 
   float m[G], l[G], acc[G][8];
+  // scattered softmax state: the reference max of the lane's head and the
+  // running sum of its (row, head) logit (lanes of one head share ms)
+  float ms = -INFINITY, ls = 0.f;
+  const int s_row = ((lane % NP) >> S::SH) / G;  // the lane's row of the two (0 or 1)
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     m[g] = -INFINITY;
@@ -398,65 +494,114 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           }
         }
       }
-      float d = -INFINITY;
+      // probabilities of the lane's two rows per head as bf16 pairs (row 0
+      // low), and as fp32 for the residual V entries
+      uint32_t pp[G];
+      float p[NL][G];
+      if constexpr (S::SCATTER) {
+        // Lane pc of the row ends up with the full logit of row s_row, head
+        // (pc >> SH) % G, so the scale, the mask, the exp2 and the running sum
+        // are taken once per logit rather than on every lane of the row.
+        float a[NL * G];
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const int row = r0 + i * RPL + rg;
+        for (int i = 0; i < NL; ++i)
+#pragma unroll
+          for (int g = 0; g < G; ++g) a[i * G + g] = s[i][g];
+        const float red = row_reduce_scatter<S::NPB>(a, lane);
+        const int row = r0 + s_row * RPL + rg;
         const bool valid = row < T && (RES != 3 || ((b.tm >> (row & 31)) & 1u) == 0u);
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float x = group_sum<NP>(s[i][g]) * P.scale_log2;
-          s[i][g] = valid ? x : -INFINITY;
-          d = fmaxf(d, s[i][g] - m[g]);
-        }
-      }
-      // The reference max moves only when some logit exceeds it by more than
-      // kSlack (probabilities then stay below 2^kSlack); moving it takes the
-      // tile max over the wave's rows and rescales the running sums.
-      if (__ballot(d > kSlack) != 0) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          float mt = s[0][g];
-#pragma unroll
-          for (int i = 1; i < NL; ++i) mt = fmaxf(mt, s[i][g]);
+        const float x = valid ? red * P.scale_log2 : -INFINITY;
+        // The reference max moves only when some logit exceeds it by more than
+        // kSlack (probabilities then stay below 2^kSlack); moving it takes the
+        // head's max over the wave's rows and rescales the running sums.
+        if (__ballot(x - ms > kSlack) != 0) {
+          float mt = fmaxf(x, swap_half<NP>(x));
 #pragma unroll
           for (int o = NP; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
-          const float mn = fmaxf(m[g], mt);
-          const float alpha = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
-          l[g] *= alpha;
+          const float mn = fmaxf(ms, mt);
+          const float al = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - mn);
+          ls *= al;
+          ms = mn;
 #pragma unroll
-          for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
-          if constexpr (RES == 1 || RES == 2) {
+          for (int g = 0; g < G; ++g) {
+            // every lane of head g holds the same factor; lane g << SH is one
+            const float alpha = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(al), g << S::SH));
 #pragma unroll
-            for (int cp = 0; cp < RPL; ++cp)
+            for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
+            if constexpr (RES == 1 || RES == 2) {
 #pragma unroll
-              for (int c = lane; c < D; c += 64) sp(wave, cp, g, c) *= alpha;
+              for (int cp = 0; cp < RPL; ++cp)
+#pragma unroll
+                for (int c = lane; c < D; c += 64) sp(wave, cp, g, c) *= alpha;
+            }
           }
-          m[g] = mn;
         }
+        // masked rows: exp2(-inf) = 0; a token-level set can mask every row
+        // of a tile before any logit has set the reference max, and
+        // exp2(-inf - -inf) would be NaN
+        const float pv = (RES == 3 && x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x - ms);
+        ls += pv;
+        const float pq = swap_half<NP>(pv);  // the same head's other row
+        row_gather<S::SH>(s_row == 0 ? cvt_bf16x2(pv, pq) : cvt_bf16x2(pq, pv), pp, lane);
+        if constexpr (RES == 1 || RES == 2) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            p[0][g] = bf16_lo(pp[g]);
+            p[1][g] = bf16_hi(pp[g]);
+          }
+        }
+      } else {
+        float d = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const int row = r0 + i * RPL + rg;
+          const bool valid = row < T && (RES != 3 || ((b.tm >> (row & 31)) & 1u) == 0u);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            const float x = group_sum<NP>(s[i][g]) * P.scale_log2;
+            s[i][g] = valid ? x : -INFINITY;
+            d = fmaxf(d, s[i][g] - m[g]);
+          }
+        }
+        if (__ballot(d > kSlack) != 0) {
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            float mt = s[0][g];
+#pragma unroll
+            for (int i = 1; i < NL; ++i) mt = fmaxf(mt, s[i][g]);
+#pragma unroll
+            for (int o = NP; o < 64; o <<= 1) mt = fmaxf(mt, __shfl_xor(mt, o, 64));
+            const float mn = fmaxf(m[g], mt);
+            const float alpha = (m[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
+            l[g] *= alpha;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) acc[g][c] *= alpha;
+            if constexpr (RES == 1 || RES == 2) {
+#pragma unroll
+              for (int cp = 0; cp < RPL; ++cp)
+#pragma unroll
+                for (int c = lane; c < D; c += 64) sp(wave, cp, g, c) *= alpha;
+            }
+            m[g] = mn;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < NL; ++i)
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            if constexpr (RES == 3)
+              p[i][g] = s[i][g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i][g] - m[g]);
+            else
+              p[i][g] = __builtin_amdgcn_exp2f(s[i][g] - m[g]);
+            l[g] += p[i][g];
+          }
+#pragma unroll
+        for (int g = 0; g < G; ++g) pp[g] = cvt_bf16x2(p[0][g], p[1][g]);
       }
-      float p[NL][G];
-#pragma unroll
-      for (int i = 0; i < NL; ++i)
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          // masked rows: exp2(-inf) = 0; a token-level set can mask every
-          // row of a tile before any logit has set the reference max, and
-          // exp2(-inf - -inf) would be NaN
-          if constexpr (RES == 3)
-            p[i][g] = s[i][g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s[i][g] - m[g]);
-          else
-            p[i][g] = __builtin_amdgcn_exp2f(s[i][g] - m[g]);
-          l[g] += p[i][g];
-        }
-      // P V over the dense plane: the lane's rows 2pr and 2pr + 1 share one dot2
-#pragma unroll
-      for (int pr = 0; pr < NL / 2; ++pr) {
-        uint32_t pp[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) pp[g] = pack_bf16x2(p[2 * pr][g], p[2 * pr + 1][g]);
-        const uint4 va = C8 ? widen_e4m3(b.v[2 * pr]) : b.v[2 * pr];
-        const uint4 vb = C8 ? widen_e4m3(b.v[2 * pr + 1]) : b.v[2 * pr + 1];
+      // P V over the dense plane: the lane's two rows share one dot2
+      {
+        const uint4 va = C8 ? widen_e4m3(b.v[0]) : b.v[0];
+        const uint4 vb = C8 ? widen_e4m3(b.v[1]) : b.v[1];
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
           const uint32_t wa = word(va, w), wb = word(vb, w);
@@ -546,6 +691,17 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
           if (j == 0 || t + j < ntiles) compute(t + j, buf[j]);
         }
       }
+    }
+
+    if constexpr (S::SCATTER) {
+      // back to values per head: the reference max, and on every lane its
+      // row group's sum over both rows (the form the set pass and the merge take)
+#pragma unroll
+      for (int g = 0; g < G; ++g) m[g] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ms), g << S::SH));
+      uint32_t lg[G];
+      row_gather<S::SH>(__float_as_uint(ls + swap_half<NP>(ls)), lg, lane);
+#pragma unroll
+      for (int g = 0; g < G; ++g) l[g] = __uint_as_float(lg[g]);
     }
 
     if constexpr (RES == 3) {
