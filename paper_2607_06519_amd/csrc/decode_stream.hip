@@ -117,7 +117,8 @@ __device__ __forceinline__ float run_sum(int c, float x, int pc, bool valid, boo
 template <int B>
 __device__ __forceinline__ uint32_t swap_bit(uint32_t x) {
   constexpr int kCtrl = B == 3 ? kDppRowMirror : B == 2 ? kDppRowHalfMirror : B == 1 ? kDppQuadXor2 : kDppQuadXor1;
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kCtrl, 0xF, 0xF, false);
+  // every source lane lies in the row: bound_ctrl needs no old value
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kCtrl, 0xF, 0xF, true);
 }
 template <int B>
 __device__ __forceinline__ float swap_bit(float x) {
@@ -130,7 +131,7 @@ __device__ __forceinline__ float swap_bit(float x) {
 template <int NP>
 __device__ __forceinline__ float swap_half(float x) {
   if constexpr (NP == 16) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, true));
   } else {
     static_assert(NP == 8, "row width");
     int y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x104, 0xF, 0x5, false);
