@@ -57,10 +57,10 @@ __device__ __forceinline__ uint4 mean_piece(const uint4* x) {
 // 16 bytes of bf16 inputs per layer (8 channels) -> 8 bytes of FP8 E4M3 block means.
 template <int NB>
 __device__ __forceinline__ uint2 mean_piece_e4m3(const uint4* x) {
-  uint32_t w[2] = {0u, 0u};
+  float m[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) w[i >> 2] |= (uint32_t)f32_to_e4m3(block_mean<true, NB>(x, i)) << (8 * (i & 3));
-  return make_uint2(w[0], w[1]);
+  for (int i = 0; i < 8; ++i) m[i] = block_mean<true, NB>(x, i);
+  return make_uint2(e4m3_quad(m[0], m[1], m[2], m[3]), e4m3_quad(m[4], m[5], m[6], m[7]));
 }
 
 // The dense pass reads every input row once and writes every plane once:
@@ -129,7 +129,7 @@ __device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b,
       const int e = e0 + __builtin_popcount(sel & ((1u << c) - 1u));
       si[e] = (uint8_t)(lr * CPP + c);
       if constexpr (C8)
-        sv[e] = f32_to_e4m3(dv[c]);
+        sv[e] = e4m3_one(dv[c]);
       else if constexpr (BF16)
         reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)(hv[c >> 1] >> (16 * (c & 1)));
       else
@@ -208,7 +208,7 @@ __device__ __forceinline__ void residual_entries4(const uint4 (&x)[4], int k, in
         const int e = e0 + __builtin_popcount(sel & ((1u << b) - 1u));
         si[e] = (uint16_t)(4 * (lr * CPP + c) + j + 1);
         if constexpr (C8)
-          sv[e] = f32_to_e4m3(z[j]);
+          sv[e] = e4m3_one(z[j]);
         else if constexpr (BF16)
           reinterpret_cast<uint16_t*>(sv)[e] = (uint16_t)f32_to_bf16_bits(z[j]);
         else

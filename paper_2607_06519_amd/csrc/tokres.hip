@@ -461,10 +461,8 @@ __global__ __launch_bounds__(256) void token_rows_kernel(TokenParams P) {
     for (int f = 0; f < NF; ++f) {
       uint8_t* o = dst + ((uint64_t)f * D + pc * 8) * CE;
       if (c8) {
-        uint32_t w[2] = {0u, 0u};
-#pragma unroll
-        for (int c = 0; c < 8; ++c) w[c >> 2] |= (uint32_t)f32_to_e4m3(h[f][c]) << (8 * (c & 3));
-        *reinterpret_cast<uint2*>(o) = make_uint2(w[0], w[1]);
+        *reinterpret_cast<uint2*>(o) = make_uint2(e4m3_quad(h[f][0], h[f][1], h[f][2], h[f][3]),
+                                                  e4m3_quad(h[f][4], h[f][5], h[f][6], h[f][7]));
       } else if constexpr (BF16) {
         *reinterpret_cast<uint4*>(o) = make_uint4(pack_bf16x2(h[f][0], h[f][1]), pack_bf16x2(h[f][2], h[f][3]),
                                                   pack_bf16x2(h[f][4], h[f][5]), pack_bf16x2(h[f][6], h[f][7]));
