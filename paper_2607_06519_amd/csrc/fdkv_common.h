@@ -133,25 +133,39 @@ FDKV_HD float bf16_lo(uint32_t w) { return as_f32(w << 16); }
 FDKV_HD float bf16_hi(uint32_t w) { return as_f32(w & 0xFFFF0000u); }
 FDKV_HD float bf16_to_f32(uint16_t h) { return as_f32((uint32_t)h << 16); }
 
-// Round to nearest even; inputs are finite.
-FDKV_HD uint32_t f32_to_bf16_bits(float f) {
-  uint32_t u = as_u32(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-FDKV_HD uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
-}
-
 #ifdef __HIPCC__
-// Two fp32 values as a bf16 pair, round to nearest even (the gfx950
-// conversion instruction: one per pair; finite inputs round as f32_to_bf16_bits).
+// Two fp32 values as a bf16 pair, round to nearest even: the gfx950
+// conversion instruction, one per pair.  For every input other than NaN it
+// gives the integer rounding below (checked over all 2^32 bit patterns,
+// subnormals and infinities included).
 __device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
   typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
   typedef float f32x2v __attribute__((ext_vector_type(2)));
   const f32x2v v = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
 }
+#endif
+
+// Round to nearest even; inputs are not NaN.  Device code takes the
+// conversion instruction, host code the integer form.
+FDKV_HD uint32_t f32_to_bf16_bits(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return cvt_bf16x2(f, 0.f) & 0xFFFFu;
+#else
+  uint32_t u = as_u32(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+#endif
+}
+FDKV_HD uint32_t pack_bf16x2(float lo, float hi) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return cvt_bf16x2(lo, hi);
+#else
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+#endif
+}
+
+#ifdef __HIPCC__
 
 // Two fp32 values as a sum of two bf16 pairs, hi = bf16(x) and
 // lo = bf16(x - hi) (x - hi is exact in fp32): hi + lo is x to within
