@@ -113,6 +113,14 @@ CASES = {
                                 seq_lens=(450,), n_needles=3, needle_channels=8, schedule=2, fixed_modes=(1, 1)),
     "quads_bf16_k40": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=40,
                              seq_lens=(260,), n_needles=2, schedule=2, fixed_modes=(1, 2)),
+    # the remaining shapes of the decode's reduce-scatter softmax: rows of 8 lanes (d = 64) with G = 4
+    # (one logit per lane) and G = 1 (two butterfly stages), rows of 16 lanes with G = 1
+    "bf16_d64_g4": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=8, head_dim=64, topk=8,
+                          seq_lens=(600,), n_needles=3, needle_channels=8, fixed_modes=(1, 0)),
+    "e4m3_d64_g1": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=2, head_dim=64, topk=8,
+                          seq_lens=(530,), n_needles=3, needle_channels=8, dtype="bf16_e4m3", fixed_modes=(1, 2)),
+    "bf16_g1": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=2, seq_lens=(520,), n_needles=3,
+                      fixed_modes=(1, 0)),
 }
 
 
