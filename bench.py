@@ -22,6 +22,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import math
 import os
@@ -124,11 +125,23 @@ def unit_read_bytes(w, mode, T, B):
     return T * 2 * d * c + -(-T // 32) * 4 + (-(-T // 128) + 1) * 4 + n * 2 * (B - 1) * d * c
 
 
-def kernel_source_hash():
+def code_tokens(text):
+    """C++ source without comments and whitespace: edits to comments keep the hash."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def kernel_source_hash(read=None):
+    """Hash of the code the decode kernels build from; counter runs recorded under another hash
+    are not used.  ``read(name)`` returns a file's text (default: the working tree)."""
+    if read is None:
+        def read(name):
+            with open(os.path.join(ROOT, "paper_2607_06519_amd", "csrc", name)) as f:
+                return f.read()
     h = hashlib.sha256()
     for name in ("decode.hip", "decode_stream.hip", "fdkv_common.h", "fdkv_kernels.h"):
-        with open(os.path.join(ROOT, "paper_2607_06519_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        h.update(code_tokens(read(name)).encode())
     return h.hexdigest()[:16]
 
 

@@ -15,14 +15,17 @@
 //        registers); residual heads add the lane's residual entry
 //        w * q[c] * value (B = 2: c the channel, w = +-1 for the stored half
 //        difference; B = 4: code 4c + j, w = F_4[j][p] for layer p of the
-//        block); a DPP butterfly then sums over the row's lanes,
-//        which leaves every lane of the row with the row's logits -- exactly
-//        the probabilities its V pass needs, so nothing goes through LDS;
-//  max - a running reference max, uniform over the wave, that moves (cross-
-//        row max, rescale by exp2(m_old - m_new)) only when a logit exceeds
-//        it by more than 2^8;
-//  V   - the lane's rows are taken in pairs so one dot2 multiplies two
-//        tokens' values by their two bf16 probabilities; residual heads add
+//        block); a DPP reduce-scatter over the row's lanes then leaves each
+//        lane one full (row, head) logit (2G <= NP: d = 128, or d = 64 with
+//        G <= 4; d = 64 with G = 8 sums every logit on every lane instead);
+//  max - a running reference max per head, equal on the lanes of that head,
+//        that moves (the head's max over the wave, rescale by
+//        exp2(m_old - m_new)) only when a logit exceeds it by more than 2^8;
+//        scale, mask, exp2 and running sum run once per logit;
+//  V   - each lane's probability goes back to the row as a bf16 pair (the
+//        same head's other row) and an all-gather over the heads, so nothing
+//        goes through LDS; the lane's two rows share one dot2 that
+//        multiplies two tokens' values by their probabilities; residual heads add
 //        w * p * value into LDS accumulators, one copy per row of a load
 //        (a row's entries sit on distinct channels for B = 2, so a plain
 //        read-add-write is safe; for B = 4 up to three frequencies of one
