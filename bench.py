@@ -8,7 +8,9 @@ shared/residual/exact head mix).  Inputs are resident in HBM before timing.
 Layers run in cold order (all even layers, then all odd ones) so the shared
 planes of a pair are evicted from the 256 MB Infinity Cache before the pair's
 second layer re-reads them; the headline bandwidth is therefore HBM
-bandwidth.  The step is captured once in a HIP graph and replayed.
+bandwidth.  The step is captured once in a HIP graph and replayed: by default
+10 untimed steps, then 100 timed together (the mean is `value`), then the same
+100 again each between its own events (p50 and p95 in `step_ms_stats`).
 
 Printed: one JSON line with the metric, a roofline object for the decode
 launch (split-K + combine per layer, timed with HIP events on the launch
@@ -44,8 +46,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--order", choices=["cold", "model"], default="cold")
     ap.add_argument("--no-graph", action="store_true")
