@@ -377,6 +377,21 @@ fdkv_status fdkv_decode_spans(const fdkv_dims* dims, int32_t batch, int32_t n_sp
                               const fdkv_tail* tail, int32_t layer, const void* q, void* out, float sm_scale,
                               void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * fdkv_check_conversions - diagnostic, synchronous on `stream`.  Runs the
+ * device's number encoders over every fp32 bit pattern except NaN and
+ * counts where they differ from their integer definitions (0 expected):
+ *   mismatches[0]  the E4M3 encoder of the compress kernels (the conversion
+ *                  instruction on inputs clamped to +-448) against round to
+ *                  nearest even with saturation at 448 (Section 3's
+ *                  quantised coefficients, OCP E4M3)
+ *   mismatches[1]  the bf16 pair conversion against round to nearest even
+ *                  on the bit pattern
+ *   mismatches     host uint64 [2], out
+ * Allocates and frees 16 bytes of device memory; FDKV_E_HIP on a runtime error.
+ */
+fdkv_status fdkv_check_conversions(uint64_t* mismatches, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,8 @@ STATUS = {0: "FDKV_OK", -1: "FDKV_E_INVALID_ARG", -2: "FDKV_E_UNSUPPORTED", -3: 
 SYMBOLS = ("fdkv_status_string", "fdkv_last_error", "fdkv_blocks", "fdkv_layout", "fdkv_route",
            "fdkv_probe_workspace", "fdkv_probe", "fdkv_compress", "fdkv_decode_workspace", "fdkv_decode_attn",
            "fdkv_append", "fdkv_decode_spans_workspace", "fdkv_decode_spans", "fdkv_decode_static_scratch_bytes",
-           "fdkv_decode_attn_static", "fdkv_decode_partial", "fdkv_decode_combine", "fdkv_selection_bytes")
+           "fdkv_decode_attn_static", "fdkv_decode_partial", "fdkv_decode_combine", "fdkv_selection_bytes",
+           "fdkv_check_conversions")
 PAIRS, MIXED, QUADS = 0, 1, 2    # block schedules (fdkv_schedule)
 RES_CHANNELS, RES_TOKENS = 0, 1  # residual kinds (fdkv_residual)
 
@@ -97,6 +98,8 @@ def load():
     lib.fdkv_compress.argtypes = [DP, I32, P, P, P, P, P, P, P, P]
     lib.fdkv_selection_bytes.restype = I32
     lib.fdkv_selection_bytes.argtypes = [DP, I32, P]
+    lib.fdkv_check_conversions.restype = I32
+    lib.fdkv_check_conversions.argtypes = [P, P]
     lib.fdkv_decode_workspace.restype = I32
     lib.fdkv_decode_workspace.argtypes = [DP, I32, I32, P]
     lib.fdkv_decode_attn.restype = I32
@@ -194,6 +197,14 @@ def selection_bytes(d: Dims, seq_len: int) -> int:
     n = ctypes.c_size_t(0)
     _check(load().fdkv_selection_bytes(ctypes.byref(d), int(seq_len), ctypes.byref(n)), "fdkv_selection_bytes")
     return int(n.value)
+
+
+def check_conversions(stream=None) -> tuple:
+    """Mismatches of the device E4M3 encoder and bf16 rounding against their integer
+    definitions over every non-NaN fp32 bit pattern (fdkv_check_conversions)."""
+    out = (ctypes.c_uint64 * 2)()
+    _check(load().fdkv_check_conversions(out, _stream(stream)), "fdkv_check_conversions")
+    return int(out[0]), int(out[1])
 
 
 def decode_workspace(d: Dims, batch: int, max_seq_len: int) -> int:

@@ -577,6 +577,25 @@ fdkv_status fdkv_append(const fdkv_dims* dims, int32_t batch, const int32_t* pos
   return FDKV_OK;
 }
 
+fdkv_status fdkv_check_conversions(uint64_t* mismatches, void* stream) {
+  if (!mismatches) return FDKV_E_INVALID_ARG;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned long long* counts = nullptr;
+  hipError_t e = hipMalloc(&counts, 2 * sizeof(unsigned long long));
+  if (e != hipSuccess) return hip_fail(e, "check_conversions");
+  unsigned long long host[2] = {0ull, 0ull};
+  e = hipMemsetAsync(counts, 0, sizeof(host), s);
+  if (e == hipSuccess) e = launch_check_conversions(counts, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(host, counts, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  const hipError_t ef = hipFree(counts);
+  if (e == hipSuccess) e = ef;
+  if (e != hipSuccess) return hip_fail(e, "check_conversions");
+  mismatches[0] = host[0];
+  mismatches[1] = host[1];
+  return FDKV_OK;
+}
+
 }  // extern "C"
 
 namespace {

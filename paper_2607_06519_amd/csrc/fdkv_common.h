@@ -136,8 +136,8 @@ FDKV_HD float bf16_to_f32(uint16_t h) { return as_f32((uint32_t)h << 16); }
 #ifdef __HIPCC__
 // Two fp32 values as a bf16 pair, round to nearest even: the gfx950
 // conversion instruction, one per pair.  For every input other than NaN it
-// gives the integer rounding below (checked over all 2^32 bit patterns,
-// subnormals and infinities included).
+// gives the integer rounding below, subnormals and infinities included
+// (fdkv_check_conversions compares the two over all 2^32 bit patterns).
 __device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
   typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
   typedef float f32x2v __attribute__((ext_vector_type(2)));
@@ -146,15 +146,19 @@ __device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
 }
 #endif
 
-// Round to nearest even; inputs are not NaN.  Device code takes the
-// conversion instruction, host code the integer form.
+// Round to nearest even in integer arithmetic; inputs are not NaN.
+FDKV_HD uint32_t bf16_bits_int(float f) {
+  uint32_t u = as_u32(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+// The same rounding: device code takes the conversion instruction, host
+// code the integer form.
 FDKV_HD uint32_t f32_to_bf16_bits(float f) {
 #if defined(__HIP_DEVICE_COMPILE__)
   return cvt_bf16x2(f, 0.f) & 0xFFFFu;
 #else
-  uint32_t u = as_u32(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
+  return bf16_bits_int(f);
 #endif
 }
 FDKV_HD uint32_t pack_bf16x2(float lo, float hi) {

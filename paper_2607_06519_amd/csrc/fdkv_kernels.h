@@ -157,6 +157,8 @@ hipError_t launch_decode(const DecodeParams& P, hipStream_t s);        // split-
 hipError_t launch_decode_stream(const DecodeParams& P, hipStream_t s);  // bf16 split-K
 hipError_t launch_decode_merge(const DecodeParams& P, hipStream_t s);   // log-sum-exp merge of the records
 hipError_t launch_append(const AppendParams& P, hipStream_t s);
+// counts[0] += E4M3 encoder mismatches, counts[1] += bf16 rounding mismatches
+hipError_t launch_check_conversions(unsigned long long* counts, hipStream_t s);
 hipError_t launch_token_scores(const TokenParams& P, hipStream_t s);   // the blocks of P.bl (one size)
 hipError_t launch_token_select(const TokenParams& P, hipStream_t s);   // probe: errors; compress: mask, counts
 hipError_t launch_token_rows(const TokenParams& P, hipStream_t s);     // compress: rows of the selected tokens

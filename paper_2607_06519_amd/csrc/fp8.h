@@ -49,8 +49,9 @@ FDKV_F8_HD uint8_t f32_to_e4m3(float x) {
 #if defined(__HIPCC__)
 // The device encoder: the gfx950 conversion instruction (OCP E4M3, round to
 // nearest even) on inputs clamped to +-448, two values per instruction.  For
-// every fp32 input other than NaN it gives f32_to_e4m3's code (checked over
-// all 2^32 bit patterns); the stored coefficients are finite.  Writes the
+// every fp32 input other than NaN it gives f32_to_e4m3's code
+// (fdkv_check_conversions compares the two over all 2^32 bit patterns); the
+// stored coefficients are finite.  Writes the
 // codes of a and b to bytes 0-1 (hi = false) or 2-3 (hi = true) of old.
 __device__ __forceinline__ uint32_t e4m3_pair(float a, float b, uint32_t old, bool hi) {
   const float ca = __builtin_amdgcn_fmed3f(a, -448.f, 448.f), cb = __builtin_amdgcn_fmed3f(b, -448.f, 448.f);
