@@ -41,6 +41,9 @@ CASES = {
                          n_needles=2, fixed_modes=(0, 1, 1, 2, 0, 1, 1, 0, 2, 1)),
     "quads_f32_k7": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, topk=7, seq_lens=(300, 129),
                            schedule=2, needle_channels=7, fixed_modes=(1, 2)),
+    # FP8 E4M3 coefficients in the prefix span and in every refreshed span (the tail stays bf16)
+    "pairs_e4m3": scaled(WORKLOADS["llama8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(520, 260),
+                         n_needles=3, dtype="bf16_e4m3", fixed_modes=(1, 0, 2, 1)),
 }
 
 
