@@ -349,3 +349,103 @@ def test_token_rates_routed_per_unit(torch_dev, name):
                     worst = max(worst, e)
                     assert e <= 1e-2, (name, layer, h, g, e)
     log(f"  compress and decode with per-unit fractions ok; worst rel-L2 {worst:.3e}")
+
+
+GEN_CASES = {
+    "pairs_bf16_gen": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=2, n_q_heads=8, seq_lens=(600,),
+                           n_probe=16, res_ppm=100000),
+    # one block of four: three heads, so the prefix holds a shared, a token-set and an exact unit
+    "quads_e4m3_gen": _tok(WORKLOADS["prefill8b"], n_layers=4, n_kv_heads=3, n_q_heads=12, seq_lens=(400,),
+                           n_probe=16, res_ppm=100000, schedule=2, dtype="bf16_e4m3"),
+}
+
+
+@pytest.mark.parametrize("name", list(GEN_CASES))
+def test_token_sets_in_generation(torch_dev, name):
+    """Decode over spans that hold token-level sets (the prefix, then two refreshed tails) and
+    the exact tail, i.e. the multi-part decode of a generation: against attention over the
+    oracle's reconstruction of every span (Eq. 3 with the GPU's own sets, whose validity
+    test_token_residual_parity checks) followed by the tail rows."""
+    torch = torch_dev
+    from paper_2607_06519_amd import binding as Bn
+    from paper_2607_06519_amd.cache import CompressedCache, Generation, probe, to_device
+    from test_gpu_generation import _new_token
+    w = GEN_CASES[name]
+    T, P, G, d, H, L = w.seq_lens[0], w.n_probe, w.group, w.head_dim, w.n_kv_heads, w.n_layers
+    ppm, cap, steps = w.res_ppm, 24, 2 * 24 + 3
+    log(f"[case] token sets in generation {name}: prefix {T}, tail {cap}, {steps} steps, blocks {w.block_sizes} "
+        f"{w.dtype}")
+    dm = Bn.dims(**w.dims())
+    K, V = gen.layer_cache(w, 0)
+    Q = gen.probe_queries(w, 0)
+    Kd, Vd, Qd = to_device(K, w.dtype), to_device(V, w.dtype), to_device(Q, w.dtype)
+    kl, vl, ql = ([X[l] for l in range(L)] for X in (Kd, Vd, Qd))
+    _, scores = probe(dm, T, kl, ql, P)
+    modes = np.full((w.n_blocks, H), O.RESIDUAL, np.uint8)
+    modes[0, 0] = O.SHARED
+    modes[-1, -1] = O.EXACT
+    cache = CompressedCache(dm, w.seq_lens, modes[None])
+    cache.compress(0, kl, vl, token_scores=scores)
+    torch.cuda.synchronize()
+
+    def span_units(span, smodes, KX, VX, n_tok):
+        """(unit, mode, B) per (block, head): the oracle's unit built on the span's own set."""
+        buf = span.host_bytes()
+        units = {}
+        for b, (f, B) in enumerate(w.blocks):
+            for h in range(H):
+                m = int(smodes[b, h])
+                got, _ = unpack_tok_unit(buf, int(span.offsets_host[0, b, h]), m, n_tok, d, ppm, w.dtype, B)
+                S = got["TS"] if m == O.RESIDUAL else None
+                if m == O.RESIDUAL:
+                    assert S.size == O.n_residual_tokens(n_tok, ppm), (b, h, S.size)
+                units[(b, h)] = (O.compress_unit_tokens(KX[f:f + B, h], VX[f:f + B, h], m, S, w.dtype), m, B)
+        return units
+
+    spans = [span_units(cache, modes, K, V, T)]
+    g = Generation(dm, cache, cap)
+    rng = np.random.default_rng(11)
+    tailK, tailV, recent = ([[] for _ in range(L)] for _ in range(3))
+    blk = {l: (b, f, B) for b, (f, B) in enumerate(w.blocks) for l in range(f, f + B)}
+    tol = 1e-2
+    worst, refreshes, n_res = 0.0, 0, int((modes == O.RESIDUAL).sum())
+    for step in range(steps):
+        if g.full:
+            probe_rows = [to_device(np.stack(recent[l][-P:], axis=2), w.dtype) for l in range(L)]
+            # a byte budget halfway between the all-shared and the all-exact tail span routes a mix
+            size = lambda m: sum(O.unit_bytes_tokens(m, cap, d, ppm, w.dtype, B) for _, B in w.blocks) * H
+            budget = (size(O.SHARED) + size(O.EXACT)) // 2
+            new_modes = g.refresh(probe_rows, P, budget_bytes=budget)[0]
+            refreshes += 1
+            n_res += int(((new_modes & 3) == O.RESIDUAL).sum())
+            Kt = np.stack([np.stack(tailK[l], axis=2)[0] for l in range(L)])   # [L][H][cap][d]
+            Vt = np.stack([np.stack(tailV[l], axis=2)[0] for l in range(L)])
+            spans.append(span_units(g.spans[-1], new_modes & 3, Kt, Vt, cap))
+            tailK, tailV = [[] for _ in range(L)], [[] for _ in range(L)]
+            log(f"  refresh {refreshes}: modes {np.bincount((new_modes & 3).ravel(), minlength=3).tolist()}")
+        kn, vn = _new_token(w, rng)
+        qs = gen.decode_queries(w, step, scale=4.0)
+        for layer in range(L):
+            g.append(layer, to_device(kn[layer], w.dtype), to_device(vn[layer], w.dtype))
+            out = g.decode(layer, to_device(qs[layer], w.dtype)).float().cpu().numpy()[0]
+            tailK[layer].append(kn[layer])
+            tailV[layer].append(vn[layer])
+            b, f, B = blk[layer]
+            for h in range(H):
+                Ks, Vs = [], []
+                for span in spans:
+                    unit, m, _ = span[(b, h)]
+                    Ks.append(O.reconstruct_layer_tokens(unit, m, layer - f, d, "K", B))
+                    Vs.append(O.reconstruct_layer_tokens(unit, m, layer - f, d, "V", B))
+                Ks.append(np.stack([r[0, h] for r in tailK[layer]]).astype(np.float64))
+                Vs.append(np.stack([r[0, h] for r in tailV[layer]]).astype(np.float64))
+                want = O.attention(qs[layer][0, h * G:(h + 1) * G].astype(np.float64), np.concatenate(Ks),
+                                   np.concatenate(Vs), 1.0 / math.sqrt(d))
+                for gg in range(G):
+                    e = rel_l2(out[h * G + gg], want[gg])
+                    worst = max(worst, e)
+                    assert e <= tol, (name, step, layer, h, gg, e)
+            recent[layer].append(qs[layer])
+        g.advance()
+    assert refreshes == 2 and len(g.spans) == 3
+    log(f"  {steps} steps ok; worst rel-L2 {worst:.3e} (tol {tol}); {n_res} token-set units over the spans")
