@@ -233,30 +233,8 @@ __global__ __launch_bounds__(kScoreThreads) void token_score_kernel(TokenParams 
 namespace {
 
 constexpr int kSelThreads = 1024;
-
-// Exclusive prefix sum over the workgroup (1024 threads, 16 waves); returns
-// this thread's prefix and writes the total to *total.
-__device__ __forceinline__ uint32_t block_scan(uint32_t x, uint32_t* lds16, uint32_t* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t incl = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += y;
-  }
-  __syncthreads();
-  if (lane == 63) lds16[wave] = incl;
-  __syncthreads();
-  uint32_t before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kSelThreads / 64; ++w) {
-    const uint32_t v = lds16[w];
-    before += w < wave ? v : 0u;
-    all += v;
-  }
-  *total = all;
-  return before + incl - x;
-}
+constexpr int kSelBatch = 16;   // keys per thread and batch of a radix pass
+constexpr int kSelGroups = 8;   // groups of 64 tokens per batch of a wave's walk
 
 }  // namespace
 
@@ -267,8 +245,8 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t x, uint32_t* lds16, uint
 // counts.
 __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P) {
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t scan16[kSelThreads / 64];
   __shared__ uint32_t pick[2];
+  __shared__ uint32_t run_eq[kSelThreads / 64], run_gt[kSelThreads / 64];
   __shared__ double red[kSelThreads / 64][2];
   const int bi = blockIdx.x / P.hkv, head = blockIdx.x % P.hkv;
   const int unit = P.bl.block[bi] * P.hkv + head;
@@ -286,20 +264,43 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
   for (int shift = 24; shift >= 0 && n > 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int t = tid; t < T; t += kSelThreads) {
-      const uint32_t k = key[t];
-      if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    // kSelBatch keys per thread in flight, then their counts
+    for (int t0 = tid; t0 < T; t0 += kSelBatch * kSelThreads) {
+      uint32_t kb[kSelBatch];
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j) {
+        const int t = t0 + j * kSelThreads;
+        kb[j] = t < T ? key[t] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kSelBatch; ++j)
+        if (t0 + j * kSelThreads < T && (kb[j] & pmask) == prefix) atomicAdd(&hist[(kb[j] >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      uint32_t above = 0;
-      int b = 255;
-      for (; b > 0; --b) {
-        if (above + hist[b] >= need) break;
-        above += hist[b];
+    if (tid < 64) {
+      // the digit: the highest bin b whose count of keys in bins >= b
+      // reaches need (the suffix counts fall with b, so b + 1 is how many
+      // bins reach it); lane l holds bins 4l .. 4l + 3
+      const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2], h3 = hist[4 * tid + 3];
+      const uint32_t mine = h0 + h1 + h2 + h3;
+      uint32_t incl = mine;  // keys in this lane's bins and above
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_down(incl, o, 64);
+        if (tid + o < 64) incl += y;
       }
-      pick[0] = (uint32_t)b;
-      pick[1] = need - above;
+      const uint32_t s3 = incl - mine + h3, s2 = s3 + h2, s1 = s2 + h1, s0 = s1 + h0;
+      uint32_t c = (s0 >= need) + (s1 >= need) + (s2 >= need) + (s3 >= need);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
+      const uint32_t bstar = c > 0 ? c - 1 : 0;
+      if ((uint32_t)tid == bstar >> 2) {
+        const uint32_t j = bstar & 3u;
+        const uint32_t sj = j == 0 ? s0 : j == 1 ? s1 : j == 2 ? s2 : s3;
+        const uint32_t hj = j == 0 ? h0 : j == 1 ? h1 : j == 2 ? h2 : h3;
+        pick[0] = bstar;
+        pick[1] = need - (sj - hj);  // need less the keys in the bins above b
+      }
     }
     __syncthreads();
     prefix |= pick[0] << shift;
@@ -309,21 +310,50 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
   }
   const uint32_t tau = prefix;
 
-  // 2. each thread walks a contiguous run of 128-token chunks in token order
+  // 2. each wave takes a contiguous run of 128-token chunks and walks it 64
+  //    tokens at a time (coalesced loads, ballots): a first walk counts the
+  //    run's keys above and equal to tau, the waves' counts in order give
+  //    each run the equal keys and the selected tokens before it, and a
+  //    second walk ranks the equal keys in token order and emits the set
+  const int lane = tid & 63, wave = tid >> 6;
+  constexpr int kW = kSelThreads / 64;
   const int words = (T + 31) / 32, chunks = (T + kTokChunk - 1) / kTokChunk;
-  const int cpt = (chunks + kSelThreads - 1) / kSelThreads;    // chunks per thread
-  const int c0 = min(tid * cpt, chunks), c1 = min(c0 + cpt, chunks);
-  const int w0 = c0 * 4, w1 = min(c1 * 4, words);
-  uint32_t eq_mine = 0;
-  for (int w = w0; w < w1; ++w)
-    for (int b = 0; b < 32; ++b) {
-      const int t = w * 32 + b;
-      if (t < T && n > 0 && key[t] == tau) ++eq_mine;
+  const int cpw = (chunks + kW - 1) / kW;                     // chunks per wave
+  const int c0 = min(wave * cpw, chunks), c1 = min(c0 + cpw, chunks);
+  const int t0 = c0 * kTokChunk, t1 = min(c1 * kTokChunk, T);
+  uint32_t n_eq = 0, n_gt = 0;
+  if (n > 0)
+    for (int g0 = t0; g0 < t1; g0 += kSelGroups * 64) {  // kSelGroups groups of 64 tokens in flight
+      uint32_t kb[kSelGroups];
+#pragma unroll
+      for (int j = 0; j < kSelGroups; ++j) {
+        const int t = g0 + 64 * j + lane;
+        kb[j] = t < t1 ? key[t] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kSelGroups; ++j) {
+        const bool ok = g0 + 64 * j + lane < t1;
+        n_eq += (uint32_t)__popcll(__ballot(ok && kb[j] == tau));
+        n_gt += (uint32_t)__popcll(__ballot(ok && kb[j] > tau));
+      }
     }
-  uint32_t eq_total;
-  uint32_t eq_rank = block_scan(eq_mine, scan16, &eq_total);
+  if (lane == 0) {
+    run_eq[wave] = n_eq;
+    run_gt[wave] = n_gt;
+  }
+  __syncthreads();
+  // equal keys and selected tokens before this run, and the set's size:
+  // a run takes its keys above tau and the equal ones still needed
+  uint32_t eq_acc = 0, rank = 0, sel_run = 0, sel_total = 0;
+  for (int w = 0; w < kW; ++w) {
+    if (w == wave) {
+      rank = eq_acc;
+      sel_run = sel_total;
+    }
+    sel_total += run_gt[w] + (need > eq_acc ? min(run_eq[w], need - eq_acc) : 0u);
+    eq_acc += run_eq[w];
+  }
   double sum_all = 0.0, sum_kept = 0.0;
-  uint32_t sel_mine = 0;
   uint32_t* mask_out = nullptr;
   uint32_t* count_out = nullptr;
   if (P.modes) {
@@ -333,40 +363,46 @@ __global__ __launch_bounds__(kSelThreads) void token_select_kernel(TokenParams P
     mask_out = reinterpret_cast<uint32_t*>(seg + L.mask);
     count_out = reinterpret_cast<uint32_t*>(seg + L.count);
   }
-  for (int w = w0; w < w1; ++w) {
-    uint32_t m = 0;
-    for (int b = 0; b < 32; ++b) {
-      const int t = w * 32 + b;
-      if (t >= T) break;
-      const uint32_t k = key[t];
-      bool sel = false;
-      if (n > 0) {
-        sel = k > tau;
-        if (k == tau) {
-          sel = eq_rank < need;
-          ++eq_rank;
-        }
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (int g0 = t0; g0 < t1; g0 += kSelGroups * 64) {
+    // kSelGroups groups of 64 tokens: keys and losses in flight, then in token order
+    uint32_t kb[kSelGroups];
+    float eb[kSelGroups];
+#pragma unroll
+    for (int j = 0; j < kSelGroups; ++j) {
+      const int t = g0 + 64 * j + lane;
+      kb[j] = t < t1 ? key[t] : 0u;
+      eb[j] = (P.sumsq && t < t1) ? P.sumsq[(uint64_t)unit * T + t] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelGroups; ++j) {
+      const int g = g0 + 64 * j;
+      if (g >= t1) break;
+      const int t = g + lane;
+      const bool ok = t < t1;
+      const uint32_t k = kb[j];
+      const bool eq = ok && n > 0 && k == tau;
+      const uint64_t beq = __ballot(eq);
+      const uint32_t r = rank + (uint32_t)__popcll(beq & below);
+      const bool sel = ok && n > 0 && (k > tau || (eq && r < need));
+      rank += (uint32_t)__popcll(beq);
+      const uint64_t bsel = __ballot(sel);
+      // 3. compress: the token mask, and the running count before every chunk
+      if (mask_out) {
+        if (lane == 0) mask_out[g >> 5] = (uint32_t)bsel;
+        if (lane == 32 && (g >> 5) + 1 < words) mask_out[(g >> 5) + 1] = (uint32_t)(bsel >> 32);
       }
-      m |= sel ? 1u << b : 0u;
-      if (P.sumsq) {
-        const double e = (double)P.sumsq[(uint64_t)unit * T + t];
+      if (count_out && lane == 0 && (g & (kTokChunk - 1)) == 0) count_out[g / kTokChunk] = sel_run;
+      sel_run += (uint32_t)__popcll(bsel);
+      if (P.sumsq && ok) {
+        const double e = (double)eb[j];
         sum_all += e;
         sum_kept += sel ? e : 0.0;
       }
     }
-    sel_mine += (uint32_t)__builtin_popcount(m);
-    if (mask_out) mask_out[w] = m;
   }
-  // 3. compress: running counts before every chunk; probe: the losses
-  if (count_out) {
-    uint32_t sel_total;
-    uint32_t run = block_scan(sel_mine, scan16, &sel_total);
-    for (int c = c0; c < c1; ++c) {
-      count_out[c] = run;
-      for (int w = c * 4; w < min(c * 4 + 4, words); ++w) run += (uint32_t)__builtin_popcount(mask_out[w]);
-    }
-    if (tid == 0) count_out[chunks] = sel_total;
-  }
+  if (count_out && tid == 0) count_out[chunks] = sel_total;
+  //    probe: the losses
   if (P.sumsq) {
     // fixed-order reduction: waves by shuffles, then wave 0 over the 16 partials
     const int lane = tid & 63, wave = tid >> 6;
