@@ -279,6 +279,14 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
   constexpr int WPM = 4, TPW = (NT + WPM - 1) / WPM;  // four waves per matrix: block t on wave t % WPM
   constexpr int R = kGramRows, LDR = D + 16;
   constexpr int LPT = R * NPc / 512;             // loads per thread per layer per step
+  // a thread holds PPT pieces of one token row, one from each of its PPT
+  // runs of LPR = NPc / PPT pieces (at least 8 lanes, at most 16 keys a lane:
+  // fewer count reductions per bisection step of the top-k, more rows per
+  // wave, and the LPR lanes' loads of a run are contiguous)
+  constexpr int PPT0 = LPT < NPc / 8 ? LPT : NPc / 8;
+  constexpr int PPT = PPT0 < 16 / CPP ? PPT0 : 16 / CPP;
+  constexpr int LPR = NPc / PPT, KPT = PPT * CPP;
+  static_assert(PPT >= 1 && LPT % PPT == 0 && LPR >= 8, "row layout");
   constexpr TriTiles<NB> tri{};
   // [D hi, D lo, Dbar hi, Dbar lo][token][channel]
   __shared__ __attribute__((aligned(16))) uint16_t tile[4][R * LDR];
@@ -303,11 +311,13 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
   for (int i = 0; i < TPW; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  // ra[j], rb[j]: piece (j % PPT) LPR + g % LPR of token row g / LPR,
+  // g = tid + 512 (j / PPT)
   uint4 ra[LPT], rb[LPT];
   auto load = [&](int t0) {
 #pragma unroll
     for (int j = 0; j < LPT; ++j) {
-      const int i = tid + 512 * j, t = t0 + i / NPc, pc = i % NPc;
+      const int g = tid + 512 * (j / PPT), t = t0 + g / LPR, pc = (j % PPT) * LPR + g % LPR;
       const bool ok = t < t_end;
       ra[j] = load16(ka, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
       rb[j] = load16(kb, ok ? (uint32_t)(t * RB + pc * 16) : kOobOff);
@@ -316,53 +326,64 @@ __global__ __launch_bounds__(512) void probe_dgram_kernel(ProbeParams P) {
   load(t_begin);
   for (int t0 = t_begin; t0 < t_end; t0 += R) {
 #pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      const int i = tid + 512 * j, row = i / NPc, pc = i % NPc;
-      const uint32_t* pa = reinterpret_cast<const uint32_t*>(&ra[j]);
-      const uint32_t* pb = reinterpret_cast<const uint32_t*>(&rb[j]);
-      // the half differences, and the token's top-k keys |fl32(a - b)| (the
-      // NPc lanes of the row hold its pieces; rows past the chunk read zeros)
-      float dv[CPP];
-      uint32_t key[CPP];
+    for (int q = 0; q < LPT / PPT; ++q) {
+      const int g = tid + 512 * q, row = g / LPR, lr = g % LPR;
+      // the half differences, and the token's top-k keys |fl32(a - b)|: key
+      // h CPP + c is channel CPP (h LPR + lr) + c (rows past the chunk read
+      // zeros)
+      float dv[KPT];
+      uint32_t key[KPT];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        if constexpr (BF16) {
-          const float d0 = bf16_lo(pa[w]) - bf16_lo(pb[w]), d1 = bf16_hi(pa[w]) - bf16_hi(pb[w]);
-          key[2 * w] = as_u32(d0) & 0x7FFFFFFFu;
-          key[2 * w + 1] = as_u32(d1) & 0x7FFFFFFFu;
-          dv[2 * w] = d0 * 0.5f;
-          dv[2 * w + 1] = d1 * 0.5f;
-        } else {
-          const float d0 = as_f32(pa[w]) - as_f32(pb[w]);
-          key[w] = as_u32(d0) & 0x7FFFFFFFu;
-          dv[w] = d0 * 0.5f;
+      for (int h = 0; h < PPT; ++h) {
+        const uint32_t* pa = reinterpret_cast<const uint32_t*>(&ra[q * PPT + h]);
+        const uint32_t* pb = reinterpret_cast<const uint32_t*>(&rb[q * PPT + h]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if constexpr (BF16) {
+            const float d0 = bf16_lo(pa[w]) - bf16_lo(pb[w]), d1 = bf16_hi(pa[w]) - bf16_hi(pb[w]);
+            key[h * CPP + 2 * w] = as_u32(d0) & 0x7FFFFFFFu;
+            key[h * CPP + 2 * w + 1] = as_u32(d1) & 0x7FFFFFFFu;
+            dv[h * CPP + 2 * w] = d0 * 0.5f;
+            dv[h * CPP + 2 * w + 1] = d1 * 0.5f;
+          } else {
+            const float d0 = as_f32(pa[w]) - as_f32(pb[w]);
+            key[h * CPP + w] = as_u32(d0) & 0x7FFFFFFFu;
+            dv[h * CPP + w] = d0 * 0.5f;
+          }
         }
       }
-      // Dbar: drop the channels of this piece that are among the token's top-k
-      const uint32_t sel = row_topk_mask<NPc, CPP>(key, k);
-      const uint32_t keep = ~sel & ((1u << CPP) - 1u);
+      // Dbar: drop the thread's channels that are among the token's top-k
+      const uint32_t sel = row_topk_mask<LPR, KPT, PPT>(key, k);
+      const uint32_t keep = ~sel & ((1u << KPT) - 1u);
       if (P.ksel) {  // the selection, for compress to reuse
         const int t = t0 + row;
-        if (t < t_end) P.ksel[selection_offset(unit, T, t, pc, D, E, P.ksel_bytes)] = (uint8_t)sel;
+        if (t < t_end)
+#pragma unroll
+          for (int h = 0; h < PPT; ++h)
+            P.ksel[selection_offset(unit, T, t, h * LPR + lr, D, E, P.ksel_bytes)] =
+                (uint8_t)((sel >> (h * CPP)) & ((1u << CPP) - 1u));
       }
-      uint32_t wd[CPP / 2], wl[CPP / 2], wr[CPP / 2], wrl[CPP / 2];
+      uint32_t wd[KPT / 2], wl[KPT / 2], wr[KPT / 2], wrl[KPT / 2];
 #pragma unroll
-      for (int c = 0; c < CPP / 2; ++c) split_bf16x2(dv[2 * c], dv[2 * c + 1], wd[c], wl[c]);
+      for (int c = 0; c < KPT / 2; ++c) split_bf16x2(dv[2 * c], dv[2 * c + 1], wd[c], wl[c]);
 #pragma unroll
-      for (int c = 0; c < CPP / 2; ++c) {
+      for (int c = 0; c < KPT / 2; ++c) {
         const uint32_t km = (((keep >> (2 * c)) & 1) ? 0xFFFFu : 0u) | (((keep >> (2 * c + 1)) & 1) ? 0xFFFF0000u : 0u);
         wr[c] = wd[c] & km;
         wrl[c] = wl[c] & km;
       }
       const uint32_t* src[4] = {wd, wl, wr, wrl};
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        uint16_t* dst = &tile[m][row * LDR + pc * CPP];
-        if constexpr (CPP == 8)
-          *reinterpret_cast<uint4*>(dst) = make_uint4(src[m][0], src[m][1], src[m][2], src[m][3]);
-        else
-          *reinterpret_cast<uint2*>(dst) = make_uint2(src[m][0], src[m][1]);
-      }
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int h = 0; h < PPT; ++h) {
+          uint16_t* dst = &tile[m][row * LDR + (h * LPR + lr) * CPP];
+          const uint32_t* sp = src[m] + h * (CPP / 2);
+          if constexpr (CPP == 8)
+            *reinterpret_cast<uint4*>(dst) = make_uint4(sp[0], sp[1], sp[2], sp[3]);
+          else
+            *reinterpret_cast<uint2*>(dst) = make_uint2(sp[0], sp[1]);
+        }
     }
     load(t0 + R);
     __syncthreads();

@@ -3,8 +3,12 @@
 // row, ties to the lower channel, found by the lanes that hold the row.
 //
 // A row of d channels sits on LPR consecutive lanes (a DPP row or part of
-// one; 32 lanes for fp32 rows of 128 channels), lane j holding channels
-// CPL j .. CPL j + CPL - 1.  Keys are the bit patterns of the non-negative
+// one; 32 lanes for fp32 rows of 128 channels).  A lane's CPL keys form H
+// segments of S = CPL / H consecutive channels: key s S + c of lane j is
+// channel s LPR S + j S + c (H = 1: lane j holds channels CPL j ..
+// CPL j + CPL - 1; H = 2: a lane holds one run in each half of the row, so
+// that loads of a segment over the row's lanes are contiguous).  Keys are
+// the bit patterns of the non-negative
 // fp32 magnitudes, which order like the values.  Every lane of a row keeps
 // the same bounds lo < hi with clo = #(keys >= lo) >= k and chi = #(keys >=
 // hi) < k, and bisects [lo, hi) on the bit patterns, counting keys >= mid
@@ -15,10 +19,11 @@
 // either one (lo becomes the largest key below hi) or all but one (lo
 // becomes the smallest key at or above lo), and the selection is every key
 // above lo plus the first k - #(keys > lo) keys equal to lo in channel
-// order.  The first lo is the smallest lane maximum (at least LPR keys reach
-// it, so it is valid for k <= LPR, else 0) and the first hi is the row
-// maximum plus one; an open row's interval halves every step, so every row
-// stops within 32 steps.  Returns the lane's selection as a CPL-bit mask.
+// order (segment by segment, lanes in order within a segment).  The first lo is the smallest lane maximum (at least LPR keys reach
+// it, so it is valid for k <= LPR), for LPR < k <= 2 LPR the smallest lane's
+// second-largest key, else 0; the first hi is the row maximum plus one; an
+// open row's interval halves every step, so every row stops within 32 steps.
+// Returns the lane's selection as a CPL-bit mask.
 #pragma once
 
 #include "fdkv_common.h"
@@ -76,10 +81,12 @@ __device__ __forceinline__ uint32_t row_count_ge(const uint32_t (&key)[CPL], uin
   return row_sum_u32<LPR>(c);
 }
 
-// The lane's selected channels (bit i: channel CPL * (lane % LPR) + i) of
-// the k largest keys of its row, ties to the lower channel.  0 <= k <= d.
-template <int LPR, int CPL>
+// The lane's selected keys (bit i: key i, the channel given above) of the k
+// largest keys of its row, ties to the lower channel.  0 <= k <= d.
+template <int LPR, int CPL, int H = 1>
 __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], int k) {
+  static_assert(H >= 1 && CPL % H == 0, "segments");
+  constexpr int S = CPL / H;
   constexpr uint32_t kAll = (1u << CPL) - 1u;
   if (k <= 0) return 0u;
   if (k >= LPR * CPL) return kAll;
@@ -87,7 +94,20 @@ __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], in
 #pragma unroll
   for (int i = 1; i < CPL; ++i) lmax = key[i] > lmax ? key[i] : lmax;
   const uint32_t rmax = row_ext_u32<LPR, true>(lmax);
-  uint32_t lo = k <= LPR ? row_ext_u32<LPR, false>(lmax) : 0u;
+  uint32_t lo = 0u;
+  if (k <= LPR) {
+    lo = row_ext_u32<LPR, false>(lmax);
+  } else if (CPL >= 2 && k <= 2 * LPR) {
+    // every lane's second-largest key: at least 2 LPR keys reach the smallest
+    uint32_t m1 = 0u, m2 = 0u;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const uint32_t x = key[i];
+      m2 = max(m2, min(m1, x));
+      m1 = max(m1, x);
+    }
+    lo = row_ext_u32<LPR, false>(m2);
+  }
   uint32_t hi = rmax + 1u;
   uint32_t clo = row_count_ge<LPR, CPL>(key, lo), chi = 0;
   const uint32_t ku = (uint32_t)k;
@@ -137,19 +157,30 @@ __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], in
     uint32_t eq = 0;
 #pragma unroll
     for (int i = 0; i < CPL; ++i) eq |= key[i] == lo ? 1u << i : 0u;
-    const uint32_t neq = (uint32_t)__builtin_popcount(eq);
-    // exclusive prefix of the equal counts over the row's lower lanes
-    const uint32_t incl = row_prefix_u32<LPR>(neq);
+    // rank of the lane's first equal key of each segment: the equal keys of
+    // the row's earlier segments, then those of the segment's lower lanes
+    uint32_t start[H];
+    uint32_t base = 0;
+#pragma unroll
+    for (int sg = 0; sg < H; ++sg) {
+      const uint32_t n = (uint32_t)__builtin_popcount(eq & (((1u << S) - 1u) << (sg * S)));
+      start[sg] = base + row_prefix_u32<LPR>(n) - n;
+      if (sg + 1 < H) base += row_sum_u32<LPR>(n);
+    }
     if (tied) {
       const uint32_t need = ku - cgt;
-      uint32_t rank = incl - neq;
       uint32_t s2 = 0;
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-        if (key[i] > lo) s2 |= 1u << i;
-        if (key[i] == lo) {
-          if (rank < need) s2 |= 1u << i;
-          ++rank;
+      for (int sg = 0; sg < H; ++sg) {
+        uint32_t rank = start[sg];
+#pragma unroll
+        for (int c = 0; c < S; ++c) {
+          const int i = sg * S + c;
+          if (key[i] > lo) s2 |= 1u << i;
+          if (key[i] == lo) {
+            if (rank < need) s2 |= 1u << i;
+            ++rank;
+          }
         }
       }
       sel = s2;

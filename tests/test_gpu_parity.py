@@ -249,6 +249,8 @@ PROBE_CASES = {
                                 seq_lens=(700,), n_probe=20, needle_channels=7, schedule=1),
     "quads_f32": scaled(WORKLOADS["tiny"], n_layers=4, n_kv_heads=2, n_q_heads=4, seq_lens=(600,), n_probe=24,
                         schedule=2),
+    "f32_d128": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=128, topk=16,
+                       seq_lens=(700,), n_probe=16, needle_channels=16),
 }
 
 
@@ -372,6 +374,9 @@ REUSE_CASES = {
                        n_needles=4, fixed_modes=(1, 0, 1, 2)),
     "f32_d64_k7": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=7,
                          seq_lens=(333,), n_probe=8, n_needles=0, fixed_modes=(1, 1)),
+    # fp32 rows of 128: the probe ranks them on 8 lanes of four runs each
+    "f32_k16": scaled(WORKLOADS["tiny"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=128, topk=16,
+                      seq_lens=(290,), n_probe=8, n_needles=0, needle_channels=16, fixed_modes=(1, 1)),
     "e4m3_d64_k5": scaled(WORKLOADS["llama8b"], n_layers=2, n_kv_heads=2, n_q_heads=4, head_dim=64, topk=5,
                           seq_lens=(517,), n_probe=8, n_needles=2, dtype="bf16_e4m3", fixed_modes=(1, 1)),
     "mixed_bf16": scaled(WORKLOADS["llama8b"], n_layers=12, n_kv_heads=2, n_q_heads=4, seq_lens=(300,), n_probe=8,
