@@ -85,7 +85,7 @@ __device__ __forceinline__ uint32_t row_count_ge(const uint32_t (&key)[CPL], uin
 // largest keys of its row, ties to the lower channel.  0 <= k <= d.
 template <int LPR, int CPL, int H = 1>
 __device__ __forceinline__ uint32_t row_topk_mask(const uint32_t (&key)[CPL], int k) {
-  static_assert(H >= 1 && CPL % H == 0, "segments");
+  static_assert(H >= 1 && CPL % H == 0 && CPL < 32, "segments, and one mask bit per key");
   constexpr int S = CPL / H;
   constexpr uint32_t kAll = (1u << CPL) - 1u;
   if (k <= 0) return 0u;
