@@ -75,59 +75,79 @@ __device__ __forceinline__ void store_stream(uint8_t* p, const uint4& x) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4v*>(p));
 }
 
+// Pieces of one token row a thread of the pairs' dense pass holds: two where
+// the row then still spans at least 8 lanes (fewer count reductions per
+// bisection step of the top-k, more rows per wave), else one.  Lane lr of a
+// row holds pieces h LPR + lr, h < PPT, so that the row's lanes load and
+// store each run of LPR pieces as one contiguous span.  Blocks of four keep
+// one piece (3 CPP keys a lane already).
+template <int D, bool BF16, int NB>
+struct DenseLayout {
+  static constexpr int E = BF16 ? 2 : 4;
+  static constexpr int NP = D * E / 16;               // 16-byte pieces per row
+  static constexpr int PPT = (NB == 2 && NP >= 16) ? 2 : 1;
+  static constexpr int LPR = NP / PPT;                // lanes per row
+  static constexpr int RPP = 256 / LPR;               // rows per pass of 256 threads
+  static constexpr int RPW = 64 / LPR;                // rows of a pass per wave
+};
+
 // Residual entries of pairs, from the rows the dense pass holds: the lanes
 // of a token row find its top-k channels of |fl32(a - b)| (row_topk_mask),
 // each lane puts its selected channels and their half differences D at
-// their slots (the row's selected channels in ascending order: the lanes'
-// counts before it, then its own order) into the wave's LDS staging, and the
-// wave writes its rows' index and value runs with 4-byte stores (bytes where
-// a run does not start on a 4-byte boundary, and for its last partial word).
-template <int D, bool BF16, bool C8>
-__device__ __forceinline__ void residual_entries(const uint4& a, const uint4& b, int k, int row_in_wave, int t0w,
-                                                 int T, uint8_t* idx_plane, uint8_t* val_plane, uint8_t* stage,
-                                                 int preset = -1) {
-  constexpr int E = BF16 ? 2 : 4;
-  constexpr int NP = D * E / 16, CPP = 16 / E, RPW = 64 / NP;
+// their slots (the row's selected channels in ascending order: those of the
+// row's earlier runs of pieces, then the lanes' counts before it in its run,
+// then its own order) into the wave's LDS staging, and the wave writes its
+// rows' index and value runs with 4-byte stores (bytes where a run does not
+// start on a 4-byte boundary, and for its last partial word).
+// x[h][n]: piece h LPR + lr of layer n (lr: the lane's place in the row), so
+// key h CPP + c is channel CPP (h LPR + lr) + c.  PRESET: the lane's
+// selection is `preset` (the probe's, of the same keys, so the same
+// channels), and no keys are formed.
+template <int D, bool BF16, bool C8, bool PRESET = false>
+__device__ __forceinline__ void residual_entries(const uint4 (&x)[DenseLayout<D, BF16, 2>::PPT][2], int k,
+                                                 int row_in_wave, int t0w, int T, uint8_t* idx_plane,
+                                                 uint8_t* val_plane, uint8_t* stage, uint32_t preset = 0) {
+  using Ly = DenseLayout<D, BF16, 2>;
+  constexpr int E = Ly::E, CPP = 16 / E, PPT = Ly::PPT, LPR = Ly::LPR, RPW = Ly::RPW, KPT = PPT * CPP;
   constexpr int VB = C8 ? 1 : E;                       // bytes per stored value
-  const uint32_t* pa = reinterpret_cast<const uint32_t*>(&a);
-  const uint32_t* pb = reinterpret_cast<const uint32_t*>(&b);
-  uint32_t key[CPP];
-  float dv[CPP];
+  uint32_t key[KPT];
+  float dv[KPT];
 #pragma unroll
-  for (int c = 0; c < CPP; ++c) {
-    float x, y;
-    if constexpr (BF16) {
-      x = (c & 1) ? bf16_hi(pa[c >> 1]) : bf16_lo(pa[c >> 1]);
-      y = (c & 1) ? bf16_hi(pb[c >> 1]) : bf16_lo(pb[c >> 1]);
-    } else {
-      x = as_f32(pa[c]);
-      y = as_f32(pb[c]);
+  for (int h = 0; h < PPT; ++h)
+#pragma unroll
+    for (int c = 0; c < CPP; ++c) {
+      const float df = chan<BF16>(x[h][0], c) - chan<BF16>(x[h][1], c);
+      if constexpr (!PRESET) key[h * CPP + c] = as_u32(df) & 0x7FFFFFFFu;
+      dv[h * CPP + c] = df * 0.5f;
     }
-    const float df = x - y;
-    key[c] = as_u32(df) & 0x7FFFFFFFu;
-    dv[c] = df * 0.5f;
-  }
+  uint32_t sel = preset;
+  if constexpr (!PRESET) sel = row_topk_mask<LPR, KPT, PPT>(key, k);
   // bf16 values: every channel's rounded half difference, one conversion per pair
-  uint32_t hv[CPP / 2];
+  uint32_t hv[KPT / 2];
   if constexpr (BF16 && !C8) {
 #pragma unroll
-    for (int c = 0; c < CPP / 2; ++c) hv[c] = cvt_bf16x2(dv[2 * c], dv[2 * c + 1]);
+    for (int c = 0; c < KPT / 2; ++c) hv[c] = cvt_bf16x2(dv[2 * c], dv[2 * c + 1]);
   }
-  // the probe's selection of this row when given (the same keys, so the same channels)
-  const uint32_t sel = preset >= 0 ? (uint32_t)preset : row_topk_mask<NP, CPP>(key, k);
-  const uint32_t mine = (uint32_t)__builtin_popcount(sel);
-  const uint32_t incl = row_prefix_u32<NP>(mine);
-  const int lr = (int)(threadIdx.x & (NP - 1));
+  const int lr = (int)(threadIdx.x & (LPR - 1));
   // staging of the wave: RPW rows x k index bytes, then RPW rows x k values
   uint8_t* si = stage;
   uint8_t* sv = stage + ((RPW * k + 3) & ~3);
-  // the lane's selected channels go to consecutive slots from its first one
-  const int e0 = row_in_wave * k + (int)(incl - mine);
+  // the slot of the lane's first selected channel of each piece; the others
+  // follow it
+  int e0[PPT];
+  uint32_t base = 0;
 #pragma unroll
-  for (int c = 0; c < CPP; ++c) {
+  for (int h = 0; h < PPT; ++h) {
+    const uint32_t mine = (uint32_t)__builtin_popcount((sel >> (h * CPP)) & ((1u << CPP) - 1u));
+    e0[h] = row_in_wave * k + (int)(base + row_prefix_u32<LPR>(mine) - mine);
+    if (h + 1 < PPT) base += row_sum_u32<LPR>(mine);
+  }
+#pragma unroll
+  for (int c = 0; c < KPT; ++c) {
     if ((sel >> c) & 1u) {
-      const int e = e0 + __builtin_popcount(sel & ((1u << c) - 1u));
-      si[e] = (uint8_t)(lr * CPP + c);
+      const int h = c / CPP, cc = c % CPP;
+      const int e = e0[h] + __builtin_popcount((sel >> (h * CPP)) & ((1u << cc) - 1u));
+      si[e] = (uint8_t)((h * LPR + lr) * CPP + cc);
       if constexpr (C8)
         sv[e] = e4m3_one(dv[c]);
       else if constexpr (BF16)
@@ -234,15 +254,19 @@ __device__ __forceinline__ void residual_entries4(const uint4 (&x)[4], int k, in
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// At least three waves per SIMD: left to itself the compiler gives blocks of
-// four with bf16 inputs 180 VGPRs (two waves per SIMD); held to 168 it spills
-// three and the mixed 8B prefill compress takes 2.15 instead of 2.68 ms.
+// Waves per SIMD: four for pairs (128 VGPRs with K and V taken in turn),
+// three for blocks of four.  Left to itself the compiler gives blocks of
+// four with bf16 inputs 180 VGPRs (two waves); held to 168 they spill three
+// and the mixed 8B prefill compress takes 2.15 instead of 2.68 ms (held to
+// 128 they spill 31 and take 2.58 ms).
 template <int D, bool BF16, int NB>
-__global__ __launch_bounds__(256, 3) void compress_dense_kernel(CompressParams P) {
-  constexpr int E = BF16 ? 2 : 4;
-  constexpr int NP = D * E / 16;        // 16-byte pieces per row
-  constexpr int RPP = 256 / NP;         // rows per pass
-  constexpr int RPW = 64 / NP;          // rows of a pass per wave
+__global__ __launch_bounds__(256, NB == 2 ? 4 : 3) void compress_dense_kernel(CompressParams P) {
+  using Ly = DenseLayout<D, BF16, NB>;
+  constexpr int E = Ly::E;
+  constexpr int PPT = Ly::PPT, LPR = Ly::LPR;  // a thread: pieces h LPR + lr, h < PPT, of a row
+  constexpr int RPP = Ly::RPP;          // rows per pass
+  constexpr int RPW = Ly::RPW;          // rows of a pass per wave
+  static_assert(kCompressTile % RPP == 0, "passes per tile");
   // per wave: RPW rows x (k indices of up to 2 bytes + k values of up to 4 bytes)
   __shared__ __attribute__((aligned(16))) uint8_t stage[4][RPW * D * 6 + 16];
   const int bi = blockIdx.y / P.hkv, head = blockIdx.y % P.hkv;
@@ -262,8 +286,8 @@ __global__ __launch_bounds__(256, 3) void compress_dense_kernel(CompressParams P
   uint8_t* seg = P.cache + P.seg_off[unit];
   const bool c8 = BF16 && P.coef8;      // shared planes in FP8 E4M3: 8 bytes per 16-byte input piece
   const SegLayout L = seg_layout(mode, T, D, P.topk, E, c8 ? 1 : E, NB);
-  const int piece = threadIdx.x % NP;
-  const int row0 = blockIdx.x * kCompressTile + threadIdx.x / NP;
+  const int lr = threadIdx.x % LPR;
+  const int row0 = blockIdx.x * kCompressTile + threadIdx.x / LPR;
   // residual heads with per-token channel (pairs) or coefficient (fours)
   // entries take them in this pass too
   const bool resid = mode == kResidual && !P.tokres && P.topk > 0;
@@ -284,68 +308,132 @@ __global__ __launch_bounds__(256, 3) void compress_dense_kernel(CompressParams P
     if (!resid && t >= t_end) break;
     if (resid && blockIdx.x * kCompressTile + r >= T) break;
     const bool live = t < T;
-    const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
-    uint4 ka[NB], va[NB];
+    uint4 ka[PPT][NB], va[PPT][NB];
+    // a tensor's rows of the pass (pairs)
+    auto load_rows = [&](const uint8_t* const* x, uint4 (&a)[PPT][NB]) {
 #pragma unroll
-    for (int n = 0; n < NB; ++n) {
-      ka[n] = live ? load_stream(kx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
-      va[n] = live ? load_stream(vx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
-    }
-    if (!live) {
-      if (pad8 && t < t_end) {
-        const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);
-        *reinterpret_cast<uint2*>(seg + L.mk + o8) = make_uint2(0u, 0u);
-        *reinterpret_cast<uint2*>(seg + L.mv + o8) = make_uint2(0u, 0u);
-      }
-    } else if (mode == kExact) {
+      for (int h = 0; h < PPT; ++h) {
+        const uint64_t off = (uint64_t)t * row_bytes + (h * LPR + lr) * 16;
 #pragma unroll
-      for (int n = 0; n < NB; ++n) {
-        store_stream(seg + L.ek[n] + off, ka[n]);
-        store_stream(seg + L.ev[n] + off, va[n]);
+        for (int n = 0; n < NB; ++n) a[h][n] = live ? load_stream(x[n] + off) : make_uint4(0u, 0u, 0u, 0u);
       }
-    } else if (c8) {
-      const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);  // the 1 KB block layout of FP8 planes
-      *reinterpret_cast<uint2*>(seg + L.mk + o8) = mean_piece_e4m3<NB>(ka);
-      *reinterpret_cast<uint2*>(seg + L.mv + o8) = mean_piece_e4m3<NB>(va);
-    } else {
-      store_stream(seg + L.mk + off, mean_piece<BF16, NB>(ka));
-      store_stream(seg + L.mv + off, mean_piece<BF16, NB>(va));
-    }
-    if constexpr (NB == 4) {
-      if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
-        const int wave = threadIdx.x >> 6;
-        const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
-        const int rw = (threadIdx.x & 63) / NP;
-        // the probe's K selection of this row, when given (rows past the end take 0)
-        uint32_t kpre = 0;
-        if (P.ksel && live)
-          kpre = *reinterpret_cast<const uint32_t*>(P.ksel + selection_offset(unit, T, t, piece, D, E, 4));
-        const uint32_t* kp = P.ksel ? &kpre : nullptr;
-        if (c8) {
-          residual_entries4<D, BF16, true>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
-          residual_entries4<D, BF16, true>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+    };
+    // the planes' stores of piece h LPR + lr of one tensor of a pair (called
+    // once per piece: around these stores a loop, even of one trip, gave the
+    // register allocation more VGPRs)
+    auto store_piece = [&](const int h, const uint4 (&a)[PPT][NB], const uint64_t mplane, const uint64_t* eplane) {
+      const int piece = h * LPR + lr;
+      const uint64_t off = (uint64_t)t * row_bytes + piece * 16;
+      if (!live) {
+        if (pad8 && t < t_end) {
+          const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);
+          *reinterpret_cast<uint2*>(seg + mplane + o8) = make_uint2(0u, 0u);
+        }
+      } else if (mode == kExact) {
+#pragma unroll
+        for (int n = 0; n < NB; ++n) store_stream(seg + eplane[n] + off, a[h][n]);
+      } else if (c8) {
+        const uint64_t o8 = c8_piece_offset((uint64_t)t, piece, D);  // the 1 KB block layout of FP8 planes
+        *reinterpret_cast<uint2*>(seg + mplane + o8) = mean_piece_e4m3<NB>(a[h]);
+      } else {
+        store_stream(seg + mplane + off, mean_piece<BF16, NB>(a[h]));
+      }
+    };
+    static_assert(PPT <= 2, "pieces per thread");
+    static_assert(PPT == 1 || NB == 2, "blocks of four: one piece a thread");
+    const int wave = threadIdx.x >> 6;
+    const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
+    const int rw = (threadIdx.x & 63) / LPR;
+    if constexpr (NB == 2) {
+      // pairs: K, then V (a tensor's rows load, store their planes and, for
+      // residual heads, their entries before the other tensor's rows load;
+      // both tensors' rows in flight together took 150 VGPRs, or 128 with
+      // spills whose scratch writes reached HBM); residual heads are uniform
+      // over the workgroup (one unit) and every lane of a row takes part;
+      // K's entries take the probe's selection of the row's pieces when
+      // given (rows past the end take 0)
+      // V's rows load with K's unless K selects its own channels first
+      const bool early_v = !resid || P.ksel != nullptr;
+      load_rows(kx, ka);
+      if (early_v) load_rows(vx, va);
+      store_piece(0, ka, L.mk, L.ek);
+      if constexpr (PPT == 2) store_piece(1, ka, L.mk, L.ek);
+      if (resid) {
+        if (P.ksel) {
+          uint32_t kpre = 0;
+          if (live) {
+            constexpr int CPP = 16 / E;
+#pragma unroll
+            for (int h = 0; h < PPT; ++h)
+              kpre |= (uint32_t)P.ksel[selection_offset(unit, T, t, h * LPR + lr, D, E, P.ksel_bytes)] << (h * CPP);
+          }
+          if (c8)
+            residual_entries<D, BF16, true, true>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kpre);
+          else
+            residual_entries<D, BF16, false, true>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kpre);
         } else {
-          residual_entries4<D, BF16, false>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
-          residual_entries4<D, BF16, false>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+          if (c8)
+            residual_entries<D, BF16, true>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave]);
+          else
+            residual_entries<D, BF16, false>(ka, P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave]);
         }
       }
-    }
-    if constexpr (NB == 2) {
-      if (resid) {  // uniform over the workgroup (one unit); every lane of a row takes part
-        const int wave = threadIdx.x >> 6;
-        const int t0w = blockIdx.x * kCompressTile + r + wave * RPW;
-        const int kpre = (P.ksel && live) ? (int)P.ksel[selection_offset(unit, T, t, piece, D, E, P.ksel_bytes)]
-                                          : (P.ksel ? 0 : -1);
-        if (c8) {
-          residual_entries<D, BF16, true>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
-                                          seg + L.vk, stage[wave], kpre);
-          residual_entries<D, BF16, true>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
-                                          seg + L.vv, stage[wave]);
+      if (!early_v) load_rows(vx, va);
+      store_piece(0, va, L.mv, L.ev);
+      if constexpr (PPT == 2) store_piece(1, va, L.mv, L.ev);
+      if (resid) {
+        if (c8)
+          residual_entries<D, BF16, true>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+        else
+          residual_entries<D, BF16, false>(va, P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+      }
+    } else {
+      // blocks of four: both tensors' rows in flight together, both planes'
+      // stores, then the entries (of the orders tried, the one that spills
+      // the fewest registers at three waves per SIMD)
+#pragma unroll
+      for (int h = 0; h < PPT; ++h) {
+        const uint64_t off = (uint64_t)t * row_bytes + (h * LPR + lr) * 16;
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+          ka[h][n] = live ? load_stream(kx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
+          va[h][n] = live ? load_stream(vx[n] + off) : make_uint4(0u, 0u, 0u, 0u);
+        }
+      }
+      {
+        const uint64_t off = (uint64_t)t * row_bytes + lr * 16;
+        if (!live) {
+          if (pad8 && t < t_end) {
+            const uint64_t o8 = c8_piece_offset((uint64_t)t, lr, D);
+            *reinterpret_cast<uint2*>(seg + L.mk + o8) = make_uint2(0u, 0u);
+            *reinterpret_cast<uint2*>(seg + L.mv + o8) = make_uint2(0u, 0u);
+          }
+        } else if (mode == kExact) {
+#pragma unroll
+          for (int n = 0; n < NB; ++n) {
+            store_stream(seg + L.ek[n] + off, ka[0][n]);
+            store_stream(seg + L.ev[n] + off, va[0][n]);
+          }
+        } else if (c8) {
+          const uint64_t o8 = c8_piece_offset((uint64_t)t, lr, D);
+          *reinterpret_cast<uint2*>(seg + L.mk + o8) = mean_piece_e4m3<NB>(ka[0]);
+          *reinterpret_cast<uint2*>(seg + L.mv + o8) = mean_piece_e4m3<NB>(va[0]);
         } else {
-          residual_entries<D, BF16, false>(ka[0], ka[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.ik,
-                                           seg + L.vk, stage[wave], kpre);
-          residual_entries<D, BF16, false>(va[0], va[1], P.topk, (threadIdx.x & 63) / NP, t0w, T, seg + L.iv,
-                                           seg + L.vv, stage[wave]);
+          store_stream(seg + L.mk + off, mean_piece<BF16, NB>(ka[0]));
+          store_stream(seg + L.mv + off, mean_piece<BF16, NB>(va[0]));
+        }
+      }
+      if (resid) {
+        uint32_t kpre = 0;
+        if (P.ksel && live)
+          kpre = *reinterpret_cast<const uint32_t*>(P.ksel + selection_offset(unit, T, t, lr, D, E, 4));
+        const uint32_t* kp = P.ksel ? &kpre : nullptr;
+        if (c8) {
+          residual_entries4<D, BF16, true>(ka[0], P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
+          residual_entries4<D, BF16, true>(va[0], P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
+        } else {
+          residual_entries4<D, BF16, false>(ka[0], P.topk, rw, t0w, T, seg + L.ik, seg + L.vk, stage[wave], kp);
+          residual_entries4<D, BF16, false>(va[0], P.topk, rw, t0w, T, seg + L.iv, seg + L.vv, stage[wave]);
         }
       }
     }
