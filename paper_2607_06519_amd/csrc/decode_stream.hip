@@ -6,8 +6,8 @@
 // online softmax, keeping the next tiles' loads in flight while it computes
 // the current one.  The waves take the workgroup's tiles in turn (tile t of
 // wave w: tile 4t + w), so at any time they read one short run of each
-// plane; token-level sets keep 128 consecutive tokens a wave (one chunk of
-// the running counts).
+// plane; the rows of a token-level set are taken afterwards by the wave
+// whose 128 consecutive tokens (one chunk of the running counts) hold them.
 //
 // One lane layout serves the K pass, the softmax and the V pass: NP = d/8
 // lanes per token row, each holding one 16-byte piece (8 channels), so one
@@ -375,8 +375,9 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     qraw[j] = __builtin_amdgcn_raw_buffer_load_b16(qr, i < D * G ? i * 2 : kOob, 0, 0);
   }
 
+  // the wave's 128 consecutive tokens: its chunk of a token-level set's
+  // running counts
   const int wtok0 = wg_tok0 + wave * CW;
-  const int ntiles = wtok0 < T ? min(CW / TILE, (T - wtok0 + TILE - 1) / TILE) : 0;
 
   float m[G], l[G], acc[G][8];
   // scattered softmax state: the reference max of the lane's head and the
@@ -421,11 +422,10 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     // the wave's tile t: rows from row0(t), nt of them in the sequence
     // (interleaved over the waves: 1.1% off the 8B decode step against a
     // contiguous 128 tokens a wave)
-    constexpr bool IL = RES != 3;
-    auto row0 = [&](int t) -> int { return IL ? wg_tok0 + (t * W + wave) * TILE : wtok0 + t * TILE; };
-    const int nt = !IL ? ntiles
-                       : wg_tok0 + wave * TILE < T ? min(CW / TILE, (T - wg_tok0 - wave * TILE + W * TILE - 1) / (W * TILE))
-                                                   : 0;
+    auto row0 = [&](int t) -> int { return wg_tok0 + (t * W + wave) * TILE; };
+    const int nt = wg_tok0 + wave * TILE < T
+                       ? min(CW / TILE, (T - wg_tok0 - wave * TILE + W * TILE - 1) / (W * TILE))
+                       : 0;
 
     // FP8 planes: a tile is one 1 KB block, and the lane's 16-byte slot of it
     // holds its piece of both of its rows (rows rg and rg + RPL)
@@ -720,10 +720,11 @@ __global__ __launch_bounds__(256) void decode_stream_kernel(DecodeParams P) {
     }
 
     if constexpr (RES == 3) {
-      // The wave's tokens of the residual set (its 128 tokens are one chunk
-      // of the running counts), RPL at a time: the lanes of row group rg
-      // rebuild the rg-th one in full, K~ = M + sum_f w_f H_f and V~ alike,
-      // and fold it into the online softmax.
+      // The residual set's tokens among the wave's 128 consecutive tokens
+      // (one chunk of the running counts; the dense walk above skipped them
+      // whichever wave read their tile), RPL at a time: the lanes of row
+      // group rg rebuild the rg-th one in full, K~ = M + sum_f w_f H_f and V~
+      // alike, and fold it into the online softmax.
       constexpr int NF = Q4 ? 3 : 1;
       static_assert(CW == kTokChunk, "one count per wave");
       const uint32_t tw = (uint32_t)wtok0 >> 5;
